@@ -1,0 +1,149 @@
+// Device helpers and launch-argument structs shared by the HIP kernels of the
+// draft-and-verify step.  gfx950 (CDNA4) only: 64-lane wavefronts.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define OSP_WAVE 64
+#define OSP_DEV __device__ __forceinline__
+
+namespace osp {
+
+typedef uint16_t bf16_t;   // raw bfloat16 storage
+
+OSP_DEV float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
+OSP_DEV float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+OSP_DEV float bf16_to_f32(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+// float -> bfloat16, round to nearest, ties to even (NaN stays NaN).
+OSP_DEV bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+template <typename T> OSP_DEV float load_f32(const T* p, long i);
+template <> OSP_DEV float load_f32<float>(const float* p, long i) { return p[i]; }
+template <> OSP_DEV float load_f32<bf16_t>(const bf16_t* p, long i) { return bf16_to_f32(p[i]); }
+
+template <typename T> OSP_DEV void store_from_f32(T* p, long i, float v);
+template <> OSP_DEV void store_from_f32<float>(float* p, long i, float v) { p[i] = v; }
+template <> OSP_DEV void store_from_f32<bf16_t>(bf16_t* p, long i, float v) { p[i] = f32_to_bf16(v); }
+
+// Elements per 16-byte vector load.
+template <typename T> struct Vec;
+template <> struct Vec<float> { static constexpr int N = 4; };
+template <> struct Vec<bf16_t> { static constexpr int N = 8; };
+
+// Load one 16-byte vector and widen to floats.
+template <typename T> OSP_DEV void load_vec(const T* p, float* out);
+template <> OSP_DEV void load_vec<float>(const float* p, float* out) {
+  float4 v = *reinterpret_cast<const float4*>(p);
+  out[0] = v.x; out[1] = v.y; out[2] = v.z; out[3] = v.w;
+}
+template <> OSP_DEV void load_vec<bf16_t>(const bf16_t* p, float* out) {
+  uint4 v = *reinterpret_cast<const uint4*>(p);
+  out[0] = bf16_lo(v.x); out[1] = bf16_hi(v.x);
+  out[2] = bf16_lo(v.y); out[3] = bf16_hi(v.y);
+  out[4] = bf16_lo(v.z); out[5] = bf16_hi(v.z);
+  out[6] = bf16_lo(v.w); out[7] = bf16_hi(v.w);
+}
+
+OSP_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, OSP_WAVE);
+  return v;
+}
+OSP_DEV double wave_sum_d(double v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, OSP_WAVE);
+  return v;
+}
+OSP_DEV float wave_max(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, OSP_WAVE));
+  return v;
+}
+
+// Reduce V = 2^LOGV per-lane values over all 64 lanes at once.  On return
+// v[0] of lane l holds the full sum of value index (l >> (6 - LOGV)); every
+// lane of that group holds the same total.  Costs about V + 6 shuffles
+// instead of 6 V.
+template <int LOGV>
+OSP_DEV float transpose_reduce(float* v, int lane) {
+  constexpr int V = 1 << LOGV;
+#pragma unroll
+  for (int s = 0; s < LOGV; ++s) {
+    const int m = 32 >> s;
+    const int c = V >> s;
+    const int h = c >> 1;
+    const bool hi = (lane & m) != 0;
+#pragma unroll
+    for (int i = 0; i < h; ++i) {
+      float mine = hi ? v[i + h] : v[i];
+      float other = hi ? v[i] : v[i + h];
+      v[i] = mine + __shfl_xor(other, m, OSP_WAVE);
+    }
+  }
+#pragma unroll
+  for (int m = 32 >> LOGV; m >= 1; m >>= 1) v[0] += __shfl_xor(v[0], m, OSP_WAVE);
+  return v[0];
+}
+
+// Order-preserving float <-> uint key (for lowest-index argmax merges).
+OSP_DEV uint32_t float_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+}  // namespace osp
+
+namespace osp {
+
+// Inclusive prefix sum across the 64 lanes of a wavefront (fixed order).
+template <typename T>
+OSP_DEV T wave_incl_scan(T v) {
+  const int lane = threadIdx.x & (OSP_WAVE - 1);
+#pragma unroll
+  for (int s = 1; s < OSP_WAVE; s <<= 1) {
+    const T o = __shfl_up(v, s, OSP_WAVE);
+    if (lane >= s) v += o;
+  }
+  return v;
+}
+
+// Prefix sums over a block of NT threads (NT/64 wavefronts), in a fixed order.
+// Returns the exclusive prefix of this thread; `incl` receives the inclusive
+// prefix and `tot` the block total.  The intervals [excl, incl) of consecutive
+// threads tile [0, tot) exactly (no rounding gaps).  `sm` needs NT/64 floats.
+template <int NT, typename T>
+OSP_DEV T block_scan(T v, T* sm, T& incl, T& tot) {
+  constexpr int NW = NT / OSP_WAVE;
+  const int lane = threadIdx.x & (OSP_WAVE - 1), wave = threadIdx.x >> 6;
+  const T inc = wave_incl_scan<T>(v);
+  T prev = __shfl_up(inc, 1, OSP_WAVE);
+  if (lane == 0) prev = T(0);
+  if (lane == OSP_WAVE - 1) sm[wave] = inc;
+  __syncthreads();
+  T before = T(0), all = T(0);
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const T t = sm[w];
+    if (w < wave) before += t;
+    all += t;
+  }
+  __syncthreads();
+  tot = all;
+  incl = before + inc;
+  return lane == 0 ? before : before + prev;
+}
+
+OSP_DEV int wave_min_i(int v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = min(v, __shfl_xor(v, m, OSP_WAVE));
+  return v;
+}
+
+}  // namespace osp

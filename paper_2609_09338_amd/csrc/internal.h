@@ -1,0 +1,215 @@
+// Internal interface between the host runtime (osprey.cpp) and the kernels.
+// Not part of the public C-ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace osp {
+
+// Rows processed by one forward pass of the drafter body.
+struct RowMeta {
+  const int32_t* seq;    // [rows] batch index of each row (nullptr: row r is sequence r)
+  const int32_t* pos;    // [rows] absolute position of each row
+  const int32_t* tok;    // [rows] target token id of each row
+  const int32_t* count;  // device-side row count (nullptr: max_rows)
+  int max_rows;          // host-side upper bound on the row count
+};
+
+// Input of a GEMV-family launch: how row r, column c of the virtual input X is formed.
+enum SrcKind {
+  SRC_PLAIN = 0,  // X[r][c] = xin[r*ldx + c] (fp32)
+  SRC_NORM = 1,   // X[r][c] = rmsnorm(xin[row(r)])[c] * gamma[c] (row(r) = gather[r] or r)
+  SRC_QKV = 2,    // c < d: s[srow(r)][c]; else rmsnorm(x or embed[tok])[c-d] * gamma
+  SRC_TAPS = 3,   // X[r][c] = taps[tap_row[r]*ldt + c] (weight dtype)
+};
+enum EpiKind {
+  EPI_STORE = 0,   // y[r][n] = acc
+  EPI_RESID = 1,   // y[r][n] += acc
+  EPI_SWIGLU = 2,  // y[r][n] = silu(acc_gate) * acc_up (two weight matrices)
+  EPI_LOGITS = 3,  // logits with -inf for unmapped rows + per-block softmax statistics
+};
+
+struct GemvArgs {
+  int max_rows;
+  const int32_t* count;     // device row count (nullable)
+  // input
+  const float* xin;         // fp32 rows (PLAIN, NORM, QKV token part)
+  int ldx;
+  const int32_t* gather;    // NORM/QKV: input row index per output row (nullable)
+  const float* s;           // QKV: conditioning rows
+  int lds;
+  const int32_t* s_gather;  // QKV: conditioning row per output row (nullable)
+  const void* embed;        // QKV layer 0: embedding table (weight dtype); x = embed[tok[r]]
+  const int32_t* tok;
+  int vocab_embed;
+  float* x_out;             // QKV layer 0: where to materialise x = embed[tok] (by block 0)
+  const void* gamma;        // norm gain (weight dtype)
+  float eps;
+  int d_norm;               // width of the normalised segment
+  const void* taps;         // TAPS: [rows][ldt] weight dtype
+  const int32_t* tap_row;
+  long ldt;
+  int Kd;                   // input width
+  // weights [N][Kd] row-major
+  const void* w0;
+  const void* w1;           // SWIGLU: up matrix
+  int N;
+  // output
+  float* y;
+  int ldy;
+  // logits epilogue
+  const int32_t* d2t;       // [N]
+  const float* temp;        // [B] temperature per sequence
+  const int32_t* row_seq;   // batch index of output row r (nullable: r)
+  long ld_logits;           // stride between rows of y for logits
+  float* part;              // [rows][nblk][4]: max, sumexp, argmax, unused
+  int nblk;
+  uint32_t* err;
+};
+
+void launch_gemv(int wdtype, SrcKind src, EpiKind epi, const GemvArgs& a, hipStream_t st);
+int gemv_rows_per_block(int wdtype, EpiKind epi, int rows);
+
+// Attention.
+struct AttnArgs {
+  RowMeta rows;
+  const int32_t* cu;        // [B+1] rows of sequence b are [cu[b], cu[b+1]) (nullable: [b, b+1))
+  const int32_t* bslot;     // [B] slot of sequence b
+  int B;
+  const float* qkv;         // [rows][qkv_w] raw projections
+  int qkv_w;
+  float* q;                 // [rows][nq*hd] normalised + rotated queries (written by rope)
+  const void* q_norm;
+  const void* k_norm;
+  int qk_norm;
+  float eps;
+  const float* rope_cos;    // [max_seq][hd/2]
+  const float* rope_sin;
+  int max_seq;
+  void* kv;                 // pool base
+  int layer, n_layers;
+  const int32_t* block_table;  // [S][max_blocks]
+  const int32_t* slot_nblocks; // [S]
+  int max_blocks;
+  int kv_block;
+  int nq, nkv, hd;
+  float scale;
+  int n_split;
+  float* part;              // [rows][nq][n_split][hd + 2]
+  float* o;                 // [rows][nq*hd]
+  uint32_t* err;
+};
+void launch_rope_kvwrite(int kvdtype, const AttnArgs& a, hipStream_t st);
+void launch_attention(int kvdtype, const AttnArgs& a, hipStream_t st);
+void launch_attn_combine(const AttnArgs& a, hipStream_t st);
+
+// Sampling from the LM-head block statistics.
+struct SampleArgs {
+  int B;
+  int k;                    // draft step index
+  int K;
+  const float* logits;      // row b at logits + b*ld_logits
+  long ld_logits;
+  int V;                    // drafter vocab
+  const float* part;        // [B][nblk][4]
+  int nblk;
+  int blk_rows;             // logits per block
+  const float* temp;        // [B]
+  const float* u;           // [B][K]
+  const int32_t* d2t;
+  int32_t* drafts;          // [B][Kmax] workspace
+  int ld_drafts;
+  int32_t* drafts_out;      // optional caller copy [B][K]
+  int32_t* ar_tok;          // [B] next AR token
+  int32_t* ar_pos;          // [B] next AR position
+  const int32_t* committed; // [B]
+  const float* x;           // rows holding g
+  const int32_t* gather;    // row of g for sequence b (nullable: b)
+  int d;
+  float* gfb;               // [B][d] fed-back hidden state
+};
+void launch_sample(const SampleArgs& a, hipStream_t st);
+
+// Step setup.
+constexpr int kMaxBatch = 256;
+struct SetupArgs {
+  int B;
+  int explicit_rows;        // 1: n_new given here, tokens from new_tokens; 0: pending
+  int32_t slots[kMaxBatch];
+  int32_t n_new[kMaxBatch];
+  const int32_t* new_tokens;
+  int taps_stride;          // rows between sequences in taps (0: packed)
+  int K;
+  int max_new;              // per-sequence bound on new rows
+  int V_T;
+  int32_t* slot_len;
+  int32_t* pend_n;
+  const int32_t* pend_tok;
+  int pend_ld;
+  const int32_t* slot_nblocks;
+  int kv_block;
+  // outputs
+  int32_t* ing_seq;
+  int32_t* ing_pos;
+  int32_t* ing_tok;
+  int32_t* ing_tap;
+  int32_t* n_rows;
+  int32_t* cu;
+  int32_t* last_row;
+  int32_t* committed;
+  int32_t* bslot;
+  int32_t* ar_pos;
+  uint32_t* err;
+};
+void launch_setup(const SetupArgs& a, hipStream_t st);
+
+// Verification.
+struct VerifyArgs {
+  int B;
+  int K;
+  const float* target;      // [B][K+1][V_T]
+  const float* draft;       // row (b, k) at draft + (b*ld_draft_b + k)*V_d
+  long ld_draft_b;          // rows per sequence in draft
+  const int32_t* drafts;    // row b at drafts + b*ld_drafts
+  int ld_drafts;
+  const float* temp;
+  const float* u_acc;       // [B][K]
+  const float* u_bonus;     // [B]
+  const int32_t* d2t;
+  const int32_t* t2d;
+  int V_T, V_d;
+  int chunk;                // elements per partial block
+  int nchunk_t, nchunk_d;
+  float* part;              // [B][(K+1)*nchunk_t + K*nchunk_d][4]
+  double* res_part;         // [B][nchunk_t][2]: residual and p sums per chunk
+  int32_t* vstate;          // [B][4]: a, argmax of p_a (T = 0), flags
+  double* vstat;            // [B][4]: M_a, S_a (target), m_a, s_a (draft)
+  uint32_t* counters;       // [2*B] last-arriver counters
+  int32_t* accept_len;
+  uint8_t* accept_mask;
+  int32_t* out_tokens;
+  // state update (stateful verify); nullable
+  const int32_t* bslot;
+  int32_t* pend_n;
+  int32_t* pend_tok;
+  int pend_ld;
+  uint32_t* err;
+};
+void launch_verify(const VerifyArgs& a, hipStream_t st);
+
+// KV helpers.
+void launch_kv_append(int kvdtype, void* kv, const void* k, const void* v, int n_layers, int n,
+                      int nkv, int hd, int kv_block, const int32_t* block_table, int slot,
+                      int max_blocks, const int32_t* slot_len, int32_t* slot_len_out,
+                      hipStream_t st);
+void launch_set_len(int32_t* slot_len, int32_t* pend_n, int slot, int len, hipStream_t st);
+void launch_fill_i32(int32_t* p, int32_t v, long n, hipStream_t st);
+
+// KV pool layout: [block][layer][2 (k, v)][nkv][kv_block][hd]
+__host__ __device__ inline long kv_block_elems(int n_layers, int nkv, int kv_block, int hd) {
+  return (long)n_layers * 2 * nkv * kv_block * hd;
+}
+
+}  // namespace osp

@@ -1,0 +1,847 @@
+// Host runtime of the draft-and-verify step: argument and state validation,
+// workspace planning, slot state machine and kernel sequencing on one stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/osprey.h"
+#include "internal.h"
+
+#define OSPREY_API extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+using namespace osp;
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return OSPREY_OK;
+}
+
+#define HIP_TRY(expr)                                                              \
+  do {                                                                             \
+    hipError_t e_ = (expr);                                                        \
+    if (e_ != hipSuccess) return fail(OSPREY_E_DEVICE, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr int kMaxSplit = 64;
+constexpr int kVerifyChunk = 4096;
+constexpr int kMinLmBlock = 16;  // smallest LM-head block (rows per GEMV block)
+
+enum SlotState { S_EMPTY = 0, S_READY = 1, S_DRAFTED = 2, S_VERIFIED = 3 };
+
+struct SlotHost {
+  int state = S_EMPTY;
+  long len_max = 0;   // upper bound of the device-side cached length (exact unless pending)
+  int nblocks = 0;
+  int drafted_k = 0;  // K of the last draft (bounds the next pending ingest)
+};
+
+// Device workspace carve-up.
+struct Ws {
+  int32_t* t2d;
+  float* rope_cos;
+  float* rope_sin;
+  int32_t* slot_len;
+  int32_t* pend_n;
+  int32_t* pend_tok;
+  int32_t* block_table;
+  int32_t* slot_nblocks;
+  uint32_t* err;
+  int32_t *ing_seq, *ing_pos, *ing_tok, *ing_tap, *n_rows, *cu, *last_row, *committed, *bslot;
+  int32_t *ar_pos, *ar_tok;
+  float *x, *s, *gfb, *qkv, *q, *o, *h;
+  float* attn_part;
+  float* logits;
+  float* lm_part;
+  int32_t* drafts;
+  float* u_zero;
+  float* v_part;
+  double* v_res;
+  int32_t* vstate;
+  double* vstat;
+  uint32_t* counters;
+};
+
+struct Dims {
+  int B, Km, Rmax, max_blocks, qkv_rows, nchunk_t, nchunk_d, lm_nblk_max;
+};
+
+Dims dims_of(const osprey_config& c) {
+  Dims d;
+  d.B = c.max_batch;
+  d.Km = std::max(c.max_k, 1);
+  d.Rmax = std::max(c.max_new_rows, c.max_batch * (c.max_k + 1));
+  d.max_blocks = (c.max_seq_len + c.kv_block - 1) / c.kv_block;
+  d.qkv_rows = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  d.nchunk_t = (c.vocab_target + kVerifyChunk - 1) / kVerifyChunk;
+  d.nchunk_d = (c.vocab_draft + kVerifyChunk - 1) / kVerifyChunk;
+  d.lm_nblk_max = (c.vocab_draft + kMinLmBlock - 1) / kMinLmBlock;
+  return d;
+}
+
+// Lays out the workspace; with base == nullptr only returns the size.
+size_t plan(const osprey_config& c, char* base, Ws* w) {
+  const Dims D = dims_of(c);
+  size_t off = 0;
+  auto take = [&](size_t bytes) -> char* {
+    off = (off + 255) & ~size_t(255);
+    char* p = base ? base + off : nullptr;
+    off += bytes;
+    return p;
+  };
+  Ws t{};
+  Ws& W = w ? *w : t;
+  const long d = c.d_model, hd = c.head_dim, nq = c.n_q_heads;
+  W.t2d = (int32_t*)take(4L * c.vocab_target);
+  W.rope_cos = (float*)take(4L * c.max_seq_len * (hd / 2));
+  W.rope_sin = (float*)take(4L * c.max_seq_len * (hd / 2));
+  W.slot_len = (int32_t*)take(4L * D.B);
+  W.pend_n = (int32_t*)take(4L * D.B);
+  W.pend_tok = (int32_t*)take(4L * D.B * (c.max_k + 1));
+  W.block_table = (int32_t*)take(4L * D.B * D.max_blocks);
+  W.slot_nblocks = (int32_t*)take(4L * D.B);
+  W.err = (uint32_t*)take(16);
+  W.ing_seq = (int32_t*)take(4L * D.Rmax);
+  W.ing_pos = (int32_t*)take(4L * D.Rmax);
+  W.ing_tok = (int32_t*)take(4L * D.Rmax);
+  W.ing_tap = (int32_t*)take(4L * D.Rmax);
+  W.n_rows = (int32_t*)take(4);
+  W.cu = (int32_t*)take(4L * (D.B + 1));
+  W.last_row = (int32_t*)take(4L * D.B);
+  W.committed = (int32_t*)take(4L * D.B);
+  W.bslot = (int32_t*)take(4L * D.B);
+  W.ar_pos = (int32_t*)take(4L * D.B);
+  W.ar_tok = (int32_t*)take(4L * D.B);
+  W.x = (float*)take(4L * D.Rmax * d);
+  W.s = (float*)take(4L * D.Rmax * d);
+  W.gfb = (float*)take(4L * D.B * d);
+  W.qkv = (float*)take(4L * D.Rmax * D.qkv_rows);
+  W.q = (float*)take(4L * D.Rmax * nq * hd);
+  W.o = (float*)take(4L * D.Rmax * nq * hd);
+  W.h = (float*)take(4L * D.Rmax * c.d_ffn);
+  W.attn_part = (float*)take(4L * D.Rmax * nq * kMaxSplit * (hd + 2));
+  W.logits = (float*)take(4L * D.B * D.Km * c.vocab_draft);
+  W.lm_part = (float*)take(16L * D.B * D.lm_nblk_max);
+  W.drafts = (int32_t*)take(4L * D.B * D.Km);
+  W.u_zero = (float*)take(4L * D.B * D.Km);
+  W.v_part = (float*)take(16L * D.B * ((D.Km + 1) * D.nchunk_t + D.Km * D.nchunk_d));
+  W.v_res = (double*)take(16L * D.B * D.nchunk_t);
+  W.vstate = (int32_t*)take(16L * D.B);
+  W.vstat = (double*)take(32L * D.B);
+  W.counters = (uint32_t*)take(8L * D.B);
+  return (off + 255) & ~size_t(255);
+}
+
+int validate(const osprey_config* c) {
+  if (!c) return fail(OSPREY_E_INVALID, "config is NULL");
+  if (c->n_layers < 1 || c->n_layers > 64) return fail(OSPREY_E_INVALID, "n_layers %d not in [1, 64]", c->n_layers);
+  if (c->d_model < 64 || c->d_model % 64) return fail(OSPREY_E_SHAPE, "d_model %d must be a positive multiple of 64", c->d_model);
+  if (c->d_ffn < 64 || c->d_ffn % 64) return fail(OSPREY_E_SHAPE, "d_ffn %d must be a positive multiple of 64", c->d_ffn);
+  if (c->n_q_heads < 1 || c->n_kv_heads < 1 || c->n_q_heads % c->n_kv_heads)
+    return fail(OSPREY_E_SHAPE, "n_kv_heads %d must divide n_q_heads %d", c->n_kv_heads, c->n_q_heads);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(OSPREY_E_UNSUPPORTED, "head_dim %d (supported: 64, 128)", c->head_dim);
+  if (c->vocab_draft < 1 || c->vocab_target < 1) return fail(OSPREY_E_SHAPE, "vocabularies must be non-empty");
+  if (c->target_hidden < 8 || c->target_hidden % 8) return fail(OSPREY_E_SHAPE, "target_hidden %d must be a positive multiple of 8", c->target_hidden);
+  if (c->n_taps < 1 || c->n_taps > 16) return fail(OSPREY_E_SHAPE, "n_taps %d not in [1, 16]", c->n_taps);
+  if (c->dtype != OSPREY_F32 && c->dtype != OSPREY_BF16) return fail(OSPREY_E_INVALID, "dtype %d", c->dtype);
+  if (c->qk_norm != 0 && c->qk_norm != 1) return fail(OSPREY_E_INVALID, "qk_norm must be 0 or 1");
+  if (!(c->rms_eps > 0.f) || !(c->rope_theta > 1.f)) return fail(OSPREY_E_INVALID, "rms_eps must be > 0 and rope_theta > 1");
+  if (c->max_batch < 1 || c->max_batch > kMaxBatch) return fail(OSPREY_E_INVALID, "max_batch %d not in [1, %d]", c->max_batch, kMaxBatch);
+  if (c->max_k < 0 || c->max_k > 64) return fail(OSPREY_E_INVALID, "max_k %d not in [0, 64]", c->max_k);
+  if (c->max_seq_len < 1) return fail(OSPREY_E_INVALID, "max_seq_len %d", c->max_seq_len);
+  if (c->kv_block != 16) return fail(OSPREY_E_UNSUPPORTED, "kv_block %d (supported: 16)", c->kv_block);
+  if (c->kv_num_blocks < 1) return fail(OSPREY_E_INVALID, "kv_num_blocks %d", c->kv_num_blocks);
+  if (c->max_new_rows < 1) return fail(OSPREY_E_INVALID, "max_new_rows %d", c->max_new_rows);
+  const long tap_w = (long)c->n_taps * c->target_hidden;
+  if (tap_w > (1 << 24)) return fail(OSPREY_E_SHAPE, "tap width too large");
+  return ok();
+}
+
+struct TimerRec {
+  int family;
+  hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct osprey_handle {
+  osprey_config cfg;
+  Dims D;
+  osprey_weights w;
+  std::vector<osprey_layer_weights> layers;
+  void* kv;
+  Ws W;
+  hipStream_t stream;
+  std::vector<SlotHost> slots;
+  // the last draft_step, for the stateful verify
+  int last_B = 0, last_K = 0;
+  std::vector<int> last_slots;
+  float* last_logits = nullptr;
+  long last_ld_b = 0;
+  // timing
+  bool timing = false;
+  std::vector<TimerRec> timers;
+  std::vector<hipEvent_t> free_events;
+
+  hipEvent_t ev() {
+    if (!free_events.empty()) {
+      hipEvent_t e = free_events.back();
+      free_events.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+  int t_begin(int family) {
+    if (!timing) return -1;
+    TimerRec r{family, ev(), ev()};
+    if (!r.a || !r.b) return -1;
+    hipEventRecord(r.a, stream);
+    timers.push_back(r);
+    return (int)timers.size() - 1;
+  }
+  void t_end(int i) {
+    if (i >= 0) hipEventRecord(timers[i].b, stream);
+  }
+};
+
+namespace {
+
+int check_handle(osprey_handle* h) {
+  if (!h) return fail(OSPREY_E_INVALID, "handle is NULL");
+  return OSPREY_OK;
+}
+
+int check_slot(osprey_handle* h, int slot) {
+  if (slot < 0 || slot >= h->cfg.max_batch) return fail(OSPREY_E_INVALID, "slot %d not in [0, %d)", slot, h->cfg.max_batch);
+  return OSPREY_OK;
+}
+
+int hip_last() {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(OSPREY_E_DEVICE, "kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+// One forward pass of the body over `rows`; `s` holds the conditioning rows.
+void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, const float* s,
+              bool from_embed, int n_split) {
+  const osprey_config& c = h->cfg;
+  const Ws& W = h->W;
+  const int d = c.d_model, hd = c.head_dim, nq = c.n_q_heads, nkv = c.n_kv_heads;
+  const int qkv_w = h->D.qkv_rows;
+  for (int l = 0; l < c.n_layers; ++l) {
+    const osprey_layer_weights& L = h->layers[l];
+    // expanded QKV over [s ; RMSNorm(x)] (Eq. 2-3)
+    GemvArgs g{};
+    g.max_rows = rows.max_rows;
+    g.count = rows.count;
+    g.xin = W.x;
+    g.ldx = d;
+    g.s = s;
+    g.lds = d;
+    if (l == 0 && from_embed) {
+      g.embed = h->w.embed;
+      g.tok = rows.tok;
+      g.vocab_embed = c.vocab_target;
+      g.x_out = W.x;
+    }
+    g.gamma = L.in_norm;
+    g.eps = c.rms_eps;
+    g.d_norm = d;
+    g.Kd = 2 * d;
+    g.w0 = L.w_qkv;
+    g.N = qkv_w;
+    g.y = W.qkv;
+    g.ldy = qkv_w;
+    int t = h->t_begin(4);
+    launch_gemv(c.dtype, SRC_QKV, EPI_STORE, g, h->stream);
+    h->t_end(t);
+    // QK-norm + RoPE + KV append, attention, split combine
+    AttnArgs a{};
+    a.rows = rows;
+    a.cu = cu;
+    a.bslot = W.bslot;
+    a.B = B;
+    a.qkv = W.qkv;
+    a.qkv_w = qkv_w;
+    a.q = W.q;
+    a.q_norm = L.q_norm;
+    a.k_norm = L.k_norm;
+    a.qk_norm = c.qk_norm;
+    a.eps = c.rms_eps;
+    a.rope_cos = W.rope_cos;
+    a.rope_sin = W.rope_sin;
+    a.max_seq = c.max_seq_len;
+    a.kv = h->kv;
+    a.layer = l;
+    a.n_layers = c.n_layers;
+    a.block_table = W.block_table;
+    a.slot_nblocks = W.slot_nblocks;
+    a.max_blocks = h->D.max_blocks;
+    a.kv_block = c.kv_block;
+    a.nq = nq;
+    a.nkv = nkv;
+    a.hd = hd;
+    a.scale = 1.0f / std::sqrt((float)hd);
+    a.n_split = n_split;
+    a.part = W.attn_part;
+    a.o = W.o;
+    a.err = W.err;
+    launch_rope_kvwrite(c.dtype, a, h->stream);
+    t = h->t_begin(1);
+    launch_attention(c.dtype, a, h->stream);
+    h->t_end(t);
+    launch_attn_combine(a, h->stream);
+    // O projection + residual
+    GemvArgs go{};
+    go.max_rows = rows.max_rows;
+    go.count = rows.count;
+    go.xin = W.o;
+    go.ldx = nq * hd;
+    go.Kd = nq * hd;
+    go.w0 = L.w_o;
+    go.N = d;
+    go.y = W.x;
+    go.ldy = d;
+    launch_gemv(c.dtype, SRC_PLAIN, EPI_RESID, go, h->stream);
+    // post-attention RMSNorm + gate/up + SwiGLU
+    GemvArgs gu{};
+    gu.max_rows = rows.max_rows;
+    gu.count = rows.count;
+    gu.xin = W.x;
+    gu.ldx = d;
+    gu.gamma = L.post_norm;
+    gu.eps = c.rms_eps;
+    gu.d_norm = d;
+    gu.Kd = d;
+    gu.w0 = L.w_gate;
+    gu.w1 = L.w_up;
+    gu.N = c.d_ffn;
+    gu.y = W.h;
+    gu.ldy = c.d_ffn;
+    launch_gemv(c.dtype, SRC_NORM, EPI_SWIGLU, gu, h->stream);
+    // down projection + residual
+    GemvArgs gd{};
+    gd.max_rows = rows.max_rows;
+    gd.count = rows.count;
+    gd.xin = W.h;
+    gd.ldx = c.d_ffn;
+    gd.Kd = c.d_ffn;
+    gd.w0 = L.w_down;
+    gd.N = d;
+    gd.y = W.x;
+    gd.ldy = d;
+    launch_gemv(c.dtype, SRC_PLAIN, EPI_RESID, gd, h->stream);
+  }
+}
+
+// Final norm + LM head + block statistics, then the draft pick of step k.
+void run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, const float* temp,
+              const float* u, float* logits, long ld_b, int32_t* drafts_out) {
+  const osprey_config& c = h->cfg;
+  const Ws& W = h->W;
+  const int tn = gemv_rows_per_block(c.dtype, EPI_LOGITS, B);
+  const int nblk = (c.vocab_draft + tn - 1) / tn;
+  GemvArgs g{};
+  g.max_rows = B;
+  g.xin = W.x;
+  g.ldx = c.d_model;
+  g.gather = gather;
+  g.gamma = h->w.final_norm;
+  g.eps = c.rms_eps;
+  g.d_norm = c.d_model;
+  g.Kd = c.d_model;
+  g.w0 = h->w.lm_head;
+  g.N = c.vocab_draft;
+  g.y = logits + (long)k * c.vocab_draft;
+  g.ld_logits = ld_b * c.vocab_draft;
+  g.d2t = h->w.d2t;
+  g.temp = temp;
+  g.part = W.lm_part;
+  g.nblk = nblk;
+  int t = h->t_begin(0);
+  launch_gemv(c.dtype, SRC_NORM, EPI_LOGITS, g, h->stream);
+  h->t_end(t);
+  SampleArgs s{};
+  s.B = B;
+  s.k = k;
+  s.K = K;
+  s.logits = logits + (long)k * c.vocab_draft;
+  s.ld_logits = ld_b * c.vocab_draft;
+  s.V = c.vocab_draft;
+  s.part = W.lm_part;
+  s.nblk = nblk;
+  s.blk_rows = tn;
+  s.temp = temp;
+  s.u = u;
+  s.d2t = h->w.d2t;
+  s.drafts = W.drafts;
+  s.ld_drafts = h->D.Km;
+  s.drafts_out = drafts_out;
+  s.ar_tok = W.ar_tok;
+  s.ar_pos = W.ar_pos;
+  s.committed = W.committed;
+  s.x = W.x;
+  s.gather = gather;
+  s.d = c.d_model;
+  s.gfb = W.gfb;
+  launch_sample(s, h->stream);
+}
+
+int pick_split(const osprey_handle* h, int B, long ctx) {
+  const int by_len = (int)std::max<long>(1, (ctx + 63) / 64);
+  const int by_grid = std::max(1, 1024 / std::max(1, B * h->cfg.n_kv_heads));
+  return std::max(1, std::min(kMaxSplit, std::min(by_len, by_grid)));
+}
+
+void fill_verify_common(osprey_handle* h, VerifyArgs& v, int B, int K) {
+  const osprey_config& c = h->cfg;
+  v.B = B;
+  v.K = K;
+  v.d2t = h->w.d2t;
+  v.t2d = h->W.t2d;
+  v.V_T = c.vocab_target;
+  v.V_d = c.vocab_draft;
+  v.chunk = kVerifyChunk;
+  v.nchunk_t = h->D.nchunk_t;
+  v.nchunk_d = h->D.nchunk_d;
+  v.part = h->W.v_part;
+  v.res_part = h->W.v_res;
+  v.vstate = h->W.vstate;
+  v.vstat = h->W.vstat;
+  v.counters = h->W.counters;
+  v.err = h->W.err;
+}
+
+}  // namespace
+
+// =====================================================================================
+OSPREY_API int osprey_config_validate(const osprey_config* cfg) { return validate(cfg); }
+
+OSPREY_API size_t osprey_kv_bytes(const osprey_config* c) {
+  if (validate(c) != OSPREY_OK) return 0;
+  const size_t el = c->dtype == OSPREY_BF16 ? 2 : 4;
+  return (size_t)c->kv_num_blocks * kv_block_elems(c->n_layers, c->n_kv_heads, c->kv_block, c->head_dim) * el;
+}
+
+OSPREY_API size_t osprey_workspace_bytes(const osprey_config* c) {
+  if (validate(c) != OSPREY_OK) return 0;
+  return plan(*c, nullptr, nullptr);
+}
+
+OSPREY_API int osprey_draft_init(const osprey_config* cfg, const osprey_weights* w, void* kv_pool,
+                                 size_t kv_bytes, void* workspace, size_t ws_bytes,
+                                 void* hip_stream, osprey_handle** out) {
+  int rc = validate(cfg);
+  if (rc != OSPREY_OK) return rc;
+  if (!w || !out) return fail(OSPREY_E_INVALID, "weights and out must be non-NULL");
+  if (!w->embed || !w->w_c || !w->final_norm || !w->lm_head || !w->d2t || !w->layers)
+    return fail(OSPREY_E_INVALID, "a top-level weight pointer is NULL");
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    const osprey_layer_weights& L = w->layers[l];
+    if (!L.in_norm || !L.w_qkv || !L.w_o || !L.post_norm || !L.w_gate || !L.w_up || !L.w_down ||
+        (cfg->qk_norm && (!L.q_norm || !L.k_norm)))
+      return fail(OSPREY_E_INVALID, "a weight pointer of layer %d is NULL", l);
+  }
+  if (!kv_pool || !workspace) return fail(OSPREY_E_INVALID, "kv_pool and workspace must be non-NULL");
+  if (((uintptr_t)kv_pool & 255) || ((uintptr_t)workspace & 255))
+    return fail(OSPREY_E_INVALID, "kv_pool and workspace must be 256-byte aligned");
+  if (kv_bytes < osprey_kv_bytes(cfg)) return fail(OSPREY_E_CAPACITY, "kv_bytes %zu < %zu", kv_bytes, osprey_kv_bytes(cfg));
+  const size_t need = plan(*cfg, nullptr, nullptr);
+  if (ws_bytes < need) return fail(OSPREY_E_CAPACITY, "ws_bytes %zu < %zu", ws_bytes, need);
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) return fail(OSPREY_E_DEVICE, "no HIP device");
+
+  osprey_handle* h = new osprey_handle();
+  h->cfg = *cfg;
+  h->D = dims_of(*cfg);
+  h->w = *w;
+  h->layers.assign(w->layers, w->layers + cfg->n_layers);
+  h->w.layers = h->layers.data();
+  h->kv = kv_pool;
+  h->stream = (hipStream_t)hip_stream;
+  h->slots.assign(cfg->max_batch, SlotHost{});
+  plan(*cfg, (char*)workspace, &h->W);
+
+  auto bail = [&](int code) { delete h; return code; };
+  // vocabulary map: validate and invert on the host
+  const int Vd = cfg->vocab_draft, Vt = cfg->vocab_target;
+  std::vector<int32_t> d2t(Vd), t2d(Vt, -1);
+  if (hipMemcpy(d2t.data(), w->d2t, 4L * Vd, hipMemcpyDeviceToHost) != hipSuccess)
+    return bail(fail(OSPREY_E_DEVICE, "reading d2t failed"));
+  int mapped = 0;
+  for (int i = 0; i < Vd; ++i) {
+    const int t = d2t[i];
+    if (t == -1) continue;
+    if (t < 0 || t >= Vt) return bail(fail(OSPREY_E_INVALID, "d2t[%d] = %d not in [-1, %d)", i, t, Vt));
+    if (t2d[t] != -1) return bail(fail(OSPREY_E_INVALID, "d2t maps rows %d and %d to target id %d", t2d[t], i, t));
+    t2d[t] = i;
+    ++mapped;
+  }
+  if (!mapped) return bail(fail(OSPREY_E_INVALID, "d2t maps no row"));
+  // RoPE table in float64, stored as float32
+  const int half = cfg->head_dim / 2;
+  std::vector<float> cs((size_t)cfg->max_seq_len * half), sn(cs.size());
+  for (int p = 0; p < cfg->max_seq_len; ++p)
+    for (int i = 0; i < half; ++i) {
+      const double inv = std::pow((double)cfg->rope_theta, -(2.0 * i) / cfg->head_dim);
+      const double ang = (double)p * inv;
+      cs[(size_t)p * half + i] = (float)std::cos(ang);
+      sn[(size_t)p * half + i] = (float)std::sin(ang);
+    }
+  const Ws& W = h->W;
+  if (hipMemcpy(W.t2d, t2d.data(), 4L * Vt, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(W.rope_cos, cs.data(), 4 * cs.size(), hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(W.rope_sin, sn.data(), 4 * sn.size(), hipMemcpyHostToDevice) != hipSuccess)
+    return bail(fail(OSPREY_E_DEVICE, "uploading tables failed"));
+  const long B = h->D.B;
+  if (hipMemset(W.slot_len, 0, 4 * B) != hipSuccess || hipMemset(W.pend_n, 0, 4 * B) != hipSuccess ||
+      hipMemset(W.slot_nblocks, 0, 4 * B) != hipSuccess ||
+      hipMemset(W.block_table, 0, 4L * B * h->D.max_blocks) != hipSuccess ||
+      hipMemset(W.pend_tok, 0, 4L * B * (cfg->max_k + 1)) != hipSuccess ||
+      hipMemset(W.err, 0, 16) != hipSuccess ||
+      hipMemset(W.u_zero, 0, 4L * B * h->D.Km) != hipSuccess ||
+      hipMemset(W.counters, 0, 8 * B) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
+    return bail(fail(OSPREY_E_DEVICE, "clearing the workspace failed"));
+  *out = h;
+  return ok();
+}
+
+OSPREY_API int osprey_seq_reset(osprey_handle* h, int32_t slot, const int32_t* block_ids, int32_t n_blocks) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if ((rc = check_slot(h, slot))) return rc;
+  if (n_blocks < 0 || n_blocks > h->D.max_blocks)
+    return fail(OSPREY_E_CAPACITY, "n_blocks %d not in [0, %d]", n_blocks, h->D.max_blocks);
+  if (n_blocks > 0 && !block_ids) return fail(OSPREY_E_INVALID, "block_ids is NULL");
+  for (int i = 0; i < n_blocks; ++i)
+    if (block_ids[i] < 0 || block_ids[i] >= h->cfg.kv_num_blocks)
+      return fail(OSPREY_E_INVALID, "block_ids[%d] = %d not in [0, %d)", i, block_ids[i], h->cfg.kv_num_blocks);
+  const Ws& W = h->W;
+  HIP_TRY(hipStreamSynchronize(h->stream));
+  if (n_blocks) HIP_TRY(hipMemcpy(W.block_table + (long)slot * h->D.max_blocks, block_ids, 4L * n_blocks, hipMemcpyHostToDevice));
+  HIP_TRY(hipMemcpy(W.slot_nblocks + slot, &n_blocks, 4, hipMemcpyHostToDevice));
+  launch_set_len(W.slot_len, W.pend_n, slot, 0, h->stream);
+  HIP_TRY(hipStreamSynchronize(h->stream));
+  SlotHost& s = h->slots[slot];
+  s.state = S_READY;
+  s.len_max = 0;
+  s.nblocks = n_blocks;
+  s.drafted_k = 0;
+  return hip_last();
+}
+
+OSPREY_API int osprey_kv_append(osprey_handle* h, int32_t slot, int32_t n, const void* k, const void* v) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if ((rc = check_slot(h, slot))) return rc;
+  SlotHost& s = h->slots[slot];
+  if (s.state != S_READY) return fail(OSPREY_E_STATE, "slot %d is not READY", slot);
+  if (n < 0) return fail(OSPREY_E_INVALID, "n %d < 0", n);
+  if (n > 0 && (!k || !v)) return fail(OSPREY_E_INVALID, "k and v must be non-NULL");
+  if (s.len_max + n > (long)s.nblocks * h->cfg.kv_block)
+    return fail(OSPREY_E_CAPACITY, "slot %d: %ld + %d positions exceed its %d pages", slot, s.len_max, n, s.nblocks);
+  if (n == 0) return ok();
+  launch_kv_append(h->cfg.dtype, h->kv, k, v, h->cfg.n_layers, n, h->cfg.n_kv_heads, h->cfg.head_dim,
+                   h->cfg.kv_block, h->W.block_table, slot, h->D.max_blocks, h->W.slot_len,
+                   h->W.slot_len, h->stream);
+  s.len_max += n;
+  return hip_last();
+}
+
+OSPREY_API int osprey_seq_truncate(osprey_handle* h, int32_t slot, int32_t length) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if ((rc = check_slot(h, slot))) return rc;
+  SlotHost& s = h->slots[slot];
+  if (s.state != S_READY && s.state != S_VERIFIED) return fail(OSPREY_E_STATE, "slot %d is not READY or VERIFIED", slot);
+  if (length < 0 || length > s.len_max) return fail(OSPREY_E_INVALID, "length %d not in [0, %ld]", length, s.len_max);
+  launch_set_len(h->W.slot_len, h->W.pend_n, slot, length, h->stream);
+  s.len_max = length;
+  s.state = S_READY;
+  return hip_last();
+}
+
+OSPREY_API int osprey_seq_length(osprey_handle* h, int32_t slot, int32_t* length) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if ((rc = check_slot(h, slot))) return rc;
+  if (!length) return fail(OSPREY_E_INVALID, "length is NULL");
+  HIP_TRY(hipStreamSynchronize(h->stream));
+  HIP_TRY(hipMemcpy(length, h->W.slot_len + slot, 4, hipMemcpyDeviceToHost));
+  SlotHost& s = h->slots[slot];
+  if (s.state != S_DRAFTED) s.len_max = *length;
+  return ok();
+}
+
+OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (!a) return fail(OSPREY_E_INVALID, "args is NULL");
+  const osprey_config& c = h->cfg;
+  const int B = a->batch, K = a->K;
+  if (B < 1 || B > c.max_batch) return fail(OSPREY_E_INVALID, "batch %d not in [1, %d]", B, c.max_batch);
+  if (K < 0 || K > c.max_k) return fail(OSPREY_E_INVALID, "K %d not in [0, %d]", K, c.max_k);
+  if (!a->slots || !a->taps || !a->temperature) return fail(OSPREY_E_INVALID, "slots, taps and temperature must be non-NULL");
+  const bool pending = a->n_new == nullptr;
+  if (!pending && !a->new_tokens) return fail(OSPREY_E_INVALID, "new_tokens is NULL in explicit mode");
+  if (a->taps_stride < 0) return fail(OSPREY_E_INVALID, "taps_stride < 0");
+  if (pending && a->taps_stride == 0) return fail(OSPREY_E_INVALID, "pending mode needs taps_stride > 0");
+  std::vector<char> seen(c.max_batch, 0);
+  long rows = 0, ctx_max = 0;
+  int max_new = 0;
+  for (int b = 0; b < B; ++b) {
+    const int slot = a->slots[b];
+    if ((rc = check_slot(h, slot))) return rc;
+    if (seen[slot]) return fail(OSPREY_E_INVALID, "slot %d appears twice", slot);
+    seen[slot] = 1;
+    const SlotHost& s = h->slots[slot];
+    int n;
+    if (pending) {
+      if (s.state != S_VERIFIED) return fail(OSPREY_E_STATE, "slot %d has no verified tokens pending", slot);
+      n = s.drafted_k + 1;
+      if (a->taps_stride < n) return fail(OSPREY_E_INVALID, "taps_stride %d < %d pending rows of slot %d", a->taps_stride, n, slot);
+    } else {
+      if (s.state != S_READY && s.state != S_VERIFIED) return fail(OSPREY_E_STATE, "slot %d is not READY or VERIFIED", slot);
+      n = a->n_new[b];
+      if (n < 1) return fail(OSPREY_E_INVALID, "n_new[%d] = %d < 1", b, n);
+      if (a->taps_stride > 0 && n > a->taps_stride) return fail(OSPREY_E_INVALID, "n_new[%d] = %d > taps_stride", b, n);
+    }
+    const long need = s.len_max + n + std::max(K - 1, 0);
+    if (need > (long)s.nblocks * c.kv_block || need > c.max_seq_len)
+      return fail(OSPREY_E_CAPACITY, "slot %d: up to %ld positions exceed its %d pages / max_seq_len", slot, need, s.nblocks);
+    rows += n;
+    max_new = std::max(max_new, n);
+    ctx_max = std::max(ctx_max, need);
+  }
+  if (rows > h->D.Rmax) return fail(OSPREY_E_CAPACITY, "%ld new rows exceed the workspace's %d", rows, h->D.Rmax);
+  if (!pending && rows > std::max(c.max_new_rows, c.max_batch * (c.max_k + 1)))
+    return fail(OSPREY_E_CAPACITY, "%ld new rows exceed max_new_rows", rows);
+
+  const Ws& W = h->W;
+  int tt = h->t_begin(3);
+  // ---- row layout of the ingest ---------------------------------------------------------
+  SetupArgs sa{};
+  sa.B = B;
+  sa.explicit_rows = pending ? 0 : 1;
+  for (int b = 0; b < B; ++b) {
+    sa.slots[b] = a->slots[b];
+    sa.n_new[b] = pending ? 0 : a->n_new[b];
+  }
+  sa.new_tokens = a->new_tokens;
+  sa.taps_stride = a->taps_stride;
+  sa.K = K;
+  sa.max_new = pending ? c.max_k + 1 : std::max(max_new, 1);
+  sa.V_T = c.vocab_target;
+  sa.slot_len = W.slot_len;
+  sa.pend_n = W.pend_n;
+  sa.pend_tok = W.pend_tok;
+  sa.pend_ld = c.max_k + 1;
+  sa.slot_nblocks = W.slot_nblocks;
+  sa.kv_block = c.kv_block;
+  sa.ing_seq = W.ing_seq;
+  sa.ing_pos = W.ing_pos;
+  sa.ing_tok = W.ing_tok;
+  sa.ing_tap = W.ing_tap;
+  sa.n_rows = W.n_rows;
+  sa.cu = W.cu;
+  sa.last_row = W.last_row;
+  sa.committed = W.committed;
+  sa.bslot = W.bslot;
+  sa.ar_pos = W.ar_pos;
+  sa.err = W.err;
+  launch_setup(sa, h->stream);
+
+  // ---- ingest: tap projection (Eq. 1) then the body over every new row ------------------
+  RowMeta ing{W.ing_seq, W.ing_pos, W.ing_tok, W.n_rows, (int)rows};
+  GemvArgs gt{};
+  gt.max_rows = (int)rows;
+  gt.count = W.n_rows;
+  gt.taps = a->taps;
+  gt.tap_row = W.ing_tap;
+  gt.ldt = (long)c.n_taps * c.target_hidden;
+  gt.Kd = c.n_taps * c.target_hidden;
+  gt.w0 = h->w.w_c;
+  gt.N = c.d_model;
+  gt.y = W.s;
+  gt.ldy = c.d_model;
+  launch_gemv(c.dtype, SRC_TAPS, EPI_STORE, gt, h->stream);
+  run_body(h, ing, W.cu, B, W.s, true, pick_split(h, B, ctx_max));
+
+  // ---- K autoregressive draft steps ---------------------------------------------------------
+  float* logits = a->draft_logits ? a->draft_logits : W.logits;
+  const long ld_b = a->draft_logits ? K : h->D.Km;
+  const float* u = a->u_draft ? a->u_draft : W.u_zero;
+  if (K >= 1) {
+    run_head(h, B, 0, K, W.last_row, a->temperature, u, logits, ld_b, a->draft_tokens);
+    RowMeta ar{nullptr, W.ar_pos, W.ar_tok, nullptr, B};
+    const int split = pick_split(h, B, ctx_max);
+    for (int k = 1; k < K; ++k) {
+      run_body(h, ar, nullptr, B, W.gfb, true, split);
+      run_head(h, B, k, K, nullptr, a->temperature, u, logits, ld_b, a->draft_tokens);
+    }
+  }
+  h->t_end(tt);
+  if ((rc = hip_last())) return rc;
+  for (int b = 0; b < B; ++b) {
+    SlotHost& s = h->slots[a->slots[b]];
+    const int n = pending ? s.drafted_k + 1 : a->n_new[b];
+    s.len_max += n;
+    s.state = K >= 1 ? S_DRAFTED : S_READY;
+    s.drafted_k = K;
+  }
+  h->last_B = B;
+  h->last_K = K;
+  h->last_slots.assign(a->slots, a->slots + B);
+  h->last_logits = logits;
+  h->last_ld_b = ld_b;
+  return ok();
+}
+
+OSPREY_API int osprey_verify(osprey_handle* h, const osprey_verify_args* a) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (!a) return fail(OSPREY_E_INVALID, "args is NULL");
+  if (!a->slots || !a->target_logits || !a->temperature || !a->u_accept || !a->u_bonus ||
+      !a->accept_len || !a->accept_mask || !a->out_tokens)
+    return fail(OSPREY_E_INVALID, "a verify pointer is NULL");
+  if (a->batch != h->last_B || a->K != h->last_K)
+    return fail(OSPREY_E_STATE, "verify (batch %d, K %d) does not match the last draft_step (batch %d, K %d)",
+                a->batch, a->K, h->last_B, h->last_K);
+  if (a->K < 1) return fail(OSPREY_E_STATE, "the last draft_step proposed no drafts");
+  for (int b = 0; b < a->batch; ++b) {
+    if (a->slots[b] != h->last_slots[b]) return fail(OSPREY_E_STATE, "slots differ from the last draft_step");
+    if (h->slots[a->slots[b]].state != S_DRAFTED) return fail(OSPREY_E_STATE, "slot %d is not DRAFTED", a->slots[b]);
+  }
+  VerifyArgs v{};
+  fill_verify_common(h, v, a->batch, a->K);
+  v.target = a->target_logits;
+  v.draft = h->last_logits;
+  v.ld_draft_b = h->last_ld_b;
+  v.drafts = h->W.drafts;
+  v.ld_drafts = h->D.Km;
+  v.temp = a->temperature;
+  v.u_acc = a->u_accept;
+  v.u_bonus = a->u_bonus;
+  v.accept_len = a->accept_len;
+  v.accept_mask = a->accept_mask;
+  v.out_tokens = a->out_tokens;
+  v.bslot = h->W.bslot;
+  v.pend_n = h->W.pend_n;
+  v.pend_tok = h->W.pend_tok;
+  v.pend_ld = h->cfg.max_k + 1;
+  int t = h->t_begin(2);
+  launch_verify(v, h->stream);
+  h->t_end(t);
+  if ((rc = hip_last())) return rc;
+  for (int b = 0; b < a->batch; ++b) h->slots[a->slots[b]].state = S_VERIFIED;
+  h->last_B = 0;
+  return ok();
+}
+
+OSPREY_API int osprey_verify_rows(osprey_handle* h, const osprey_verify_rows_args* a) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (!a) return fail(OSPREY_E_INVALID, "args is NULL");
+  if (a->batch < 1 || a->batch > h->cfg.max_batch) return fail(OSPREY_E_INVALID, "batch %d not in [1, %d]", a->batch, h->cfg.max_batch);
+  if (a->K < 0 || a->K > h->cfg.max_k) return fail(OSPREY_E_INVALID, "K %d not in [0, %d]", a->K, h->cfg.max_k);
+  if (!a->target_logits || !a->temperature || !a->u_bonus || !a->accept_len || !a->accept_mask ||
+      !a->out_tokens || (a->K > 0 && (!a->draft_logits || !a->draft_tokens || !a->u_accept)))
+    return fail(OSPREY_E_INVALID, "a verify pointer is NULL");
+  VerifyArgs v{};
+  fill_verify_common(h, v, a->batch, a->K);
+  v.target = a->target_logits;
+  v.draft = a->draft_logits;
+  v.ld_draft_b = a->K;
+  v.drafts = a->draft_tokens;
+  v.ld_drafts = a->K;
+  v.temp = a->temperature;
+  v.u_acc = a->u_accept;
+  v.u_bonus = a->u_bonus;
+  v.accept_len = a->accept_len;
+  v.accept_mask = a->accept_mask;
+  v.out_tokens = a->out_tokens;
+  int t = h->t_begin(2);
+  launch_verify(v, h->stream);
+  h->t_end(t);
+  return hip_last();
+}
+
+OSPREY_API int osprey_device_errors(osprey_handle* h, uint32_t* flags) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (!flags) return fail(OSPREY_E_INVALID, "flags is NULL");
+  HIP_TRY(hipStreamSynchronize(h->stream));
+  HIP_TRY(hipMemcpy(flags, h->W.err, 4, hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemset(h->W.err, 0, 4));
+  return ok();
+}
+
+OSPREY_API int osprey_kernel_timing(osprey_handle* h, int32_t enable) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  HIP_TRY(hipStreamSynchronize(h->stream));
+  for (auto& r : h->timers) { h->free_events.push_back(r.a); h->free_events.push_back(r.b); }
+  h->timers.clear();
+  h->timing = enable != 0;
+  return ok();
+}
+
+OSPREY_API int osprey_kernel_time(osprey_handle* h, int32_t family, double* total_ms, int64_t* launches) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (!total_ms || !launches) return fail(OSPREY_E_INVALID, "outputs are NULL");
+  HIP_TRY(hipStreamSynchronize(h->stream));
+  double tot = 0;
+  int64_t n = 0;
+  for (auto& r : h->timers) {
+    if (r.family != family) continue;
+    float ms = 0;
+    HIP_TRY(hipEventElapsedTime(&ms, r.a, r.b));
+    tot += ms;
+    ++n;
+  }
+  *total_ms = tot;
+  *launches = n;
+  return ok();
+}
+
+OSPREY_API int osprey_set_stream(osprey_handle* h, void* hip_stream) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  h->stream = (hipStream_t)hip_stream;
+  return ok();
+}
+
+OSPREY_API int osprey_draft_destroy(osprey_handle* h) {
+  if (!h) return ok();
+  hipStreamSynchronize(h->stream);
+  for (auto& r : h->timers) { hipEventDestroy(r.a); hipEventDestroy(r.b); }
+  for (auto e : h->free_events) hipEventDestroy(e);
+  delete h;
+  return ok();
+}
+
+OSPREY_API const char* osprey_last_error(void) { return g_err.c_str(); }

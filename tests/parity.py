@@ -1,0 +1,90 @@
+"""Comparison of GPU results with the oracle's, with near-tie flags.
+
+Token choices are compared exactly.  A choice the two sides may legitimately
+make differently -- because fp32 arithmetic on the GPU and fp64 arithmetic in
+the oracle put a decision point on opposite sides of a threshold -- is
+"flagged" instead of failed; each flag rule bounds how far the GPU's value
+can be from the oracle's:
+
+* argmax at T = 0: the top-2 margin of the oracle's logits is below 2 delta,
+  delta = max |logit_gpu - logit_oracle| on that row (mapped rows).
+* inverse-CDF draw at T > 0: the draw point u*S lies within
+  8 (delta/T) sqrt(sum_{i<=j} w_i^2) + 1e-9 S of a breakpoint C_{j-1} or C_j
+  (w = oracle weights): the drafter's logit errors shift the cumulative sums
+  by about (delta/T) sqrt(sum w^2) when the errors are independent.
+* acceptance u_k < r_k: |u_k - r_k| < 1e-5 + 4 (delta/T) r_k (delta = 0 when
+  both sides read the same drafter logits).
+* residual / bonus draw: the draw point is within 8 (delta/T) sqrt(sum q^2) +
+  1e-8 of a breakpoint (absolute probability units).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from oracle import sampling
+
+
+def argmax_flag(logits: np.ndarray, delta: float) -> bool:
+    l = np.asarray(logits, dtype=np.float64)
+    l = l[np.isfinite(l)]
+    if l.size < 2:
+        return False
+    top2 = np.partition(l, -2)[-2:]
+    return float(top2[1] - top2[0]) < 2.0 * delta + 1e-12
+
+
+def cdf_margin(w: np.ndarray, u: float):
+    """(index chosen, margin to the nearest breakpoint, running sums)."""
+    w = np.asarray(w, dtype=np.float64)
+    run = np.cumsum(w)
+    tot = run[-1]
+    tgt = float(u) * tot
+    i = sampling.pick_weights(w, u)
+    lo = run[i - 1] if i > 0 else 0.0
+    return i, min(tgt - lo, run[i] - tgt), run
+
+
+def draw_flag(logits: np.ndarray, T: float, u: float, delta: float) -> bool:
+    """Flag for the drafter's inverse-CDF draw (relative to the total S)."""
+    if T == 0.0:
+        return argmax_flag(logits, delta)
+    w = sampling.softmax_weights(logits, T)
+    i, margin, run = cdf_margin(w, u)
+    S = run[-1]
+    err = 8.0 * (delta / T) * np.sqrt(np.sum(w[: i + 1] ** 2)) + 1e-9 * S
+    return margin < err
+
+
+def accept_flag(u: float, r: float, delta: float, T: float) -> bool:
+    extra = 4.0 * (delta / T) * r if T > 0 else 0.0
+    return abs(float(u) - float(r)) < 1e-5 + extra
+
+
+def residual_flag(w: np.ndarray, q: np.ndarray, u: float, delta: float, T: float) -> bool:
+    if w.sum() <= 0:
+        return True
+    i, margin, _ = cdf_margin(w, u)
+    err = 1e-8 + (8.0 * (delta / T) * np.sqrt(np.sum(np.asarray(q[: i + 1]) ** 2)) if T > 0 else 0.0)
+    return margin < err
+
+
+def verify_flags(res, target_logits, draft_logits, d2t, drafts, T, u_acc, u_bonus, delta=0.0):
+    """True if any decision of this verification is within its flag window."""
+    from oracle.verify import drafter_probs_on_target
+    K = len(drafts)
+    if T == 0.0:
+        # the oracle's decisions are exact comparisons of identical fp32 inputs
+        return False
+    for k in range(min(res.accept_len + 1, K)):
+        if accept_flag(u_acc[k], res.ratios[k], delta, T):
+            return True
+    a = res.accept_len
+    tl = np.asarray(target_logits, dtype=np.float64)
+    p = sampling.probs(tl[a], T)
+    if a < K:
+        q = drafter_probs_on_target(draft_logits[a], d2t, tl.shape[1], T)
+        w = np.maximum(p - q, 0.0)
+        if w.sum() <= 0:
+            w = p
+        return residual_flag(w, q, u_bonus, delta, T)
+    return residual_flag(p, np.zeros_like(p), u_bonus, 0.0, T)
