@@ -1,0 +1,227 @@
+"""Benchmark of the Osprey draft-and-verify step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps 32] [--warmup 4] [--workload c2]
+                    [--no-cpu-baseline] [--cpu-seconds 15]
+
+A step is one iteration of the hot path for the whole batch: osprey_draft_step
+(ingest of the tokens the previous verification committed + K autoregressive
+draft steps) followed by osprey_verify.  The target model is not part of the
+path: its logits for each iteration are synthetic (the drafter's logits plus
+seeded noise) and, like every other input, are staged in HBM before the timed
+region.  Because the whole path is deterministic, a first (untimed) pass
+records the trajectory and its target logits; the timed pass replays it from
+the same starting state.
+
+Prints one JSON line: whole-job draft+verify tokens/s (sum over sequences of
+accepted drafts + 1 per iteration, divided by the time of the draft_step and
+verify calls), µs per draft step, the LM-head kernel against the HBM roofline
+(timed with HIP events on the library's stream), and the CPU oracle on a
+bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=32)
+    ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--workload", default="c2")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-kernel-timing", action="store_true")
+    return ap.parse_args()
+
+
+def lm_head_bytes(w, rows: int) -> int:
+    """Algorithmic HBM bytes of one LM-head launch: every weight byte once, the
+    final-norm gain, the masked logits written and the vocabulary map read."""
+    el = 2 if w.dtype == "bf16" else 4
+    return w.vocab_draft * w.d_model * el + w.d_model * el + rows * w.vocab_draft * 4 \
+        + w.vocab_draft * 4
+
+
+def step_bytes(w, ctx_mean: float) -> dict:
+    """Algorithmic bytes of one autoregressive draft step (all sequences)."""
+    el = 2 if w.dtype == "bf16" else 4
+    d, hd, L = w.d_model, w.head_dim, w.n_layers
+    body = L * (w.qkv_rows * 2 * d + d * w.n_q_heads * hd + 3 * w.d_ffn * d + 2 * d + 2 * hd) * el
+    lm = w.vocab_draft * d * el
+    kv = w.batch * ctx_mean * L * 2 * w.n_kv_heads * hd * el
+    return dict(body=body, lm=lm, kv=kv, total=body + lm + kv)
+
+
+def run_gpu(args):
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2609_09338_amd import binding as BD
+    from paper_2609_09338_amd import workload as WL
+
+    w = synth.get(args.workload)
+    n_it = args.warmup + args.steps
+    dev = torch.device("cuda:0")
+    s = WL.make_drafter(w, n_it, device=dev)
+    WL.reset_sequences(s)
+    d2t = synth.make_d2t(w)
+    out = WL.alloc_outputs(s)
+
+    # ---- record: inputs and synthetic target logits of every iteration ------------------
+    gen = torch.Generator(device=dev)
+    staged = []
+    rec_accept = []
+    for it in range(n_it):
+        inp = WL.iter_inputs(s, it)
+        WL.draft(s, it, inp, out)
+        gen.manual_seed(1000003 * w.cfg_id + it)
+        noise = torch.randn((w.batch, w.K + 1, w.vocab_target), generator=gen, device=dev)
+        tl = torch.stack([synth.target_logits(w, out.logits[b], d2t, noise[b])
+                          for b in range(w.batch)]).contiguous()
+        del noise
+        WL.verify(s, inp, tl, out)
+        staged.append((inp, tl))
+        rec_accept.append(out.accept_len.clone())
+    torch.cuda.synchronize()
+    rec_accept = torch.stack(rec_accept).cpu().numpy()
+
+    def rewind():
+        for b in range(w.batch):
+            s.drafter.seq_truncate(b, int(s.ctx[b]) - 1)
+
+    def replay(lo, hi, accept_out=None):
+        for it in range(lo, hi):
+            inp, tl = staged[it]
+            WL.draft(s, it, inp, out)
+            WL.verify(s, inp, tl, out)
+            if accept_out is not None:
+                accept_out.append(out.accept_len.clone())
+
+    # ---- timed pass ---------------------------------------------------------------------
+    rewind()
+    replay(0, args.warmup)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    acc = []
+    t0 = time.perf_counter()
+    ev0.record(s.drafter.stream)
+    replay(args.warmup, n_it, acc)
+    ev1.record(s.drafter.stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    got = torch.stack(acc).cpu().numpy()
+    assert (got == rec_accept[args.warmup:]).all(), "replay diverged from the recorded trajectory"
+    tokens = int((got + 1).sum())
+    elapsed = max(gpu_ms / 1e3, 1e-9)
+    res = dict(tokens=tokens, seconds=elapsed, wall=wall, mean_accept=float(got.mean()))
+
+    # ---- per-call and per-kernel timing: the same steps again, with HIP events ----------
+    if not args.no_kernel_timing:
+        rewind()
+        replay(0, args.warmup)
+        s.drafter.kernel_timing(True)
+        replay(args.warmup, n_it)
+        torch.cuda.synchronize()
+        kt = {name: s.drafter.kernel_time(fam) for name, fam in
+              (("lm_head", BD.KERNEL_LM_HEAD), ("attention", BD.KERNEL_ATTENTION),
+               ("verify", BD.KERNEL_VERIFY), ("draft_step", BD.KERNEL_DRAFT_STEP),
+               ("qkv", BD.KERNEL_QKV))}
+        s.drafter.kernel_timing(False)
+        res["kernels"] = kt
+    assert s.drafter.device_errors() == 0
+    res["ctx_mean"] = float(np.mean(s.ctx))
+    return w, res
+
+
+def run_cpu_baseline(w, seconds: float):
+    """The oracle, untuned, on one sequence of the same workload for ~`seconds`."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import harness as OH
+    dr = OH.build_drafter(w)
+    t0 = time.perf_counter()
+    tokens, iters = 0, 0
+    seq_iters = OH.run_sequence_timed(w, 0, 64, seconds, drafter=dr)
+    for it in seq_iters:
+        tokens += it.result.accept_len + 1
+        iters += 1
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return dict(value=tokens / dt, unit="tokens/s", cores=int(threads), kind="oracle",
+                sample=f"{iters} iteration(s) of sequence 0 of workload {w.name} "
+                       f"(K={w.K}, {w.K} drafter forward passes + verify each), "
+                       f"{dt:.1f} s incl. setup, numpy float64")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}), flush=True)
+        sys.exit(2)
+    w, r = run_gpu(args)
+    K = args.steps
+    ms_per_step = r["seconds"] * 1e3 / K
+    value = r["tokens"] / r["seconds"]
+    sb = step_bytes(w, r["ctx_mean"])
+    line = {
+        "metric": "draft+verify tokens/s per GPU; µs per draft step at batch 1; % HBM peak",
+        "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "storage_dtype": w.dtype,
+        "data": "synthetic (seeded N(0,0.02) weights, N(0,1) taps and context KV, target "
+                "logits = drafter logits + N(0, sigma))",
+        "config": {"workload": f"{w.name}: {w.n_layers}-layer drafter d={w.d_model}, "
+                               f"{w.n_q_heads}/{w.n_kv_heads} heads x {w.head_dim}, FFN {w.d_ffn}, "
+                               f"V_d={w.vocab_draft}, V_T={w.vocab_target}, taps 3x{w.target_hidden}, "
+                               f"batch {w.batch}, context {w.ctx_lo}"
+                               + (f"-{w.ctx_hi}" if w.ctx_hi != w.ctx_lo else "")
+                               + f", K={w.K}, T={list(w.temps)}",
+                   "batch": w.batch, "K": w.K},
+        "mean_accepted_drafts": round(r["mean_accept"], 3),
+        "tokens_timed": r["tokens"],
+    }
+    kt = r.get("kernels")
+    if kt:
+        ds_ms, ds_n = kt["draft_step"]
+        vf_ms, vf_n = kt["verify"]
+        line["us_per_draft_step_call"] = round(ds_ms * 1e3 / max(ds_n, 1), 2)
+        line["us_per_draft_token"] = round(ds_ms * 1e3 / max(ds_n, 1) / w.K, 2)
+        line["us_per_verify"] = round(vf_ms * 1e3 / max(vf_n, 1), 2)
+        lm_ms, lm_n = kt["lm_head"]
+        at_ms, at_n = kt["attention"]
+        lm_us = lm_ms * 1e3 / max(lm_n, 1)
+        bytes_launch = lm_head_bytes(w, w.batch)
+        ach = bytes_launch / (lm_us * 1e-6) / 1e9
+        line["roofline"] = {"bound": "hbm", "kernel": "LM head (final RMSNorm + vocabulary GEMV "
+                            "+ masked logits + softmax block statistics)",
+                            "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                            "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                            "bytes_per_launch": bytes_launch, "us_per_launch": round(lm_us, 3),
+                            "launches": lm_n}
+        line["ar_step_algorithmic_bytes"] = int(sb["total"])
+        line["attention_us_per_launch"] = round(at_ms * 1e3 / max(at_n, 1), 3)
+        line["qkv_us_per_launch"] = round(kt["qkv"][0] * 1e3 / max(kt["qkv"][1], 1), 3)
+        ar_us = ds_ms * 1e3 / max(ds_n, 1) / w.K
+        line["draft_token_hbm_frac"] = round(sb["total"] / (ar_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = run_cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -60,8 +60,17 @@ def start_sequence(w, drafter: Drafter, b: int, n_iters: int) -> Sequence:
     return seq
 
 
+def run_sequence_timed(w, b: int, n_max: int, seconds: float,
+                       drafter: Optional[Drafter] = None) -> List[Iteration]:
+    """Iterations of sequence b until `seconds` have elapsed (at least one)."""
+    import time
+    t0 = time.perf_counter()
+    return run_sequence(w, b, n_max, drafter=drafter,
+                        stop=lambda: time.perf_counter() - t0 > seconds)
+
+
 def run_sequence(w, b: int, n_iters: int, drafter: Optional[Drafter] = None,
-                 residual_fn=None) -> List[Iteration]:
+                 residual_fn=None, stop=None) -> List[Iteration]:
     drafter = drafter or build_drafter(w)
     seq = start_sequence(w, drafter, b, n_iters)
     ctx = int(synth.context_lengths(w)[b])
@@ -79,4 +88,6 @@ def run_sequence(w, b: int, n_iters: int, drafter: Optional[Drafter] = None,
         out.append(Iteration(pre, new_tokens.copy(), committed, drafts, rows, logits, tl, res))
         drafter.rollback(seq, committed)
         new_tokens = res.tokens[: res.accept_len + 1].copy()
+        if stop is not None and stop():
+            break
     return out

@@ -1,16 +1,20 @@
 // Attention of the drafter over its paged KV cache.
 //
-// k_rope_kvwrite: per row and head, the Qwen3 per-head RMSNorm of q and k,
-//   rotate-half RoPE at the row's absolute position (cos/sin table built on the
-//   host in float64), then k and v are stored (rounded to bf16 in bf16 pools)
-//   into the row's cache slot; q is kept in fp32.
-// k_attn: one block per (sequence, kv head, context split).  Each wavefront
-//   walks 16-token cache blocks of the split (one KV page per step): 4 lanes per
-//   token, each lane holding a quarter of the head dimension, so a page of K or V
-//   is one fully coalesced 4 KB read.  Every query vector of the sequence that
-//   reads this kv head (all new rows x the GQA group) is scored against the page,
-//   with a causal mask at the row's position and an online softmax; the four
-//   wavefronts' partial results are merged in LDS and written per split.
+// k_attn: one block per (sequence, kv head, context split).
+//   0. Each wavefront prefetches its first KV page when it holds only older
+//      positions, so the page read overlaps steps 1-2.
+//   1. New rows whose position falls in this split: Qwen3 per-head RMSNorm of k,
+//      rotate-half RoPE at the row's absolute position (cos/sin table built on
+//      the host in float64), then k and v are stored into the row's cache page
+//      (rounded to bf16 in bf16 pools).  Every position belongs to exactly one
+//      split, so each new key/value is written once, by the block that reads it.
+//   2. The query vectors of the sequence that read this kv head (new rows x GQA
+//      group) are normalised and rotated into LDS, a few per pass.
+//   3. Each wavefront walks 16-token pages of the split: 16 lanes per token, each
+//      lane holding 1/16 of the head dimension, so a page of K or V is four fully
+//      coalesced wavefront reads of 4 tokens.  Scores use a causal mask at the
+//      row's position and an online softmax; the four wavefronts are merged in
+//      LDS and the split's (max, sum, unnormalised output) is written.
 // k_attn_combine: merges the splits of each (row, head) with their log-sum-exp
 //   weights (flash-decoding) and normalises.
 #include "common.h"
@@ -18,84 +22,102 @@
 
 namespace osp {
 
-template <typename TKV>
-__global__ void __launch_bounds__(64) k_rope_kvwrite(AttnArgs a) {
-  const int r = blockIdx.x;
-  const int hh = blockIdx.y;
-  const int rows = a.rows.count ? min(*a.rows.count, a.rows.max_rows) : a.rows.max_rows;
-  if (r >= rows) return;
-  const int lane = threadIdx.x;
-  const int hd = a.hd, half = hd >> 1;
-  const int pos = a.rows.pos[r];
-  const int b = a.rows.seq ? a.rows.seq[r] : r;
-  const bool is_q = hh < a.nq;
-  const int g = is_q ? 0 : hh - a.nq;
-  const float* src = a.qkv + (long)r * a.qkv_w + (is_q ? hh * hd : (a.nq + g) * hd);
-  const bool act = lane < half;
-  float x1 = act ? src[lane] : 0.f, x2 = act ? src[lane + half] : 0.f;
+// DPL consecutive cache elements kept in their storage form (bf16 pairs or fp32).
+template <typename TKV, int DPL> struct Seg;
+template <int DPL> struct Seg<bf16_t, DPL> {
+  static_assert(DPL == 4 || DPL == 8, "bf16 segments of 4 or 8 elements");
+  uint32_t raw[DPL / 2];
+  OSP_DEV void load(const bf16_t* p) {
+    if constexpr (DPL == 8) {
+      const uint4 v = *reinterpret_cast<const uint4*>(p);
+      raw[0] = v.x; raw[1] = v.y; raw[2] = v.z; raw[3] = v.w;
+    } else {
+      const uint2 v = *reinterpret_cast<const uint2*>(p);
+      raw[0] = v.x; raw[1] = v.y;
+    }
+  }
+  OSP_DEV void zero() {
+#pragma unroll
+    for (int i = 0; i < DPL / 2; ++i) raw[i] = 0u;
+  }
+  OSP_DEV float get(int e) const { return (e & 1) ? bf16_hi(raw[e >> 1]) : bf16_lo(raw[e >> 1]); }
+};
+template <int DPL> struct Seg<float, DPL> {
+  float raw[DPL];
+  OSP_DEV void load(const float* p) {
+#pragma unroll
+    for (int j = 0; j < DPL / 4; ++j) {
+      const float4 v = *reinterpret_cast<const float4*>(p + j * 4);
+      raw[4 * j] = v.x; raw[4 * j + 1] = v.y; raw[4 * j + 2] = v.z; raw[4 * j + 3] = v.w;
+    }
+  }
+  OSP_DEV void zero() {
+#pragma unroll
+    for (int i = 0; i < DPL; ++i) raw[i] = 0.f;
+  }
+  OSP_DEV float get(int e) const { return raw[e]; }
+};
+
+// Per-head RMSNorm (optional) + rotate-half RoPE of one head vector held as
+// (x1 = element lane, x2 = element lane + HD/2) by lanes < HD/2 of a wavefront.
+template <typename TKV, int HD>
+OSP_DEV void norm_rope(const AttnArgs& a, const void* gain, int pos, int lane, float& x1,
+                       float& x2) {
+  constexpr int HALF = HD / 2;
+  const bool act = lane < HALF;
   if (a.qk_norm) {
-    const float ss = wave_sum(x1 * x1 + x2 * x2);
-    const float inv = 1.0f / sqrtf(ss / (float)hd + a.eps);
-    const TKV* gn = reinterpret_cast<const TKV*>(is_q ? a.q_norm : a.k_norm);
+    const float ss = wave_sum(act ? x1 * x1 + x2 * x2 : 0.f);
+    const float inv = 1.0f / sqrtf(ss / (float)HD + a.eps);
     if (act) {
+      const TKV* gn = reinterpret_cast<const TKV*>(gain);
       x1 = x1 * inv * load_f32(gn, lane);
-      x2 = x2 * inv * load_f32(gn, lane + half);
+      x2 = x2 * inv * load_f32(gn, lane + HALF);
     }
   }
   const int p = min(max(pos, 0), a.max_seq - 1);
-  const float c = act ? a.rope_cos[(long)p * half + lane] : 0.f;
-  const float s = act ? a.rope_sin[(long)p * half + lane] : 0.f;
+  const float c = act ? a.rope_cos[(long)p * HALF + lane] : 0.f;
+  const float s = act ? a.rope_sin[(long)p * HALF + lane] : 0.f;
   const float y1 = x1 * c - x2 * s;
   const float y2 = x2 * c + x1 * s;
-  if (is_q) {
-    if (act) {
-      float* q = a.q + (long)r * (a.nq * hd) + hh * hd;
-      q[lane] = y1;
-      q[lane + half] = y2;
-    }
-    return;
-  }
-  const int slot = a.bslot[b];
-  const int blk = pos / a.kv_block, within = pos - blk * a.kv_block;
-  if (pos < 0 || blk >= a.slot_nblocks[slot]) {
-    if (lane == 0) atomicOr(a.err, 1u << 3);
-    return;
-  }
-  const long phys = a.block_table[(long)slot * a.max_blocks + blk];
-  TKV* base = reinterpret_cast<TKV*>(a.kv) +
-              phys * kv_block_elems(a.n_layers, a.nkv, a.kv_block, hd);
-  TKV* kp = base + (((long)a.layer * 2 + 0) * a.nkv + g) * a.kv_block * hd + (long)within * hd;
-  TKV* vp = base + (((long)a.layer * 2 + 1) * a.nkv + g) * a.kv_block * hd + (long)within * hd;
-  const float* vs = a.qkv + (long)r * a.qkv_w + (a.nq + a.nkv + g) * hd;
-  if (act) {
-    store_from_f32(kp, lane, y1);
-    store_from_f32(kp, lane + half, y2);
-    store_from_f32(vp, lane, vs[lane]);
-    store_from_f32(vp, lane + half, vs[lane + half]);
-  }
+  x1 = y1;
+  x2 = y2;
 }
 
-// Load DPL consecutive cache elements as floats.
-template <typename TKV, int DPL>
-OSP_DEV void load_seg(const TKV* p, float* out) {
-  constexpr int VEC = Vec<TKV>::N;
-#pragma unroll
-  for (int j = 0; j < DPL / VEC; ++j) load_vec<TKV>(p + j * VEC, out + j * VEC);
-}
-
+// One 16-token page of one kv head: lane l holds head dims [DPL*(l%16), +DPL) of
+// tokens 4u + l/16, u = 0..3 (each of the 4 loads of K or V is one coalesced
+// 1 KB / 512 B wavefront read of 4 consecutive tokens).
 template <typename TKV, int HD>
+struct Page {
+  static constexpr int DPL = HD / 16;
+  Seg<TKV, DPL> k[4], v[4];
+  OSP_DEV void load(const TKV* kbase, const TKV* vbase, int lane) {
+    const int off = (lane >> 4) * HD + (lane & 15) * DPL;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      k[u].load(kbase + u * 4 * HD + off);
+      v[u].load(vbase + u * 4 * HD + off);
+    }
+  }
+  OSP_DEV void zero() {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) { k[u].zero(); v[u].zero(); }
+  }
+};
+
+template <typename TKV, int HD, int QV>
 __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
-  constexpr int LPT = 4;               // lanes per token
-  constexpr int DPL = HD / LPT;        // head dims per lane
-  constexpr int QV = 256 / HD;         // query vectors per pass (q + o = 2*QV*DPL = 128 regs)
-  constexpr int TPW = OSP_WAVE / LPT;  // tokens per wavefront step (= KV page size 16)
+  constexpr int DPL = HD / 16;         // head dims per lane (QV query vectors per pass)
+  constexpr int PG = 16;               // tokens per KV page
+  constexpr int HALF = HD / 2;
+  __shared__ float sm_q[QV][HD];
   __shared__ float sm_m[4][QV];
   __shared__ float sm_l[4][QV];
   __shared__ float sm_o[4][QV][HD];
 
   const int b = blockIdx.x, g = blockIdx.y, sp = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int tok = lane / LPT, seg = lane % LPT;
+  const int dseg = (lane & 15) * DPL;  // this lane's head dims
+  const int tsub = lane >> 4;          // token within each group of 4
   int r_beg, r_end;
   if (a.cu) { r_beg = a.cu[b]; r_end = a.cu[b + 1]; } else { r_beg = b; r_end = b + 1; }
   const int rows_total = a.rows.count ? min(*a.rows.count, a.rows.max_rows) : a.rows.max_rows;
@@ -103,21 +125,70 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   if (r_beg >= r_end) return;
   const int G = a.nq / a.nkv;
   const int nvec = (r_end - r_beg) * G;
+  const int first_new = a.rows.pos[r_beg];
   const int n_ctx = a.rows.pos[r_end - 1] + 1;
   int ts = (n_ctx + a.n_split - 1) / a.n_split;
-  ts = (ts + TPW - 1) / TPW * TPW;
+  ts = (ts + PG - 1) / PG * PG;
   const int p_lo = sp * ts;
   const int p_hi = min(n_ctx, p_lo + ts);
   const int slot = a.bslot[b];
   const int nblocks = a.slot_nblocks[slot];
   const int32_t* bt = a.block_table + (long)slot * a.max_blocks;
-  const TKV* kvb = reinterpret_cast<const TKV*>(a.kv);
+  TKV* kvb = reinterpret_cast<TKV*>(a.kv);
   const long blk_elems = kv_block_elems(a.n_layers, a.nkv, a.kv_block, HD);
   const long k_off = (((long)a.layer * 2 + 0) * a.nkv + g) * a.kv_block * HD;
   const long v_off = (((long)a.layer * 2 + 1) * a.nkv + g) * a.kv_block * HD;
-  const int nq_hd = a.nq * HD;
+
+  // ---- 0. prefetch this wavefront's first page if it holds only older positions -------
+  Page<TKV, HD> pre;
+  const int t_first = p_lo + wave * PG;
+  const bool prefetched = t_first < p_hi && t_first + PG <= first_new && t_first / PG < nblocks;
+  if (prefetched) {
+    const long base = (long)bt[t_first / PG] * blk_elems;
+    pre.load(kvb + base + k_off, kvb + base + v_off, lane);
+  }
+
+  // ---- 1. keys/values of the new rows that fall in this split ------------------------
+  {
+    bool wrote = false;
+    for (int r = r_beg + (3 - wave); r < r_end; r += 4) {
+      const int pos = a.rows.pos[r];
+      if (pos < p_lo || pos >= p_hi) continue;
+      const int blk = pos / a.kv_block;
+      if (blk >= nblocks) { if (lane == 0) atomicOr(a.err, 1u << 3); continue; }
+      const float* src = a.qkv + (long)r * a.qkv_w + (a.nq + g) * HD;
+      const float* vs = a.qkv + (long)r * a.qkv_w + (a.nq + a.nkv + g) * HD;
+      float k1 = lane < HALF ? src[lane] : 0.f, k2 = lane < HALF ? src[lane + HALF] : 0.f;
+      const float v1 = lane < HALF ? vs[lane] : 0.f, v2 = lane < HALF ? vs[lane + HALF] : 0.f;
+      norm_rope<TKV, HD>(a, a.k_norm, pos, lane, k1, k2);
+      const long base = (long)bt[blk] * blk_elems + (long)(pos - blk * a.kv_block) * HD;
+      if (lane < HALF) {
+        store_from_f32(kvb, base + k_off + lane, k1);
+        store_from_f32(kvb, base + k_off + lane + HALF, k2);
+        store_from_f32(kvb, base + v_off + lane, v1);
+        store_from_f32(kvb, base + v_off + lane + HALF, v2);
+      }
+      wrote = true;
+    }
+    if (wrote) __threadfence_block();
+  }
 
   for (int j0 = 0; j0 < nvec; j0 += QV) {
+    // ---- 2. this pass's query vectors: norm + RoPE into LDS (scaled by 1/sqrt(hd)) ----
+    for (int j = wave; j < QV; j += 4) {
+      const int jj = j0 + j;
+      if (jj < nvec) {
+        const int r = r_beg + jj / G, h = g * G + jj % G;
+        const float* src = a.qkv + (long)r * a.qkv_w + h * HD;
+        float q1 = lane < HALF ? src[lane] : 0.f, q2 = lane < HALF ? src[lane + HALF] : 0.f;
+        norm_rope<TKV, HD>(a, a.q_norm, a.rows.pos[r], lane, q1, q2);
+        if (lane < HALF) { sm_q[j][lane] = q1 * a.scale; sm_q[j][lane + HALF] = q2 * a.scale; }
+      } else if (lane < HALF) {
+        sm_q[j][lane] = 0.f;
+        sm_q[j][lane + HALF] = 0.f;
+      }
+    }
+    __syncthreads();
     float q[QV][DPL], o[QV][DPL], m[QV], l[QV];
     int qpos[QV];
 #pragma unroll
@@ -125,70 +196,74 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
       const int jj = j0 + j;
       m[j] = -INFINITY;
       l[j] = 0.f;
-      qpos[j] = -1;
+      qpos[j] = jj < nvec ? a.rows.pos[r_beg + jj / G] : -1;
 #pragma unroll
-      for (int e = 0; e < DPL; ++e) o[j][e] = 0.f;
-      if (jj < nvec) {
-        const int r = r_beg + jj / G, h = g * G + jj % G;
-        qpos[j] = a.rows.pos[r];
-        const float* qp = a.q + (long)r * nq_hd + h * HD + seg * DPL;
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) q[j][e] = qp[e] * a.scale;
-      } else {
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) q[j][e] = 0.f;
-      }
+      for (int e = 0; e < DPL; ++e) { o[j][e] = 0.f; q[j][e] = sm_q[j][dseg + e]; }
     }
-    for (int t0 = p_lo + wave * TPW; t0 < p_hi; t0 += 4 * TPW) {
-      const int p = t0 + tok;
-      const int blk = t0 / a.kv_block;
-      const bool valid = p < p_hi && blk < nblocks;
-      float kf[DPL], vf[DPL];
-      if (valid) {
-        const long phys = bt[blk];
-        const TKV* kp = kvb + phys * blk_elems + k_off + (long)(p - blk * a.kv_block) * HD + seg * DPL;
-        const TKV* vp = kvb + phys * blk_elems + v_off + (long)(p - blk * a.kv_block) * HD + seg * DPL;
-        load_seg<TKV, DPL>(kp, kf);
-        load_seg<TKV, DPL>(vp, vf);
+    // ---- 3. walk the split's pages -------------------------------------------------------
+    for (int t0 = t_first; t0 < p_hi; t0 += 4 * PG) {
+      const int blk = t0 / PG;
+      Page<TKV, HD> pg;
+      if (j0 == 0 && t0 == t_first && prefetched) {
+        pg = pre;
+      } else if (blk < nblocks) {
+        const long base = (long)bt[blk] * blk_elems;
+        pg.load(kvb + base + k_off, kvb + base + v_off, lane);
       } else {
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) { kf[e] = 0.f; vf[e] = 0.f; }
+        pg.zero();
       }
 #pragma unroll
       for (int j = 0; j < QV; ++j) {
-        float s = 0.f;
+        float sc[4];
+        float bm = -INFINITY;
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) s = fmaf(q[j][e], kf[e], s);
-        s += __shfl_xor(s, 1, OSP_WAVE);
-        s += __shfl_xor(s, 2, OSP_WAVE);
-        if (!valid || p > qpos[j]) s = -INFINITY;
-        float bm = s;
-        bm = fmaxf(bm, __shfl_xor(bm, 4, OSP_WAVE));
-        bm = fmaxf(bm, __shfl_xor(bm, 8, OSP_WAVE));
+        for (int u = 0; u < 4; ++u) {
+          float s = 0.f;
+#pragma unroll
+          for (int e = 0; e < DPL; ++e) s = fmaf(q[j][e], pg.k[u].get(e), s);
+          s += __shfl_xor(s, 1, OSP_WAVE);
+          s += __shfl_xor(s, 2, OSP_WAVE);
+          s += __shfl_xor(s, 4, OSP_WAVE);
+          s += __shfl_xor(s, 8, OSP_WAVE);
+          const int p = t0 + 4 * u + tsub;
+          if (p >= p_hi || p > qpos[j] || blk >= nblocks) s = -INFINITY;
+          sc[u] = s;
+          bm = fmaxf(bm, s);
+        }
         bm = fmaxf(bm, __shfl_xor(bm, 16, OSP_WAVE));
         bm = fmaxf(bm, __shfl_xor(bm, 32, OSP_WAVE));
         const float mn = fmaxf(m[j], bm);
         if (mn == -INFINITY) continue;
         const float so = __expf(m[j] - mn);
-        const float pe = __expf(s - mn);
-        l[j] = l[j] * so + pe;
+        l[j] *= so;
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) o[j][e] = fmaf(pe, vf[e], o[j][e] * so);
+        for (int e = 0; e < DPL; ++e) o[j][e] *= so;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          // masked tokens (past the sequence end: unwritten cache memory) contribute
+          // nothing, not even 0 * NaN
+          if (sc[u] > -INFINITY) {
+            const float pe = __expf(sc[u] - mn);
+            l[j] += pe;
+#pragma unroll
+            for (int e = 0; e < DPL; ++e) o[j][e] = fmaf(pe, pg.v[u].get(e), o[j][e]);
+          }
+        }
         m[j] = mn;
       }
     }
-    // ---- merge lanes of one wave: sum over the 16 token lanes of each segment ---------
+    // ---- merge the 4 token groups of each wave (lanes l, l^16, l^32, l^48) -------------
 #pragma unroll
     for (int j = 0; j < QV; ++j) {
 #pragma unroll
-      for (int sft = 4; sft < 64; sft <<= 1) {
+      for (int sft = 16; sft < 64; sft <<= 1) {
         l[j] += __shfl_xor(l[j], sft, OSP_WAVE);
 #pragma unroll
         for (int e = 0; e < DPL; ++e) o[j][e] += __shfl_xor(o[j][e], sft, OSP_WAVE);
       }
-      if (lane < LPT) {
+      if (lane < 16) {
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) sm_o[wave][j][seg * DPL + e] = o[j][e];
+        for (int e = 0; e < DPL; ++e) sm_o[wave][j][dseg + e] = o[j][e];
       }
       if (lane == 0) { sm_m[wave][j] = m[j]; sm_l[wave][j] = l[j]; }
     }
@@ -219,46 +294,59 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   }
 }
 
-__global__ void __launch_bounds__(128) k_attn_combine(AttnArgs a) {
+// One wavefront per (row, head): lane t reads split t's (max, sum); the output
+// elements are accumulated over splits with all loads independent.
+__global__ void __launch_bounds__(64) k_attn_combine(AttnArgs a) {
   const int r = blockIdx.x, h = blockIdx.y;
   const int rows = a.rows.count ? min(*a.rows.count, a.rows.max_rows) : a.rows.max_rows;
   if (r >= rows) return;
-  const int hd = a.hd;
-  const float* pp = a.part + ((long)r * a.nq + h) * a.n_split * (hd + 2);
-  float M = -INFINITY;
-  for (int sp = 0; sp < a.n_split; ++sp) M = fmaxf(M, pp[sp * (hd + 2)]);
-  for (int e = threadIdx.x; e < hd; e += blockDim.x) {
-    float L = 0.f, O = 0.f;
-    for (int sp = 0; sp < a.n_split; ++sp) {
-      const float m = pp[sp * (hd + 2)];
-      if (m == -INFINITY) continue;
-      const float f = __expf(m - M);
-      L += pp[sp * (hd + 2) + 1] * f;
-      O += pp[sp * (hd + 2) + 2 + e] * f;
+  const int lane = threadIdx.x;
+  const int hd = a.hd, ns = a.n_split;
+  const float* pp = a.part + ((long)r * a.nq + h) * ns * (hd + 2);
+  const float m = lane < ns ? pp[lane * (hd + 2)] : -INFINITY;
+  const float lsum = lane < ns ? pp[lane * (hd + 2) + 1] : 0.f;
+  const float M = wave_max(m);
+  const float f = (m > -INFINITY) ? __expf(m - M) : 0.f;
+  const float L = wave_sum(lsum * f);
+  const float inv = L > 0.f ? 1.0f / L : 0.f;
+  float* out = a.o + (long)r * a.nq * hd + h * hd;
+  for (int e = lane; e < hd; e += 64) {
+    float O = 0.f;
+    for (int s0 = 0; s0 < ns; s0 += 8) {
+      float v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = s0 + i < ns ? pp[(s0 + i) * (hd + 2) + 2 + e] : 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) O += v[i] * __shfl(f, (s0 + i) & 63, OSP_WAVE);
     }
-    a.o[(long)r * a.nq * hd + h * hd + e] = L > 0.f ? O / L : 0.f;
+    out[e] = O * inv;
   }
 }
 
-void launch_rope_kvwrite(int kvdtype, const AttnArgs& a, hipStream_t st) {
-  dim3 grid(a.rows.max_rows, a.nq + a.nkv);
-  if (kvdtype == 1) hipLaunchKernelGGL(k_rope_kvwrite<bf16_t>, grid, dim3(64), 0, st, a);
-  else hipLaunchKernelGGL(k_rope_kvwrite<float>, grid, dim3(64), 0, st, a);
+// Query vectors per pass: enough for every row of a sequence times its GQA group,
+// at most 8 (head_dim 128) or 16 (head_dim 64) so q + o stay within 128 registers.
+template <typename TKV, int HD>
+static void launch_hd(const AttnArgs& a, hipStream_t st) {
+  dim3 grid(a.B, a.nkv, a.n_split);
+  const int need = a.rows_per_seq * (a.nq / a.nkv);
+  constexpr int QMAX = 1024 / HD;
+  if (need <= 1) hipLaunchKernelGGL((k_attn<TKV, HD, 1>), grid, dim3(256), 0, st, a);
+  else if (need <= 2) hipLaunchKernelGGL((k_attn<TKV, HD, 2>), grid, dim3(256), 0, st, a);
+  else if (need <= 4 || QMAX == 4) hipLaunchKernelGGL((k_attn<TKV, HD, 4>), grid, dim3(256), 0, st, a);
+  else if (need <= 8 || QMAX == 8) hipLaunchKernelGGL((k_attn<TKV, HD, (QMAX >= 8 ? 8 : 4)>), grid, dim3(256), 0, st, a);
+  else hipLaunchKernelGGL((k_attn<TKV, HD, QMAX>), grid, dim3(256), 0, st, a);
 }
 
 void launch_attention(int kvdtype, const AttnArgs& a, hipStream_t st) {
-  dim3 grid(a.B, a.nkv, a.n_split);
   if (kvdtype == 1) {
-    if (a.hd == 128) hipLaunchKernelGGL((k_attn<bf16_t, 128>), grid, dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((k_attn<bf16_t, 64>), grid, dim3(256), 0, st, a);
+    if (a.hd == 128) launch_hd<bf16_t, 128>(a, st); else launch_hd<bf16_t, 64>(a, st);
   } else {
-    if (a.hd == 128) hipLaunchKernelGGL((k_attn<float, 128>), grid, dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((k_attn<float, 64>), grid, dim3(256), 0, st, a);
+    if (a.hd == 128) launch_hd<float, 128>(a, st); else launch_hd<float, 64>(a, st);
   }
 }
 
 void launch_attn_combine(const AttnArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(k_attn_combine, dim3(a.rows.max_rows, a.nq), dim3(128), 0, st, a);
+  hipLaunchKernelGGL(k_attn_combine, dim3(a.rows.max_rows, a.nq), dim3(64), 0, st, a);
 }
 
 }  // namespace osp

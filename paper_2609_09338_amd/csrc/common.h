@@ -140,6 +140,12 @@ OSP_DEV T block_scan(T v, T* sm, T& incl, T& tot) {
   return lane == 0 ? before : before + prev;
 }
 
+OSP_DEV int wave_max_i(int v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = max(v, __shfl_xor(v, m, OSP_WAVE));
+  return v;
+}
+
 OSP_DEV int wave_min_i(int v) {
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) v = min(v, __shfl_xor(v, m, OSP_WAVE));

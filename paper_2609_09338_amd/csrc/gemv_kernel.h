@@ -1,0 +1,393 @@
+// Weight-streaming matrix-vector products of the drafter (few rows at a time).
+//
+// Y[r][n] = sum_c X[r][c] * W[n][c] for the rows r of one forward pass.  Every
+// weight byte is read from HBM once per block of RB rows.  Each wavefront is
+// independent (no LDS, no barriers): it owns a contiguous range of weight rows
+// and walks it NW rows at a time; lane l reads the 16-byte column vectors
+// l, l+64, ..., l+64(XV-1) of those rows, i.e. NW*XV fully coalesced 1 KB
+// wavefront loads in flight per step.  The lane's matching input values are
+// loaded once per wavefront and kept in registers when the row fits
+// (Kd <= 64*XV*VEC; otherwise they are re-read per step, chunk by chunk).  The
+// NW*RB partial sums are reduced across the 64 lanes with one transposed
+// butterfly.
+//
+// The virtual input X is formed on the fly (the norm prologues of the body):
+//   SRC_PLAIN  fp32 rows (attention output, FFN hidden)
+//   SRC_NORM   RMSNorm(x) * gain (post-attention norm, final norm)
+//   SRC_QKV    [s ; RMSNorm(x) * gain] -- the expanded-QKV input of Eq. 2-3, read
+//              from its two segments with no concatenated copy; in layer 0 x is
+//              the embedding row of the token (one wavefront materialises it)
+//   SRC_TAPS   target hidden-state taps (Eq. 1)
+// and the epilogue writes, accumulates into the residual, applies SwiGLU, or
+// writes masked logits plus, per wavefront range, the (max, sum exp((l-max)/T),
+// lowest argmax) statistics that sampling merges.
+#pragma once
+
+#include "common.h"
+#include "internal.h"
+
+namespace osp {
+
+constexpr int kGemvThreads = 256;
+constexpr int kGemvWavesPerBlock = kGemvThreads / OSP_WAVE;
+
+template <int N> struct Log2 { static constexpr int v = 1 + Log2<N / 2>::v; };
+template <> struct Log2<1> { static constexpr int v = 0; };
+
+// Raw 16-byte weight vector and its widening.
+template <typename TW> struct WRaw;
+template <> struct WRaw<bf16_t> {
+  uint4 v;
+  OSP_DEV void load(const bf16_t* p) { v = *reinterpret_cast<const uint4*>(p); }
+  OSP_DEV void zero() { v = make_uint4(0u, 0u, 0u, 0u); }
+  OSP_DEV float dot(const float* x, float s) const {
+    s = fmaf(bf16_lo(v.x), x[0], s); s = fmaf(bf16_hi(v.x), x[1], s);
+    s = fmaf(bf16_lo(v.y), x[2], s); s = fmaf(bf16_hi(v.y), x[3], s);
+    s = fmaf(bf16_lo(v.z), x[4], s); s = fmaf(bf16_hi(v.z), x[5], s);
+    s = fmaf(bf16_lo(v.w), x[6], s); s = fmaf(bf16_hi(v.w), x[7], s);
+    return s;
+  }
+};
+template <> struct WRaw<float> {
+  float4 v;
+  OSP_DEV void load(const float* p) { v = *reinterpret_cast<const float4*>(p); }
+  OSP_DEV void zero() { v = make_float4(0.f, 0.f, 0.f, 0.f); }
+  OSP_DEV float dot(const float* x, float s) const {
+    s = fmaf(v.x, x[0], s); s = fmaf(v.y, x[1], s); s = fmaf(v.z, x[2], s); s = fmaf(v.w, x[3], s);
+    return s;
+  }
+};
+
+OSP_DEV void load_f4s(const float* p, float* out, int n) {
+  for (int e = 0; e < n; e += 4) {
+    const float4 v = *reinterpret_cast<const float4*>(p + e);
+    out[e] = v.x; out[e + 1] = v.y; out[e + 2] = v.z; out[e + 3] = v.w;
+  }
+}
+
+// Raw input values X[rr][col .. col+VEC) before normalisation, and whether they
+// belong to the normalised segment (norm factor still to be applied).
+template <typename TW, int SRC, int VEC>
+OSP_DEV bool load_x_raw(const GemvArgs& a, int rr, int col, float* out) {
+  if constexpr (SRC == SRC_PLAIN) {
+    load_f4s(a.xin + (long)rr * a.ldx + col, out, VEC);
+    return false;
+  } else if constexpr (SRC == SRC_TAPS) {
+    load_vec<TW>(reinterpret_cast<const TW*>(a.taps) + (long)a.tap_row[rr] * a.ldt + col, out);
+    return false;
+  } else {
+    int c = col;
+    if constexpr (SRC == SRC_QKV) {
+      if (col < a.d_norm) {   // conditioning segment, used as is
+        const int sr = a.s_gather ? a.s_gather[rr] : rr;
+        load_f4s(a.s + (long)sr * a.lds + col, out, VEC);
+        return false;
+      }
+      c = col - a.d_norm;
+      if (a.embed) {
+        int t = a.tok[rr];
+        t = min(max(t, 0), a.vocab_embed - 1);
+        load_vec<TW>(reinterpret_cast<const TW*>(a.embed) + (long)t * a.d_norm + c, out);
+        return true;
+      }
+    }
+    const int xr = a.gather ? a.gather[rr] : rr;
+    load_f4s(a.xin + (long)xr * a.ldx + c, out, VEC);
+    return true;
+  }
+}
+
+// Apply RMSNorm factor and gain to a normalised-segment vector.
+template <typename TW, int SRC, int VEC>
+OSP_DEV void norm_x(const GemvArgs& a, int col, float inv_rms, float* v) {
+  const int c = (SRC == SRC_QKV) ? col - a.d_norm : col;
+  float g[VEC];
+  load_vec<TW>(reinterpret_cast<const TW*>(a.gamma) + c, g);
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) v[e] = v[e] * inv_rms * g[e];
+}
+
+// 1 / sqrt(mean(x^2) + eps) of the normalised segment of row rr, by one wavefront.
+template <typename TW, int SRC>
+OSP_DEV float row_inv_rms(const GemvArgs& a, int rr, int lane) {
+  constexpr int VEC = Vec<TW>::N;
+  const int d = a.d_norm;
+  const int base = (SRC == SRC_QKV) ? d : 0;
+  float ss = 0.f;
+  for (int c = lane * VEC; c < d; c += OSP_WAVE * VEC) {
+    float v[VEC];
+    load_x_raw<TW, SRC, VEC>(a, rr, base + c, v);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) ss += v[e] * v[e];
+  }
+  ss = wave_sum(ss);
+  return 1.0f / sqrtf(ss / (float)d + a.eps);
+}
+
+template <typename TW, int SRC, int EPI, int RB, int NW, int XV>
+__global__ void __launch_bounds__(kGemvThreads) k_gemv(GemvArgs a, int rows_per_wave) {
+  constexpr int VEC = Vec<TW>::N;
+  constexpr int NWV = (EPI == EPI_SWIGLU) ? 2 * NW : NW;
+  constexpr int V = NWV * RB;
+  constexpr int LOGV = Log2<V>::v;
+  constexpr int SH = 6 - LOGV;
+  constexpr bool NORMED = (SRC == SRC_NORM || SRC == SRC_QKV);
+  static_assert((1 << LOGV) == V && V <= 64, "values per lane must be a power of two <= 64");
+
+  const int lane = threadIdx.x & (OSP_WAVE - 1);
+  const int gw = blockIdx.x * kGemvWavesPerBlock + (threadIdx.x >> 6);
+  const int n_lo = gw * rows_per_wave;
+  if (n_lo >= a.N) return;
+  const int n_hi = min(a.N, n_lo + rows_per_wave);
+  const int rows = a.count ? min(*a.count, a.max_rows) : a.max_rows;
+  const TW* __restrict__ w0 = reinterpret_cast<const TW*>(a.w0);
+  const TW* __restrict__ w1 = reinterpret_cast<const TW*>(a.w1);
+  const int nvec = a.Kd / VEC;                 // 16-byte vectors per weight row
+  const bool cached = nvec <= OSP_WAVE * XV;   // the whole input row fits in registers
+
+  for (int r0 = 0; r0 < rows; r0 += RB) {
+    float xc[RB][XV][VEC];                     // this lane's input values (cached mode)
+    float inv_rms[RB];
+#pragma unroll
+    for (int r = 0; r < RB; ++r) inv_rms[r] = 1.f;
+    if (cached) {
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        bool isn[XV];
+        float ss = 0.f;
+#pragma unroll
+        for (int u = 0; u < XV; ++u) {
+          const int j = lane + OSP_WAVE * u;
+          isn[u] = false;
+          if (r0 + r < rows && j < nvec) {
+            isn[u] = load_x_raw<TW, SRC, VEC>(a, r0 + r, j * VEC, xc[r][u]);
+            if (isn[u]) {
+#pragma unroll
+              for (int e = 0; e < VEC; ++e) ss += xc[r][u][e] * xc[r][u][e];
+            }
+          } else {
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) xc[r][u][e] = 0.f;
+          }
+        }
+        if constexpr (NORMED) {
+          ss = wave_sum(ss);
+          inv_rms[r] = 1.0f / sqrtf(ss / (float)a.d_norm + a.eps);
+#pragma unroll
+          for (int u = 0; u < XV; ++u)
+            if (isn[u]) norm_x<TW, SRC, VEC>(a, (lane + OSP_WAVE * u) * VEC, inv_rms[r], xc[r][u]);
+        }
+      }
+    } else if constexpr (NORMED) {
+#pragma unroll
+      for (int r = 0; r < RB; ++r)
+        if (r0 + r < rows) inv_rms[r] = row_inv_rms<TW, SRC>(a, r0 + r, lane);
+    }
+    // layer 0 of the expanded QKV: one wavefront writes x = embed[token] for the residual
+    if constexpr (SRC == SRC_QKV) {
+      if (a.embed && a.x_out && gw == 0) {
+        for (int r = 0; r < RB && r0 + r < rows; ++r) {
+          int t = a.tok[r0 + r];
+          t = min(max(t, 0), a.vocab_embed - 1);
+          const TW* e = reinterpret_cast<const TW*>(a.embed) + (long)t * a.d_norm;
+          for (int c = lane; c < a.d_norm; c += OSP_WAVE)
+            a.x_out[(long)(r0 + r) * a.ldx + c] = load_f32(e, c);
+        }
+      }
+    }
+    // logits: temperature of each row; running (max, sum exp, argmax) of owner lanes
+    float st_m[RB], st_s[RB], temp[RB];
+    int st_a[RB];
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+      st_m[r] = -INFINITY;
+      st_s[r] = 0.f;
+      st_a[r] = 0x7fffffff;
+      temp[r] = 0.f;
+      if constexpr (EPI == EPI_LOGITS)
+        if (r0 + r < rows) temp[r] = a.temp[a.row_seq ? a.row_seq[r0 + r] : r0 + r];
+    }
+
+    for (int n0 = n_lo; n0 < n_hi; n0 += NW) {
+      const int idx = lane >> SH;
+      const int vi = idx / RB, rsel = idx - vi * RB;
+      int mapped = 1;
+      if constexpr (EPI == EPI_LOGITS)   // prefetch the vocabulary map of this step's rows
+        mapped = (n0 + vi < n_hi) ? a.d2t[n0 + vi] : -1;
+      float acc[V];
+#pragma unroll
+      for (int i = 0; i < V; ++i) acc[i] = 0.f;
+      for (int jb = 0; jb < nvec; jb += OSP_WAVE * XV) {
+        WRaw<TW> wr[NWV][XV];
+#pragma unroll
+        for (int i = 0; i < NWV; ++i) {
+          const int n = n0 + (i % NW);
+#pragma unroll
+          for (int u = 0; u < XV; ++u) {
+            const int j = jb + lane + OSP_WAVE * u;
+            if (n < n_hi && j < nvec)
+              wr[i][u].load(((EPI == EPI_SWIGLU && i >= NW) ? w1 : w0) + (long)n * a.Kd + j * VEC);
+            else
+              wr[i][u].zero();
+          }
+        }
+        if (!cached) {
+#pragma unroll
+          for (int r = 0; r < RB; ++r)
+#pragma unroll
+            for (int u = 0; u < XV; ++u) {
+              const int j = jb + lane + OSP_WAVE * u;
+              if (r0 + r < rows && j < nvec) {
+                const bool isn = load_x_raw<TW, SRC, VEC>(a, r0 + r, j * VEC, xc[r][u]);
+                if constexpr (NORMED)
+                  if (isn) norm_x<TW, SRC, VEC>(a, j * VEC, inv_rms[r], xc[r][u]);
+              } else {
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) xc[r][u][e] = 0.f;
+              }
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < NWV; ++i)
+#pragma unroll
+          for (int r = 0; r < RB; ++r) {
+            float s = acc[i * RB + r];
+#pragma unroll
+            for (int u = 0; u < XV; ++u) s = wr[i][u].dot(xc[r][u], s);
+            acc[i * RB + r] = s;
+          }
+      }
+      // ---- reduce across lanes: lane l ends with value index l >> SH --------------------
+      const float tot = transpose_reduce<LOGV>(acc, lane);
+      const bool owner = (lane & ((1 << SH) - 1)) == 0;
+      const int rr = r0 + rsel;
+      const int n = n0 + vi;
+      if constexpr (EPI == EPI_SWIGLU) {
+        // gate rows are values [0, NW), up rows [NW, 2 NW)
+        const int up_lane = ((vi + NW) * RB + rsel) << SH;
+        const float up = __shfl(tot, up_lane < OSP_WAVE ? up_lane : 0, OSP_WAVE);
+        if (owner && vi < NW && rr < rows && n < n_hi)
+          a.y[(long)rr * a.ldy + n] = tot / (1.0f + __expf(-tot)) * up;
+      } else if constexpr (EPI == EPI_LOGITS) {
+        const bool live = owner && rr < rows && n < n_hi;
+        const float lv = (live && mapped >= 0) ? tot : -INFINITY;
+        if (live) a.y[(long)rr * a.ld_logits + n] = lv;
+#pragma unroll
+        for (int q = 0; q < RB; ++q) {
+          if (q == rsel && lv > -INFINITY) {
+            const float T = temp[q];
+            if (lv > st_m[q]) {
+              st_s[q] = (T > 0.f && st_m[q] > -INFINITY) ? st_s[q] * __expf((st_m[q] - lv) / T) : 0.f;
+              st_m[q] = lv;
+              st_a[q] = n;
+            }
+            if (T > 0.f) st_s[q] += __expf((lv - st_m[q]) / T);
+          }
+        }
+      } else {
+        if (owner && rr < rows && n < n_hi) {
+          float* yp = a.y + (long)rr * a.ldy + n;
+          if constexpr (EPI == EPI_RESID) *yp += tot; else *yp = tot;
+        }
+      }
+    }
+    if constexpr (EPI == EPI_LOGITS) {
+      // merge the lanes' statistics of each row and write this wavefront's record
+#pragma unroll
+      for (int q = 0; q < RB; ++q) {
+        const int rr = r0 + q;
+        if (rr >= rows) continue;
+        const float M = wave_max(st_m[q]);
+        int am = (st_m[q] == M && M > -INFINITY) ? st_a[q] : 0x7fffffff;
+        am = wave_min_i(am);
+        const float T = temp[q];
+        float s = (T > 0.f && st_m[q] > -INFINITY) ? st_s[q] * __expf((st_m[q] - M) / T) : 0.f;
+        s = wave_sum(s);
+        if (lane == 0) {
+          float* p = a.part + ((long)rr * a.nblk + gw) * 4;
+          p[0] = M;
+          p[1] = s;
+          p[2] = __int_as_float(am == 0x7fffffff ? -1 : am);
+          p[3] = 0.f;
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------
+// Launch shape.  RB rows per pass in {1, 2, 4, 8}; XV = 16-byte vectors per lane and
+// row in one step ({1, 2, 4, 8}, RB * XV <= 8 so the cached input is <= 64 values);
+// NW weight rows per step with NW * XV * RB <= 16 vectors in flight (SwiGLU counts
+// gate and up); NW shrinks until the grid has enough wavefronts.
+struct GemvPlan {
+  int rb, xv, nw, rpw, waves;
+};
+
+inline GemvPlan gemv_plan(int wdtype, EpiKind epi, int rows, int N, int Kd) {
+  GemvPlan p;
+  const int vec = wdtype == 1 ? 8 : 4;
+  p.rb = rows <= 1 ? 1 : rows <= 2 ? 2 : rows <= 4 ? 4 : 8;
+  const int per_lane = (Kd / vec + OSP_WAVE - 1) / OSP_WAVE;
+  int xv = 1;
+  while (xv < per_lane && xv * 2 * p.rb <= 8) xv *= 2;
+  p.xv = xv;
+  const int f = epi == EPI_SWIGLU ? 2 : 1;
+  int nw = 8;
+  while (nw > 1 && nw * xv * p.rb * f > 16) nw /= 2;
+  const int min_waves = epi == EPI_LOGITS ? 1024 : 2048;
+  while (nw > 1 && (N + nw - 1) / nw < min_waves) nw /= 2;
+  p.nw = nw;
+  int rpw = (N + kGemvMaxWaves - 1) / kGemvMaxWaves;
+  rpw = (rpw + nw - 1) / nw * nw;
+  p.rpw = rpw < nw ? nw : rpw;
+  p.waves = (N + p.rpw - 1) / p.rpw;
+  return p;
+}
+
+template <typename TW, int SRC, int EPI, int RB, int NW, int XV>
+void launch_gemv_t(const GemvArgs& a, int rpw, hipStream_t st) {
+  const int waves = (a.N + rpw - 1) / rpw;
+  const int grid = (waves + kGemvWavesPerBlock - 1) / kGemvWavesPerBlock;
+  hipLaunchKernelGGL((k_gemv<TW, SRC, EPI, RB, NW, XV>), dim3(grid), dim3(kGemvThreads), 0, st, a,
+                     rpw);
+}
+
+template <typename TW, int SRC, int EPI, int RB, int XV>
+void launch_gemv_nw(const GemvPlan& p, const GemvArgs& a, hipStream_t st) {
+  constexpr int F = (EPI == EPI_SWIGLU) ? 2 : 1;
+  if constexpr (8 * XV * RB * F <= 16) { if (p.nw == 8) return launch_gemv_t<TW, SRC, EPI, RB, 8, XV>(a, p.rpw, st); }
+  if constexpr (4 * XV * RB * F <= 16) { if (p.nw == 4) return launch_gemv_t<TW, SRC, EPI, RB, 4, XV>(a, p.rpw, st); }
+  if constexpr (2 * XV * RB * F <= 16) { if (p.nw == 2) return launch_gemv_t<TW, SRC, EPI, RB, 2, XV>(a, p.rpw, st); }
+  return launch_gemv_t<TW, SRC, EPI, RB, 1, XV>(a, p.rpw, st);
+}
+
+template <typename TW, int SRC, int EPI, int RB>
+void launch_gemv_xv(const GemvPlan& p, const GemvArgs& a, hipStream_t st) {
+  if constexpr (RB * 8 <= 8) { if (p.xv == 8) return launch_gemv_nw<TW, SRC, EPI, RB, 8>(p, a, st); }
+  if constexpr (RB * 4 <= 8) { if (p.xv == 4) return launch_gemv_nw<TW, SRC, EPI, RB, 4>(p, a, st); }
+  if constexpr (RB * 2 <= 8) { if (p.xv == 2) return launch_gemv_nw<TW, SRC, EPI, RB, 2>(p, a, st); }
+  return launch_gemv_nw<TW, SRC, EPI, RB, 1>(p, a, st);
+}
+
+template <int SRC, int EPI>
+void launch_gemv_kind(int wdtype, const GemvArgs& a, hipStream_t st) {
+  const GemvPlan p = gemv_plan(wdtype, (EpiKind)EPI, a.max_rows, a.N, a.Kd);
+  if (wdtype == 1) {
+    switch (p.rb) {
+      case 1: return launch_gemv_xv<bf16_t, SRC, EPI, 1>(p, a, st);
+      case 2: return launch_gemv_xv<bf16_t, SRC, EPI, 2>(p, a, st);
+      case 4: return launch_gemv_xv<bf16_t, SRC, EPI, 4>(p, a, st);
+      default: return launch_gemv_xv<bf16_t, SRC, EPI, 8>(p, a, st);
+    }
+  } else {
+    switch (p.rb) {
+      case 1: return launch_gemv_xv<float, SRC, EPI, 1>(p, a, st);
+      case 2: return launch_gemv_xv<float, SRC, EPI, 2>(p, a, st);
+      case 4: return launch_gemv_xv<float, SRC, EPI, 4>(p, a, st);
+      default: return launch_gemv_xv<float, SRC, EPI, 8>(p, a, st);
+    }
+  }
+}
+
+}  // namespace osp

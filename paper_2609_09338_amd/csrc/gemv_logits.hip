@@ -1,0 +1,11 @@
+// Instantiations of the weight-streaming GEMV for one input/epilogue kind
+// (one file per kind so that they compile in parallel).
+#include "gemv_kernel.h"
+
+namespace osp {
+
+void launch_gemv_logits(int wdtype, const GemvArgs& a, hipStream_t st) {
+  launch_gemv_kind<SRC_NORM, EPI_LOGITS>(wdtype, a, st);
+}
+
+}  // namespace osp

@@ -1,0 +1,11 @@
+// Instantiations of the weight-streaming GEMV for one input/epilogue kind
+// (one file per kind so that they compile in parallel).
+#include "gemv_kernel.h"
+
+namespace osp {
+
+void launch_gemv_resid(int wdtype, const GemvArgs& a, hipStream_t st) {
+  launch_gemv_kind<SRC_PLAIN, EPI_RESID>(wdtype, a, st);
+}
+
+}  // namespace osp

@@ -70,7 +70,15 @@ struct GemvArgs {
 };
 
 void launch_gemv(int wdtype, SrcKind src, EpiKind epi, const GemvArgs& a, hipStream_t st);
-int gemv_rows_per_block(int wdtype, EpiKind epi, int rows);
+// Partition of the N weight rows of a launch: each wavefront owns rows_per_wave
+// consecutive rows; `waves` wavefronts carry rows (the logits epilogue writes
+// one statistics record per wavefront).
+struct GemvShape {
+  int rows_per_wave;
+  int waves;
+};
+constexpr int kGemvMaxWaves = 4096;
+GemvShape gemv_shape(int wdtype, EpiKind epi, int rows, int N, int Kd);
 
 // Attention.
 struct AttnArgs {
@@ -78,9 +86,9 @@ struct AttnArgs {
   const int32_t* cu;        // [B+1] rows of sequence b are [cu[b], cu[b+1]) (nullable: [b, b+1))
   const int32_t* bslot;     // [B] slot of sequence b
   int B;
+  int rows_per_seq;         // host bound on the rows of one sequence in this pass
   const float* qkv;         // [rows][qkv_w] raw projections
   int qkv_w;
-  float* q;                 // [rows][nq*hd] normalised + rotated queries (written by rope)
   const void* q_norm;
   const void* k_norm;
   int qk_norm;
@@ -101,7 +109,6 @@ struct AttnArgs {
   float* o;                 // [rows][nq*hd]
   uint32_t* err;
 };
-void launch_rope_kvwrite(int kvdtype, const AttnArgs& a, hipStream_t st);
 void launch_attention(int kvdtype, const AttnArgs& a, hipStream_t st);
 void launch_attn_combine(const AttnArgs& a, hipStream_t st);
 

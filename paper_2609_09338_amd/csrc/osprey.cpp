@@ -44,7 +44,6 @@ int ok() {
 
 constexpr int kMaxSplit = 64;
 constexpr int kVerifyChunk = 4096;
-constexpr int kMinLmBlock = 16;  // smallest LM-head block (rows per GEMV block)
 
 enum SlotState { S_EMPTY = 0, S_READY = 1, S_DRAFTED = 2, S_VERIFIED = 3 };
 
@@ -68,7 +67,7 @@ struct Ws {
   uint32_t* err;
   int32_t *ing_seq, *ing_pos, *ing_tok, *ing_tap, *n_rows, *cu, *last_row, *committed, *bslot;
   int32_t *ar_pos, *ar_tok;
-  float *x, *s, *gfb, *qkv, *q, *o, *h;
+  float *x, *s, *gfb, *qkv, *o, *h;
   float* attn_part;
   float* logits;
   float* lm_part;
@@ -94,7 +93,7 @@ Dims dims_of(const osprey_config& c) {
   d.qkv_rows = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
   d.nchunk_t = (c.vocab_target + kVerifyChunk - 1) / kVerifyChunk;
   d.nchunk_d = (c.vocab_draft + kVerifyChunk - 1) / kVerifyChunk;
-  d.lm_nblk_max = (c.vocab_draft + kMinLmBlock - 1) / kMinLmBlock;
+  d.lm_nblk_max = kGemvMaxWaves;
   return d;
 }
 
@@ -135,7 +134,6 @@ size_t plan(const osprey_config& c, char* base, Ws* w) {
   W.s = (float*)take(4L * D.Rmax * d);
   W.gfb = (float*)take(4L * D.B * d);
   W.qkv = (float*)take(4L * D.Rmax * D.qkv_rows);
-  W.q = (float*)take(4L * D.Rmax * nq * hd);
   W.o = (float*)take(4L * D.Rmax * nq * hd);
   W.h = (float*)take(4L * D.Rmax * c.d_ffn);
   W.attn_part = (float*)take(4L * D.Rmax * nq * kMaxSplit * (hd + 2));
@@ -246,7 +244,7 @@ int hip_last() {
 
 // One forward pass of the body over `rows`; `s` holds the conditioning rows.
 void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, const float* s,
-              bool from_embed, int n_split) {
+              bool from_embed, int n_split, int rows_per_seq) {
   const osprey_config& c = h->cfg;
   const Ws& W = h->W;
   const int d = c.d_model, hd = c.head_dim, nq = c.n_q_heads, nkv = c.n_kv_heads;
@@ -284,9 +282,9 @@ void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, c
     a.cu = cu;
     a.bslot = W.bslot;
     a.B = B;
+    a.rows_per_seq = rows_per_seq;
     a.qkv = W.qkv;
     a.qkv_w = qkv_w;
-    a.q = W.q;
     a.q_norm = L.q_norm;
     a.k_norm = L.k_norm;
     a.qk_norm = c.qk_norm;
@@ -309,7 +307,6 @@ void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, c
     a.part = W.attn_part;
     a.o = W.o;
     a.err = W.err;
-    launch_rope_kvwrite(c.dtype, a, h->stream);
     t = h->t_begin(1);
     launch_attention(c.dtype, a, h->stream);
     h->t_end(t);
@@ -362,8 +359,9 @@ void run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, cons
               const float* u, float* logits, long ld_b, int32_t* drafts_out) {
   const osprey_config& c = h->cfg;
   const Ws& W = h->W;
-  const int tn = gemv_rows_per_block(c.dtype, EPI_LOGITS, B);
-  const int nblk = (c.vocab_draft + tn - 1) / tn;
+  const GemvShape sh = gemv_shape(c.dtype, EPI_LOGITS, B, c.vocab_draft, c.d_model);
+  const int tn = sh.rows_per_wave;
+  const int nblk = sh.waves;
   GemvArgs g{};
   g.max_rows = B;
   g.xin = W.x;
@@ -688,7 +686,7 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
   gt.y = W.s;
   gt.ldy = c.d_model;
   launch_gemv(c.dtype, SRC_TAPS, EPI_STORE, gt, h->stream);
-  run_body(h, ing, W.cu, B, W.s, true, pick_split(h, B, ctx_max));
+  run_body(h, ing, W.cu, B, W.s, true, pick_split(h, B, ctx_max), max_new);
 
   // ---- K autoregressive draft steps ---------------------------------------------------------
   float* logits = a->draft_logits ? a->draft_logits : W.logits;
@@ -699,7 +697,7 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
     RowMeta ar{nullptr, W.ar_pos, W.ar_tok, nullptr, B};
     const int split = pick_split(h, B, ctx_max);
     for (int k = 1; k < K; ++k) {
-      run_body(h, ar, nullptr, B, W.gfb, true, split);
+      run_body(h, ar, nullptr, B, W.gfb, true, split, 1);
       run_head(h, B, k, K, nullptr, a->temperature, u, logits, ld_b, a->draft_tokens);
     }
   }

@@ -23,41 +23,34 @@ namespace osp {
 
 constexpr int kVThreads = 256;
 
-OSP_DEV void block_max_argmax(float& m, int& am, float* sm, int* si) {
-  const int tid = threadIdx.x;
-  sm[tid] = m;
-  si[tid] = am;
-  __syncthreads();
-  for (int s = kVThreads / 2; s > 0; s >>= 1) {
-    if (tid < s) {
-      const float o = sm[tid + s];
-      const int oi = si[tid + s];
-      if (o > sm[tid] || (o == sm[tid] && oi < si[tid])) { sm[tid] = o; si[tid] = oi; }
-    }
-    __syncthreads();
-  }
-  m = sm[0];
-  am = si[0];
-  __syncthreads();
-}
+constexpr int kVPer = 16;   // elements per thread of a 4096-element chunk
 
-OSP_DEV double block_sum(double v, double* sm) {
-  const int tid = threadIdx.x;
-  sm[tid] = v;
+// Block-wide (max, lowest index) and float64 sum; results broadcast to every thread.
+OSP_DEV void block_stats(float& m, int& am, double& s, float* sm, int* si, double* sd) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const float wm = wave_max(m);
+  const int wi = wave_min_i((m == wm && m > -INFINITY) ? am : 0x7fffffff);
+  const double ws = wave_sum_d(s);
+  if (lane == 0) { sm[wave] = wm; si[wave] = wi; sd[wave] = ws; }
   __syncthreads();
-  for (int s = kVThreads / 2; s > 0; s >>= 1) {
-    if (tid < s) sm[tid] += sm[tid + s];
-    __syncthreads();
+  float gm = -INFINITY;
+  int gi = 0x7fffffff;
+  double gs = 0.0;
+  for (int w = 0; w < kVThreads / 64; ++w) {
+    if (sm[w] > gm) { gm = sm[w]; gi = si[w]; }
+    else if (sm[w] == gm && si[w] < gi) gi = si[w];
+    gs += sd[w];
   }
-  const double r = sm[0];
   __syncthreads();
-  return r;
+  m = gm;
+  am = gi;
+  s = gs;
 }
 
 __global__ void __launch_bounds__(kVThreads) k_vstats(VerifyArgs a) {
-  __shared__ float sm[kVThreads];
-  __shared__ int si[kVThreads];
-  __shared__ double sd[kVThreads];
+  __shared__ float sm[4];
+  __shared__ int si[4];
+  __shared__ double sd[4];
   const int b = blockIdx.x, j = blockIdx.y;
   const int tid = threadIdx.x;
   const int nt = (a.K + 1) * a.nchunk_t;
@@ -76,18 +69,29 @@ __global__ void __launch_bounds__(kVThreads) k_vstats(VerifyArgs a) {
     V = a.V_d;
   }
   const int i0 = c * a.chunk, i1 = min(V, i0 + a.chunk);
+  float v[kVPer];
+#pragma unroll
+  for (int q = 0; q < kVPer; ++q) {
+    const int i = i0 + tid + q * kVThreads;
+    v[q] = i < i1 ? row[i] : -INFINITY;
+  }
   float m = -INFINITY;
   int am = 0x7fffffff;
-  for (int i = i0 + tid; i < i1; i += kVThreads) {
-    const float v = row[i];
-    if (v > m) { m = v; am = i; }
-  }
-  block_max_argmax(m, am, sm, si);
+#pragma unroll
+  for (int q = 0; q < kVPer; ++q)
+    if (v[q] > m) { m = v[q]; am = i0 + tid + q * kVThreads; }
+  double dummy = 0.0;
+  block_stats(m, am, dummy, sm, si, sd);
   const float T = a.temp[b];
   double se = 0.0;   // float64 sums: exactness of the 10^5-entry CDFs that follow
-  if (T > 0.f && m > -INFINITY)
-    for (int i = i0 + tid; i < i1; i += kVThreads) se += (double)__expf((row[i] - m) / T);
-  se = block_sum(se, sd);
+  if (T > 0.f && m > -INFINITY) {
+#pragma unroll
+    for (int q = 0; q < kVPer; ++q)
+      if (v[q] > -INFINITY) se += (double)__expf((v[q] - m) / T);
+  }
+  int am2 = am;
+  float m2 = m;
+  block_stats(m2, am2, se, sm, si, sd);
   if (tid == 0) {
     float* p = a.part + ((long)b * gridDim.y + j) * 4;
     p[0] = m;
@@ -120,65 +124,73 @@ OSP_DEV void merge_row(const float* p, int n, float T, float& M, double& S, int&
   S = wave_sum_d(s);
 }
 
-__global__ void __launch_bounds__(64) k_vaccept(VerifyArgs a) {
+// One block per sequence: all row statistics are merged in parallel (one
+// wavefront per row), then thread k decides draft k, and the accepted length is
+// the first rejection.
+__global__ void __launch_bounds__(kVThreads) k_vaccept(VerifyArgs a) {
+  __shared__ float s_M[2 * 64 + 1];
+  __shared__ double s_S[2 * 64 + 1];
+  __shared__ int s_am[2 * 64 + 1];
+  __shared__ int s_ok[64];
   const int b = blockIdx.x;
-  const bool lead = threadIdx.x == 0;
-  const int nt = (a.K + 1) * a.nchunk_t;
-  const int nj = nt + a.K * a.nchunk_d;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int K = a.K;
+  const int nt = (K + 1) * a.nchunk_t;
+  const int nj = nt + K * a.nchunk_d;
   const float* part = a.part + (long)b * nj * 4;
   const float T = a.temp[b];
+  const int nrows = (K + 1) + (T > 0.f ? K : 0);
+  for (int q = wave; q < nrows; q += kVThreads / 64) {
+    float M;
+    double S;
+    int am;
+    if (q <= K) merge_row(part + (long)q * a.nchunk_t * 4, a.nchunk_t, T, M, S, am);
+    else merge_row(part + ((long)nt + (long)(q - K - 1) * a.nchunk_d) * 4, a.nchunk_d, T, M, S, am);
+    if (lane == 0) { s_M[q] = M; s_S[q] = S; s_am[q] = am; }
+  }
+  __syncthreads();
   const int32_t* dr = a.drafts + (long)b * a.ld_drafts;
-  int acc = 0;
-  for (; acc < a.K; ++acc) {
-    const int k = acc;
-    float Mt, Md;
-    double St, Sd;
-    int at, ad;
-    merge_row(part + (long)k * a.nchunk_t * 4, a.nchunk_t, T, Mt, St, at);
-    int d = dr[k];
-    if (d < 0 || d >= a.V_T) { if (lead) atomicOr(a.err, 1u << 4); break; }
-    bool ok;
-    if (T <= 0.f) {
-      ok = (d == at);
+  if (tid < K) {
+    const int k = tid;
+    const int d = dr[k];
+    int ok = 0;
+    if (d < 0 || d >= a.V_T) {
+      atomicOr(a.err, 1u << 4);
+    } else if (T <= 0.f) {
+      ok = d == s_am[k];
     } else {
-      merge_row(part + ((long)nt + (long)k * a.nchunk_d) * 4, a.nchunk_d, T, Md, Sd, ad);
-      const float* tl = a.target + ((long)b * (a.K + 1) + k) * a.V_T;
-      const double pd = (double)__expf((tl[d] - Mt) / T) / St;
+      const float* tl = a.target + ((long)b * (K + 1) + k) * a.V_T;
       const int s = a.t2d[d];
+      const float tv = tl[d];
       double qd = 0.0;
       if (s >= 0) {
-        const float* dl = a.draft + ((long)b * a.ld_draft_b + k) * a.V_d;
-        const float ls = dl[s];
-        qd = ls > -INFINITY ? (double)__expf((ls - Md) / T) / Sd : 0.0;
+        const float ls = a.draft[((long)b * a.ld_draft_b + k) * a.V_d + s];
+        if (ls > -INFINITY) qd = (double)__expf((ls - s_M[K + 1 + k]) / T) / s_S[K + 1 + k];
       }
+      const double pd = (double)__expf((tv - s_M[k]) / T) / s_S[k];
       const double r = qd > 0.0 ? fmin(1.0, pd / qd) : (pd > 0.0 ? 1.0 : 0.0);
-      ok = (double)a.u_acc[(long)b * a.K + k] < r;
+      ok = (double)a.u_acc[(long)b * K + k] < r;
     }
-    if (!ok) break;
+    s_ok[k] = ok;
   }
-  const int A = acc;
-  if (lead) for (int k = 0; k < a.K; ++k) {
-    a.accept_mask[(long)b * a.K + k] = k < A ? 1 : 0;
-    a.out_tokens[(long)b * (a.K + 1) + k] = k < A ? dr[k] : -1;
+  __syncthreads();
+  int A = 0;
+  while (A < K && s_ok[A]) ++A;
+  if (tid < K) {
+    a.accept_mask[(long)b * K + tid] = tid < A ? 1 : 0;
+    a.out_tokens[(long)b * (K + 1) + tid] = tid < A ? dr[tid] : -1;
   }
-  if (lead) {
-    a.out_tokens[(long)b * (a.K + 1) + a.K] = -1;
+  if (tid == 0) {
+    a.out_tokens[(long)b * (K + 1) + K] = -1;
     a.accept_len[b] = A;
-  }
-  // statistics of row A for the residual pass
-  float Mt, Md = 0.f;
-  double St, Sd = 1.0;
-  int at, ad = -1;
-  merge_row(part + (long)A * a.nchunk_t * 4, a.nchunk_t, T, Mt, St, at);
-  if (A < a.K && T > 0.f)
-    merge_row(part + ((long)nt + (long)A * a.nchunk_d) * 4, a.nchunk_d, T, Md, Sd, ad);
-  if (lead) {
+    // statistics of row A for the residual pass
     a.vstate[b * 4 + 0] = A;
-    a.vstate[b * 4 + 1] = at;
-    a.vstat[b * 4 + 0] = Mt;
-    a.vstat[b * 4 + 1] = St;
-    a.vstat[b * 4 + 2] = Md;
-    a.vstat[b * 4 + 3] = Sd;
+    a.vstate[b * 4 + 1] = s_am[A];
+    a.vstat[b * 4 + 0] = s_M[A];
+    a.vstat[b * 4 + 1] = s_S[A];
+    const bool dq = A < K && T > 0.f;
+    a.vstat[b * 4 + 2] = dq ? s_M[K + 1 + A] : 0.0;
+    a.vstat[b * 4 + 3] = dq ? s_S[K + 1 + A] : 1.0;
   }
 }
 
@@ -202,6 +214,28 @@ struct ResidRow {
     }
     w = fmax(p - q, 0.0);
   }
+  // Residual weights (which = 0) or target probabilities (which = 1) of the kVPer
+  // ids i0 + q*stride, q < kVPer (0 past V_T); all loads of a phase are issued together.
+  OSP_DEV void eval_many(int i0, int stride, int V, int which, double* out) const {
+    float tv[kVPer];
+    int sidx[kVPer];
+#pragma unroll
+    for (int q = 0; q < kVPer; ++q) {
+      const int v = i0 + q * stride;
+      const bool in = v < V;
+      tv[q] = in ? tl[v] : -INFINITY;
+      sidx[q] = (in && dl && !which) ? t2d[v] : -1;
+    }
+    float dv[kVPer];
+#pragma unroll
+    for (int q = 0; q < kVPer; ++q) dv[q] = sidx[q] >= 0 ? dl[sidx[q]] : -INFINITY;
+#pragma unroll
+    for (int q = 0; q < kVPer; ++q) {
+      const double p = tv[q] > -INFINITY ? (double)__expf((tv[q] - Mt) / T) * iSt : 0.0;
+      const double qq = dv[q] > -INFINITY ? (double)__expf((dv[q] - Md) / T) * iSd : 0.0;
+      out[q] = which ? p : fmax(p - qq, 0.0);
+    }
+  }
 };
 
 OSP_DEV ResidRow resid_row(const VerifyArgs& a, int b) {
@@ -223,12 +257,15 @@ __global__ void __launch_bounds__(kVThreads) k_vresid(VerifyArgs a) {
   const int b = blockIdx.x, c = blockIdx.y;
   if (!(a.temp[b] > 0.f)) return;
   const ResidRow rr = resid_row(a, b);
-  const int i0 = c * a.chunk, i1 = min(a.V_T, i0 + a.chunk);
-  // thread t owns a contiguous run of the chunk (the same split as the final scan)
-  const int per = (a.chunk + kVThreads - 1) / kVThreads;
-  const int t0 = min(i1, i0 + (int)threadIdx.x * per), t1 = min(i1, t0 + per);
+  // thread t owns the contiguous run [i0 + 16 t, i0 + 16 t + 16) (the same split as the final scan)
+  const int i0 = c * a.chunk + threadIdx.x * kVPer;
+  const int i1 = min(a.V_T, c * a.chunk + a.chunk);
+  double w[kVPer], p[kVPer];
+  rr.eval_many(i0, 1, i1, 0, w);
+  rr.eval_many(i0, 1, i1, 1, p);
   double sw = 0.0, sp = 0.0;
-  for (int v = t0; v < t1; ++v) { double w, p; rr.eval(v, w, p); sw += w; sp += p; }
+#pragma unroll
+  for (int q = 0; q < kVPer; ++q) { sw += w[q]; sp += p[q]; }
   // fixed-order block sums in float64
   double incl, tw, tp;
   block_scan<kVThreads, double>(sw, sm, incl, tw);
@@ -243,6 +280,7 @@ __global__ void __launch_bounds__(kVThreads) k_vfinal(VerifyArgs a) {
   __shared__ double sm[4];
   __shared__ int s_chunk, s_tok;
   __shared__ double s_before, s_target;
+  __shared__ int s_wlast[kVThreads / 64];
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int A = a.vstate[b * 4 + 0];
   const float T = a.temp[b];
@@ -298,33 +336,43 @@ __global__ void __launch_bounds__(kVThreads) k_vfinal(VerifyArgs a) {
     }
     __syncthreads();
     const int ch = s_chunk >> 1, which = s_chunk & 1;
-    const int i0 = ch * a.chunk, i1 = min(a.V_T, i0 + a.chunk);
-    const int per = (a.chunk + kVThreads - 1) / kVThreads;
-    const int t0 = min(i1, i0 + tid * per), t1 = min(i1, t0 + per);
+    const int c0 = ch * a.chunk;
+    const int i1 = min(a.V_T, c0 + a.chunk);
+    const int t0 = c0 + tid * kVPer;
+    double x[kVPer];
+    rr.eval_many(t0, 1, i1, which, x);
     double loc = 0.0;
-    for (int v = t0; v < t1; ++v) { double w, p; rr.eval(v, w, p); loc += which ? p : w; }
+#pragma unroll
+    for (int q = 0; q < kVPer; ++q) loc += x[q];
     double incl_l, tot_l;
     const double excl_l = block_scan<kVThreads, double>(loc, sm, incl_l, tot_l);
     const double target = s_target;
     const double excl = s_before + excl_l;
-    if (t0 < t1 && excl <= target && s_before + incl_l > target) {
+    if (excl <= target && s_before + incl_l > target) {
       double run = excl;
-      for (int v = t0; v < t1; ++v) {
-        double w, p;
-        rr.eval(v, w, p);
-        const double x = which ? p : w;
-        if (x > 0.0 && run + x > target) { s_tok = v; break; }
-        run += x;
+      int hit = -1;
+#pragma unroll
+      for (int q = 0; q < kVPer; ++q) {
+        if (hit < 0 && t0 + q < i1 && x[q] > 0.0) {
+          if (run + x[q] > target) hit = q; else run += x[q];
+        }
       }
+      if (hit >= 0) s_tok = t0 + hit;
     }
     __syncthreads();
-    if (tid == 0 && s_tok < 0) {       // rounding: take the last positive id of the chunk
-      for (int v = i1 - 1; v >= i0; --v) {
-        double w, p;
-        rr.eval(v, w, p);
-        if ((which ? p : w) > 0.0) { s_tok = v; break; }
+    if (s_tok < 0) {     // rounding: the last positive id of the chunk
+      int last = -1;
+#pragma unroll
+      for (int q = 0; q < kVPer; ++q)
+        if (t0 + q < i1 && x[q] > 0.0) last = t0 + q;
+      const int wl = wave_max_i(last);
+      if (lane == 0) s_wlast[wave] = wl;
+      __syncthreads();
+      if (tid == 0) {
+        int best = -1;
+        for (int w = 0; w < kVThreads / 64; ++w) best = max(best, s_wlast[w]);
+        s_tok = best >= 0 ? best : a.vstate[b * 4 + 1];
       }
-      if (s_tok < 0) s_tok = a.vstate[b * 4 + 1];
     }
     __syncthreads();
     tok = s_tok;
@@ -343,7 +391,7 @@ __global__ void __launch_bounds__(kVThreads) k_vfinal(VerifyArgs a) {
 void launch_verify(const VerifyArgs& a, hipStream_t st) {
   const int nj = (a.K + 1) * a.nchunk_t + a.K * a.nchunk_d;
   hipLaunchKernelGGL(k_vstats, dim3(a.B, nj), dim3(kVThreads), 0, st, a);
-  hipLaunchKernelGGL(k_vaccept, dim3(a.B), dim3(64), 0, st, a);
+  hipLaunchKernelGGL(k_vaccept, dim3(a.B), dim3(kVThreads), 0, st, a);
   hipLaunchKernelGGL(k_vresid, dim3(a.B, a.nchunk_t), dim3(kVThreads), 0, st, a);
   hipLaunchKernelGGL(k_vfinal, dim3(a.B), dim3(kVThreads), 0, st, a);
 }
