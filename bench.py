@@ -41,7 +41,23 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="first copy a buffer of this many MiB device-to-device three times "
+                         "(a reference for HBM traffic counters)")
     return ap.parse_args()
+
+
+def copy_calibration(mib: int) -> None:
+    """A plain device-to-device copy of known size: under rocprofv3 --pmc FETCH_SIZE /
+    WRITE_SIZE its counters give the scale between counter units and bytes."""
+    import torch
+    n = mib * (1 << 20)
+    src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 def lm_head_bytes(w, rows: int) -> int:
@@ -60,6 +76,20 @@ def step_bytes(w, ctx_mean: float) -> dict:
     lm = w.vocab_draft * d * el
     kv = w.batch * ctx_mean * L * 2 * w.n_kv_heads * hd * el
     return dict(body=body, lm=lm, kv=kv, total=body + lm + kv)
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per LM-head launch from the committed rocprofv3 --pmc summary, or None
+    when there is none for this workload or the kernel source changed since."""
+    import hashlib
+    try:
+        t = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))[workload]
+        sha = hashlib.sha256(open(os.path.join(ROOT, t["source"]), "rb").read()).hexdigest()
+    except (OSError, KeyError, ValueError):
+        return None
+    if not sha.startswith(t["sha256_prefix"]):
+        return None
+    return int(t["fetch_bytes"] + t["write_bytes"])
 
 
 def run_gpu(args):
@@ -172,6 +202,8 @@ def main():
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}), flush=True)
         sys.exit(2)
+    if args.calibrate_copy_mib > 0:
+        copy_calibration(args.calibrate_copy_mib)
     w, r = run_gpu(args)
     K = args.steps
     ms_per_step = r["seconds"] * 1e3 / K
@@ -210,7 +242,8 @@ def main():
         line["roofline"] = {"bound": "hbm", "kernel": "LM head (final RMSNorm + vocabulary GEMV "
                             "+ masked logits + softmax block statistics)",
                             "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                            "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                            "frac": round(ach / HBM_PEAK_GBS, 4),
+                            "traffic": measured_traffic(args.workload),
                             "bytes_per_launch": bytes_launch, "us_per_launch": round(lm_us, 3),
                             "launches": lm_n}
         line["ar_step_algorithmic_bytes"] = int(sb["total"])
