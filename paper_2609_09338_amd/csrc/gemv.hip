@@ -1,4 +1,5 @@
 // Dispatch of the weight-streaming GEMV kinds (kernel in gemv_kernel.h).
+#include "gemm_mfma.h"
 #include "gemv_kernel.h"
 
 namespace osp {
@@ -18,6 +19,12 @@ void launch_gemv(int wdtype, SrcKind src, EpiKind epi, const GemvArgs& a, hipStr
 }
 
 GemvShape gemv_shape(int wdtype, EpiKind epi, int rows, int N, int Kd) {
+  if (gemm_use_mfma(wdtype, rows)) {
+    GemvShape s;
+    s.rows_per_wave = gemm_mfma_rows_per_block(epi);
+    s.waves = (N + s.rows_per_wave - 1) / s.rows_per_wave;
+    return s;
+  }
   const GemvPlan p = gemv_plan(wdtype, epi, rows, N, Kd);
   GemvShape s;
   s.rows_per_wave = p.rpw;

@@ -66,8 +66,10 @@ struct GemvArgs {
   long ld_logits;           // stride between rows of y for logits
   float* part;              // [rows][nblk][4]: max, sumexp, argmax, unused
   int nblk;
+  float* split_buf;         // matrix-core K-split partials [kMaxKSplit][max_rows][2 N]
   uint32_t* err;
 };
+constexpr int kMaxKSplit = 16;
 
 void launch_gemv(int wdtype, SrcKind src, EpiKind epi, const GemvArgs& a, hipStream_t st);
 // Partition of the N weight rows of a launch: each wavefront owns rows_per_wave

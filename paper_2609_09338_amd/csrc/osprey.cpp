@@ -69,6 +69,7 @@ struct Ws {
   int32_t *ar_pos, *ar_tok;
   float *x, *s, *gfb, *qkv, *o, *h;
   float* attn_part;
+  float* split;
   float* logits;
   float* lm_part;
   int32_t* drafts;
@@ -137,6 +138,10 @@ size_t plan(const osprey_config& c, char* base, Ws* w) {
   W.o = (float*)take(4L * D.Rmax * nq * hd);
   W.h = (float*)take(4L * D.Rmax * c.d_ffn);
   W.attn_part = (float*)take(4L * D.Rmax * nq * kMaxSplit * (hd + 2));
+  {
+    const long nmax = std::max<long>(std::max<long>(D.qkv_rows, 2L * c.d_ffn), d);
+    W.split = (float*)take(4L * kMaxKSplit * D.Rmax * nmax);
+  }
   W.logits = (float*)take(4L * D.B * D.Km * c.vocab_draft);
   W.lm_part = (float*)take(16L * D.B * D.lm_nblk_max);
   W.drafts = (int32_t*)take(4L * D.B * D.Km);
@@ -273,6 +278,7 @@ void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, c
     g.N = qkv_w;
     g.y = W.qkv;
     g.ldy = qkv_w;
+    g.split_buf = W.split;
     int t = h->t_begin(4);
     launch_gemv(c.dtype, SRC_QKV, EPI_STORE, g, h->stream);
     h->t_end(t);
@@ -322,6 +328,7 @@ void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, c
     go.N = d;
     go.y = W.x;
     go.ldy = d;
+    go.split_buf = W.split;
     launch_gemv(c.dtype, SRC_PLAIN, EPI_RESID, go, h->stream);
     // post-attention RMSNorm + gate/up + SwiGLU
     GemvArgs gu{};
@@ -338,6 +345,7 @@ void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, c
     gu.N = c.d_ffn;
     gu.y = W.h;
     gu.ldy = c.d_ffn;
+    gu.split_buf = W.split;
     launch_gemv(c.dtype, SRC_NORM, EPI_SWIGLU, gu, h->stream);
     // down projection + residual
     GemvArgs gd{};
@@ -350,6 +358,7 @@ void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, c
     gd.N = d;
     gd.y = W.x;
     gd.ldy = d;
+    gd.split_buf = W.split;
     launch_gemv(c.dtype, SRC_PLAIN, EPI_RESID, gd, h->stream);
   }
 }
@@ -685,6 +694,7 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
   gt.N = c.d_model;
   gt.y = W.s;
   gt.ldy = c.d_model;
+  gt.split_buf = W.split;
   launch_gemv(c.dtype, SRC_TAPS, EPI_STORE, gt, h->stream);
   run_body(h, ing, W.cu, B, W.s, true, pick_split(h, B, ctx_max), max_new);
 

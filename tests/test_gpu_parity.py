@@ -234,3 +234,17 @@ def test_runs_are_deterministic_and_page_order_free():
     for a, b in zip(outs[0], outs[2]):
         for x, y in zip(a, b):
             assert np.array_equal(x, y)
+
+
+# ----------------------------------------------------------------------------------------
+# full-size workloads, sampled sequences (the GPU runs the whole batch)
+# ----------------------------------------------------------------------------------------
+@pytest.mark.parametrize("name,seqs,iters", [("c2", [0], 2), ("c3", [7], 2), ("c4", [31], 1),
+                                             ("c5", [62, 63], 2)])
+def test_full_size_sampled_sequences_match_oracle(name, seqs, iters):
+    """Benchmark-size shapes in the launch configuration the benchmark uses; the oracle
+    follows the sampled sequences one by one (sequences of a batch are independent)."""
+    _require_gpu()
+    w = synth.get(name)
+    stats = _run_parity(w, iters, seqs, 2e-2)
+    assert stats["compared"] >= len(seqs)
