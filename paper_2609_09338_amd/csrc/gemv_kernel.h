@@ -124,8 +124,15 @@ OSP_DEV float row_inv_rms(const GemvArgs& a, int rr, int lane) {
   return 1.0f / sqrtf(ss / (float)d + a.eps);
 }
 
-template <typename TW, int SRC, int EPI, int RB, int NW, int XV>
-__global__ void __launch_bounds__(kGemvThreads) k_gemv(GemvArgs a, int rows_per_wave) {
+// Register budget: the streaming kernels want >= 4 wavefronts per SIMD (<= 128 VGPRs)
+// so that enough loads are in flight; small-row variants fit that budget.
+template <int RB, int NW, int XV> struct GemvOcc {
+  static constexpr int value = (RB * NW * XV <= 8 && RB * XV <= 4) ? 4 : 1;
+};
+
+template <typename TW, int SRC, int EPI, int RB, int NW, int XV, bool CACHED>
+__global__ void __launch_bounds__(kGemvThreads, (GemvOcc<RB, NW, XV>::value))
+k_gemv(GemvArgs a, int rows_per_wave) {
   constexpr int VEC = Vec<TW>::N;
   constexpr int NWV = (EPI == EPI_SWIGLU) ? 2 * NW : NW;
   constexpr int V = NWV * RB;
@@ -143,14 +150,14 @@ __global__ void __launch_bounds__(kGemvThreads) k_gemv(GemvArgs a, int rows_per_
   const TW* __restrict__ w0 = reinterpret_cast<const TW*>(a.w0);
   const TW* __restrict__ w1 = reinterpret_cast<const TW*>(a.w1);
   const int nvec = a.Kd / VEC;                 // 16-byte vectors per weight row
-  const bool cached = nvec <= OSP_WAVE * XV;   // the whole input row fits in registers
+  constexpr bool cached = CACHED;              // the whole input row fits in registers
 
   for (int r0 = 0; r0 < rows; r0 += RB) {
     float xc[RB][XV][VEC];                     // this lane's input values (cached mode)
     float inv_rms[RB];
 #pragma unroll
     for (int r = 0; r < RB; ++r) inv_rms[r] = 1.f;
-    if (cached) {
+    if constexpr (cached) {
 #pragma unroll
       for (int r = 0; r < RB; ++r) {
         bool isn[XV];
@@ -231,7 +238,7 @@ __global__ void __launch_bounds__(kGemvThreads) k_gemv(GemvArgs a, int rows_per_
               wr[i][u].zero();
           }
         }
-        if (!cached) {
+        if constexpr (!cached) {
 #pragma unroll
           for (int r = 0; r < RB; ++r)
 #pragma unroll
@@ -318,8 +325,9 @@ __global__ void __launch_bounds__(kGemvThreads) k_gemv(GemvArgs a, int rows_per_
 // ---------------------------------------------------------------------------------------
 // Launch shape.  RB rows per pass in {1, 2, 4, 8}; XV = 16-byte vectors per lane and
 // row in one step ({1, 2, 4, 8}, RB * XV <= 8 so the cached input is <= 64 values);
-// NW weight rows per step with NW * XV * RB <= 16 vectors in flight (SwiGLU counts
-// gate and up); NW shrinks until the grid has enough wavefronts.
+// NW weight rows per step with NW * XV * RB <= 8 vectors in flight per lane (SwiGLU
+// counts gate and up) so that 4 wavefronts fit per SIMD; NW shrinks further until
+// the grid has enough wavefronts.
 struct GemvPlan {
   int rb, xv, nw, rpw, waves;
 };
@@ -334,7 +342,7 @@ inline GemvPlan gemv_plan(int wdtype, EpiKind epi, int rows, int N, int Kd) {
   p.xv = xv;
   const int f = epi == EPI_SWIGLU ? 2 : 1;
   int nw = 8;
-  while (nw > 1 && nw * xv * p.rb * f > 16) nw /= 2;
+  while (nw > 1 && nw * xv * p.rb * f > 8) nw /= 2;
   const int min_waves = epi == EPI_LOGITS ? 1024 : 2048;
   while (nw > 1 && (N + nw - 1) / nw < min_waves) nw /= 2;
   p.nw = nw;
@@ -349,16 +357,21 @@ template <typename TW, int SRC, int EPI, int RB, int NW, int XV>
 void launch_gemv_t(const GemvArgs& a, int rpw, hipStream_t st) {
   const int waves = (a.N + rpw - 1) / rpw;
   const int grid = (waves + kGemvWavesPerBlock - 1) / kGemvWavesPerBlock;
-  hipLaunchKernelGGL((k_gemv<TW, SRC, EPI, RB, NW, XV>), dim3(grid), dim3(kGemvThreads), 0, st, a,
-                     rpw);
+  const bool cached = a.Kd / Vec<TW>::N <= OSP_WAVE * XV;
+  if (cached)
+    hipLaunchKernelGGL((k_gemv<TW, SRC, EPI, RB, NW, XV, true>), dim3(grid), dim3(kGemvThreads), 0,
+                       st, a, rpw);
+  else
+    hipLaunchKernelGGL((k_gemv<TW, SRC, EPI, RB, NW, XV, false>), dim3(grid), dim3(kGemvThreads), 0,
+                       st, a, rpw);
 }
 
 template <typename TW, int SRC, int EPI, int RB, int XV>
 void launch_gemv_nw(const GemvPlan& p, const GemvArgs& a, hipStream_t st) {
   constexpr int F = (EPI == EPI_SWIGLU) ? 2 : 1;
-  if constexpr (8 * XV * RB * F <= 16) { if (p.nw == 8) return launch_gemv_t<TW, SRC, EPI, RB, 8, XV>(a, p.rpw, st); }
-  if constexpr (4 * XV * RB * F <= 16) { if (p.nw == 4) return launch_gemv_t<TW, SRC, EPI, RB, 4, XV>(a, p.rpw, st); }
-  if constexpr (2 * XV * RB * F <= 16) { if (p.nw == 2) return launch_gemv_t<TW, SRC, EPI, RB, 2, XV>(a, p.rpw, st); }
+  if constexpr (8 * XV * RB * F <= 8) { if (p.nw == 8) return launch_gemv_t<TW, SRC, EPI, RB, 8, XV>(a, p.rpw, st); }
+  if constexpr (4 * XV * RB * F <= 8) { if (p.nw == 4) return launch_gemv_t<TW, SRC, EPI, RB, 4, XV>(a, p.rpw, st); }
+  if constexpr (2 * XV * RB * F <= 8) { if (p.nw == 2) return launch_gemv_t<TW, SRC, EPI, RB, 2, XV>(a, p.rpw, st); }
   return launch_gemv_t<TW, SRC, EPI, RB, 1, XV>(a, p.rpw, st);
 }
 
