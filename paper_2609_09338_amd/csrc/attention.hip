@@ -104,6 +104,19 @@ struct Page {
   }
 };
 
+// Element `off` of the projections: the sum of the K-split partials (in split
+// order) on the matrix-core path, else the plain row.
+OSP_DEV float qkv_at(const AttnArgs& a, long off) {
+  if (a.qkv_ks <= 1) return a.qkv[off];
+  float v[kMaxKSplit];
+#pragma unroll
+  for (int k = 0; k < kMaxKSplit; ++k) v[k] = k < a.qkv_ks ? a.qkv[k * a.qkv_split + off] : 0.f;
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < kMaxKSplit; ++k) s += v[k];
+  return s;
+}
+
 template <typename TKV, int HD, int QV>
 __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   constexpr int DPL = HD / 16;         // head dims per lane (QV query vectors per pass)
@@ -156,10 +169,11 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
       if (pos < p_lo || pos >= p_hi) continue;
       const int blk = pos / a.kv_block;
       if (blk >= nblocks) { if (lane == 0) atomicOr(a.err, 1u << 3); continue; }
-      const float* src = a.qkv + (long)r * a.qkv_w + (a.nq + g) * HD;
-      const float* vs = a.qkv + (long)r * a.qkv_w + (a.nq + a.nkv + g) * HD;
-      float k1 = lane < HALF ? src[lane] : 0.f, k2 = lane < HALF ? src[lane + HALF] : 0.f;
-      const float v1 = lane < HALF ? vs[lane] : 0.f, v2 = lane < HALF ? vs[lane + HALF] : 0.f;
+      const long ko = (long)r * a.qkv_w + (a.nq + g) * HD;
+      const long vo = (long)r * a.qkv_w + (a.nq + a.nkv + g) * HD;
+      float k1 = lane < HALF ? qkv_at(a, ko + lane) : 0.f, k2 = lane < HALF ? qkv_at(a, ko + lane + HALF) : 0.f;
+      const float v1 = lane < HALF ? qkv_at(a, vo + lane) : 0.f;
+      const float v2 = lane < HALF ? qkv_at(a, vo + lane + HALF) : 0.f;
       norm_rope<TKV, HD>(a, a.k_norm, pos, lane, k1, k2);
       const long base = (long)bt[blk] * blk_elems + (long)(pos - blk * a.kv_block) * HD;
       if (lane < HALF) {
@@ -179,8 +193,8 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
       const int jj = j0 + j;
       if (jj < nvec) {
         const int r = r_beg + jj / G, h = g * G + jj % G;
-        const float* src = a.qkv + (long)r * a.qkv_w + h * HD;
-        float q1 = lane < HALF ? src[lane] : 0.f, q2 = lane < HALF ? src[lane + HALF] : 0.f;
+        const long qo = (long)r * a.qkv_w + h * HD;
+        float q1 = lane < HALF ? qkv_at(a, qo + lane) : 0.f, q2 = lane < HALF ? qkv_at(a, qo + lane + HALF) : 0.f;
         norm_rope<TKV, HD>(a, a.q_norm, a.rows.pos[r], lane, q1, q2);
         if (lane < HALF) { sm_q[j][lane] = q1 * a.scale; sm_q[j][lane + HALF] = q2 * a.scale; }
       } else if (lane < HALF) {
@@ -309,7 +323,7 @@ __global__ void __launch_bounds__(64) k_attn_combine(AttnArgs a) {
   const float f = (m > -INFINITY) ? __expf(m - M) : 0.f;
   const float L = wave_sum(lsum * f);
   const float inv = L > 0.f ? 1.0f / L : 0.f;
-  float* out = a.o + (long)r * a.nq * hd + h * hd;
+  const long obase = (long)r * a.nq * hd + h * hd;
   for (int e = lane; e < hd; e += 64) {
     float O = 0.f;
     for (int s0 = 0; s0 < ns; s0 += 8) {
@@ -319,7 +333,14 @@ __global__ void __launch_bounds__(64) k_attn_combine(AttnArgs a) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) O += v[i] * __shfl(f, (s0 + i) & 63, OSP_WAVE);
     }
-    out[e] = O * inv;
+    const float y = O * inv;
+    if (a.o_hi) {
+      const bf16_t yh = f32_to_bf16(y);
+      a.o_hi[obase + e] = yh;
+      a.o_lo[obase + e] = f32_to_bf16(y - bf16_to_f32(yh));
+    } else {
+      a.o[obase + e] = y;
+    }
   }
 }
 

@@ -14,10 +14,17 @@
 // close to fp32 (weights are exact bf16; accumulation is fp32).  Taps are bf16
 // already and use the hi part only.
 //
-// Block: 8 wavefronts sharing one input stage; wavefront w owns WT = 2 tiles of
-// 16 weight rows (SwiGLU: a gate tile and the matching up tile).  K is walked in
-// chunks of 256 columns: the weights of a chunk are requested before the input
-// chunk is staged, so both transfers overlap.
+// Inputs arrive prepared: the row kernels that precede each product (norms,
+// residual, SwiGLU, attention combine) write every input element once as bf16
+// hi / lo pairs, so a block only copies its input chunk into LDS.  The
+// expanded-QKV input [c ; RMSNorm(x)] of Eq. 2-3 is read from its two segments.
+//
+// Block: 4 wavefronts (8 for the LM head) sharing one staged input chunk of 256
+// columns.  K is split across blocks when N alone gives too few blocks; every
+// block writes its partial sums to [split][row][N] (SwiGLU: gate then up, 2 N
+// wide) and the row kernel that follows adds the splits in a fixed order.  The
+// LM head (never split) writes masked logits and one (max, sum exp((l - max)/T),
+// lowest argmax) record per block of consecutive rows.
 #pragma once
 
 #include "common.h"
@@ -43,57 +50,8 @@ template <int EPI> struct MmShape {
   static constexpr int ROWS = WAVES * NT * 16;            // output rows per block
 };
 
-OSP_DEV uint32_t pack_bf16x2(bf16_t lo, bf16_t hi) { return (uint32_t)lo | ((uint32_t)hi << 16); }
-
-// Input values X[rr][col .. col+8) (fp32) of the pass; the normalised segment is
-// scaled by inv_rms * gain.
-template <int SRC>
-OSP_DEV void mm_load_x8(const GemvArgs& a, int rr, int col, float inv_rms, float* out) {
-  if constexpr (SRC == SRC_PLAIN) {
-    const float* p = a.xin + (long)rr * a.ldx + col;
-    const float4 v0 = *reinterpret_cast<const float4*>(p);
-    const float4 v1 = *reinterpret_cast<const float4*>(p + 4);
-    out[0] = v0.x; out[1] = v0.y; out[2] = v0.z; out[3] = v0.w;
-    out[4] = v1.x; out[5] = v1.y; out[6] = v1.z; out[7] = v1.w;
-  } else if constexpr (SRC == SRC_TAPS) {
-    load_vec<bf16_t>(reinterpret_cast<const bf16_t*>(a.taps) + (long)a.tap_row[rr] * a.ldt + col, out);
-  } else {
-    int c = col;
-    if constexpr (SRC == SRC_QKV) {
-      if (col < a.d_norm) {
-        const int sr = a.s_gather ? a.s_gather[rr] : rr;
-        const float* p = a.s + (long)sr * a.lds + col;
-        const float4 v0 = *reinterpret_cast<const float4*>(p);
-        const float4 v1 = *reinterpret_cast<const float4*>(p + 4);
-        out[0] = v0.x; out[1] = v0.y; out[2] = v0.z; out[3] = v0.w;
-        out[4] = v1.x; out[5] = v1.y; out[6] = v1.z; out[7] = v1.w;
-        return;
-      }
-      c = col - a.d_norm;
-    }
-    if (SRC == SRC_QKV && a.embed) {
-      int t = a.tok[rr];
-      t = min(max(t, 0), a.vocab_embed - 1);
-      load_vec<bf16_t>(reinterpret_cast<const bf16_t*>(a.embed) + (long)t * a.d_norm + c, out);
-    } else {
-      const int xr = a.gather ? a.gather[rr] : rr;
-      const float* p = a.xin + (long)xr * a.ldx + c;
-      const float4 v0 = *reinterpret_cast<const float4*>(p);
-      const float4 v1 = *reinterpret_cast<const float4*>(p + 4);
-      out[0] = v0.x; out[1] = v0.y; out[2] = v0.z; out[3] = v0.w;
-      out[4] = v1.x; out[5] = v1.y; out[6] = v1.z; out[7] = v1.w;
-    }
-    float g[8];
-    load_vec<bf16_t>(reinterpret_cast<const bf16_t*>(a.gamma) + c, g);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) out[e] = out[e] * inv_rms * g[e];
-  }
-}
-
 template <int SRC, int EPI>
-__global__ void __launch_bounds__(MmShape<EPI>::THREADS) k_gemm_mfma(GemvArgs a, float* split_out,
-                                                                      int chunks_per_split) {
-  constexpr bool NORMED = (SRC == SRC_NORM || SRC == SRC_QKV);
+__global__ void __launch_bounds__(MmShape<EPI>::THREADS) k_gemm_mfma(GemvArgs a, int chunks_per_split) {
   constexpr bool EXACT_X = (SRC == SRC_TAPS);          // inputs already bf16: no lo part
   constexpr int kMmWaves = MmShape<EPI>::WAVES;
   constexpr int kMmThreads = MmShape<EPI>::THREADS;
@@ -101,10 +59,10 @@ __global__ void __launch_bounds__(MmShape<EPI>::THREADS) k_gemm_mfma(GemvArgs a,
   constexpr int NT = MmShape<EPI>::NT;
   __shared__ __attribute__((aligned(16))) bf16_t xs_hi[kMmRows * kMmPitch];
   __shared__ __attribute__((aligned(16))) bf16_t xs_lo[EXACT_X ? 8 : kMmRows * kMmPitch];
-  __shared__ float s_inv[kMmRows];
-  __shared__ float s_m[kMmWaves][kMmRows];
-  __shared__ float s_s[kMmWaves][kMmRows];
-  __shared__ int s_a[kMmWaves][kMmRows];
+  constexpr int SW = EPI == EPI_LOGITS ? kMmWaves : 1;
+  __shared__ float s_m[SW][kMmRows];
+  __shared__ float s_s[SW][kMmRows];
+  __shared__ int s_a[SW][kMmRows];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int rows = a.count ? min(*a.count, a.max_rows) : a.max_rows;
@@ -114,60 +72,18 @@ __global__ void __launch_bounds__(MmShape<EPI>::THREADS) k_gemm_mfma(GemvArgs a,
   const int nb0 = blockIdx.x * rows_per_block;          // first output row of the block
   const int nw0 = nb0 + wave * NT * 16;                 // first output row of this wavefront
   const int wrow = lane & 15, kg = lane >> 4;           // B operand: weight row, 8-column group
+  const int k_begin = blockIdx.y * chunks_per_split * kMmKc;
+  const int k_end = min(a.Kd, k_begin + chunks_per_split * kMmKc);
 
   for (int r0 = 0; r0 < rows; r0 += kMmRows) {
     const int rcount = min(kMmRows, rows - r0);
     const int mt_n = (rcount + 15) >> 4;                // M tiles in use
-    // ---- RMSNorm factors of the rows of this pass ------------------------------------
-    if constexpr (NORMED) {
-      for (int r = wave; r < rcount; r += kMmWaves) {
-        const int rr = r0 + r;
-        float ss = 0.f;
-        // sum of squares of the raw (un-normalised) segment
-        if (SRC == SRC_QKV && a.embed) {
-          int t = a.tok[rr];
-          t = min(max(t, 0), a.vocab_embed - 1);
-          const bf16_t* e = reinterpret_cast<const bf16_t*>(a.embed) + (long)t * a.d_norm;
-          for (int c = lane * 8; c < a.d_norm; c += OSP_WAVE * 8) {
-            float v[8];
-            load_vec<bf16_t>(e + c, v);
-#pragma unroll
-            for (int q = 0; q < 8; ++q) ss += v[q] * v[q];
-          }
-        } else {
-          const int xr = a.gather ? a.gather[rr] : rr;
-          const float* xp = a.xin + (long)xr * a.ldx;
-          for (int c = lane * 4; c < a.d_norm; c += OSP_WAVE * 4) {
-            const float4 v = *reinterpret_cast<const float4*>(xp + c);
-            ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-          }
-        }
-        ss = wave_sum(ss);
-        if (lane == 0) s_inv[r] = 1.0f / sqrtf(ss / (float)a.d_norm + a.eps);
-      }
-    }
-    // layer 0 of the expanded QKV: block 0 writes x = embed[token] for the residual
-    if constexpr (SRC == SRC_QKV) {
-      if (a.embed && a.x_out && blockIdx.x == 0 && blockIdx.y == 0) {
-        for (int i = tid; i < rcount * a.d_norm; i += kMmThreads) {
-          const int r = i / a.d_norm, c = i - r * a.d_norm;
-          int t = a.tok[r0 + r];
-          t = min(max(t, 0), a.vocab_embed - 1);
-          a.x_out[(long)(r0 + r) * a.ldx + c] =
-              load_f32(reinterpret_cast<const bf16_t*>(a.embed), (long)t * a.d_norm + c);
-        }
-      }
-    }
-    __syncthreads();
-
     mfma_f32x4 acc[4][kMmWT];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
       for (int wt = 0; wt < kMmWT; ++wt) acc[mt][wt] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int k_begin = blockIdx.y * chunks_per_split * kMmKc;
-    const int k_end = min(a.Kd, k_begin + chunks_per_split * kMmKc);
     for (int k0 = k_begin; k0 < k_end; k0 += kMmKc) {
       // ---- request this chunk's weights (8 K steps x kMmWT tiles) ----------------------
       uint4 wb[kMmWT][kMmKc / 32];
@@ -184,33 +100,28 @@ __global__ void __launch_bounds__(MmShape<EPI>::THREADS) k_gemm_mfma(GemvArgs a,
             wb[wt][t] = make_uint4(0u, 0u, 0u, 0u);
         }
       }
-      // ---- stage the input chunk as bf16 hi / lo ----------------------------------------
+      // ---- stage the input chunk (bf16 hi / lo, 16-byte copies) ---------------------------
       for (int i = tid; i < kMmRows * (kMmKc / 8); i += kMmThreads) {
         const int r = i / (kMmKc / 8), cv = i - r * (kMmKc / 8);
         const int col = k0 + cv * 8;
-        float v[8];
+        uint4 ph = make_uint4(0u, 0u, 0u, 0u), pl = ph;
         if (r < rcount && col < a.Kd) {
-          float inv = 1.f;
-          if constexpr (NORMED) inv = s_inv[r];
-          mm_load_x8<SRC>(a, r0 + r, col, inv, v);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) v[e] = 0.f;
+          const int rr = r0 + r;
+          if constexpr (SRC == SRC_TAPS) {
+            ph = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16_t*>(a.taps) +
+                                                 (long)a.tap_row[rr] * a.ldt + col);
+          } else if (col < a.seg) {
+            const long o = (long)rr * a.ld_xs + col;
+            ph = *reinterpret_cast<const uint4*>(a.xs_hi + o);
+            pl = *reinterpret_cast<const uint4*>(a.xs_lo + o);
+          } else {
+            const long o = (long)(a.gather ? a.gather[rr] : rr) * a.ld_xa + (col - a.seg);
+            ph = *reinterpret_cast<const uint4*>(a.xa_hi + o);
+            pl = *reinterpret_cast<const uint4*>(a.xa_lo + o);
+          }
         }
-        bf16_t hi[8], lo[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          hi[e] = f32_to_bf16(v[e]);
-          lo[e] = f32_to_bf16(v[e] - bf16_to_f32(hi[e]));
-        }
-        uint4 ph = make_uint4(pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3]),
-                              pack_bf16x2(hi[4], hi[5]), pack_bf16x2(hi[6], hi[7]));
         *reinterpret_cast<uint4*>(xs_hi + r * kMmPitch + cv * 8) = ph;
-        if constexpr (!EXACT_X) {
-          uint4 pl = make_uint4(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]),
-                                pack_bf16x2(lo[4], lo[5]), pack_bf16x2(lo[6], lo[7]));
-          *reinterpret_cast<uint4*>(xs_lo + r * kMmPitch + cv * 8) = pl;
-        }
+        if constexpr (!EXACT_X) *reinterpret_cast<uint4*>(xs_lo + r * kMmPitch + cv * 8) = pl;
       }
       __syncthreads();
       // ---- MFMAs --------------------------------------------------------------------------
@@ -310,8 +221,8 @@ __global__ void __launch_bounds__(MmShape<EPI>::THREADS) k_gemm_mfma(GemvArgs a,
         p[3] = 0.f;
       }
       __syncthreads();
-    } else if (split_out) {
-      // split K: this block's partial sums, [split][row][N] (SwiGLU: gate then up, 2N)
+    } else {
+      // partial sums of this K split: [split][row][N] (SwiGLU: gate then up, 2 N wide)
       const int W = (EPI == EPI_SWIGLU) ? 2 * a.N : a.N;
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) {
@@ -320,37 +231,11 @@ __global__ void __launch_bounds__(MmShape<EPI>::THREADS) k_gemm_mfma(GemvArgs a,
         for (int e = 0; e < 4; ++e) {
           const int m = mt * 16 + 4 * kg + e;
           if (m >= rcount) continue;
-          float* pr = split_out + ((long)blockIdx.y * a.max_rows + r0 + m) * W;
+          float* pr = a.split_buf + ((long)blockIdx.y * a.max_rows + r0 + m) * W;
 #pragma unroll
           for (int wt = 0; wt < kMmWT; ++wt) {
             const int n = (EPI == EPI_SWIGLU) ? nw0 + ncol : nw0 + wt * 16 + ncol;
             if (n < a.N) pr[(EPI == EPI_SWIGLU ? wt * a.N : 0) + n] = acc[mt][wt][e];
-          }
-        }
-      }
-    } else {
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
-        if (mt >= mt_n) continue;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int m = mt * 16 + 4 * kg + e;
-          if (m >= rcount) continue;
-          float* yr = a.y + (long)(r0 + m) * a.ldy;
-          if constexpr (EPI == EPI_SWIGLU) {
-            const int n = nw0 + ncol;
-            if (n < a.N) {
-              const float g = acc[mt][0][e], u = acc[mt][1][e];
-              yr[n] = g / (1.0f + __expf(-g)) * u;
-            }
-          } else {
-#pragma unroll
-            for (int wt = 0; wt < kMmWT; ++wt) {
-              const int n = nw0 + wt * 16 + ncol;
-              if (n < a.N) {
-                if constexpr (EPI == EPI_RESID) yr[n] += acc[mt][wt][e]; else yr[n] = acc[mt][wt][e];
-              }
-            }
           }
         }
       }
@@ -359,61 +244,35 @@ __global__ void __launch_bounds__(MmShape<EPI>::THREADS) k_gemm_mfma(GemvArgs a,
   }
 }
 
-// The matrix-core path serves passes of two or more rows of bf16 weights.
-inline bool gemm_use_mfma(int wdtype, int rows) { return wdtype == 1 && rows >= 2; }
-
 inline int gemm_mfma_rows_per_block(EpiKind epi) {
   return epi == EPI_LOGITS ? MmShape<EPI_LOGITS>::ROWS
                            : (epi == EPI_SWIGLU ? MmShape<EPI_SWIGLU>::ROWS : MmShape<EPI_STORE>::ROWS);
 }
 
-// K splits: enough blocks to cover the chip (about 2 per CU), never for logits.
-inline int gemm_mfma_splits(EpiKind epi, int N, int Kd) {
-  if (epi == EPI_LOGITS) return 1;
-  const int nb = (N + gemm_mfma_rows_per_block(epi) - 1) / gemm_mfma_rows_per_block(epi);
+// K splits: enough blocks to cover the chip (about 2 per CU); never for logits.
+// Returns the chunks per split; *ks receives the splits actually used.
+inline int gemm_mfma_split_plan(EpiKind epi, int N, int Kd, int* ks_out) {
   const int chunks = (Kd + kMmKc - 1) / kMmKc;
-  int ks = (512 + nb - 1) / nb;
-  ks = ks < 1 ? 1 : (ks > chunks ? chunks : ks);
-  return ks > kMaxKSplit ? kMaxKSplit : ks;
-}
-
-// Sum of the K-split partials in split order, then the kind's epilogue.
-template <int EPI>
-__global__ void __launch_bounds__(256) k_splitk_reduce(GemvArgs a, const float* split_out, int ks) {
-  const int rows = a.count ? min(*a.count, a.max_rows) : a.max_rows;
-  const long total = (long)rows * a.N;
-  const int W = (EPI == EPI_SWIGLU) ? 2 * a.N : a.N;
-  for (long i = blockIdx.x * 256L + threadIdx.x; i < total; i += (long)gridDim.x * 256) {
-    const int m = (int)(i / a.N), n = (int)(i - (long)m * a.N);
-    float s0 = 0.f, s1 = 0.f;
-    for (int k = 0; k < ks; ++k) {
-      const float* pr = split_out + ((long)k * a.max_rows + m) * W;
-      s0 += pr[n];
-      if constexpr (EPI == EPI_SWIGLU) s1 += pr[a.N + n];
-    }
-    float* yp = a.y + (long)m * a.ldy + n;
-    if constexpr (EPI == EPI_SWIGLU) *yp = s0 / (1.0f + __expf(-s0)) * s1;
-    else if constexpr (EPI == EPI_RESID) *yp += s0;
-    else *yp = s0;
+  int ks = 1;
+  if (epi != EPI_LOGITS) {
+    const int nb = (N + gemm_mfma_rows_per_block(epi) - 1) / gemm_mfma_rows_per_block(epi);
+    ks = (512 + nb - 1) / nb;
+    ks = ks < 1 ? 1 : (ks > chunks ? chunks : ks);
+    ks = ks > kMaxKSplit ? kMaxKSplit : ks;
   }
+  const int cps = (chunks + ks - 1) / ks;
+  *ks_out = (chunks + cps - 1) / cps;
+  return cps;
 }
 
 template <int SRC, int EPI>
-void launch_gemm_mfma_t(const GemvArgs& a, hipStream_t st) {
+int launch_gemm_mfma_t(const GemvArgs& a, hipStream_t st) {
   const int rpb = gemm_mfma_rows_per_block((EpiKind)EPI);
   const int nb = (a.N + rpb - 1) / rpb;
-  const int ks = gemm_mfma_splits((EpiKind)EPI, a.N, a.Kd);
-  const int chunks = (a.Kd + kMmKc - 1) / kMmKc;
-  const int cps = (chunks + ks - 1) / ks;
-  const int ks_used = (chunks + cps - 1) / cps;
-  float* split = ks_used > 1 ? a.split_buf : nullptr;
-  hipLaunchKernelGGL((k_gemm_mfma<SRC, EPI>), dim3(nb, ks_used), dim3(MmShape<EPI>::THREADS), 0, st,
-                     a, split, cps);
-  if (split) {
-    const long total = (long)a.max_rows * a.N;
-    const int grid = (int)((total + 255) / 256 < 2048 ? (total + 255) / 256 : 2048);
-    hipLaunchKernelGGL((k_splitk_reduce<EPI>), dim3(grid), dim3(256), 0, st, a, split, ks_used);
-  }
+  int ks = 1;
+  const int cps = gemm_mfma_split_plan((EpiKind)EPI, a.N, a.Kd, &ks);
+  hipLaunchKernelGGL((k_gemm_mfma<SRC, EPI>), dim3(nb, ks), dim3(MmShape<EPI>::THREADS), 0, st, a, cps);
+  return ks;
 }
 
 }  // namespace osp

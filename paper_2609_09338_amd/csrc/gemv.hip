@@ -1,5 +1,4 @@
 // Dispatch of the weight-streaming GEMV kinds (kernel in gemv_kernel.h).
-#include "gemm_mfma.h"
 #include "gemv_kernel.h"
 
 namespace osp {
@@ -21,7 +20,7 @@ void launch_gemv(int wdtype, SrcKind src, EpiKind epi, const GemvArgs& a, hipStr
 GemvShape gemv_shape(int wdtype, EpiKind epi, int rows, int N, int Kd) {
   if (gemm_use_mfma(wdtype, rows)) {
     GemvShape s;
-    s.rows_per_wave = gemm_mfma_rows_per_block(epi);
+    s.rows_per_wave = gemm_rows_per_block(epi);
     s.waves = (N + s.rows_per_wave - 1) / s.rows_per_wave;
     return s;
   }

@@ -1,14 +1,11 @@
-// Instantiations of the weight-streaming products for one input/epilogue kind
-// (one file per kind so that they compile in parallel): the wavefront GEMV for
-// one row or fp32 weights, the matrix-core GEMM for several rows of bf16 weights.
-#include "gemm_mfma.h"
+// Instantiations of the wavefront GEMV for one input/epilogue kind (one file per
+// kind so that they compile in parallel).
 #include "gemv_kernel.h"
 
 namespace osp {
 
 void launch_gemv_swiglu(int wdtype, const GemvArgs& a, hipStream_t st) {
-  if (gemm_use_mfma(wdtype, a.max_rows)) launch_gemm_mfma_t<SRC_NORM, EPI_SWIGLU>(a, st);
-  else launch_gemv_kind<SRC_NORM, EPI_SWIGLU>(wdtype, a, st);
+  launch_gemv_kind<SRC_NORM, EPI_SWIGLU>(wdtype, a, st);
 }
 
 }  // namespace osp

@@ -23,6 +23,8 @@ enum SrcKind {
   SRC_NORM = 1,   // X[r][c] = rmsnorm(xin[row(r)])[c] * gamma[c] (row(r) = gather[r] or r)
   SRC_QKV = 2,    // c < d: s[srow(r)][c]; else rmsnorm(x or embed[tok])[c-d] * gamma
   SRC_TAPS = 3,   // X[r][c] = taps[tap_row[r]*ldt + c] (weight dtype)
+  SRC_PREP = 4,   // matrix-core passes: X[r][c] prepared as bf16 hi + lo pairs,
+                  // c < seg from (xs_hi, xs_lo) row r, else (xa_hi, xa_lo) row gather[r] or r
 };
 enum EpiKind {
   EPI_STORE = 0,   // y[r][n] = acc
@@ -66,12 +68,56 @@ struct GemvArgs {
   long ld_logits;           // stride between rows of y for logits
   float* part;              // [rows][nblk][4]: max, sumexp, argmax, unused
   int nblk;
-  float* split_buf;         // matrix-core K-split partials [kMaxKSplit][max_rows][2 N]
+  float* split_buf;         // matrix-core K-split partials [split][max_rows][N] (SwiGLU: 2 N)
+  // SRC_PREP inputs (bf16 hi / lo pairs)
+  const uint16_t* xs_hi;
+  const uint16_t* xs_lo;
+  int ld_xs;
+  int seg;                  // columns [0, seg) come from xs, the rest from xa
+  const uint16_t* xa_hi;
+  const uint16_t* xa_lo;
+  int ld_xa;
   uint32_t* err;
 };
 constexpr int kMaxKSplit = 16;
 
 void launch_gemv(int wdtype, SrcKind src, EpiKind epi, const GemvArgs& a, hipStream_t st);
+
+// Matrix-core GEMM for passes of several rows of bf16 weights: src SRC_TAPS or
+// SRC_PREP; epi EPI_STORE or EPI_SWIGLU (K-split partial sums into split_buf, summed
+// by the row kernels below) or EPI_LOGITS.  Returns the number of K splits written.
+int launch_gemm(SrcKind src, EpiKind epi, const GemvArgs& a, hipStream_t st);
+// True when a pass of `rows` rows takes the matrix-core path.
+bool gemm_use_mfma(int wdtype, int rows);
+int gemm_rows_per_block(EpiKind epi);
+
+// Row kernels of the matrix-core path: one block per row.
+struct RowArgs {
+  int max_rows;
+  const int32_t* count;     // device row count (nullable: max_rows)
+  int W;                    // row width
+  const float* part;        // partial sums: split k, row r at part + (k * max_rows + r) * ldp
+  int ks;
+  int ldp;
+  float* x;                 // residual rows [max_rows][W]
+  const void* gamma;        // RMSNorm gain (bf16)
+  float eps;
+  uint16_t* out_hi;         // next product's input, bf16 hi / lo [max_rows][W]
+  uint16_t* out_lo;
+  // prologue of a pass (conditioning segment + embedding)
+  const float* s_src;       // conditioning rows (nullable: summed from part)
+  uint16_t* s_hi;
+  uint16_t* s_lo;
+  const void* embed;
+  const int32_t* tok;
+  int vocab_embed;
+};
+// s = sum of partials or s_src -> (s_hi, s_lo); x = embed[tok]; out = rmsnorm(x) * gamma.
+void launch_rows_prep(const RowArgs& a, hipStream_t st);
+// x += sum of partials; out = rmsnorm(x) * gamma.
+void launch_rows_resid_norm(const RowArgs& a, hipStream_t st);
+// out = silu(sum of gate partials) * sum of up partials (columns [0, W) and [W, 2 W)).
+void launch_rows_swiglu(const RowArgs& a, hipStream_t st);
 // Partition of the N weight rows of a launch: each wavefront owns rows_per_wave
 // consecutive rows; `waves` wavefronts carry rows (the logits epilogue writes
 // one statistics record per wavefront).
@@ -89,8 +135,10 @@ struct AttnArgs {
   const int32_t* bslot;     // [B] slot of sequence b
   int B;
   int rows_per_seq;         // host bound on the rows of one sequence in this pass
-  const float* qkv;         // [rows][qkv_w] raw projections
+  const float* qkv;         // [rows][qkv_w] raw projections (split 0 of qkv_ks partials)
   int qkv_w;
+  int qkv_ks;               // K-split partials to sum on load (1: plain rows)
+  long qkv_split;           // elements between splits
   const void* q_norm;
   const void* k_norm;
   int qk_norm;
@@ -109,6 +157,8 @@ struct AttnArgs {
   int n_split;
   float* part;              // [rows][nq][n_split][hd + 2]
   float* o;                 // [rows][nq*hd]
+  uint16_t* o_hi;           // matrix-core path: o as bf16 hi / lo pairs instead (nullable)
+  uint16_t* o_lo;
   uint32_t* err;
 };
 void launch_attention(int kvdtype, const AttnArgs& a, hipStream_t st);

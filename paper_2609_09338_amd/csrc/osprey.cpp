@@ -68,6 +68,7 @@ struct Ws {
   int32_t *ing_seq, *ing_pos, *ing_tok, *ing_tap, *n_rows, *cu, *last_row, *committed, *bslot;
   int32_t *ar_pos, *ar_tok;
   float *x, *s, *gfb, *qkv, *o, *h;
+  uint16_t *s_hi, *s_lo, *xa_hi, *xa_lo;   // matrix-core path inputs (bf16 hi / lo)
   float* attn_part;
   float* split;
   float* logits;
@@ -137,6 +138,13 @@ size_t plan(const osprey_config& c, char* base, Ws* w) {
   W.qkv = (float*)take(4L * D.Rmax * D.qkv_rows);
   W.o = (float*)take(4L * D.Rmax * nq * hd);
   W.h = (float*)take(4L * D.Rmax * c.d_ffn);
+  {
+    const long wa = std::max<long>(std::max<long>(d, nq * hd), c.d_ffn);
+    W.s_hi = (uint16_t*)take(2L * D.Rmax * d);
+    W.s_lo = (uint16_t*)take(2L * D.Rmax * d);
+    W.xa_hi = (uint16_t*)take(2L * D.Rmax * wa);
+    W.xa_lo = (uint16_t*)take(2L * D.Rmax * wa);
+  }
   W.attn_part = (float*)take(4L * D.Rmax * nq * kMaxSplit * (hd + 2));
   {
     const long nmax = std::max<long>(std::max<long>(D.qkv_rows, 2L * c.d_ffn), d);
@@ -363,6 +371,138 @@ void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, c
   }
 }
 
+// The same pass on the matrix-core path (bf16 weights, two or more rows).  Row
+// kernels close every product (split-K sums in fixed order, residual, norms,
+// SwiGLU) and write the next product's input as bf16 hi / lo pairs; the last one
+// leaves RMSNorm_final(x) for the LM head.  `s_src` holds the conditioning rows,
+// or is null when they are the tap projection's `ks_taps` partial sums.
+void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, const float* s_src,
+                 int ks_taps, int n_split, int rows_per_seq) {
+  const osprey_config& c = h->cfg;
+  const Ws& W = h->W;
+  const int d = c.d_model, hd = c.head_dim, nq = c.n_q_heads, nkv = c.n_kv_heads, F = c.d_ffn;
+  const int qkv_w = h->D.qkv_rows;
+  RowArgs ra{};
+  ra.max_rows = rows.max_rows;
+  ra.count = rows.count;
+  ra.part = W.split;
+  ra.x = W.x;
+  ra.eps = c.rms_eps;
+  ra.out_hi = W.xa_hi;
+  ra.out_lo = W.xa_lo;
+  {
+    RowArgs p = ra;
+    p.W = d;
+    p.ks = ks_taps;
+    p.ldp = d;
+    p.gamma = h->layers[0].in_norm;
+    p.s_src = s_src;
+    p.s_hi = W.s_hi;
+    p.s_lo = W.s_lo;
+    p.embed = h->w.embed;
+    p.tok = rows.tok;
+    p.vocab_embed = c.vocab_target;
+    launch_rows_prep(p, h->stream);
+  }
+  GemvArgs gb{};
+  gb.max_rows = rows.max_rows;
+  gb.count = rows.count;
+  gb.split_buf = W.split;
+  gb.xa_hi = W.xa_hi;
+  gb.xa_lo = W.xa_lo;
+  for (int l = 0; l < c.n_layers; ++l) {
+    const osprey_layer_weights& L = h->layers[l];
+    // expanded QKV over [s ; RMSNorm(x)] (Eq. 2-3)
+    GemvArgs g = gb;
+    g.xs_hi = W.s_hi;
+    g.xs_lo = W.s_lo;
+    g.ld_xs = d;
+    g.seg = d;
+    g.ld_xa = d;
+    g.Kd = 2 * d;
+    g.w0 = L.w_qkv;
+    g.N = qkv_w;
+    int t = h->t_begin(4);
+    const int ks_qkv = launch_gemm(SRC_PREP, EPI_STORE, g, h->stream);
+    h->t_end(t);
+    // QK-norm + RoPE + KV append, attention (sums the QKV splits), split combine
+    AttnArgs a{};
+    a.rows = rows;
+    a.cu = cu;
+    a.bslot = W.bslot;
+    a.B = B;
+    a.rows_per_seq = rows_per_seq;
+    a.qkv = W.split;
+    a.qkv_w = qkv_w;
+    a.qkv_ks = ks_qkv;
+    a.qkv_split = (long)rows.max_rows * qkv_w;
+    a.q_norm = L.q_norm;
+    a.k_norm = L.k_norm;
+    a.qk_norm = c.qk_norm;
+    a.eps = c.rms_eps;
+    a.rope_cos = W.rope_cos;
+    a.rope_sin = W.rope_sin;
+    a.max_seq = c.max_seq_len;
+    a.kv = h->kv;
+    a.layer = l;
+    a.n_layers = c.n_layers;
+    a.block_table = W.block_table;
+    a.slot_nblocks = W.slot_nblocks;
+    a.max_blocks = h->D.max_blocks;
+    a.kv_block = c.kv_block;
+    a.nq = nq;
+    a.nkv = nkv;
+    a.hd = hd;
+    a.scale = 1.0f / std::sqrt((float)hd);
+    a.n_split = n_split;
+    a.part = W.attn_part;
+    a.o = W.o;
+    a.o_hi = W.xa_hi;
+    a.o_lo = W.xa_lo;
+    a.err = W.err;
+    t = h->t_begin(1);
+    launch_attention(c.dtype, a, h->stream);
+    h->t_end(t);
+    launch_attn_combine(a, h->stream);
+    // O projection; residual + post-attention RMSNorm
+    GemvArgs go = gb;
+    go.ld_xa = nq * hd;
+    go.Kd = nq * hd;
+    go.w0 = L.w_o;
+    go.N = d;
+    RowArgs rn = ra;
+    rn.W = d;
+    rn.ldp = d;
+    rn.ks = launch_gemm(SRC_PREP, EPI_STORE, go, h->stream);
+    rn.gamma = L.post_norm;
+    launch_rows_resid_norm(rn, h->stream);
+    // gate/up, SwiGLU
+    GemvArgs gu = gb;
+    gu.ld_xa = d;
+    gu.Kd = d;
+    gu.w0 = L.w_gate;
+    gu.w1 = L.w_up;
+    gu.N = F;
+    RowArgs rs = ra;
+    rs.W = F;
+    rs.ldp = 2 * F;
+    rs.ks = launch_gemm(SRC_PREP, EPI_SWIGLU, gu, h->stream);
+    launch_rows_swiglu(rs, h->stream);
+    // down projection; residual + the next layer's input norm (final norm after the last)
+    GemvArgs gd = gb;
+    gd.ld_xa = F;
+    gd.Kd = F;
+    gd.w0 = L.w_down;
+    gd.N = d;
+    RowArgs rd = ra;
+    rd.W = d;
+    rd.ldp = d;
+    rd.ks = launch_gemm(SRC_PREP, EPI_STORE, gd, h->stream);
+    rd.gamma = l + 1 < c.n_layers ? h->layers[l + 1].in_norm : h->w.final_norm;
+    launch_rows_resid_norm(rd, h->stream);
+  }
+}
+
 // Final norm + LM head + block statistics, then the draft pick of step k.
 void run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, const float* temp,
               const float* u, float* logits, long ld_b, int32_t* drafts_out) {
@@ -371,11 +511,15 @@ void run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, cons
   const GemvShape sh = gemv_shape(c.dtype, EPI_LOGITS, B, c.vocab_draft, c.d_model);
   const int tn = sh.rows_per_wave;
   const int nblk = sh.waves;
+  const bool mr = gemm_use_mfma(c.dtype, B);
   GemvArgs g{};
   g.max_rows = B;
   g.xin = W.x;
   g.ldx = c.d_model;
   g.gather = gather;
+  g.xa_hi = W.xa_hi;   // matrix-core path: RMSNorm_final(x) prepared by the body
+  g.xa_lo = W.xa_lo;
+  g.ld_xa = c.d_model;
   g.gamma = h->w.final_norm;
   g.eps = c.rms_eps;
   g.d_norm = c.d_model;
@@ -389,7 +533,8 @@ void run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, cons
   g.part = W.lm_part;
   g.nblk = nblk;
   int t = h->t_begin(0);
-  launch_gemv(c.dtype, SRC_NORM, EPI_LOGITS, g, h->stream);
+  if (mr) launch_gemm(SRC_PREP, EPI_LOGITS, g, h->stream);
+  else launch_gemv(c.dtype, SRC_NORM, EPI_LOGITS, g, h->stream);
   h->t_end(t);
   SampleArgs s{};
   s.B = B;
@@ -695,8 +840,14 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
   gt.y = W.s;
   gt.ldy = c.d_model;
   gt.split_buf = W.split;
-  launch_gemv(c.dtype, SRC_TAPS, EPI_STORE, gt, h->stream);
-  run_body(h, ing, W.cu, B, W.s, true, pick_split(h, B, ctx_max), max_new);
+  const int split = pick_split(h, B, ctx_max);
+  if (gemm_use_mfma(c.dtype, (int)rows)) {
+    const int ks_taps = launch_gemm(SRC_TAPS, EPI_STORE, gt, h->stream);
+    run_body_mr(h, ing, W.cu, B, nullptr, ks_taps, split, max_new);
+  } else {
+    launch_gemv(c.dtype, SRC_TAPS, EPI_STORE, gt, h->stream);
+    run_body(h, ing, W.cu, B, W.s, true, split, max_new);
+  }
 
   // ---- K autoregressive draft steps ---------------------------------------------------------
   float* logits = a->draft_logits ? a->draft_logits : W.logits;
@@ -705,9 +856,10 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
   if (K >= 1) {
     run_head(h, B, 0, K, W.last_row, a->temperature, u, logits, ld_b, a->draft_tokens);
     RowMeta ar{nullptr, W.ar_pos, W.ar_tok, nullptr, B};
-    const int split = pick_split(h, B, ctx_max);
+    const bool ar_mr = gemm_use_mfma(c.dtype, B);
     for (int k = 1; k < K; ++k) {
-      run_body(h, ar, nullptr, B, W.gfb, true, split, 1);
+      if (ar_mr) run_body_mr(h, ar, nullptr, B, W.gfb, 1, split, 1);
+      else run_body(h, ar, nullptr, B, W.gfb, true, split, 1);
       run_head(h, B, k, K, nullptr, a->temperature, u, logits, ld_b, a->draft_tokens);
     }
   }
