@@ -202,7 +202,9 @@ typedef struct {
 /* Host-only check of a configuration.  Returns OSPREY_OK or the first problem. */
 int osprey_config_validate(const osprey_config* cfg);
 
-/* Bytes of the KV pool: kv_num_blocks pages of [n_layers][2][n_kv][kv_block][hd] (dtype).
+/* Bytes of the KV pool: kv_num_blocks pages of [n_layers][2][n_kv][kv_block * hd] (dtype);
+ * within a page keys are token-major [kv_block][hd] and values dimension-major
+ * [hd][kv_block].
  * Returns 0 for an invalid configuration. */
 size_t osprey_kv_bytes(const osprey_config* cfg);
 

@@ -1,22 +1,29 @@
-// Attention of the drafter over its paged KV cache.
+// Attention of the drafter over its paged KV cache (flash-decoding: each block
+// covers one context split of one (sequence, kv head); k_attn_combine merges the
+// splits with their log-sum-exp weights and normalises).
 //
-// k_attn: one block per (sequence, kv head, context split).
-//   0. Each wavefront prefetches its first KV page when it holds only older
-//      positions, so the page read overlaps steps 1-2.
-//   1. New rows whose position falls in this split: Qwen3 per-head RMSNorm of k,
-//      rotate-half RoPE at the row's absolute position (cos/sin table built on
-//      the host in float64), then k and v are stored into the row's cache page
-//      (rounded to bf16 in bf16 pools).  Every position belongs to exactly one
-//      split, so each new key/value is written once, by the block that reads it.
-//   2. The query vectors of the sequence that read this kv head (new rows x GQA
-//      group) are normalised and rotated into LDS, a few per pass.
-//   3. Each wavefront walks 16-token pages of the split: 16 lanes per token, each
-//      lane holding 1/16 of the head dimension, so a page of K or V is four fully
-//      coalesced wavefront reads of 4 tokens.  Scores use a causal mask at the
-//      row's position and an online softmax; the four wavefronts are merged in
-//      LDS and the split's (max, sum, unnormalised output) is written.
-// k_attn_combine: merges the splits of each (row, head) with their log-sum-exp
-//   weights (flash-decoding) and normalises.
+// Both kernels first do the row work of the pass:
+//   * new rows whose position falls in the block's split: Qwen3 per-head RMSNorm
+//     of k, rotate-half RoPE at the row's absolute position (cos/sin table built
+//     on the host in float64), then k and v go into the row's cache page
+//     (rounded to bf16 in bf16 pools).  Every position belongs to exactly one
+//     split, so each new key/value is written once, by the block that reads it;
+//   * the query vectors that read this kv head (new rows x GQA group) are
+//     normalised, rotated and scaled by 1/sqrt(hd) into LDS.
+// Projections come either as plain rows or as K-split partial sums (matrix-core
+// path), which are added on load in split order.
+//
+// k_attn_mfma (bf16 pools): up to 16 query vectors per pass.  Each wavefront
+// walks 16-token pages of the split, one page ahead in registers:
+//   S^T = K Q^T   (tokens x queries; 16x16x32 bf16 MFMA over the head dimension,
+//                  queries as bf16 hi + lo pairs),
+//   online softmax per query (a lane owns one query, 4 tokens),
+//   O^T += V^T P^T (head dims x queries; 16x16x16 bf16 MFMA over the page's
+//                  tokens, P as bf16 hi + lo pairs).
+// The transposed value page gives V^T tiles as 8-byte loads, and the score
+// tile's register layout is exactly the B operand of the second product, so no
+// data moves between lanes except the per-query max/sum reductions.
+// k_attn (fp32 pools): 16 lanes per token, online softmax on the vector units.
 #include "common.h"
 #include "internal.h"
 
@@ -44,6 +51,10 @@ template <int DPL> struct Seg<bf16_t, DPL> {
 };
 template <int DPL> struct Seg<float, DPL> {
   float raw[DPL];
+  OSP_DEV void load_t(const float* p, int stride) {
+#pragma unroll
+    for (int i = 0; i < DPL; ++i) raw[i] = p[(long)i * stride];
+  }
   OSP_DEV void load(const float* p) {
 #pragma unroll
     for (int j = 0; j < DPL / 4; ++j) {
@@ -83,9 +94,9 @@ OSP_DEV void norm_rope(const AttnArgs& a, const void* gain, int pos, int lane, f
   x2 = y2;
 }
 
-// One 16-token page of one kv head: lane l holds head dims [DPL*(l%16), +DPL) of
-// tokens 4u + l/16, u = 0..3 (each of the 4 loads of K or V is one coalesced
-// 1 KB / 512 B wavefront read of 4 consecutive tokens).
+// One 16-token page of one kv head (fp32): lane l holds head dims [DPL*(l%16), +DPL)
+// of tokens 4u + l/16, u = 0..3 (each of the 4 key loads is one coalesced
+// wavefront read of 4 consecutive tokens; values come from the transposed page).
 template <typename TKV, int HD>
 struct Page {
   static constexpr int DPL = HD / 16;
@@ -95,7 +106,7 @@ struct Page {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       k[u].load(kbase + u * 4 * HD + off);
-      v[u].load(vbase + u * 4 * HD + off);
+      v[u].load_t(vbase + kv_v_at(4 * u + (lane >> 4), (lane & 15) * DPL, 16), 16);
     }
   }
   OSP_DEV void zero() {
@@ -115,6 +126,60 @@ OSP_DEV float qkv_at(const AttnArgs& a, long off) {
 #pragma unroll
   for (int k = 0; k < kMaxKSplit; ++k) s += v[k];
   return s;
+}
+
+// New keys/values of rows r_beg..r_end whose position lies in [p_lo, p_hi):
+// k normalised and rotated, both stored into the row's cache page.
+template <typename TKV, int HD>
+OSP_DEV void append_new_kv(const AttnArgs& a, int r_beg, int r_end, int p_lo, int p_hi,
+                           const int32_t* bt, int nblocks, TKV* kvb, long blk_elems, long k_off,
+                           long v_off, int g, int wave, int lane) {
+  constexpr int HALF = HD / 2;
+  bool wrote = false;
+  for (int r = r_beg + (3 - wave); r < r_end; r += 4) {
+    const int pos = a.rows.pos[r];
+    if (pos < p_lo || pos >= p_hi) continue;
+    const int blk = pos / a.kv_block;
+    if (blk >= nblocks) { if (lane == 0) atomicOr(a.err, 1u << 3); continue; }
+    const long ko = (long)r * a.qkv_w + (a.nq + g) * HD;
+    const long vo = (long)r * a.qkv_w + (a.nq + a.nkv + g) * HD;
+    float k1 = lane < HALF ? qkv_at(a, ko + lane) : 0.f, k2 = lane < HALF ? qkv_at(a, ko + lane + HALF) : 0.f;
+    const float v1 = lane < HALF ? qkv_at(a, vo + lane) : 0.f;
+    const float v2 = lane < HALF ? qkv_at(a, vo + lane + HALF) : 0.f;
+    norm_rope<TKV, HD>(a, a.k_norm, pos, lane, k1, k2);
+    const long base = (long)bt[blk] * blk_elems;
+    const int w = pos - blk * a.kv_block;
+    if (lane < HALF) {
+      store_from_f32(kvb, base + k_off + kv_k_at(w, lane, HD), k1);
+      store_from_f32(kvb, base + k_off + kv_k_at(w, lane + HALF, HD), k2);
+      store_from_f32(kvb, base + v_off + kv_v_at(w, lane, a.kv_block), v1);
+      store_from_f32(kvb, base + v_off + kv_v_at(w, lane + HALF, a.kv_block), v2);
+    }
+    wrote = true;
+  }
+  if (wrote) __threadfence_block();
+}
+
+// Query vectors j0 .. j0+NV of the block (vector j: row r_beg + j / G, head
+// g G + j % G): per-head norm + RoPE, scaled by 1/sqrt(hd), into sm_q; vectors
+// past nvec are zero.
+template <typename TKV, int HD, int NV>
+OSP_DEV void stage_queries(const AttnArgs& a, float (*sm_q)[HD], int j0, int nvec, int r_beg, int G,
+                           int g, int wave, int lane) {
+  constexpr int HALF = HD / 2;
+  for (int j = wave; j < NV; j += 4) {
+    const int jj = j0 + j;
+    if (jj < nvec) {
+      const int r = r_beg + jj / G, h = g * G + jj % G;
+      const long qo = (long)r * a.qkv_w + h * HD;
+      float q1 = lane < HALF ? qkv_at(a, qo + lane) : 0.f, q2 = lane < HALF ? qkv_at(a, qo + lane + HALF) : 0.f;
+      norm_rope<TKV, HD>(a, a.q_norm, a.rows.pos[r], lane, q1, q2);
+      if (lane < HALF) { sm_q[j][lane] = q1 * a.scale; sm_q[j][lane + HALF] = q2 * a.scale; }
+    } else if (lane < HALF) {
+      sm_q[j][lane] = 0.f;
+      sm_q[j][lane + HALF] = 0.f;
+    }
+  }
 }
 
 template <typename TKV, int HD, int QV>
@@ -162,46 +227,12 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   }
 
   // ---- 1. keys/values of the new rows that fall in this split ------------------------
-  {
-    bool wrote = false;
-    for (int r = r_beg + (3 - wave); r < r_end; r += 4) {
-      const int pos = a.rows.pos[r];
-      if (pos < p_lo || pos >= p_hi) continue;
-      const int blk = pos / a.kv_block;
-      if (blk >= nblocks) { if (lane == 0) atomicOr(a.err, 1u << 3); continue; }
-      const long ko = (long)r * a.qkv_w + (a.nq + g) * HD;
-      const long vo = (long)r * a.qkv_w + (a.nq + a.nkv + g) * HD;
-      float k1 = lane < HALF ? qkv_at(a, ko + lane) : 0.f, k2 = lane < HALF ? qkv_at(a, ko + lane + HALF) : 0.f;
-      const float v1 = lane < HALF ? qkv_at(a, vo + lane) : 0.f;
-      const float v2 = lane < HALF ? qkv_at(a, vo + lane + HALF) : 0.f;
-      norm_rope<TKV, HD>(a, a.k_norm, pos, lane, k1, k2);
-      const long base = (long)bt[blk] * blk_elems + (long)(pos - blk * a.kv_block) * HD;
-      if (lane < HALF) {
-        store_from_f32(kvb, base + k_off + lane, k1);
-        store_from_f32(kvb, base + k_off + lane + HALF, k2);
-        store_from_f32(kvb, base + v_off + lane, v1);
-        store_from_f32(kvb, base + v_off + lane + HALF, v2);
-      }
-      wrote = true;
-    }
-    if (wrote) __threadfence_block();
-  }
+  append_new_kv<TKV, HD>(a, r_beg, r_end, p_lo, p_hi, bt, nblocks, kvb, blk_elems, k_off, v_off, g,
+                         wave, lane);
 
   for (int j0 = 0; j0 < nvec; j0 += QV) {
     // ---- 2. this pass's query vectors: norm + RoPE into LDS (scaled by 1/sqrt(hd)) ----
-    for (int j = wave; j < QV; j += 4) {
-      const int jj = j0 + j;
-      if (jj < nvec) {
-        const int r = r_beg + jj / G, h = g * G + jj % G;
-        const long qo = (long)r * a.qkv_w + h * HD;
-        float q1 = lane < HALF ? qkv_at(a, qo + lane) : 0.f, q2 = lane < HALF ? qkv_at(a, qo + lane + HALF) : 0.f;
-        norm_rope<TKV, HD>(a, a.q_norm, a.rows.pos[r], lane, q1, q2);
-        if (lane < HALF) { sm_q[j][lane] = q1 * a.scale; sm_q[j][lane + HALF] = q2 * a.scale; }
-      } else if (lane < HALF) {
-        sm_q[j][lane] = 0.f;
-        sm_q[j][lane + HALF] = 0.f;
-      }
-    }
+    stage_queries<TKV, HD, QV>(a, sm_q, j0, nvec, r_beg, G, g, wave, lane);
     __syncthreads();
     float q[QV][DPL], o[QV][DPL], m[QV], l[QV];
     int qpos[QV];
@@ -308,6 +339,216 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   }
 }
 
+typedef __bf16 att_bf16x8 __attribute__((ext_vector_type(8)));
+typedef short att_i16x4 __attribute__((ext_vector_type(4)));
+typedef float att_f32x4 __attribute__((ext_vector_type(4)));
+
+// One 16-token page as matrix-core operands: lane l holds
+//   k[c] = K[token l%16][32 c + 8 (l/16) .. +8]          (A of S^T = K Q^T)
+//   v[n] = V^T[16 n + l%16][tokens 4 (l/16) .. +4]       (A of O^T = V^T P^T)
+template <int HD> struct MPage {
+  uint4 k[HD / 32];
+  uint2 v[HD / 16];
+  OSP_DEV void load(const bf16_t* kb, const bf16_t* vb, int lane) {
+    const int row = lane & 15, grp = lane >> 4;
+#pragma unroll
+    for (int c = 0; c < HD / 32; ++c)
+      k[c] = *reinterpret_cast<const uint4*>(kb + kv_k_at(row, 32 * c + 8 * grp, HD));
+#pragma unroll
+    for (int n = 0; n < HD / 16; ++n)
+      v[n] = *reinterpret_cast<const uint2*>(vb + kv_v_at(4 * grp, 16 * n + row, 16));
+  }
+  OSP_DEV void zero() {
+#pragma unroll
+    for (int c = 0; c < HD / 32; ++c) k[c] = make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+    for (int n = 0; n < HD / 16; ++n) v[n] = make_uint2(0u, 0u);
+  }
+};
+
+template <int HD>
+__global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
+  constexpr int PG = 16;               // tokens per KV page
+  constexpr int NV = 16;               // query vectors per pass
+  constexpr int KC = HD / 32;          // 32-wide head-dim chunks of Q K^T
+  constexpr int NT = HD / 16;          // 16-dim output tiles
+  constexpr int OP = HD + 4;           // LDS pitch of the output merge
+  __shared__ float sm_q[NV][HD];
+  __shared__ float sm_m[4][NV];
+  __shared__ float sm_l[4][NV];
+  __shared__ __attribute__((aligned(16))) float sm_o[4][NV][OP];
+
+  const int b = blockIdx.x, g = blockIdx.y, sp = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int row = lane & 15, grp = lane >> 4;
+  int r_beg, r_end;
+  if (a.cu) { r_beg = a.cu[b]; r_end = a.cu[b + 1]; } else { r_beg = b; r_end = b + 1; }
+  const int rows_total = a.rows.count ? min(*a.rows.count, a.rows.max_rows) : a.rows.max_rows;
+  r_end = min(r_end, rows_total);
+  if (r_beg >= r_end) return;
+  const int G = a.nq / a.nkv;
+  const int nvec = (r_end - r_beg) * G;
+  const int first_new = a.rows.pos[r_beg];
+  const int n_ctx = a.rows.pos[r_end - 1] + 1;
+  int ts = (n_ctx + a.n_split - 1) / a.n_split;
+  ts = (ts + PG - 1) / PG * PG;
+  const int p_lo = sp * ts;
+  const int p_hi = min(n_ctx, p_lo + ts);
+  const int slot = a.bslot[b];
+  const int nblocks = a.slot_nblocks[slot];
+  const int32_t* bt = a.block_table + (long)slot * a.max_blocks;
+  bf16_t* kvb = reinterpret_cast<bf16_t*>(a.kv);
+  const long blk_elems = kv_block_elems(a.n_layers, a.nkv, a.kv_block, HD);
+  const long k_off = (((long)a.layer * 2 + 0) * a.nkv + g) * a.kv_block * HD;
+  const long v_off = (((long)a.layer * 2 + 1) * a.nkv + g) * a.kv_block * HD;
+
+  // this wavefront's pages: split pages wave, wave + 4, ...; page table entries for
+  // 64 of them at a time, one per lane (-1: beyond the slot's pages)
+  const int pg_lo = p_lo / PG;
+  const int n_pg = p_hi > p_lo ? (p_hi - p_lo + PG - 1) / PG : 0;
+  const int n_mine = n_pg > wave ? (n_pg - wave + 3) / 4 : 0;
+  auto fetch_bt = [&](int win) {
+    const int i = win * 64 + lane;
+    const int pid = pg_lo + wave + 4 * i;
+    return (i < n_mine && pid < nblocks) ? bt[pid] : -1;
+  };
+  int win = 0;
+  int bt_reg = fetch_bt(0);
+  auto load_page = [&](MPage<HD>& pg, int i) {
+    if ((i >> 6) != win) { win = i >> 6; bt_reg = fetch_bt(win); }
+    const int phys = __shfl(bt_reg, i & 63, OSP_WAVE);
+    if (phys >= 0) {
+      const long base = (long)phys * blk_elems;
+      pg.load(kvb + base + k_off, kvb + base + v_off, lane);
+    } else {
+      pg.zero();
+    }
+  };
+
+  // ---- 0. the first page early when it holds only older positions ---------------------
+  MPage<HD> cur;
+  const bool early = n_mine > 0 && (pg_lo + wave + 1) * PG <= first_new;
+  if (early) load_page(cur, 0);
+
+  // ---- 1. keys/values of the new rows that fall in this split ------------------------
+  append_new_kv<bf16_t, HD>(a, r_beg, r_end, p_lo, p_hi, bt, nblocks, kvb, blk_elems, k_off, v_off,
+                            g, wave, lane);
+
+  for (int j0 = 0; j0 < nvec; j0 += NV) {
+    // ---- 2. queries: norm + RoPE into LDS, then Q^T fragments as bf16 hi / lo ---------
+    stage_queries<bf16_t, HD, NV>(a, sm_q, j0, nvec, r_beg, G, g, wave, lane);
+    __syncthreads();
+    uint4 qh[KC], ql[KC];
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+      uint32_t h[4], l[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float v0 = sm_q[row][32 * c + 8 * grp + 2 * e];
+        const float v1 = sm_q[row][32 * c + 8 * grp + 2 * e + 1];
+        const bf16_t h0 = f32_to_bf16(v0), h1 = f32_to_bf16(v1);
+        h[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+        l[e] = (uint32_t)f32_to_bf16(v0 - bf16_to_f32(h0)) |
+               ((uint32_t)f32_to_bf16(v1 - bf16_to_f32(h1)) << 16);
+      }
+      qh[c] = make_uint4(h[0], h[1], h[2], h[3]);
+      ql[c] = make_uint4(l[0], l[1], l[2], l[3]);
+    }
+    const int qj = j0 + row;
+    const int qpos = qj < nvec ? a.rows.pos[r_beg + qj / G] : -1;
+    float m = -INFINITY, lsum = 0.f;
+    att_f32x4 acc[NT];
+#pragma unroll
+    for (int n = 0; n < NT; ++n) acc[n] = att_f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // ---- 3. pages, one ahead in registers ------------------------------------------------
+    if (n_mine > 0 && !(early && j0 == 0)) load_page(cur, 0);
+    for (int i = 0; i < n_mine; ++i) {
+      MPage<HD> nxt;
+      if (i + 1 < n_mine) load_page(nxt, i + 1);
+      const int t0 = (pg_lo + wave + 4 * i) * PG;
+      // S^T[token][query]: lane holds tokens 4 grp + e of query `row`
+      att_f32x4 sc = att_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < KC; ++c) {
+        const att_bf16x8 ka = *reinterpret_cast<const att_bf16x8*>(&cur.k[c]);
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, *reinterpret_cast<const att_bf16x8*>(&qh[c]), sc, 0, 0, 0);
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, *reinterpret_cast<const att_bf16x8*>(&ql[c]), sc, 0, 0, 0);
+      }
+      // causal / sequence-end mask; value entries past the sequence end are cleared so
+      // that unwritten cache memory cannot reach the products (0 * NaN)
+      float s4[4];
+      float bm = -INFINITY;
+      uint32_t keep[2] = {0u, 0u};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int p = t0 + 4 * grp + e;
+        s4[e] = (p < p_hi && p <= qpos) ? sc[e] : -INFINITY;
+        bm = fmaxf(bm, s4[e]);
+        if (p < p_hi) keep[e >> 1] |= (e & 1) ? 0xffff0000u : 0x0000ffffu;
+      }
+#pragma unroll
+      for (int n = 0; n < NT; ++n) { cur.v[n].x &= keep[0]; cur.v[n].y &= keep[1]; }
+      bm = fmaxf(bm, __shfl_xor(bm, 16, OSP_WAVE));
+      bm = fmaxf(bm, __shfl_xor(bm, 32, OSP_WAVE));
+      const float mn = fmaxf(m, bm);
+      const float f = (mn == -INFINITY) ? 1.f : __expf(m - mn);
+      float pe[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) pe[e] = (s4[e] == -INFINITY) ? 0.f : __expf(s4[e] - mn);
+      lsum = lsum * f + ((pe[0] + pe[1]) + (pe[2] + pe[3]));
+      m = mn;
+      att_i16x4 ph, pl;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bf16_t hb = f32_to_bf16(pe[e]);
+        ph[e] = (short)hb;
+        pl[e] = (short)f32_to_bf16(pe[e] - bf16_to_f32(hb));
+      }
+      // O^T[dim][query] += V^T P^T
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        acc[n] *= f;
+        const att_i16x4 va = *reinterpret_cast<const att_i16x4*>(&cur.v[n]);
+        acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, ph, acc[n], 0, 0, 0);
+        acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pl, acc[n], 0, 0, 0);
+      }
+      cur = nxt;
+    }
+    // ---- merge the wavefronts: lane holds O^T[16 n + 4 grp + e][row] ------------------
+    lsum += __shfl_xor(lsum, 16, OSP_WAVE);
+    lsum += __shfl_xor(lsum, 32, OSP_WAVE);
+    if (grp == 0) { sm_m[wave][row] = m; sm_l[wave][row] = lsum; }
+#pragma unroll
+    for (int n = 0; n < NT; ++n)
+      *reinterpret_cast<float4*>(&sm_o[wave][row][16 * n + 4 * grp]) =
+          make_float4(acc[n][0], acc[n][1], acc[n][2], acc[n][3]);
+    __syncthreads();
+    for (int i = tid; i < NV * HD; i += 256) {
+      const int j = i / HD, e = i - j * HD;
+      const int jj = j0 + j;
+      if (jj >= nvec) continue;
+      float M = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) M = fmaxf(M, sm_m[w][j]);
+      float L = 0.f, O = 0.f;
+      if (M > -INFINITY) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const float fw = __expf(sm_m[w][j] - M);
+          L += sm_l[w][j] * fw;
+          O += sm_o[w][j][e] * fw;
+        }
+      }
+      const int r = r_beg + jj / G, h = g * G + jj % G;
+      float* pp = a.part + (((long)r * a.nq + h) * a.n_split + sp) * (HD + 2);
+      pp[2 + e] = O;
+      if (e == 0) { pp[0] = M; pp[1] = L; }
+    }
+    __syncthreads();
+  }
+}
+
 // One wavefront per (row, head): lane t reads split t's (max, sum); the output
 // elements are accumulated over splits with all loads independent.
 __global__ void __launch_bounds__(64) k_attn_combine(AttnArgs a) {
@@ -360,7 +601,9 @@ static void launch_hd(const AttnArgs& a, hipStream_t st) {
 
 void launch_attention(int kvdtype, const AttnArgs& a, hipStream_t st) {
   if (kvdtype == 1) {
-    if (a.hd == 128) launch_hd<bf16_t, 128>(a, st); else launch_hd<bf16_t, 64>(a, st);
+    dim3 grid(a.B, a.nkv, a.n_split);
+    if (a.hd == 128) hipLaunchKernelGGL(k_attn_mfma<128>, grid, dim3(256), 0, st, a);
+    else hipLaunchKernelGGL(k_attn_mfma<64>, grid, dim3(256), 0, st, a);
   } else {
     if (a.hd == 128) launch_hd<float, 128>(a, st); else launch_hd<float, 64>(a, st);
   }

@@ -266,9 +266,13 @@ void launch_kv_append(int kvdtype, void* kv, const void* k, const void* v, int n
 void launch_set_len(int32_t* slot_len, int32_t* pend_n, int slot, int len, hipStream_t st);
 void launch_fill_i32(int32_t* p, int32_t v, long n, hipStream_t st);
 
-// KV pool layout: [block][layer][2 (k, v)][nkv][kv_block][hd]
+// KV pool layout: [block][layer][2 (k, v)][nkv][page], where the key page is
+// [kv_block][hd] (token-major) and the value page [hd][kv_block] (transposed, so
+// that the matrix-core attention reads 4 consecutive tokens of one dimension).
 __host__ __device__ inline long kv_block_elems(int n_layers, int nkv, int kv_block, int hd) {
   return (long)n_layers * 2 * nkv * kv_block * hd;
 }
+__host__ __device__ inline long kv_k_at(int tok, int e, int hd) { return (long)tok * hd + e; }
+__host__ __device__ inline long kv_v_at(int tok, int e, int kv_block) { return (long)e * kv_block + tok; }
 
 }  // namespace osp

@@ -97,8 +97,8 @@ __global__ void k_kv_append(T* kv, const T* k, const T* v, int n_layers, int n, 
     if (blk >= max_blocks) continue;
     const long phys = block_table[(long)slot * max_blocks + blk];
     T* base = kv + phys * blk_elems;
-    base[(((long)l * 2 + 0) * nkv + g) * kv_block * hd + (long)within * hd + e] = k[i];
-    base[(((long)l * 2 + 1) * nkv + g) * kv_block * hd + (long)within * hd + e] = v[i];
+    base[(((long)l * 2 + 0) * nkv + g) * kv_block * hd + kv_k_at(within, e, hd)] = k[i];
+    base[(((long)l * 2 + 1) * nkv + g) * kv_block * hd + kv_v_at(within, e, kv_block)] = v[i];
   }
 }
 

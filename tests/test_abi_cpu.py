@@ -67,7 +67,7 @@ def test_config_validation_codes(lib):
 def test_pool_and_workspace_sizes(lib):
     from paper_2609_09338_amd import binding as bd
     c = _cfg()
-    # [blocks][layers][k, v][kv heads][16 tokens][head_dim] bf16
+    # [blocks][layers][k, v][kv heads][16 tokens x head_dim] bf16
     assert bd.kv_bytes(c) == 256 * 2 * 2 * 8 * 16 * 128 * 2
     assert bd.kv_bytes(_cfg(dtype=0)) == 2 * bd.kv_bytes(c)
     ws = bd.workspace_bytes(c)
