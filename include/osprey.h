@@ -89,7 +89,7 @@ typedef struct {
   float rope_theta;
   int32_t max_batch;      /* sequences per call and number of slots (<= 256) */
   int32_t max_k;          /* largest K (<= 64) */
-  int32_t max_seq_len;    /* largest position + 1 */
+  int32_t max_seq_len;    /* largest position + 1; at most 262144 */
   int32_t kv_block;       /* tokens per KV page; must be 16 */
   int32_t kv_num_blocks;  /* pages in the pool */
   int32_t max_new_rows;   /* largest explicit ingest (prompt prefill) summed over the batch */

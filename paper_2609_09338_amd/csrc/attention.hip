@@ -14,12 +14,13 @@
 // path), which are added on load in split order.
 //
 // k_attn_mfma (bf16 pools): up to 16 query vectors per pass.  Each wavefront
-// walks 16-token pages of the split, one page ahead in registers:
+// walks 16-token pages of the split:
 //   S^T = K Q^T   (tokens x queries; 16x16x32 bf16 MFMA over the head dimension,
 //                  queries as bf16 hi + lo pairs),
 //   online softmax per query (a lane owns one query, 4 tokens),
 //   O^T += V^T P^T (head dims x queries; 16x16x16 bf16 MFMA over the page's
-//                  tokens, P as bf16 hi + lo pairs).
+//                  tokens, P as bf16 hi + lo pairs),
+// with the next pages already requested.
 // The transposed value page gives V^T tiles as 8-byte loads, and the score
 // tile's register layout is exactly the B operand of the second product, so no
 // data moves between lanes except the per-query max/sum reductions.
@@ -169,7 +170,11 @@ OSP_DEV void stage_queries(const AttnArgs& a, float (*sm_q)[HD], int j0, int nve
   constexpr int HALF = HD / 2;
   for (int j = wave; j < NV; j += 4) {
     const int jj = j0 + j;
-    if (jj < nvec) {
+    if (jj < nvec && a.q_prep) {
+      const int r = r_beg + jj / G, h = g * G + jj % G;
+      const float* qp = a.q_prep + ((long)r * a.nq + h) * HD;
+      if (lane < HALF) { sm_q[j][lane] = qp[lane]; sm_q[j][lane + HALF] = qp[lane + HALF]; }
+    } else if (jj < nvec) {
       const int r = r_beg + jj / G, h = g * G + jj % G;
       const long qo = (long)r * a.qkv_w + h * HD;
       float q1 = lane < HALF ? qkv_at(a, qo + lane) : 0.f, q2 = lane < HALF ? qkv_at(a, qo + lane + HALF) : 0.f;
@@ -205,10 +210,9 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   const int nvec = (r_end - r_beg) * G;
   const int first_new = a.rows.pos[r_beg];
   const int n_ctx = a.rows.pos[r_end - 1] + 1;
-  int ts = (n_ctx + a.n_split - 1) / a.n_split;
-  ts = (ts + PG - 1) / PG * PG;
-  const int p_lo = sp * ts;
-  const int p_hi = min(n_ctx, p_lo + ts);
+  const int p_lo = sp * a.split_len;
+  if (p_lo >= n_ctx) return;           // beyond this sequence: the combine reads no partial here
+  const int p_hi = min(n_ctx, p_lo + a.split_len);
   const int slot = a.bslot[b];
   const int nblocks = a.slot_nblocks[slot];
   const int32_t* bt = a.block_table + (long)slot * a.max_blocks;
@@ -220,15 +224,16 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   // ---- 0. prefetch this wavefront's first page if it holds only older positions -------
   Page<TKV, HD> pre;
   const int t_first = p_lo + wave * PG;
-  const bool prefetched = t_first < p_hi && t_first + PG <= first_new && t_first / PG < nblocks;
+  const bool prefetched = t_first < p_hi && (a.q_prep || t_first + PG <= first_new) && t_first / PG < nblocks;
   if (prefetched) {
     const long base = (long)bt[t_first / PG] * blk_elems;
     pre.load(kvb + base + k_off, kvb + base + v_off, lane);
   }
 
   // ---- 1. keys/values of the new rows that fall in this split ------------------------
-  append_new_kv<TKV, HD>(a, r_beg, r_end, p_lo, p_hi, bt, nblocks, kvb, blk_elems, k_off, v_off, g,
-                         wave, lane);
+  if (!a.q_prep)
+    append_new_kv<TKV, HD>(a, r_beg, r_end, p_lo, p_hi, bt, nblocks, kvb, blk_elems, k_off, v_off, g,
+                           wave, lane);
 
   for (int j0 = 0; j0 < nvec; j0 += QV) {
     // ---- 2. this pass's query vectors: norm + RoPE into LDS (scaled by 1/sqrt(hd)) ----
@@ -339,6 +344,12 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   }
 }
 
+// Pages held in registers by each wavefront of k_attn_mfma (DEPTH - 1 in flight).
+#ifndef OSP_ATTN_DEPTH
+#define OSP_ATTN_DEPTH 2
+#endif
+constexpr int kAttnDepth = OSP_ATTN_DEPTH;
+
 typedef __bf16 att_bf16x8 __attribute__((ext_vector_type(8)));
 typedef short att_i16x4 __attribute__((ext_vector_type(4)));
 typedef float att_f32x4 __attribute__((ext_vector_type(4)));
@@ -366,7 +377,7 @@ template <int HD> struct MPage {
   }
 };
 
-template <int HD>
+template <int HD, int DEPTH>
 __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
   constexpr int PG = 16;               // tokens per KV page
   constexpr int NV = 16;               // query vectors per pass
@@ -390,10 +401,9 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
   const int nvec = (r_end - r_beg) * G;
   const int first_new = a.rows.pos[r_beg];
   const int n_ctx = a.rows.pos[r_end - 1] + 1;
-  int ts = (n_ctx + a.n_split - 1) / a.n_split;
-  ts = (ts + PG - 1) / PG * PG;
-  const int p_lo = sp * ts;
-  const int p_hi = min(n_ctx, p_lo + ts);
+  const int p_lo = sp * a.split_len;
+  if (p_lo >= n_ctx) return;           // beyond this sequence: the combine reads no partial here
+  const int p_hi = min(n_ctx, p_lo + a.split_len);
   const int slot = a.bslot[b];
   const int nblocks = a.slot_nblocks[slot];
   const int32_t* bt = a.block_table + (long)slot * a.max_blocks;
@@ -402,21 +412,18 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
   const long k_off = (((long)a.layer * 2 + 0) * a.nkv + g) * a.kv_block * HD;
   const long v_off = (((long)a.layer * 2 + 1) * a.nkv + g) * a.kv_block * HD;
 
-  // this wavefront's pages: split pages wave, wave + 4, ...; page table entries for
-  // 64 of them at a time, one per lane (-1: beyond the slot's pages)
+  // this wavefront's pages: split pages wave, wave + 4, ... (at most 64: the host keeps
+  // split_len <= 4096), their page-table entries one per lane (-1: beyond the slot's pages)
   const int pg_lo = p_lo / PG;
   const int n_pg = p_hi > p_lo ? (p_hi - p_lo + PG - 1) / PG : 0;
-  const int n_mine = n_pg > wave ? (n_pg - wave + 3) / 4 : 0;
-  auto fetch_bt = [&](int win) {
-    const int i = win * 64 + lane;
-    const int pid = pg_lo + wave + 4 * i;
-    return (i < n_mine && pid < nblocks) ? bt[pid] : -1;
-  };
-  int win = 0;
-  int bt_reg = fetch_bt(0);
+  const int n_mine = min(64, n_pg > wave ? (n_pg - wave + 3) / 4 : 0);
+  int bt_reg;
+  {
+    const int pid = pg_lo + wave + 4 * lane;
+    bt_reg = (lane < n_mine && pid < nblocks) ? bt[pid] : -1;
+  }
   auto load_page = [&](MPage<HD>& pg, int i) {
-    if ((i >> 6) != win) { win = i >> 6; bt_reg = fetch_bt(win); }
-    const int phys = __shfl(bt_reg, i & 63, OSP_WAVE);
+    const int phys = __shfl(bt_reg, i, OSP_WAVE);
     if (phys >= 0) {
       const long base = (long)phys * blk_elems;
       pg.load(kvb + base + k_off, kvb + base + v_off, lane);
@@ -426,13 +433,14 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
   };
 
   // ---- 0. the first page early when it holds only older positions ---------------------
-  MPage<HD> cur;
-  const bool early = n_mine > 0 && (pg_lo + wave + 1) * PG <= first_new;
-  if (early) load_page(cur, 0);
+  MPage<HD> ring[DEPTH];
+  const bool early = n_mine > 0 && (a.q_prep || (pg_lo + wave + 1) * PG <= first_new);
+  if (early) load_page(ring[0], 0);
 
   // ---- 1. keys/values of the new rows that fall in this split ------------------------
-  append_new_kv<bf16_t, HD>(a, r_beg, r_end, p_lo, p_hi, bt, nblocks, kvb, blk_elems, k_off, v_off,
-                            g, wave, lane);
+  if (!a.q_prep)
+    append_new_kv<bf16_t, HD>(a, r_beg, r_end, p_lo, p_hi, bt, nblocks, kvb, blk_elems, k_off, v_off,
+                              g, wave, lane);
 
   for (int j0 = 0; j0 < nvec; j0 += NV) {
     // ---- 2. queries: norm + RoPE into LDS, then Q^T fragments as bf16 hi / lo ---------
@@ -443,35 +451,31 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
     for (int c = 0; c < KC; ++c) {
       uint32_t h[4], l[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float v0 = sm_q[row][32 * c + 8 * grp + 2 * e];
-        const float v1 = sm_q[row][32 * c + 8 * grp + 2 * e + 1];
-        const bf16_t h0 = f32_to_bf16(v0), h1 = f32_to_bf16(v1);
-        h[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-        l[e] = (uint32_t)f32_to_bf16(v0 - bf16_to_f32(h0)) |
-               ((uint32_t)f32_to_bf16(v1 - bf16_to_f32(h1)) << 16);
-      }
+      for (int e = 0; e < 4; ++e)
+        split_bf16x2(sm_q[row][32 * c + 8 * grp + 2 * e], sm_q[row][32 * c + 8 * grp + 2 * e + 1], h[e], l[e]);
       qh[c] = make_uint4(h[0], h[1], h[2], h[3]);
       ql[c] = make_uint4(l[0], l[1], l[2], l[3]);
     }
     const int qj = j0 + row;
     const int qpos = qj < nvec ? a.rows.pos[r_beg + qj / G] : -1;
+    // consume qpos here: a first use inside the page loop would make every iteration
+    // wait for all outstanding loads, the page prefetches included
+    asm volatile("" ::"v"(qpos));
     float m = -INFINITY, lsum = 0.f;
     att_f32x4 acc[NT];
 #pragma unroll
     for (int n = 0; n < NT; ++n) acc[n] = att_f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // ---- 3. pages, one ahead in registers ------------------------------------------------
-    if (n_mine > 0 && !(early && j0 == 0)) load_page(cur, 0);
-    for (int i = 0; i < n_mine; ++i) {
-      MPage<HD> nxt;
-      if (i + 1 < n_mine) load_page(nxt, i + 1);
+    // ---- 3. pages: a ring of DEPTH register pages, DEPTH - 1 requested ahead; the
+    //      ring is unrolled so that no page is copied between registers (a copy would
+    //      wait for its load and stall the pipeline) ------------------------------------
+    auto page_step = [&](MPage<HD>& pg, int i) {
       const int t0 = (pg_lo + wave + 4 * i) * PG;
       // S^T[token][query]: lane holds tokens 4 grp + e of query `row`
       att_f32x4 sc = att_f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int c = 0; c < KC; ++c) {
-        const att_bf16x8 ka = *reinterpret_cast<const att_bf16x8*>(&cur.k[c]);
+        const att_bf16x8 ka = *reinterpret_cast<const att_bf16x8*>(&pg.k[c]);
         sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, *reinterpret_cast<const att_bf16x8*>(&qh[c]), sc, 0, 0, 0);
         sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, *reinterpret_cast<const att_bf16x8*>(&ql[c]), sc, 0, 0, 0);
       }
@@ -488,7 +492,7 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
         if (p < p_hi) keep[e >> 1] |= (e & 1) ? 0xffff0000u : 0x0000ffffu;
       }
 #pragma unroll
-      for (int n = 0; n < NT; ++n) { cur.v[n].x &= keep[0]; cur.v[n].y &= keep[1]; }
+      for (int n = 0; n < NT; ++n) { pg.v[n].x &= keep[0]; pg.v[n].y &= keep[1]; }
       bm = fmaxf(bm, __shfl_xor(bm, 16, OSP_WAVE));
       bm = fmaxf(bm, __shfl_xor(bm, 32, OSP_WAVE));
       const float mn = fmaxf(m, bm);
@@ -498,22 +502,33 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
       for (int e = 0; e < 4; ++e) pe[e] = (s4[e] == -INFINITY) ? 0.f : __expf(s4[e] - mn);
       lsum = lsum * f + ((pe[0] + pe[1]) + (pe[2] + pe[3]));
       m = mn;
-      att_i16x4 ph, pl;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const bf16_t hb = f32_to_bf16(pe[e]);
-        ph[e] = (short)hb;
-        pl[e] = (short)f32_to_bf16(pe[e] - bf16_to_f32(hb));
-      }
+      uint2 ph2, pl2;
+      split_bf16x2(pe[0], pe[1], ph2.x, pl2.x);
+      split_bf16x2(pe[2], pe[3], ph2.y, pl2.y);
+      const att_i16x4 ph = *reinterpret_cast<const att_i16x4*>(&ph2);
+      const att_i16x4 pl = *reinterpret_cast<const att_i16x4*>(&pl2);
       // O^T[dim][query] += V^T P^T
 #pragma unroll
       for (int n = 0; n < NT; ++n) {
         acc[n] *= f;
-        const att_i16x4 va = *reinterpret_cast<const att_i16x4*>(&cur.v[n]);
+        const att_i16x4 va = *reinterpret_cast<const att_i16x4*>(&pg.v[n]);
         acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, ph, acc[n], 0, 0, 0);
         acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pl, acc[n], 0, 0, 0);
       }
-      cur = nxt;
+    };
+    if (n_mine > 0 && !(early && j0 == 0)) load_page(ring[0], 0);
+#pragma unroll
+    for (int u = 1; u + 1 < DEPTH; ++u)
+      if (u < n_mine) load_page(ring[u], u);
+    for (int i0 = 0; i0 < n_mine; i0 += DEPTH) {
+#pragma unroll
+      for (int u = 0; u < DEPTH; ++u) {
+        const int i = i0 + u;
+        if (i < n_mine) {
+          if (i + DEPTH - 1 < n_mine) load_page(ring[(u + DEPTH - 1) % DEPTH], i + DEPTH - 1);
+          page_step(ring[u], i);
+        }
+      }
     }
     // ---- merge the wavefronts: lane holds O^T[16 n + 4 grp + e][row] ------------------
     lsum += __shfl_xor(lsum, 16, OSP_WAVE);
@@ -549,6 +564,57 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
   }
 }
 
+// Matrix-core path, once per row: the QKV split partials are added, q and k
+// normalised (per head) and rotated, q scaled by 1/sqrt(hd) into q_out and the
+// new key/value stored in the row's cache page.  Block (row, group of 4 heads);
+// wavefront w handles head 4 y + w of the nq query heads followed by the nkv
+// key/value heads.
+template <typename TKV, int HD>
+__global__ void __launch_bounds__(256) k_rows_qkv(AttnArgs a, float* q_out) {
+  constexpr int HALF = HD / 2;
+  const int r = blockIdx.x;
+  const int rows = a.rows.count ? min(*a.rows.count, a.rows.max_rows) : a.rows.max_rows;
+  if (r >= rows) return;
+  const int lane = threadIdx.x & 63;
+  const int hh = blockIdx.y * 4 + (threadIdx.x >> 6);
+  if (hh >= a.nq + a.nkv) return;
+  const int pos = a.rows.pos[r];
+  if (hh < a.nq) {
+    const long qo = (long)r * a.qkv_w + (long)hh * HD;
+    float q1 = lane < HALF ? qkv_at(a, qo + lane) : 0.f, q2 = lane < HALF ? qkv_at(a, qo + lane + HALF) : 0.f;
+    norm_rope<TKV, HD>(a, a.q_norm, pos, lane, q1, q2);
+    if (lane < HALF) {
+      float* qp = q_out + ((long)r * a.nq + hh) * HD;
+      qp[lane] = q1 * a.scale;
+      qp[lane + HALF] = q2 * a.scale;
+    }
+    return;
+  }
+  const int g = hh - a.nq;
+  const int b = a.rows.seq ? a.rows.seq[r] : r;
+  const int slot = a.bslot[b];
+  const int blk = pos / a.kv_block;
+  if (blk >= a.slot_nblocks[slot]) { if (lane == 0) atomicOr(a.err, 1u << 3); return; }
+  const long ko = (long)r * a.qkv_w + (long)(a.nq + g) * HD;
+  const long vo = (long)r * a.qkv_w + (long)(a.nq + a.nkv + g) * HD;
+  float k1 = lane < HALF ? qkv_at(a, ko + lane) : 0.f, k2 = lane < HALF ? qkv_at(a, ko + lane + HALF) : 0.f;
+  const float v1 = lane < HALF ? qkv_at(a, vo + lane) : 0.f;
+  const float v2 = lane < HALF ? qkv_at(a, vo + lane + HALF) : 0.f;
+  norm_rope<TKV, HD>(a, a.k_norm, pos, lane, k1, k2);
+  TKV* kvb = reinterpret_cast<TKV*>(a.kv);
+  const long base = (long)a.block_table[(long)slot * a.max_blocks + blk] *
+                    kv_block_elems(a.n_layers, a.nkv, a.kv_block, HD);
+  const long k_off = (((long)a.layer * 2 + 0) * a.nkv + g) * a.kv_block * HD;
+  const long v_off = (((long)a.layer * 2 + 1) * a.nkv + g) * a.kv_block * HD;
+  const int w = pos - blk * a.kv_block;
+  if (lane < HALF) {
+    store_from_f32(kvb, base + k_off + kv_k_at(w, lane, HD), k1);
+    store_from_f32(kvb, base + k_off + kv_k_at(w, lane + HALF, HD), k2);
+    store_from_f32(kvb, base + v_off + kv_v_at(w, lane, a.kv_block), v1);
+    store_from_f32(kvb, base + v_off + kv_v_at(w, lane + HALF, a.kv_block), v2);
+  }
+}
+
 // One wavefront per (row, head): lane t reads split t's (max, sum); the output
 // elements are accumulated over splits with all loads independent.
 __global__ void __launch_bounds__(64) k_attn_combine(AttnArgs a) {
@@ -556,8 +622,9 @@ __global__ void __launch_bounds__(64) k_attn_combine(AttnArgs a) {
   const int rows = a.rows.count ? min(*a.rows.count, a.rows.max_rows) : a.rows.max_rows;
   if (r >= rows) return;
   const int lane = threadIdx.x;
-  const int hd = a.hd, ns = a.n_split;
-  const float* pp = a.part + ((long)r * a.nq + h) * ns * (hd + 2);
+  // splits that hold any position visible to this row (later ones were not written)
+  const int hd = a.hd, ns = min(a.n_split, a.rows.pos[r] / a.split_len + 1);
+  const float* pp = a.part + ((long)r * a.nq + h) * a.n_split * (hd + 2);
   const float m = lane < ns ? pp[lane * (hd + 2)] : -INFINITY;
   const float lsum = lane < ns ? pp[lane * (hd + 2) + 1] : 0.f;
   const float M = wave_max(m);
@@ -602,10 +669,21 @@ static void launch_hd(const AttnArgs& a, hipStream_t st) {
 void launch_attention(int kvdtype, const AttnArgs& a, hipStream_t st) {
   if (kvdtype == 1) {
     dim3 grid(a.B, a.nkv, a.n_split);
-    if (a.hd == 128) hipLaunchKernelGGL(k_attn_mfma<128>, grid, dim3(256), 0, st, a);
-    else hipLaunchKernelGGL(k_attn_mfma<64>, grid, dim3(256), 0, st, a);
+    if (a.hd == 128) hipLaunchKernelGGL((k_attn_mfma<128, kAttnDepth>), grid, dim3(256), 0, st, a);
+    else hipLaunchKernelGGL((k_attn_mfma<64, kAttnDepth>), grid, dim3(256), 0, st, a);
   } else {
     if (a.hd == 128) launch_hd<float, 128>(a, st); else launch_hd<float, 64>(a, st);
+  }
+}
+
+void launch_rows_qkv(int kvdtype, const AttnArgs& a, float* q_out, hipStream_t st) {
+  dim3 grid(a.rows.max_rows, (a.nq + a.nkv + 3) / 4);
+  if (kvdtype == 1) {
+    if (a.hd == 128) hipLaunchKernelGGL((k_rows_qkv<bf16_t, 128>), grid, dim3(256), 0, st, a, q_out);
+    else hipLaunchKernelGGL((k_rows_qkv<bf16_t, 64>), grid, dim3(256), 0, st, a, q_out);
+  } else {
+    if (a.hd == 128) hipLaunchKernelGGL((k_rows_qkv<float, 128>), grid, dim3(256), 0, st, a, q_out);
+    else hipLaunchKernelGGL((k_rows_qkv<float, 64>), grid, dim3(256), 0, st, a, q_out);
   }
 }
 

@@ -16,12 +16,21 @@ OSP_DEV float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
 OSP_DEV float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
 OSP_DEV float bf16_to_f32(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 
-// float -> bfloat16, round to nearest, ties to even (NaN stays NaN).
-OSP_DEV bf16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
+// float -> bfloat16, round to nearest, ties to even (NaN stays NaN): one
+// v_cvt_pk_bf16_f32 on gfx950.
+OSP_DEV bf16_t f32_to_bf16(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
+
+// Two floats -> packed bfloat16 pair (lo in bits 0..15), one conversion instruction.
+OSP_DEV uint32_t f32x2_to_bf16x2(float lo, float hi) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// Split two floats into bf16 pairs hi = bf16(x), lo = bf16(x - hi).
+OSP_DEV void split_bf16x2(float a, float b, uint32_t& hi, uint32_t& lo) {
+  hi = f32x2_to_bf16x2(a, b);
+  lo = f32x2_to_bf16x2(a - __uint_as_float(hi << 16), b - __uint_as_float(hi & 0xffff0000u));
 }
 
 template <typename T> OSP_DEV float load_f32(const T* p, long i);

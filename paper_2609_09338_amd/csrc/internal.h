@@ -91,6 +91,20 @@ int launch_gemm(SrcKind src, EpiKind epi, const GemvArgs& a, hipStream_t st);
 bool gemm_use_mfma(int wdtype, int rows);
 int gemm_rows_per_block(EpiKind epi);
 
+// LM head on the matrix cores for 1..64 rows per pass (inputs: RMSNorm_final(x) as
+// bf16 hi / lo in xa_hi / xa_lo, rows gathered through `gather`).  One softmax record
+// per wavefront and row covers blk_rows consecutive logits; nblk records per row.
+struct LmPlan {
+  int mt;        // M tiles of 16 rows
+  int grid;      // blocks
+  int T;         // 16-row weight tiles per wavefront
+  int nblk;      // records per row
+  int blk_rows;  // logits per record (16 T)
+};
+constexpr int kLmMaxRows = 64;
+LmPlan lm_head_plan(int rows, int N, int n_cu);
+void launch_lm_head(const GemvArgs& a, const LmPlan& p, hipStream_t st);
+
 // Row kernels of the matrix-core path: one block per row.
 struct RowArgs {
   int max_rows;
@@ -154,7 +168,10 @@ struct AttnArgs {
   int kv_block;
   int nq, nkv, hd;
   float scale;
-  int n_split;
+  int n_split;              // grid splits; split sp covers positions [sp * split_len, + split_len)
+  int split_len;            // tokens per split (multiple of 64; 0: ceil(n_ctx / n_split) per sequence)
+  const float* q_prep;      // [rows][nq][hd] queries already normalised, rotated and scaled, with
+                            // the new keys/values already in the cache (nullable: done here)
   float* part;              // [rows][nq][n_split][hd + 2]
   float* o;                 // [rows][nq*hd]
   uint16_t* o_hi;           // matrix-core path: o as bf16 hi / lo pairs instead (nullable)
@@ -162,6 +179,9 @@ struct AttnArgs {
   uint32_t* err;
 };
 void launch_attention(int kvdtype, const AttnArgs& a, hipStream_t st);
+// Matrix-core path: per row, sum the QKV split partials, normalise and rotate q
+// and k, write q * (1/sqrt(hd)) to q_out and the new k, v into the cache.
+void launch_rows_qkv(int kvdtype, const AttnArgs& a, float* q_out, hipStream_t st);
 void launch_attn_combine(const AttnArgs& a, hipStream_t st);
 
 // Sampling from the LM-head block statistics.

@@ -43,6 +43,8 @@ int ok() {
   } while (0)
 
 constexpr int kMaxSplit = 64;
+constexpr int kMaxSplitLen = 4096;
+constexpr int kEvenSplitLen = 1024;   // longer splits save little and unbalance ragged batches
 constexpr int kVerifyChunk = 4096;
 
 enum SlotState { S_EMPTY = 0, S_READY = 1, S_DRAFTED = 2, S_VERIFIED = 3 };
@@ -180,6 +182,8 @@ int validate(const osprey_config* c) {
   if (c->max_batch < 1 || c->max_batch > kMaxBatch) return fail(OSPREY_E_INVALID, "max_batch %d not in [1, %d]", c->max_batch, kMaxBatch);
   if (c->max_k < 0 || c->max_k > 64) return fail(OSPREY_E_INVALID, "max_k %d not in [0, 64]", c->max_k);
   if (c->max_seq_len < 1) return fail(OSPREY_E_INVALID, "max_seq_len %d", c->max_seq_len);
+  if (c->max_seq_len > kMaxSplit * kMaxSplitLen)
+    return fail(OSPREY_E_UNSUPPORTED, "max_seq_len %d > %d", c->max_seq_len, kMaxSplit * kMaxSplitLen);
   if (c->kv_block != 16) return fail(OSPREY_E_UNSUPPORTED, "kv_block %d (supported: 16)", c->kv_block);
   if (c->kv_num_blocks < 1) return fail(OSPREY_E_INVALID, "kv_num_blocks %d", c->kv_num_blocks);
   if (c->max_new_rows < 1) return fail(OSPREY_E_INVALID, "max_new_rows %d", c->max_new_rows);
@@ -198,6 +202,7 @@ struct TimerRec {
 struct osprey_handle {
   osprey_config cfg;
   Dims D;
+  int n_cu = 1;         // compute units of the device (grid of the LM head)
   osprey_weights w;
   std::vector<osprey_layer_weights> layers;
   void* kv;
@@ -255,9 +260,33 @@ int hip_last() {
   return ok();
 }
 
+// Context splits of the attention: fixed-length pieces (a multiple of one page).
+// Every block pays a fixed start-up (query staging, page-table and first page
+// latency) and end (wavefront merge, partial write), so splits are as long as
+// possible while the grid still holds about 320 working blocks (a little over one
+// per CU), but not beyond kEvenSplitLen tokens, so that sequences of very different
+// lengths still split into blocks of about equal work; no sequence needs more than
+// kMaxSplit of them, and a split is at most kMaxSplitLen tokens (64 pages per
+// wavefront of the attention kernel).
+struct SplitPlan {
+  int n_split, split_len;
+};
+SplitPlan plan_splits(const osprey_handle* h, long ctx_max, long ctx_total) {
+  const long target_blocks = 320;
+  long len = (ctx_total * h->cfg.n_kv_heads + target_blocks - 1) / target_blocks;
+  len = std::min<long>(std::max<long>(len, 64), kEvenSplitLen);
+  len = std::max<long>(len, (ctx_max + kMaxSplit - 1) / kMaxSplit);
+  len = std::min<long>(len, kMaxSplitLen);
+  len = (len + 15) / 16 * 16;
+  SplitPlan p;
+  p.split_len = (int)len;
+  p.n_split = (int)std::max<long>(1, (ctx_max + len - 1) / len);
+  return p;
+}
+
 // One forward pass of the body over `rows`; `s` holds the conditioning rows.
 void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, const float* s,
-              bool from_embed, int n_split, int rows_per_seq) {
+              bool from_embed, const SplitPlan& sp, int rows_per_seq) {
   const osprey_config& c = h->cfg;
   const Ws& W = h->W;
   const int d = c.d_model, hd = c.head_dim, nq = c.n_q_heads, nkv = c.n_kv_heads;
@@ -317,7 +346,8 @@ void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, c
     a.nkv = nkv;
     a.hd = hd;
     a.scale = 1.0f / std::sqrt((float)hd);
-    a.n_split = n_split;
+    a.n_split = sp.n_split;
+    a.split_len = sp.split_len;
     a.part = W.attn_part;
     a.o = W.o;
     a.err = W.err;
@@ -377,7 +407,7 @@ void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, c
 // leaves RMSNorm_final(x) for the LM head.  `s_src` holds the conditioning rows,
 // or is null when they are the tap projection's `ks_taps` partial sums.
 void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, const float* s_src,
-                 int ks_taps, int n_split, int rows_per_seq) {
+                 int ks_taps, const SplitPlan& sp, int rows_per_seq) {
   const osprey_config& c = h->cfg;
   const Ws& W = h->W;
   const int d = c.d_model, hd = c.head_dim, nq = c.n_q_heads, nkv = c.n_kv_heads, F = c.d_ffn;
@@ -454,12 +484,15 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     a.nkv = nkv;
     a.hd = hd;
     a.scale = 1.0f / std::sqrt((float)hd);
-    a.n_split = n_split;
+    a.n_split = sp.n_split;
+    a.split_len = sp.split_len;
     a.part = W.attn_part;
     a.o = W.o;
     a.o_hi = W.xa_hi;
     a.o_lo = W.xa_lo;
     a.err = W.err;
+    launch_rows_qkv(c.dtype, a, W.o, h->stream);
+    a.q_prep = W.o;
     t = h->t_begin(1);
     launch_attention(c.dtype, a, h->stream);
     h->t_end(t);
@@ -508,10 +541,18 @@ void run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, cons
               const float* u, float* logits, long ld_b, int32_t* drafts_out) {
   const osprey_config& c = h->cfg;
   const Ws& W = h->W;
-  const GemvShape sh = gemv_shape(c.dtype, EPI_LOGITS, B, c.vocab_draft, c.d_model);
-  const int tn = sh.rows_per_wave;
-  const int nblk = sh.waves;
   const bool mr = gemm_use_mfma(c.dtype, B);
+  int tn, nblk;
+  LmPlan lp{};
+  if (mr) {
+    lp = lm_head_plan(std::min(B, kLmMaxRows), c.vocab_draft, h->n_cu);
+    tn = lp.blk_rows;
+    nblk = lp.nblk;
+  } else {
+    const GemvShape sh = gemv_shape(c.dtype, EPI_LOGITS, B, c.vocab_draft, c.d_model);
+    tn = sh.rows_per_wave;
+    nblk = sh.waves;
+  }
   GemvArgs g{};
   g.max_rows = B;
   g.xin = W.x;
@@ -533,8 +574,25 @@ void run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, cons
   g.part = W.lm_part;
   g.nblk = nblk;
   int t = h->t_begin(0);
-  if (mr) launch_gemm(SRC_PREP, EPI_LOGITS, g, h->stream);
-  else launch_gemv(c.dtype, SRC_NORM, EPI_LOGITS, g, h->stream);
+  if (mr) {
+    // passes of at most kLmMaxRows rows, all with the same record layout
+    for (int r0 = 0; r0 < B; r0 += kLmMaxRows) {
+      GemvArgs p = g;
+      p.max_rows = std::min(kLmMaxRows, B - r0);
+      if (gather) {
+        p.gather = gather + r0;
+      } else {
+        p.xa_hi = W.xa_hi + (long)r0 * c.d_model;
+        p.xa_lo = W.xa_lo + (long)r0 * c.d_model;
+      }
+      p.y = g.y + (long)r0 * g.ld_logits;
+      p.temp = temp + r0;
+      p.part = W.lm_part + (long)r0 * nblk * 4;
+      launch_lm_head(p, lp, h->stream);
+    }
+  } else {
+    launch_gemv(c.dtype, SRC_NORM, EPI_LOGITS, g, h->stream);
+  }
   h->t_end(t);
   SampleArgs s{};
   s.B = B;
@@ -560,12 +618,6 @@ void run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, cons
   s.d = c.d_model;
   s.gfb = W.gfb;
   launch_sample(s, h->stream);
-}
-
-int pick_split(const osprey_handle* h, int B, long ctx) {
-  const int by_len = (int)std::max<long>(1, (ctx + 63) / 64);
-  const int by_grid = std::max(1, 1024 / std::max(1, B * h->cfg.n_kv_heads));
-  return std::max(1, std::min(kMaxSplit, std::min(by_len, by_grid)));
 }
 
 void fill_verify_common(osprey_handle* h, VerifyArgs& v, int B, int K) {
@@ -623,12 +675,16 @@ OSPREY_API int osprey_draft_init(const osprey_config* cfg, const osprey_weights*
   if (kv_bytes < osprey_kv_bytes(cfg)) return fail(OSPREY_E_CAPACITY, "kv_bytes %zu < %zu", kv_bytes, osprey_kv_bytes(cfg));
   const size_t need = plan(*cfg, nullptr, nullptr);
   if (ws_bytes < need) return fail(OSPREY_E_CAPACITY, "ws_bytes %zu < %zu", ws_bytes, need);
-  int ndev = 0;
+  int ndev = 0, dev = 0, n_cu = 0;
   if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) return fail(OSPREY_E_DEVICE, "no HIP device");
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 1)
+    return fail(OSPREY_E_DEVICE, "querying the compute-unit count failed");
 
   osprey_handle* h = new osprey_handle();
   h->cfg = *cfg;
   h->D = dims_of(*cfg);
+  h->n_cu = n_cu;
   h->w = *w;
   h->layers.assign(w->layers, w->layers + cfg->n_layers);
   h->w.layers = h->layers.data();
@@ -762,7 +818,7 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
   if (a->taps_stride < 0) return fail(OSPREY_E_INVALID, "taps_stride < 0");
   if (pending && a->taps_stride == 0) return fail(OSPREY_E_INVALID, "pending mode needs taps_stride > 0");
   std::vector<char> seen(c.max_batch, 0);
-  long rows = 0, ctx_max = 0;
+  long rows = 0, ctx_max = 0, ctx_total = 0;
   int max_new = 0;
   for (int b = 0; b < B; ++b) {
     const int slot = a->slots[b];
@@ -787,6 +843,7 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
     rows += n;
     max_new = std::max(max_new, n);
     ctx_max = std::max(ctx_max, need);
+    ctx_total += need;
   }
   if (rows > h->D.Rmax) return fail(OSPREY_E_CAPACITY, "%ld new rows exceed the workspace's %d", rows, h->D.Rmax);
   if (!pending && rows > std::max(c.max_new_rows, c.max_batch * (c.max_k + 1)))
@@ -840,7 +897,7 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
   gt.y = W.s;
   gt.ldy = c.d_model;
   gt.split_buf = W.split;
-  const int split = pick_split(h, B, ctx_max);
+  const SplitPlan split = plan_splits(h, ctx_max, ctx_total);
   if (gemm_use_mfma(c.dtype, (int)rows)) {
     const int ks_taps = launch_gemm(SRC_TAPS, EPI_STORE, gt, h->stream);
     run_body_mr(h, ing, W.cu, B, nullptr, ks_taps, split, max_new);

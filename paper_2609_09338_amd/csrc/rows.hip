@@ -15,16 +15,9 @@ namespace osp {
 constexpr int kRowThreads = 256;
 
 OSP_DEV void store_pair4(uint16_t* hi, uint16_t* lo, long o, float4 v) {
-  const float f[4] = {v.x, v.y, v.z, v.w};
   uint32_t h[2], l[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const bf16_t h0 = f32_to_bf16(f[2 * i]), h1 = f32_to_bf16(f[2 * i + 1]);
-    const bf16_t l0 = f32_to_bf16(f[2 * i] - bf16_to_f32(h0));
-    const bf16_t l1 = f32_to_bf16(f[2 * i + 1] - bf16_to_f32(h1));
-    h[i] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-    l[i] = (uint32_t)l0 | ((uint32_t)l1 << 16);
-  }
+  split_bf16x2(v.x, v.y, h[0], l[0]);
+  split_bf16x2(v.z, v.w, h[1], l[1]);
   *reinterpret_cast<uint2*>(hi + o) = make_uint2(h[0], h[1]);
   *reinterpret_cast<uint2*>(lo + o) = make_uint2(l[0], l[1]);
 }
