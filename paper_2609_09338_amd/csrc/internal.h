@@ -91,8 +91,8 @@ int launch_gemm(SrcKind src, EpiKind epi, const GemvArgs& a, hipStream_t st);
 bool gemm_use_mfma(int wdtype, int rows);
 int gemm_rows_per_block(EpiKind epi);
 
-// LM head on the matrix cores for 1..64 rows per pass (inputs: RMSNorm_final(x) as
-// bf16 hi / lo in xa_hi / xa_lo, rows gathered through `gather`).  One softmax record
+// LM head on the matrix cores for 1..64 rows per pass (inputs: RMSNorm_final(x),
+// rows gathered through `gather`).  One softmax record
 // per wavefront and row covers blk_rows consecutive logits; nblk records per row.
 struct LmPlan {
   int mt;        // M tiles of 16 rows
@@ -103,7 +103,9 @@ struct LmPlan {
 };
 constexpr int kLmMaxRows = 64;
 LmPlan lm_head_plan(int rows, int N, int n_cu);
-void launch_lm_head(const GemvArgs& a, const LmPlan& p, hipStream_t st);
+// norm_in: inputs are the fp32 rows xin (ldx, gathered), normalised with gamma / eps
+// in the kernel; else prepared pairs xa_hi / xa_lo.
+void launch_lm_head(const GemvArgs& a, const LmPlan& p, bool norm_in, hipStream_t st);
 
 // Row kernels of the matrix-core path: one block per row.
 struct RowArgs {

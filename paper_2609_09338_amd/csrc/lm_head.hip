@@ -8,9 +8,9 @@
 // record (max, sum exp((l - max) / T), lowest argmax) per input row, which the
 // sampling kernel merges.
 //
-// One block per CU (8 wavefronts).  The block copies the prepared inputs (RMSNorm
-// output as bf16 hi / lo pairs, all R <= 16 MT rows, KC columns per phase) into
-// LDS once per phase; after that every wavefront works alone, with no further
+// One block per CU (8 wavefronts).  The block copies the inputs (RMSNorm output as
+// bf16 hi / lo pairs, all R <= 16 MT rows, KC columns per phase; either prepared by
+// the row kernels or normalised here from the fp32 rows) into LDS once per phase; after that every wavefront works alone, with no further
 // block barrier: it streams its T tiles of 16 weight rows in units of 16 rows x
 // 256 columns (8 KB) through a ring of three register buffers (two units in
 // flight while it multiplies the third), each unit feeding 8 K steps of
@@ -37,9 +37,11 @@ constexpr int kLmDepth = 3;               // register ring of units
 // Input columns resident per phase and tiles per wavefront: 8 wavefronts x 5 tiles
 // x 16 rows per CU cover a 152k vocabulary on 256 CUs in one wave of blocks (the
 // register budget, 2 wavefronts per SIMD, allows one block per CU).
-template <int MT> struct LmCfg { static constexpr int KC = 512, TMAX = 5; };
+template <int MT> struct LmCfg { static constexpr int KC = MT == 4 ? 512 : 1024, TMAX = 5; };
 
-template <int MT>
+// NORM: the inputs are the fp32 rows xin (gathered), normalised here (RMSNorm with
+// gain gamma) while they are staged; otherwise they arrive prepared as bf16 pairs.
+template <int MT, bool NORM>
 __global__ void __launch_bounds__(kLmThreads) k_lm_head(GemvArgs a, int T) {
   constexpr int KC = LmCfg<MT>::KC;       // input columns resident per phase
   constexpr int TMAX = LmCfg<MT>::TMAX;   // tiles per wavefront (bound)
@@ -49,6 +51,7 @@ __global__ void __launch_bounds__(kLmThreads) k_lm_head(GemvArgs a, int T) {
   constexpr int NU = TMAX * NCH;          // units per phase (bound)
   __shared__ __attribute__((aligned(16))) bf16_t xh[ROWS * PITCH];
   __shared__ __attribute__((aligned(16))) bf16_t xl[ROWS * PITCH];
+  __shared__ float s_inv[NORM ? ROWS : 1];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wrow = lane & 15, grp = lane >> 4;
@@ -65,7 +68,42 @@ __global__ void __launch_bounds__(kLmThreads) k_lm_head(GemvArgs a, int T) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[j][mt] = lm_f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // Addresses are clamped into the matrix instead of masking the loaded values: a
+  // select on a loaded register would wait for that load and serialise the ring.
+  // Rows past N only produce logits that the epilogue drops; columns past Kd meet
+  // zero inputs in LDS (the clamped weights are finite).
+  auto load_unit = [&](uint4* w, int k0, int u) {
+    const int n = min((t0 + u / NCH) * 16 + wrow, a.N - 1);
+    const int kb = k0 + (u % NCH) * kLmUnit + 8 * grp;
+    const bf16_t* wr = W + (long)n * a.Kd;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks)
+      w[ks] = *reinterpret_cast<const uint4*>(wr + min(kb + 32 * ks, a.Kd - 8));
+  };
   const int nphase = (a.Kd + KC - 1) / KC;
+  const int nu = ntiles * NCH;                          // units per phase
+  uint4 ring[kLmDepth][8];
+  // the first units of a phase are requested before its inputs are staged
+  auto prefetch_phase = [&](int k0) {
+#pragma unroll
+    for (int u = 0; u + 1 < kLmDepth; ++u)
+      if (u < nu) load_unit(ring[u], k0, u);
+  };
+  prefetch_phase(0);
+  if constexpr (NORM) {
+    // RMS of every input row (one wavefront per row)
+    for (int r = wave; r < R; r += kLmWaves) {
+      const float* xr = a.xin + (long)(a.gather ? a.gather[r] : r) * a.ldx;
+      float ss = 0.f;
+      for (int c = lane * 4; c < a.Kd; c += 64 * 4) {
+        const float4 v = *reinterpret_cast<const float4*>(xr + c);
+        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+      }
+      ss = wave_sum(ss);
+      if (lane == 0) s_inv[r] = 1.0f / sqrtf(ss / (float)a.Kd + a.eps);
+    }
+    __syncthreads();
+  }
   for (int ph = 0; ph < nphase; ++ph) {
     const int k0 = ph * KC;
     if (ph > 0) __syncthreads();
@@ -74,38 +112,32 @@ __global__ void __launch_bounds__(kLmThreads) k_lm_head(GemvArgs a, int T) {
       const int r = i / (KC / 8), col = (i - r * (KC / 8)) * 8;
       uint4 h = make_uint4(0u, 0u, 0u, 0u), l = h;
       if (r < R && k0 + col < a.Kd) {
-        const long o = (long)(a.gather ? a.gather[r] : r) * a.ld_xa + k0 + col;
-        h = *reinterpret_cast<const uint4*>(a.xa_hi + o);
-        l = *reinterpret_cast<const uint4*>(a.xa_lo + o);
+        if constexpr (NORM) {
+          const float* xr = a.xin + (long)(a.gather ? a.gather[r] : r) * a.ldx + k0 + col;
+          const float4 v0 = *reinterpret_cast<const float4*>(xr);
+          const float4 v1 = *reinterpret_cast<const float4*>(xr + 4);
+          const uint4 g = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16_t*>(a.gamma) + k0 + col);
+          const float inv = s_inv[r];
+          split_bf16x2(v0.x * inv * bf16_lo(g.x), v0.y * inv * bf16_hi(g.x), h.x, l.x);
+          split_bf16x2(v0.z * inv * bf16_lo(g.y), v0.w * inv * bf16_hi(g.y), h.y, l.y);
+          split_bf16x2(v1.x * inv * bf16_lo(g.z), v1.y * inv * bf16_hi(g.z), h.z, l.z);
+          split_bf16x2(v1.z * inv * bf16_lo(g.w), v1.w * inv * bf16_hi(g.w), h.w, l.w);
+        } else {
+          const long o = (long)(a.gather ? a.gather[r] : r) * a.ld_xa + k0 + col;
+          h = *reinterpret_cast<const uint4*>(a.xa_hi + o);
+          l = *reinterpret_cast<const uint4*>(a.xa_lo + o);
+        }
       }
       *reinterpret_cast<uint4*>(xh + r * PITCH + col) = h;
       *reinterpret_cast<uint4*>(xl + r * PITCH + col) = l;
     }
     __syncthreads();
-    if (ntiles == 0) continue;
 
     // ---- stream this wavefront's units: tile j = u / NCH, columns (u % NCH) * 256 ----
-    const int nu = ntiles * NCH;
-    uint4 ring[kLmDepth][8];
-    // Addresses are clamped into the matrix instead of masking the loaded values: a
-    // select on a loaded register would wait for that load and serialise the ring.
-    // Rows past N only produce logits that the epilogue drops; columns past Kd meet
-    // zero inputs in LDS (the clamped weights are finite).
-    auto load_unit = [&](uint4* w, int u) {
-      const int n = min((t0 + u / NCH) * 16 + wrow, a.N - 1);
-      const int kb = k0 + (u % NCH) * kLmUnit + 8 * grp;
-      const bf16_t* wr = W + (long)n * a.Kd;
-#pragma unroll
-      for (int ks = 0; ks < 8; ++ks)
-        w[ks] = *reinterpret_cast<const uint4*>(wr + min(kb + 32 * ks, a.Kd - 8));
-    };
-#pragma unroll
-    for (int u = 0; u + 1 < kLmDepth; ++u)
-      if (u < nu) load_unit(ring[u], u);
 #pragma unroll
     for (int u = 0; u < NU; ++u) {
       if (u < nu) {
-        if (u + kLmDepth - 1 < nu) load_unit(ring[(u + kLmDepth - 1) % kLmDepth], u + kLmDepth - 1);
+        if (u + kLmDepth - 1 < nu) load_unit(ring[(u + kLmDepth - 1) % kLmDepth], k0, u + kLmDepth - 1);
         // keep each unit's work in place: hoisting later units' LDS reads or loads
         // above this point only raises register pressure
         __builtin_amdgcn_sched_barrier(0);
@@ -126,6 +158,7 @@ __global__ void __launch_bounds__(kLmThreads) k_lm_head(GemvArgs a, int T) {
         }
       }
     }
+    if (ph + 1 < nphase) prefetch_phase(k0 + KC);
   }
   if (ntiles == 0) return;
 
@@ -208,10 +241,17 @@ LmPlan lm_head_plan(int rows, int N, int n_cu) {
   return p;
 }
 
-void launch_lm_head(const GemvArgs& a, const LmPlan& p, hipStream_t st) {
-  if (p.mt == 1) hipLaunchKernelGGL(k_lm_head<1>, dim3(p.grid), dim3(kLmThreads), 0, st, a, p.T);
-  else if (p.mt == 2) hipLaunchKernelGGL(k_lm_head<2>, dim3(p.grid), dim3(kLmThreads), 0, st, a, p.T);
-  else hipLaunchKernelGGL(k_lm_head<4>, dim3(p.grid), dim3(kLmThreads), 0, st, a, p.T);
+void launch_lm_head(const GemvArgs& a, const LmPlan& p, bool norm_in, hipStream_t st) {
+  const dim3 g(p.grid), b(kLmThreads);
+  if (norm_in) {
+    if (p.mt == 1) hipLaunchKernelGGL((k_lm_head<1, true>), g, b, 0, st, a, p.T);
+    else if (p.mt == 2) hipLaunchKernelGGL((k_lm_head<2, true>), g, b, 0, st, a, p.T);
+    else hipLaunchKernelGGL((k_lm_head<4, true>), g, b, 0, st, a, p.T);
+  } else {
+    if (p.mt == 1) hipLaunchKernelGGL((k_lm_head<1, false>), g, b, 0, st, a, p.T);
+    else if (p.mt == 2) hipLaunchKernelGGL((k_lm_head<2, false>), g, b, 0, st, a, p.T);
+    else hipLaunchKernelGGL((k_lm_head<4, false>), g, b, 0, st, a, p.T);
+  }
 }
 
 }  // namespace osp

@@ -541,7 +541,10 @@ void run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, cons
               const float* u, float* logits, long ld_b, int32_t* drafts_out) {
   const osprey_config& c = h->cfg;
   const Ws& W = h->W;
-  const bool mr = gemm_use_mfma(c.dtype, B);
+  // bf16 heads run on the matrix cores at every batch size; the rows come prepared
+  // by the matrix-core body, or are normalised in the head after the vector body
+  const bool mr = c.dtype == OSPREY_BF16;
+  const bool prepared = gemm_use_mfma(c.dtype, B);
   int tn, nblk;
   LmPlan lp{};
   if (mr) {
@@ -584,11 +587,12 @@ void run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, cons
       } else {
         p.xa_hi = W.xa_hi + (long)r0 * c.d_model;
         p.xa_lo = W.xa_lo + (long)r0 * c.d_model;
+        p.xin = W.x + (long)r0 * c.d_model;
       }
       p.y = g.y + (long)r0 * g.ld_logits;
       p.temp = temp + r0;
       p.part = W.lm_part + (long)r0 * nblk * 4;
-      launch_lm_head(p, lp, h->stream);
+      launch_lm_head(p, lp, !prepared, h->stream);
     }
   } else {
     launch_gemv(c.dtype, SRC_NORM, EPI_LOGITS, g, h->stream);
