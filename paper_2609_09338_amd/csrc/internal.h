@@ -107,6 +107,13 @@ LmPlan lm_head_plan(int rows, int N, int n_cu);
 // in the kernel; else prepared pairs xa_hi / xa_lo.
 void launch_lm_head(const GemvArgs& a, const LmPlan& p, bool norm_in, hipStream_t st);
 
+// Projections of passes of at most kLmMaxRows rows on the same streaming kernel:
+// src SRC_PREP (pairs; [xs ; xa] when seg > 0) or SRC_TAPS; with w1 set, the up
+// matrix supplies rows [N, 2N).  Writes K-split partial sums to
+// split_buf[split][max_rows][N or 2N]; returns the number of splits.
+int launch_skinny(SrcKind src, const GemvArgs& a, hipStream_t st);
+int skinny_splits(int rows, int Kd);
+
 // Row kernels of the matrix-core path: one block per row.
 struct RowArgs {
   int max_rows;

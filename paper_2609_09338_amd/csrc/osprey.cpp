@@ -73,6 +73,7 @@ struct Ws {
   uint16_t *s_hi, *s_lo, *xa_hi, *xa_lo;   // matrix-core path inputs (bf16 hi / lo)
   float* attn_part;
   float* split;
+  float* split_s;     // K-split partials of passes of at most kLmMaxRows rows
   float* logits;
   float* lm_part;
   int32_t* drafts;
@@ -151,6 +152,14 @@ size_t plan(const osprey_config& c, char* base, Ws* w) {
   {
     const long nmax = std::max<long>(std::max<long>(D.qkv_rows, 2L * c.d_ffn), d);
     W.split = (float*)take(4L * kMaxKSplit * D.Rmax * nmax);
+    const long rs = kLmMaxRows;
+    const long tap_w = (long)c.n_taps * c.target_hidden;
+    long need = skinny_splits(rs, (int)tap_w) * d;
+    need = std::max<long>(need, skinny_splits(rs, 2 * c.d_model) * (long)D.qkv_rows);
+    need = std::max<long>(need, skinny_splits(rs, c.n_q_heads * c.head_dim) * d);
+    need = std::max<long>(need, skinny_splits(rs, c.d_model) * 2L * c.d_ffn);
+    need = std::max<long>(need, skinny_splits(rs, c.d_ffn) * d);
+    W.split_s = (float*)take(4L * rs * need);
   }
   W.logits = (float*)take(4L * D.B * D.Km * c.vocab_draft);
   W.lm_part = (float*)take(16L * D.B * D.lm_nblk_max);
@@ -410,12 +419,20 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
                  int ks_taps, const SplitPlan& sp, int rows_per_seq) {
   const osprey_config& c = h->cfg;
   const Ws& W = h->W;
+  // passes of at most kLmMaxRows rows stream the weights once with the inputs
+  // resident in LDS; larger passes take the tiled GEMM
+  const bool skinny = rows.max_rows <= kLmMaxRows;
+  float* part = skinny ? W.split_s : W.split;
+  auto gemm = [&](SrcKind src, EpiKind epi, GemvArgs& g) -> int {
+    g.split_buf = part;
+    return skinny ? launch_skinny(src, g, h->stream) : launch_gemm(src, epi, g, h->stream);
+  };
   const int d = c.d_model, hd = c.head_dim, nq = c.n_q_heads, nkv = c.n_kv_heads, F = c.d_ffn;
   const int qkv_w = h->D.qkv_rows;
   RowArgs ra{};
   ra.max_rows = rows.max_rows;
   ra.count = rows.count;
-  ra.part = W.split;
+  ra.part = part;
   ra.x = W.x;
   ra.eps = c.rms_eps;
   ra.out_hi = W.xa_hi;
@@ -437,7 +454,6 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
   GemvArgs gb{};
   gb.max_rows = rows.max_rows;
   gb.count = rows.count;
-  gb.split_buf = W.split;
   gb.xa_hi = W.xa_hi;
   gb.xa_lo = W.xa_lo;
   for (int l = 0; l < c.n_layers; ++l) {
@@ -453,7 +469,7 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     g.w0 = L.w_qkv;
     g.N = qkv_w;
     int t = h->t_begin(4);
-    const int ks_qkv = launch_gemm(SRC_PREP, EPI_STORE, g, h->stream);
+    const int ks_qkv = gemm(SRC_PREP, EPI_STORE, g);
     h->t_end(t);
     // QK-norm + RoPE + KV append, attention (sums the QKV splits), split combine
     AttnArgs a{};
@@ -462,7 +478,7 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     a.bslot = W.bslot;
     a.B = B;
     a.rows_per_seq = rows_per_seq;
-    a.qkv = W.split;
+    a.qkv = part;
     a.qkv_w = qkv_w;
     a.qkv_ks = ks_qkv;
     a.qkv_split = (long)rows.max_rows * qkv_w;
@@ -506,7 +522,7 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     RowArgs rn = ra;
     rn.W = d;
     rn.ldp = d;
-    rn.ks = launch_gemm(SRC_PREP, EPI_STORE, go, h->stream);
+    rn.ks = gemm(SRC_PREP, EPI_STORE, go);
     rn.gamma = L.post_norm;
     launch_rows_resid_norm(rn, h->stream);
     // gate/up, SwiGLU
@@ -519,7 +535,7 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     RowArgs rs = ra;
     rs.W = F;
     rs.ldp = 2 * F;
-    rs.ks = launch_gemm(SRC_PREP, EPI_SWIGLU, gu, h->stream);
+    rs.ks = gemm(SRC_PREP, EPI_SWIGLU, gu);
     launch_rows_swiglu(rs, h->stream);
     // down projection; residual + the next layer's input norm (final norm after the last)
     GemvArgs gd = gb;
@@ -530,7 +546,7 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     RowArgs rd = ra;
     rd.W = d;
     rd.ldp = d;
-    rd.ks = launch_gemm(SRC_PREP, EPI_STORE, gd, h->stream);
+    rd.ks = gemm(SRC_PREP, EPI_STORE, gd);
     rd.gamma = l + 1 < c.n_layers ? h->layers[l + 1].in_norm : h->w.final_norm;
     launch_rows_resid_norm(rd, h->stream);
   }
@@ -903,7 +919,13 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
   gt.split_buf = W.split;
   const SplitPlan split = plan_splits(h, ctx_max, ctx_total);
   if (gemm_use_mfma(c.dtype, (int)rows)) {
-    const int ks_taps = launch_gemm(SRC_TAPS, EPI_STORE, gt, h->stream);
+    int ks_taps;
+    if (rows <= kLmMaxRows) {
+      gt.split_buf = W.split_s;
+      ks_taps = launch_skinny(SRC_TAPS, gt, h->stream);
+    } else {
+      ks_taps = launch_gemm(SRC_TAPS, EPI_STORE, gt, h->stream);
+    }
     run_body_mr(h, ing, W.cu, B, nullptr, ks_taps, split, max_new);
   } else {
     launch_gemv(c.dtype, SRC_TAPS, EPI_STORE, gt, h->stream);

@@ -1,0 +1,339 @@
+// Weight-streaming products on the matrix cores for passes of 1..64 input rows:
+// the vocabulary-aligned LM head and the drafter's projections.
+//
+//   Y[r][n] = X[r] . W[n]        (W row-major [N][K] bf16, fp32 accumulation)
+//
+// LM head (Section 3.3, Eq. 4: head rows indexed by the drafter vocabulary and
+// mapped to target ids through d2t; rows without a target id are masked): the
+// epilogue writes the masked logits and, for every wavefront's contiguous range
+// of vocabulary rows, a softmax record (max, sum exp((l - max) / T), lowest
+// argmax) per input row, which the sampling kernel merges.
+// Projections (tap projection of Eq. 1, expanded QKV of Eq. 2-3, O, gate/up, down):
+// K is split across blocks (blockIdx.y) and every block writes its partial sums
+// to [split][row][N] for the row kernel that follows (gate/up: the up matrix as
+// rows [N, 2N)).
+//
+// A block (8 wavefronts) copies its input columns (all R <= 16 MT rows, as bf16
+// hi / lo pairs) into LDS; after that every wavefront works alone, with no further
+// block barrier: it streams its T tiles of 16 weight rows in units of 16 rows x
+// 256 columns (8 KB) through a ring of three register buffers (two units in
+// flight while it multiplies the third), each unit feeding 8 K steps of
+// v_mfma_f32_16x16x32_bf16 for every M tile, hi and lo (taps are exact bf16: hi
+// only).  Two MFMAs per product keep about 16 significant bits of every input,
+// so the result stays close to fp32.
+//
+// Inputs: prepared pairs (two segments [xs ; xa] for the expanded QKV), fp32 rows
+// normalised here (LM head after the vector body), or bf16 taps rows.
+#include "common.h"
+#include "internal.h"
+
+#include <algorithm>
+
+namespace osp {
+
+typedef __bf16 sk_bf16x8 __attribute__((ext_vector_type(8)));
+typedef float sk_f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kSkWaves = 8;
+constexpr int kSkThreads = kSkWaves * 64;
+constexpr int kSkUnit = 256;              // weight columns per streamed unit
+constexpr int kSkDepth = 3;               // register ring of units
+constexpr int kSkTmaxHead = 5;            // tiles per wavefront (bound): LM head
+constexpr int kSkTmaxProj = 2;            // projections (smaller N, split K)
+
+enum SkSrc { SK_PREP = 0, SK_NORM = 1, SK_TAPS = 2 };
+enum SkEpi { SK_LOGITS = 0, SK_PART = 1 };
+
+// Input columns resident per block and phase: 64 rows x 512 or 32 rows x 1024
+// columns of hi / lo pairs fill 132 KB of LDS.
+template <int MT> struct SkCfg { static constexpr int KC = MT == 4 ? 512 : 1024; };
+
+template <int MT, int SRC, int EPI>
+__global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T) {
+  constexpr int KC = SkCfg<MT>::KC;
+  constexpr int ROWS = 16 * MT;
+  constexpr int PITCH = KC + 8;           // bf16 per LDS row (16-byte skew per row)
+  constexpr int NCH = KC / kSkUnit;       // units per tile and phase
+  constexpr int TMAX = EPI == SK_LOGITS ? kSkTmaxHead : kSkTmaxProj;
+  constexpr int NU = TMAX * NCH;          // units per phase (bound)
+  constexpr bool EXACT = SRC == SK_TAPS;  // bf16 inputs: no lo part
+  __shared__ __attribute__((aligned(16))) bf16_t xh[ROWS * PITCH];
+  __shared__ __attribute__((aligned(16))) bf16_t xl[EXACT ? 8 : ROWS * PITCH];
+  __shared__ float s_inv[SRC == SK_NORM ? ROWS : 1];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wrow = lane & 15, grp = lane >> 4;
+  // rows of this pass: the device-side count when there is one (the host bound may
+  // exceed it, and index rows past it, such as tap_row entries, are stale)
+  const int R = min(a.count ? min(*a.count, a.max_rows) : a.max_rows, ROWS);
+  const int wg = blockIdx.x * kSkWaves + wave;          // record index (LM head)
+  const int NR = (EPI == SK_PART && a.w1) ? 2 * a.N : a.N;   // weight rows
+  const int nt16 = (NR + 15) >> 4;
+  const int t0 = wg * T;
+  const int ntiles = max(0, min(T, nt16 - t0));
+  const int k_lo = EPI == SK_PART ? blockIdx.y * KC : 0;
+  const int k_hi = EPI == SK_PART ? min(a.Kd, k_lo + KC) : a.Kd;
+
+  sk_f32x4 acc[TMAX][MT];
+#pragma unroll
+  for (int j = 0; j < TMAX; ++j)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[j][mt] = sk_f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // Addresses are clamped into the matrix instead of masking the loaded values: a
+  // select on a loaded register would wait for that load and serialise the ring.
+  // Rows past the matrix only produce outputs that the epilogue drops; columns
+  // past Kd meet zero inputs in LDS (the clamped weights are finite).
+  auto load_unit = [&](uint4* w, int k0, int u) {
+    const int n = min((t0 + u / NCH) * 16 + wrow, NR - 1);
+    const int kb = k0 + (u % NCH) * kSkUnit + 8 * grp;
+    const bf16_t* wr = (n < a.N) ? reinterpret_cast<const bf16_t*>(a.w0) + (long)n * a.Kd
+                                 : reinterpret_cast<const bf16_t*>(a.w1) + (long)(n - a.N) * a.Kd;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks)
+      w[ks] = *reinterpret_cast<const uint4*>(wr + min(kb + 32 * ks, a.Kd - 8));
+  };
+  const int nphase = (k_hi - k_lo + KC - 1) / KC;
+  const int nu = ntiles * NCH;                          // units per phase
+  uint4 ring[kSkDepth][8];
+  // the first units of a phase are requested before its inputs are staged
+  auto prefetch_phase = [&](int k0) {
+#pragma unroll
+    for (int u = 0; u + 1 < kSkDepth; ++u)
+      if (u < nu) load_unit(ring[u], k0, u);
+  };
+  prefetch_phase(k_lo);
+  if constexpr (SRC == SK_NORM) {
+    // RMS of every input row (one wavefront per row)
+    for (int r = wave; r < R; r += kSkWaves) {
+      const float* xr = a.xin + (long)(a.gather ? a.gather[r] : r) * a.ldx;
+      float ss = 0.f;
+      for (int c = lane * 4; c < a.Kd; c += 64 * 4) {
+        const float4 v = *reinterpret_cast<const float4*>(xr + c);
+        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+      }
+      ss = wave_sum(ss);
+      if (lane == 0) s_inv[r] = 1.0f / sqrtf(ss / (float)a.Kd + a.eps);
+    }
+    __syncthreads();
+  }
+  for (int ph = 0; ph < nphase; ++ph) {
+    const int k0 = k_lo + ph * KC;
+    if (ph > 0) __syncthreads();
+    // ---- inputs of this phase into LDS (rows past R and columns past k_hi are zero);
+    //      each thread requests a batch of 16-byte pieces before storing any, so the
+    //      copy costs a couple of L2 round trips instead of one per piece ----------------
+    constexpr int ITEMS = ROWS * (KC / 8) / kSkThreads;
+    // (the 64-row LM head holds 80 accumulators: no room for a batch there)
+    constexpr int BATCH = (MT == 4 && EPI == SK_LOGITS) ? 1 : (ITEMS < 4 ? ITEMS : 4);
+    static_assert(ITEMS * kSkThreads == ROWS * (KC / 8) && ITEMS % BATCH == 0, "staging split");
+#pragma unroll 1
+    for (int b0 = 0; b0 < ITEMS; b0 += BATCH) {
+      uint4 hv[BATCH], lv[BATCH];
+#pragma unroll
+      for (int q = 0; q < BATCH; ++q) {
+        const int i = tid + (b0 + q) * kSkThreads;
+        const int r = i / (KC / 8), col = (i - r * (KC / 8)) * 8;
+        const int c = k0 + col;
+        uint4 h = make_uint4(0u, 0u, 0u, 0u), l = h;
+        if (r < R && c < k_hi) {
+          if constexpr (SRC == SK_NORM) {
+            const float* xr = a.xin + (long)(a.gather ? a.gather[r] : r) * a.ldx + c;
+            const float4 v0 = *reinterpret_cast<const float4*>(xr);
+            const float4 v1 = *reinterpret_cast<const float4*>(xr + 4);
+            const uint4 g = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16_t*>(a.gamma) + c);
+            const float inv = s_inv[r];
+            split_bf16x2(v0.x * inv * bf16_lo(g.x), v0.y * inv * bf16_hi(g.x), h.x, l.x);
+            split_bf16x2(v0.z * inv * bf16_lo(g.y), v0.w * inv * bf16_hi(g.y), h.y, l.y);
+            split_bf16x2(v1.x * inv * bf16_lo(g.z), v1.y * inv * bf16_hi(g.z), h.z, l.z);
+            split_bf16x2(v1.z * inv * bf16_lo(g.w), v1.w * inv * bf16_hi(g.w), h.w, l.w);
+          } else if constexpr (SRC == SK_TAPS) {
+            h = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16_t*>(a.taps) +
+                                                (long)a.tap_row[r] * a.ldt + c);
+          } else if (c < a.seg) {
+            const long o = (long)r * a.ld_xs + c;
+            h = *reinterpret_cast<const uint4*>(a.xs_hi + o);
+            l = *reinterpret_cast<const uint4*>(a.xs_lo + o);
+          } else {
+            const long o = (long)(a.gather ? a.gather[r] : r) * a.ld_xa + (c - a.seg);
+            h = *reinterpret_cast<const uint4*>(a.xa_hi + o);
+            l = *reinterpret_cast<const uint4*>(a.xa_lo + o);
+          }
+        }
+        hv[q] = h;
+        lv[q] = l;
+      }
+#pragma unroll
+      for (int q = 0; q < BATCH; ++q) {
+        const int i = tid + (b0 + q) * kSkThreads;
+        const int r = i / (KC / 8), col = (i - r * (KC / 8)) * 8;
+        *reinterpret_cast<uint4*>(xh + r * PITCH + col) = hv[q];
+        if constexpr (!EXACT) *reinterpret_cast<uint4*>(xl + r * PITCH + col) = lv[q];
+      }
+    }
+    __syncthreads();
+
+    // ---- stream this wavefront's units: tile j = u / NCH, columns (u % NCH) * 256 ----
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      if (u < nu) {
+        if (u + kSkDepth - 1 < nu) load_unit(ring[(u + kSkDepth - 1) % kSkDepth], k0, u + kSkDepth - 1);
+        // keep each unit's work in place: hoisting later units' LDS reads or loads
+        // above this point only raises register pressure
+        __builtin_amdgcn_sched_barrier(0);
+        const uint4* w = ring[u % kSkDepth];
+        const int j = u / NCH;
+        const int kl = (u % NCH) * kSkUnit + 8 * grp;   // column within the phase
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) {
+          const sk_bf16x8 bw = *reinterpret_cast<const sk_bf16x8*>(&w[ks]);
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            const int off = (mt * 16 + wrow) * PITCH + kl + 32 * ks;
+            const sk_bf16x8 ah = *reinterpret_cast<const sk_bf16x8*>(xh + off);
+            acc[j][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bw, acc[j][mt], 0, 0, 0);
+            if constexpr (!EXACT) {
+              const sk_bf16x8 al = *reinterpret_cast<const sk_bf16x8*>(xl + off);
+              acc[j][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bw, acc[j][mt], 0, 0, 0);
+            }
+          }
+        }
+      }
+    }
+    if (ph + 1 < nphase) prefetch_phase(k0 + KC);
+  }
+  if (ntiles == 0) return;
+
+  // ---- epilogue: lane holds outputs of rows 16 mt + 4 grp + e, columns tile + wrow ------
+  if constexpr (EPI == SK_PART) {
+    float* pb = a.split_buf + (long)blockIdx.y * a.max_rows * NR;
+#pragma unroll
+    for (int j = 0; j < TMAX; ++j) {
+      if (j < ntiles) {
+        const int n = (t0 + j) * 16 + wrow;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int m = mt * 16 + 4 * grp + e;
+            if (m < R && n < NR) pb[(long)m * NR + n] = acc[j][mt][e];
+          }
+      }
+    }
+    return;
+  } else {
+    float mx[MT][4];
+    int am[MT][4];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) { mx[mt][e] = -INFINITY; am[mt][e] = 0x7fffffff; }
+#pragma unroll
+    for (int j = 0; j < TMAX; ++j) {
+      if (j < ntiles) {
+        const int n = (t0 + j) * 16 + wrow;
+        const bool live = n < a.N && a.d2t[n] >= 0;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int m = mt * 16 + 4 * grp + e;
+            const float lv = live ? acc[j][mt][e] : -INFINITY;
+            acc[j][mt][e] = lv;
+            if (m < R && n < a.N) a.y[(long)m * a.ld_logits + n] = lv;
+            if (lv > mx[mt][e]) { mx[mt][e] = lv; am[mt][e] = n; }
+          }
+      }
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float M = mx[mt][e];
+        int A = am[mt][e];
+#pragma unroll
+        for (int s = 1; s < 16; s <<= 1) {
+          const float om = __shfl_xor(M, s, OSP_WAVE);
+          const int oa = __shfl_xor(A, s, OSP_WAVE);
+          if (om > M || (om == M && oa < A)) { M = om; A = oa; }
+        }
+        mx[mt][e] = M;
+        am[mt][e] = A;
+      }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int m = mt * 16 + 4 * grp + e;
+        const float Tm = m < R ? a.temp[a.row_seq ? a.row_seq[m] : m] : 0.f;
+        float s = 0.f;
+        if (Tm > 0.f && mx[mt][e] > -INFINITY) {
+#pragma unroll
+          for (int j = 0; j < TMAX; ++j)
+            if (j < ntiles && acc[j][mt][e] > -INFINITY) s += __expf((acc[j][mt][e] - mx[mt][e]) / Tm);
+        }
+#pragma unroll
+        for (int sft = 1; sft < 16; sft <<= 1) s += __shfl_xor(s, sft, OSP_WAVE);
+        if (wrow == 0 && m < R) {
+          float* p = a.part + ((long)m * a.nblk + wg) * 4;
+          p[0] = mx[mt][e];
+          p[1] = s;
+          p[2] = __int_as_float(mx[mt][e] > -INFINITY ? am[mt][e] : -1);
+          p[3] = 0.f;
+        }
+      }
+  }
+}
+
+static int sk_mt(int rows) { return rows <= 16 ? 1 : (rows <= 32 ? 2 : 4); }
+
+// ---- LM head ----------------------------------------------------------------------------
+LmPlan lm_head_plan(int rows, int N, int n_cu) {
+  LmPlan p;
+  p.mt = sk_mt(rows);
+  const int nt16 = (N + 15) / 16;
+  // one block per CU (the register budget allows 2 wavefronts per SIMD)
+  p.grid = std::min(n_cu, kGemvMaxWaves / kSkWaves);
+  p.T = (nt16 + p.grid * kSkWaves - 1) / (p.grid * kSkWaves);
+  if (p.T > kSkTmaxHead) {
+    p.T = kSkTmaxHead;
+    p.grid = (nt16 + kSkTmaxHead * kSkWaves - 1) / (kSkTmaxHead * kSkWaves);
+  }
+  p.nblk = (nt16 + p.T - 1) / p.T;
+  p.blk_rows = 16 * p.T;
+  return p;
+}
+
+template <int SRC, int EPI>
+static void sk_launch(int mt, dim3 grid, const GemvArgs& a, int T, hipStream_t st) {
+  if (mt == 1) hipLaunchKernelGGL((k_skinny<1, SRC, EPI>), grid, dim3(kSkThreads), 0, st, a, T);
+  else if (mt == 2) hipLaunchKernelGGL((k_skinny<2, SRC, EPI>), grid, dim3(kSkThreads), 0, st, a, T);
+  else hipLaunchKernelGGL((k_skinny<4, SRC, EPI>), grid, dim3(kSkThreads), 0, st, a, T);
+}
+
+void launch_lm_head(const GemvArgs& a, const LmPlan& p, bool norm_in, hipStream_t st) {
+  if (norm_in) sk_launch<SK_NORM, SK_LOGITS>(p.mt, dim3(p.grid), a, p.T, st);
+  else sk_launch<SK_PREP, SK_LOGITS>(p.mt, dim3(p.grid), a, p.T, st);
+}
+
+// ---- projections --------------------------------------------------------------------------
+int skinny_splits(int rows, int Kd) {
+  const int KC = sk_mt(rows) == 4 ? SkCfg<4>::KC : SkCfg<1>::KC;
+  return (Kd + KC - 1) / KC;
+}
+
+int launch_skinny(SrcKind src, const GemvArgs& a, hipStream_t st) {
+  const int mt = sk_mt(a.max_rows);
+  const int ks = skinny_splits(a.max_rows, a.Kd);
+  const int NR = a.w1 ? 2 * a.N : a.N;
+  const int nt16 = (NR + 15) / 16;
+  // one tile per wavefront unless the grid would exceed about 2 blocks per CU
+  int T = 1;
+  while (T < kSkTmaxProj && (long)((nt16 + kSkWaves * T - 1) / (kSkWaves * T)) * ks > 512) ++T;
+  const dim3 grid((nt16 + kSkWaves * T - 1) / (kSkWaves * T), ks);
+  if (src == SRC_TAPS) sk_launch<SK_TAPS, SK_PART>(mt, grid, a, T, st);
+  else sk_launch<SK_PREP, SK_PART>(mt, grid, a, T, st);
+  return ks;
+}
+
+}  // namespace osp
