@@ -74,7 +74,7 @@ typedef enum { OSPREY_F32 = 0, OSPREY_BF16 = 1 } osprey_dtype;
  * `dtype`; activations and logits are fp32 throughout. */
 typedef struct {
   int32_t n_layers;       /* N retained blocks (Section 3.2) */
-  int32_t d_model;        /* drafter width d (multiple of 64) */
+  int32_t d_model;        /* drafter width d (multiple of 64, at most 4096) */
   int32_t n_q_heads;
   int32_t n_kv_heads;     /* divides n_q_heads; query head h reads kv head h*n_kv/n_q */
   int32_t head_dim;       /* 64 or 128 */

@@ -177,6 +177,7 @@ int validate(const osprey_config* c) {
   if (!c) return fail(OSPREY_E_INVALID, "config is NULL");
   if (c->n_layers < 1 || c->n_layers > 64) return fail(OSPREY_E_INVALID, "n_layers %d not in [1, 64]", c->n_layers);
   if (c->d_model < 64 || c->d_model % 64) return fail(OSPREY_E_SHAPE, "d_model %d must be a positive multiple of 64", c->d_model);
+  if (c->d_model > 4096) return fail(OSPREY_E_UNSUPPORTED, "d_model %d > 4096", c->d_model);
   if (c->d_ffn < 64 || c->d_ffn % 64) return fail(OSPREY_E_SHAPE, "d_ffn %d must be a positive multiple of 64", c->d_ffn);
   if (c->n_q_heads < 1 || c->n_kv_heads < 1 || c->n_q_heads % c->n_kv_heads)
     return fail(OSPREY_E_SHAPE, "n_kv_heads %d must divide n_q_heads %d", c->n_kv_heads, c->n_q_heads);

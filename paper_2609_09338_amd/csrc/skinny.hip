@@ -39,7 +39,7 @@ constexpr int kSkThreads = kSkWaves * 64;
 constexpr int kSkUnit = 256;              // weight columns per streamed unit
 constexpr int kSkDepth = 3;               // register ring of units
 constexpr int kSkTmaxHead = 5;            // tiles per wavefront (bound): LM head
-constexpr int kSkTmaxProj = 2;            // projections (smaller N, split K)
+constexpr int kSkTmaxProj = 1;            // projections: one tile, K split across blocks
 
 enum SkSrc { SK_PREP = 0, SK_NORM = 1, SK_TAPS = 2 };
 enum SkEpi { SK_LOGITS = 0, SK_PART = 1 };
@@ -48,8 +48,10 @@ enum SkEpi { SK_LOGITS = 0, SK_PART = 1 };
 // columns of hi / lo pairs fill 132 KB of LDS.
 template <int MT> struct SkCfg { static constexpr int KC = MT == 4 ? 512 : 1024; };
 
+// T: tiles per wavefront (LM head); kc: K columns per block (projections, a multiple
+// of 256 up to KC).
 template <int MT, int SRC, int EPI>
-__global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T) {
+__global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc) {
   constexpr int KC = SkCfg<MT>::KC;
   constexpr int ROWS = 16 * MT;
   constexpr int PITCH = KC + 8;           // bf16 per LDS row (16-byte skew per row)
@@ -71,8 +73,9 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T) {
   const int nt16 = (NR + 15) >> 4;
   const int t0 = wg * T;
   const int ntiles = max(0, min(T, nt16 - t0));
-  const int k_lo = EPI == SK_PART ? blockIdx.y * KC : 0;
-  const int k_hi = EPI == SK_PART ? min(a.Kd, k_lo + KC) : a.Kd;
+  const int k_lo = EPI == SK_PART ? blockIdx.y * kc : 0;
+  const int k_hi = EPI == SK_PART ? min(a.Kd, k_lo + kc) : a.Kd;
+  const int nch = EPI == SK_PART ? kc / kSkUnit : NCH;  // units per tile and phase
 
   sk_f32x4 acc[TMAX][MT];
 #pragma unroll
@@ -85,8 +88,8 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T) {
   // Rows past the matrix only produce outputs that the epilogue drops; columns
   // past Kd meet zero inputs in LDS (the clamped weights are finite).
   auto load_unit = [&](uint4* w, int k0, int u) {
-    const int n = min((t0 + u / NCH) * 16 + wrow, NR - 1);
-    const int kb = k0 + (u % NCH) * kSkUnit + 8 * grp;
+    const int n = min((t0 + u / nch) * 16 + wrow, NR - 1);
+    const int kb = k0 + (u % nch) * kSkUnit + 8 * grp;
     const bf16_t* wr = (n < a.N) ? reinterpret_cast<const bf16_t*>(a.w0) + (long)n * a.Kd
                                  : reinterpret_cast<const bf16_t*>(a.w1) + (long)(n - a.N) * a.Kd;
 #pragma unroll
@@ -94,7 +97,7 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T) {
       w[ks] = *reinterpret_cast<const uint4*>(wr + min(kb + 32 * ks, a.Kd - 8));
   };
   const int nphase = (k_hi - k_lo + KC - 1) / KC;
-  const int nu = ntiles * NCH;                          // units per phase
+  const int nu = ntiles * nch;                          // units per phase
   uint4 ring[kSkDepth][8];
   // the first units of a phase are requested before its inputs are staged
   auto prefetch_phase = [&](int k0) {
@@ -182,7 +185,7 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T) {
         // above this point only raises register pressure
         __builtin_amdgcn_sched_barrier(0);
         const uint4* w = ring[u % kSkDepth];
-        const int j = u / NCH;
+        const int j = u / NCH;                        // (projections: one tile, j = 0)
         const int kl = (u % NCH) * kSkUnit + 8 * grp;   // column within the phase
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) {
@@ -305,34 +308,45 @@ LmPlan lm_head_plan(int rows, int N, int n_cu) {
 }
 
 template <int SRC, int EPI>
-static void sk_launch(int mt, dim3 grid, const GemvArgs& a, int T, hipStream_t st) {
-  if (mt == 1) hipLaunchKernelGGL((k_skinny<1, SRC, EPI>), grid, dim3(kSkThreads), 0, st, a, T);
-  else if (mt == 2) hipLaunchKernelGGL((k_skinny<2, SRC, EPI>), grid, dim3(kSkThreads), 0, st, a, T);
-  else hipLaunchKernelGGL((k_skinny<4, SRC, EPI>), grid, dim3(kSkThreads), 0, st, a, T);
+static void sk_launch(int mt, dim3 grid, const GemvArgs& a, int T, int kc, hipStream_t st) {
+  if (mt == 1) hipLaunchKernelGGL((k_skinny<1, SRC, EPI>), grid, dim3(kSkThreads), 0, st, a, T, kc);
+  else if (mt == 2) hipLaunchKernelGGL((k_skinny<2, SRC, EPI>), grid, dim3(kSkThreads), 0, st, a, T, kc);
+  else hipLaunchKernelGGL((k_skinny<4, SRC, EPI>), grid, dim3(kSkThreads), 0, st, a, T, kc);
 }
 
 void launch_lm_head(const GemvArgs& a, const LmPlan& p, bool norm_in, hipStream_t st) {
-  if (norm_in) sk_launch<SK_NORM, SK_LOGITS>(p.mt, dim3(p.grid), a, p.T, st);
-  else sk_launch<SK_PREP, SK_LOGITS>(p.mt, dim3(p.grid), a, p.T, st);
+  if (norm_in) sk_launch<SK_NORM, SK_LOGITS>(p.mt, dim3(p.grid), a, p.T, 0, st);
+  else sk_launch<SK_PREP, SK_LOGITS>(p.mt, dim3(p.grid), a, p.T, 0, st);
 }
 
 // ---- projections --------------------------------------------------------------------------
+// One 16-row tile per wavefront; the K columns per block shrink (down to one 256-column
+// unit) until the grid holds about 256 blocks: each wavefront then waits on few loads,
+// and the launch costs about one load round trip instead of a per-wavefront stream.
+static int skinny_kc(int rows, int N2, int Kd) {
+  const int KC = rows > 32 ? SkCfg<4>::KC : SkCfg<1>::KC;
+  const int nb = (((N2 + 15) / 16) + kSkWaves - 1) / kSkWaves;   // blocks per K range
+  int kc = KC;
+  // (the expanded QKV's partials are summed on load by the attention row kernel, which
+  // takes at most kMaxKSplit of them)
+  while (kc > kSkUnit && (long)nb * ((Kd + kc - 1) / kc) < 256 && (Kd + kc / 2 - 1) / (kc / 2) <= kMaxKSplit)
+    kc /= 2;
+  return kc;
+}
+
 int skinny_splits(int rows, int Kd) {
-  const int KC = sk_mt(rows) == 4 ? SkCfg<4>::KC : SkCfg<1>::KC;
-  return (Kd + KC - 1) / KC;
+  // upper bound over the products of a layer (workspace sizing): the smallest K range
+  return (Kd + kSkUnit - 1) / kSkUnit;
 }
 
 int launch_skinny(SrcKind src, const GemvArgs& a, hipStream_t st) {
   const int mt = sk_mt(a.max_rows);
-  const int ks = skinny_splits(a.max_rows, a.Kd);
   const int NR = a.w1 ? 2 * a.N : a.N;
-  const int nt16 = (NR + 15) / 16;
-  // one tile per wavefront unless the grid would exceed about 2 blocks per CU
-  int T = 1;
-  while (T < kSkTmaxProj && (long)((nt16 + kSkWaves * T - 1) / (kSkWaves * T)) * ks > 512) ++T;
-  const dim3 grid((nt16 + kSkWaves * T - 1) / (kSkWaves * T), ks);
-  if (src == SRC_TAPS) sk_launch<SK_TAPS, SK_PART>(mt, grid, a, T, st);
-  else sk_launch<SK_PREP, SK_PART>(mt, grid, a, T, st);
+  const int kc = skinny_kc(a.max_rows, NR, a.Kd);
+  const int ks = (a.Kd + kc - 1) / kc;
+  const dim3 grid((((NR + 15) / 16) + kSkWaves - 1) / kSkWaves, ks);
+  if (src == SRC_TAPS) sk_launch<SK_TAPS, SK_PART>(mt, grid, a, 1, kc, st);
+  else sk_launch<SK_PREP, SK_PART>(mt, grid, a, 1, kc, st);
   return ks;
 }
 
