@@ -388,6 +388,9 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
   __shared__ float sm_m[4][NV];
   __shared__ float sm_l[4][NV];
   __shared__ __attribute__((aligned(16))) float sm_o[4][NV][OP];
+  // Q^T fragments (hi, lo) in lane order; read from LDS at every page instead of
+  // being held in registers, which leaves room for a deeper page ring
+  __shared__ __attribute__((aligned(16))) uint4 sm_qf[KC][2][64];
 
   const int b = blockIdx.x, g = blockIdx.y, sp = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -446,16 +449,18 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
     // ---- 2. queries: norm + RoPE into LDS, then Q^T fragments as bf16 hi / lo ---------
     stage_queries<bf16_t, HD, NV>(a, sm_q, j0, nvec, r_beg, G, g, wave, lane);
     __syncthreads();
-    uint4 qh[KC], ql[KC];
+    if (wave == 0) {
 #pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      uint32_t h[4], l[4];
+      for (int c = 0; c < KC; ++c) {
+        uint32_t h[4], l[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        split_bf16x2(sm_q[row][32 * c + 8 * grp + 2 * e], sm_q[row][32 * c + 8 * grp + 2 * e + 1], h[e], l[e]);
-      qh[c] = make_uint4(h[0], h[1], h[2], h[3]);
-      ql[c] = make_uint4(l[0], l[1], l[2], l[3]);
+        for (int e = 0; e < 4; ++e)
+          split_bf16x2(sm_q[row][32 * c + 8 * grp + 2 * e], sm_q[row][32 * c + 8 * grp + 2 * e + 1], h[e], l[e]);
+        sm_qf[c][0][lane] = make_uint4(h[0], h[1], h[2], h[3]);
+        sm_qf[c][1][lane] = make_uint4(l[0], l[1], l[2], l[3]);
+      }
     }
+    __syncthreads();
     const int qj = j0 + row;
     const int qpos = qj < nvec ? a.rows.pos[r_beg + qj / G] : -1;
     // consume qpos here: a first use inside the page loop would make every iteration
@@ -473,11 +478,16 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
       const int t0 = (pg_lo + wave + 4 * i) * PG;
       // S^T[token][query]: lane holds tokens 4 grp + e of query `row`
       att_f32x4 sc = att_f32x4{0.f, 0.f, 0.f, 0.f};
+      // (the opaque lane index keeps the compiler from hoisting these reads out of the
+      // page loop into registers)
+      int ql_ = lane;
+      asm volatile("" : "+v"(ql_));
 #pragma unroll
       for (int c = 0; c < KC; ++c) {
         const att_bf16x8 ka = *reinterpret_cast<const att_bf16x8*>(&pg.k[c]);
-        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, *reinterpret_cast<const att_bf16x8*>(&qh[c]), sc, 0, 0, 0);
-        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, *reinterpret_cast<const att_bf16x8*>(&ql[c]), sc, 0, 0, 0);
+        const uint4 qh = sm_qf[c][0][ql_], qlo = sm_qf[c][1][ql_];
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, *reinterpret_cast<const att_bf16x8*>(&qh), sc, 0, 0, 0);
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, *reinterpret_cast<const att_bf16x8*>(&qlo), sc, 0, 0, 0);
       }
       // causal / sequence-end mask; value entries past the sequence end are cleared so
       // that unwritten cache memory cannot reach the products (0 * NaN)
