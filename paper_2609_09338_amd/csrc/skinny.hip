@@ -106,6 +106,13 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
       if (u < nu) load_unit(ring[u], k0, u);
   };
   prefetch_phase(k_lo);
+  // LM head: which of this lane's columns map to a target id (one per tile)
+  int live[TMAX];
+#pragma unroll
+  for (int j = 0; j < TMAX; ++j) {
+    const int n = (t0 + j) * 16 + wrow;
+    live[j] = (EPI == SK_LOGITS && j < ntiles && n < a.N) ? (a.d2t[n] >= 0) : 0;
+  }
   if constexpr (SRC == SK_NORM) {
     // RMS of every input row (one wavefront per row)
     for (int r = wave; r < R; r += kSkWaves) {
@@ -225,66 +232,118 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
     }
     return;
   } else {
-    float mx[MT][4];
-    int am[MT][4];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) { mx[mt][e] = -INFINITY; am[mt][e] = 0x7fffffff; }
+    // softmax record of every row over this wavefront's 16 T columns.  Lane (wrow, grp)
+    // holds V = 4 MT rows (k = 4 mt + e) of its column in every tile.  The 16 lanes of
+    // a row group are reduced by halving exchanges: at each step a lane keeps half of
+    // its rows and merges the partner's copies of them, so V rows cost about V
+    // shuffles instead of 4 V.
+    constexpr int V = 4 * MT;
+    constexpr int NH = V == 16 ? 4 : (V == 8 ? 3 : 2);    // halving steps (then plain)
+    // masked logits (written here, after the stream: stores issued between the ring's
+    // loads would lengthen every wait on them)
 #pragma unroll
     for (int j = 0; j < TMAX; ++j) {
       if (j < ntiles) {
         const int n = (t0 + j) * 16 + wrow;
-        const bool live = n < a.N && a.d2t[n] >= 0;
+        float* yc = a.y + (long)(4 * grp) * a.ld_logits + n;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const int m = mt * 16 + 4 * grp + e;
-            const float lv = live ? acc[j][mt][e] : -INFINITY;
+            const float lv = live[j] ? acc[j][mt][e] : -INFINITY;
             acc[j][mt][e] = lv;
-            if (m < R && n < a.N) a.y[(long)m * a.ld_logits + n] = lv;
-            if (lv > mx[mt][e]) { mx[mt][e] = lv; am[mt][e] = n; }
+            if (mt * 16 + 4 * grp + e < R && n < a.N) yc[(long)(mt * 16 + e) * a.ld_logits] = lv;
           }
       }
     }
+    float rv[V];
+    int ri[V];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int k = 0; k < V; ++k) {
+      rv[k] = -INFINITY;
+      ri[k] = 0x7fffffff;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        float M = mx[mt][e];
-        int A = am[mt][e];
+      for (int j = 0; j < TMAX; ++j)
+        if (j < ntiles && acc[j][k / 4][k % 4] > rv[k]) { rv[k] = acc[j][k / 4][k % 4]; ri[k] = (t0 + j) * 16 + wrow; }
+    }
+    // (1) max and lowest argmax
 #pragma unroll
-        for (int s = 1; s < 16; s <<= 1) {
-          const float om = __shfl_xor(M, s, OSP_WAVE);
-          const int oa = __shfl_xor(A, s, OSP_WAVE);
-          if (om > M || (om == M && oa < A)) { M = om; A = oa; }
+    for (int st = 0; st < 4; ++st) {
+      const int mask = 8 >> st;
+      if (st < NH) {
+        const int half = V >> (st + 1);
+        const bool up = (lane & mask) != 0;
+#pragma unroll
+        for (int i = 0; i < half; ++i) {
+          const float mv = up ? rv[i + half] : rv[i], ov = up ? rv[i] : rv[i + half];
+          const int mi = up ? ri[i + half] : ri[i], oi = up ? ri[i] : ri[i + half];
+          const float pv = __shfl_xor(ov, mask, OSP_WAVE);
+          const int pi = __shfl_xor(oi, mask, OSP_WAVE);
+          const bool take = pv > mv || (pv == mv && pi < mi);
+          rv[i] = take ? pv : mv;
+          ri[i] = take ? pi : mi;
         }
-        mx[mt][e] = M;
-        am[mt][e] = A;
+      } else {
+        const float pv = __shfl_xor(rv[0], mask, OSP_WAVE);
+        const int pi = __shfl_xor(ri[0], mask, OSP_WAVE);
+        if (pv > rv[0] || (pv == rv[0] && pi < ri[0])) { rv[0] = pv; ri[0] = pi; }
       }
+    }
+    // lane p of the group now holds row k(p) = its top NH bits, read as a number
+    auto row_of_lane = [&](int p) {
+      int k = 0;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+      for (int st = 0; st < NH; ++st) k |= ((p >> (3 - st)) & 1) << (NH - 1 - st);
+      return k;
+    };
+    auto lane_of_row = [&](int k) {
+      int p = 0;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int m = mt * 16 + 4 * grp + e;
-        const float Tm = m < R ? a.temp[a.row_seq ? a.row_seq[m] : m] : 0.f;
-        float s = 0.f;
-        if (Tm > 0.f && mx[mt][e] > -INFINITY) {
+      for (int st = 0; st < NH; ++st) p |= ((k >> (NH - 1 - st)) & 1) << (3 - st);
+      return p;
+    };
+    // (2) every lane fetches the maxima of its V rows and sums its own columns
+    float sv[V];
 #pragma unroll
-          for (int j = 0; j < TMAX; ++j)
-            if (j < ntiles && acc[j][mt][e] > -INFINITY) s += __expf((acc[j][mt][e] - mx[mt][e]) / Tm);
-        }
+    for (int k = 0; k < V; ++k) {
+      const float Mk = __shfl(rv[0], (lane & ~15) | lane_of_row(k), OSP_WAVE);
+      const int m = (k / 4) * 16 + 4 * grp + (k % 4);
+      const float Tk = m < R ? a.temp[a.row_seq ? a.row_seq[m] : m] : 0.f;
+      float sum = 0.f;
+      if (Tk > 0.f && Mk > -INFINITY) {
 #pragma unroll
-        for (int sft = 1; sft < 16; sft <<= 1) s += __shfl_xor(s, sft, OSP_WAVE);
-        if (wrow == 0 && m < R) {
-          float* p = a.part + ((long)m * a.nblk + wg) * 4;
-          p[0] = mx[mt][e];
-          p[1] = s;
-          p[2] = __int_as_float(mx[mt][e] > -INFINITY ? am[mt][e] : -1);
-          p[3] = 0.f;
-        }
+        for (int j = 0; j < TMAX; ++j)
+          if (j < ntiles && acc[j][k / 4][k % 4] > -INFINITY) sum += __expf((acc[j][k / 4][k % 4] - Mk) / Tk);
       }
+      sv[k] = sum;
+    }
+    // (3) sums, reduced like the maxima
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      const int mask = 8 >> st;
+      if (st < NH) {
+        const int half = V >> (st + 1);
+        const bool up = (lane & mask) != 0;
+#pragma unroll
+        for (int i = 0; i < half; ++i) {
+          const float mv = up ? sv[i + half] : sv[i], ov = up ? sv[i] : sv[i + half];
+          sv[i] = mv + __shfl_xor(ov, mask, OSP_WAVE);
+        }
+      } else {
+        sv[0] += __shfl_xor(sv[0], mask, OSP_WAVE);
+      }
+    }
+    if ((lane & ((16 >> NH) - 1)) == 0) {
+      const int k = row_of_lane(lane & 15);
+      const int m = (k / 4) * 16 + 4 * grp + (k % 4);
+      if (m < R) {
+        float* p = a.part + ((long)m * a.nblk + wg) * 4;
+        p[0] = rv[0];
+        p[1] = sv[0];
+        p[2] = __int_as_float(rv[0] > -INFINITY ? ri[0] : -1);
+        p[3] = 0.f;
+      }
+    }
   }
 }
 
