@@ -47,13 +47,18 @@ OSP_DEV void block_stats(float& m, int& am, double& s, float* sm, int* si, doubl
   s = gs;
 }
 
+// One wavefront per chunk (job): lane l reads ids l, l + 64, ... of the chunk (every
+// load is 256 contiguous bytes), keeps them in registers for the max and the float64
+// sum, and the chunk needs no block barrier.  Four jobs per block.
+constexpr int kVWaveElems = 4096 / 64;   // elements per lane (chunk / 64)
+
 __global__ void __launch_bounds__(kVThreads) k_vstats(VerifyArgs a) {
-  __shared__ float sm[4];
-  __shared__ int si[4];
-  __shared__ double sd[4];
-  const int b = blockIdx.x, j = blockIdx.y;
-  const int tid = threadIdx.x;
+  const int b = blockIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int j = blockIdx.y * (kVThreads / 64) + (threadIdx.x >> 6);
   const int nt = (a.K + 1) * a.nchunk_t;
+  const int nj = nt + a.K * a.nchunk_d;
+  if (j >= nj) return;
   const float* row;
   int V, c;
   if (j < nt) {
@@ -69,34 +74,32 @@ __global__ void __launch_bounds__(kVThreads) k_vstats(VerifyArgs a) {
     V = a.V_d;
   }
   const int i0 = c * a.chunk, i1 = min(V, i0 + a.chunk);
-  float v[kVPer];
+  float v[kVWaveElems];
 #pragma unroll
-  for (int q = 0; q < kVPer; ++q) {
-    const int i = i0 + tid + q * kVThreads;
+  for (int q = 0; q < kVWaveElems; ++q) {
+    const int i = i0 + lane + q * 64;
     v[q] = i < i1 ? row[i] : -INFINITY;
   }
   float m = -INFINITY;
   int am = 0x7fffffff;
 #pragma unroll
-  for (int q = 0; q < kVPer; ++q)
-    if (v[q] > m) { m = v[q]; am = i0 + tid + q * kVThreads; }
-  double dummy = 0.0;
-  block_stats(m, am, dummy, sm, si, sd);
+  for (int q = 0; q < kVWaveElems; ++q)
+    if (v[q] > m) { m = v[q]; am = i0 + lane + q * 64; }   // ascending ids: first hit is lowest
+  const float M = wave_max(m);
+  const int A = wave_min_i((m == M && m > -INFINITY) ? am : 0x7fffffff);
   const float T = a.temp[b];
   double se = 0.0;   // float64 sums: exactness of the 10^5-entry CDFs that follow
-  if (T > 0.f && m > -INFINITY) {
+  if (T > 0.f && M > -INFINITY) {
 #pragma unroll
-    for (int q = 0; q < kVPer; ++q)
-      if (v[q] > -INFINITY) se += (double)__expf((v[q] - m) / T);
+    for (int q = 0; q < kVWaveElems; ++q)
+      if (v[q] > -INFINITY) se += (double)__expf((v[q] - M) / T);
   }
-  int am2 = am;
-  float m2 = m;
-  block_stats(m2, am2, se, sm, si, sd);
-  if (tid == 0) {
-    float* p = a.part + ((long)b * gridDim.y + j) * 4;
-    p[0] = m;
+  se = wave_sum_d(se);
+  if (lane == 0) {
+    float* p = a.part + ((long)b * nj + j) * 4;
+    p[0] = M;
     p[1] = (float)se;
-    p[2] = __int_as_float(m > -INFINITY ? am : -1);
+    p[2] = __int_as_float(M > -INFINITY ? A : -1);
     p[3] = 0.f;
   }
 }
@@ -252,25 +255,46 @@ OSP_DEV ResidRow resid_row(const VerifyArgs& a, int b) {
   return r;
 }
 
+// Per chunk of target row a: the sums of the residual weights and of p.  Only the
+// chunk totals are kept (k_vfinal rescans the chosen chunk in id order), so thread t
+// takes ids t, t + 256, ...: every wavefront load is 256 contiguous bytes, and both
+// sums come from one pass over the row.
 __global__ void __launch_bounds__(kVThreads) k_vresid(VerifyArgs a) {
-  __shared__ double sm[4];
+  __shared__ double sw_[kVThreads / 64], sp_[kVThreads / 64];
   const int b = blockIdx.x, c = blockIdx.y;
   if (!(a.temp[b] > 0.f)) return;
   const ResidRow rr = resid_row(a, b);
-  // thread t owns the contiguous run [i0 + 16 t, i0 + 16 t + 16) (the same split as the final scan)
-  const int i0 = c * a.chunk + threadIdx.x * kVPer;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i0 = c * a.chunk + tid;
   const int i1 = min(a.V_T, c * a.chunk + a.chunk);
-  double w[kVPer], p[kVPer];
-  rr.eval_many(i0, 1, i1, 0, w);
-  rr.eval_many(i0, 1, i1, 1, p);
+  float tv[kVPer];
+  int sidx[kVPer];
+#pragma unroll
+  for (int q = 0; q < kVPer; ++q) {
+    const int v = i0 + q * kVThreads;
+    const bool in = v < i1;
+    tv[q] = in ? rr.tl[v] : -INFINITY;
+    sidx[q] = (in && rr.dl) ? rr.t2d[v] : -1;
+  }
+  float dv[kVPer];
+#pragma unroll
+  for (int q = 0; q < kVPer; ++q) dv[q] = sidx[q] >= 0 ? rr.dl[sidx[q]] : -INFINITY;
   double sw = 0.0, sp = 0.0;
 #pragma unroll
-  for (int q = 0; q < kVPer; ++q) { sw += w[q]; sp += p[q]; }
+  for (int q = 0; q < kVPer; ++q) {
+    const double p = tv[q] > -INFINITY ? (double)__expf((tv[q] - rr.Mt) / rr.T) * rr.iSt : 0.0;
+    const double qq = dv[q] > -INFINITY ? (double)__expf((dv[q] - rr.Md) / rr.T) * rr.iSd : 0.0;
+    sw += fmax(p - qq, 0.0);
+    sp += p;
+  }
   // fixed-order block sums in float64
-  double incl, tw, tp;
-  block_scan<kVThreads, double>(sw, sm, incl, tw);
-  block_scan<kVThreads, double>(sp, sm, incl, tp);
-  if (threadIdx.x == 0) {
+  sw = wave_sum_d(sw);
+  sp = wave_sum_d(sp);
+  if (lane == 0) { sw_[wave] = sw; sp_[wave] = sp; }
+  __syncthreads();
+  if (tid == 0) {
+    double tw = 0.0, tp = 0.0;
+    for (int w = 0; w < kVThreads / 64; ++w) { tw += sw_[w]; tp += sp_[w]; }
     a.res_part[((long)b * a.nchunk_t + c) * 2 + 0] = tw;
     a.res_part[((long)b * a.nchunk_t + c) * 2 + 1] = tp;
   }
@@ -390,7 +414,7 @@ __global__ void __launch_bounds__(kVThreads) k_vfinal(VerifyArgs a) {
 
 void launch_verify(const VerifyArgs& a, hipStream_t st) {
   const int nj = (a.K + 1) * a.nchunk_t + a.K * a.nchunk_d;
-  hipLaunchKernelGGL(k_vstats, dim3(a.B, nj), dim3(kVThreads), 0, st, a);
+  hipLaunchKernelGGL(k_vstats, dim3(a.B, (nj + kVThreads / 64 - 1) / (kVThreads / 64)), dim3(kVThreads), 0, st, a);
   hipLaunchKernelGGL(k_vaccept, dim3(a.B), dim3(kVThreads), 0, st, a);
   hipLaunchKernelGGL(k_vresid, dim3(a.B, a.nchunk_t), dim3(kVThreads), 0, st, a);
   hipLaunchKernelGGL(k_vfinal, dim3(a.B), dim3(kVThreads), 0, st, a);
