@@ -19,11 +19,14 @@
 // hi / lo pairs, so a block only copies its input chunk into LDS.  The
 // expanded-QKV input [c ; RMSNorm(x)] of Eq. 2-3 is read from its two segments.
 //
-// Block: 4 wavefronts (8 for the LM head) sharing one staged input chunk of 256
-// columns.  K is split across blocks when N alone gives too few blocks; every
-// block writes its partial sums to [split][row][N] (SwiGLU: gate then up, 2 N
+// This kernel serves passes of more than 64 rows (ingest of large batches); it
+// covers them in 64-row passes spread over blockIdx.z.  Block: 8 wavefronts with
+// two 16-row weight tiles each (SwiGLU: a gate tile and its up tile) sharing one
+// staged input chunk of 256 columns, so one chunk serves 256 (SwiGLU 128) output
+// columns.  K is split across blocks (a block walks its chunks one after another);
+// every block writes its partial sums to [split][row][N] (SwiGLU: gate then up, 2 N
 // wide) and the row kernel that follows adds the splits in a fixed order.  The
-// LM head (never split) writes masked logits and one (max, sum exp((l - max)/T),
+// logits kind (never split) writes masked logits and one (max, sum exp((l - max)/T),
 // lowest argmax) record per block of consecutive rows.
 #pragma once
 
@@ -39,12 +42,10 @@ constexpr int kMmRows = 64;          // input rows per pass (4 M tiles)
 constexpr int kMmKc = 256;           // K columns per chunk
 constexpr int kMmPitch = kMmKc + 8;  // LDS row pitch in bf16 (pads banks)
 
-// Block shape per kind: the logits kind (large N, no split) uses 8 wavefronts with
-// two weight tiles each; the others 4 wavefronts with one tile (SwiGLU: a gate
-// tile and its up tile) and split K across blocks when N alone gives too few.
+// Block shape: 8 wavefronts, two weight tiles each.
 template <int EPI> struct MmShape {
-  static constexpr int WAVES = EPI == EPI_LOGITS ? 8 : 4;
-  static constexpr int WT = EPI == EPI_LOGITS ? 2 : (EPI == EPI_SWIGLU ? 2 : 1);
+  static constexpr int WAVES = 8;
+  static constexpr int WT = 2;
   static constexpr int NT = EPI == EPI_SWIGLU ? 1 : WT;   // output tiles per wavefront
   static constexpr int THREADS = WAVES * 64;
   static constexpr int ROWS = WAVES * NT * 16;            // output rows per block
@@ -75,7 +76,8 @@ __global__ void __launch_bounds__(MmShape<EPI>::THREADS) k_gemm_mfma(GemvArgs a,
   const int k_begin = blockIdx.y * chunks_per_split * kMmKc;
   const int k_end = min(a.Kd, k_begin + chunks_per_split * kMmKc);
 
-  for (int r0 = 0; r0 < rows; r0 += kMmRows) {
+  // passes of 64 rows are spread over blockIdx.z (each block: one pass)
+  for (int r0 = blockIdx.z * kMmRows; r0 < rows && r0 < (int)(blockIdx.z + 1) * kMmRows; r0 += kMmRows) {
     const int rcount = min(kMmRows, rows - r0);
     const int mt_n = (rcount + 15) >> 4;                // M tiles in use
     mfma_f32x4 acc[4][kMmWT];
@@ -249,17 +251,16 @@ inline int gemm_mfma_rows_per_block(EpiKind epi) {
                            : (epi == EPI_SWIGLU ? MmShape<EPI_SWIGLU>::ROWS : MmShape<EPI_STORE>::ROWS);
 }
 
-// K splits: enough blocks to cover the chip (about 2 per CU); never for logits.
-// Returns the chunks per split; *ks receives the splits actually used.
-inline int gemm_mfma_split_plan(EpiKind epi, int N, int Kd, int* ks_out) {
+// K splits: a block walks its chunks one after another (load, stage, multiply), so
+// the K range is split as finely as the partial buffer allows (one chunk per block
+// up to kMaxKSplit splits); never for logits.  Returns the chunks per split; *ks
+// receives the splits actually used.
+inline int gemm_mfma_split_plan(EpiKind epi, int N, int Kd, int passes, int* ks_out) {
+  (void)N;
+  (void)passes;
   const int chunks = (Kd + kMmKc - 1) / kMmKc;
   int ks = 1;
-  if (epi != EPI_LOGITS) {
-    const int nb = (N + gemm_mfma_rows_per_block(epi) - 1) / gemm_mfma_rows_per_block(epi);
-    ks = (512 + nb - 1) / nb;
-    ks = ks < 1 ? 1 : (ks > chunks ? chunks : ks);
-    ks = ks > kMaxKSplit ? kMaxKSplit : ks;
-  }
+  if (epi != EPI_LOGITS) ks = chunks > kMaxKSplit ? kMaxKSplit : chunks;
   const int cps = (chunks + ks - 1) / ks;
   *ks_out = (chunks + cps - 1) / cps;
   return cps;
@@ -269,9 +270,10 @@ template <int SRC, int EPI>
 int launch_gemm_mfma_t(const GemvArgs& a, hipStream_t st) {
   const int rpb = gemm_mfma_rows_per_block((EpiKind)EPI);
   const int nb = (a.N + rpb - 1) / rpb;
+  const int passes = (a.max_rows + kMmRows - 1) / kMmRows;
   int ks = 1;
-  const int cps = gemm_mfma_split_plan((EpiKind)EPI, a.N, a.Kd, &ks);
-  hipLaunchKernelGGL((k_gemm_mfma<SRC, EPI>), dim3(nb, ks), dim3(MmShape<EPI>::THREADS), 0, st, a, cps);
+  const int cps = gemm_mfma_split_plan((EpiKind)EPI, a.N, a.Kd, passes, &ks);
+  hipLaunchKernelGGL((k_gemm_mfma<SRC, EPI>), dim3(nb, ks, passes), dim3(MmShape<EPI>::THREADS), 0, st, a, cps);
   return ks;
 }
 
