@@ -13,6 +13,9 @@
 // Projections come either as plain rows or as K-split partial sums (matrix-core
 // path), which are added on load in split order.
 //
+// Blocks are (kv head, work item): the head varies fastest, so the setup kernel's
+// longest-first order of (sequence, split) items holds across heads.
+//
 // k_attn_mfma (bf16 pools): up to 16 query vectors per pass.  Each wavefront
 // walks 16-token pages of the split:
 //   S^T = K Q^T   (tokens x queries; 16x16x32 bf16 MFMA over the head dimension,
@@ -129,6 +132,23 @@ OSP_DEV float qkv_at(const AttnArgs& a, long off) {
   return s;
 }
 
+// Block (kv head blockIdx.x, work item blockIdx.y) -> (sequence, split): from the
+// setup kernel's longest-first list, or split-major when there is none.  False for
+// grid slots past the list.
+OSP_DEV bool attn_block(const AttnArgs& a, int& b, int& sp) {
+  const int it = blockIdx.y;
+  if (a.items) {
+    if (it >= *a.n_items) return false;
+    const int v = a.items[it];
+    b = v & 0xffff;
+    sp = v >> 16;
+  } else {
+    b = it % a.B;
+    sp = it / a.B;
+  }
+  return true;
+}
+
 // New keys/values of rows r_beg..r_end whose position lies in [p_lo, p_hi):
 // k normalised and rotated, both stored into the row's cache page.
 template <typename TKV, int HD>
@@ -197,7 +217,9 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   __shared__ float sm_l[4][QV];
   __shared__ float sm_o[4][QV][HD];
 
-  const int b = blockIdx.x, g = blockIdx.y, sp = blockIdx.z;
+  int b, sp;
+  if (!attn_block(a, b, sp)) return;
+  const int g = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int dseg = (lane & 15) * DPL;  // this lane's head dims
   const int tsub = lane >> 4;          // token within each group of 4
@@ -392,7 +414,9 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
   // being held in registers, which leaves room for a deeper page ring
   __shared__ __attribute__((aligned(16))) uint4 sm_qf[KC][2][64];
 
-  const int b = blockIdx.x, g = blockIdx.y, sp = blockIdx.z;
+  int b, sp;
+  if (!attn_block(a, b, sp)) return;
+  const int g = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int row = lane & 15, grp = lane >> 4;
   int r_beg, r_end;
@@ -666,7 +690,7 @@ __global__ void __launch_bounds__(64) k_attn_combine(AttnArgs a) {
 // at most 8 (head_dim 128) or 16 (head_dim 64) so q + o stay within 128 registers.
 template <typename TKV, int HD>
 static void launch_hd(const AttnArgs& a, hipStream_t st) {
-  dim3 grid(a.B, a.nkv, a.n_split);
+  dim3 grid(a.nkv, a.B * a.n_split);
   const int need = a.rows_per_seq * (a.nq / a.nkv);
   constexpr int QMAX = 1024 / HD;
   if (need <= 1) hipLaunchKernelGGL((k_attn<TKV, HD, 1>), grid, dim3(256), 0, st, a);
@@ -678,7 +702,7 @@ static void launch_hd(const AttnArgs& a, hipStream_t st) {
 
 void launch_attention(int kvdtype, const AttnArgs& a, hipStream_t st) {
   if (kvdtype == 1) {
-    dim3 grid(a.B, a.nkv, a.n_split);
+    dim3 grid(a.nkv, a.B * a.n_split);
     if (a.hd == 128) hipLaunchKernelGGL((k_attn_mfma<128, kAttnDepth>), grid, dim3(256), 0, st, a);
     else hipLaunchKernelGGL((k_attn_mfma<64, kAttnDepth>), grid, dim3(256), 0, st, a);
   } else {

@@ -114,7 +114,7 @@ void launch_lm_head(const GemvArgs& a, const LmPlan& p, bool norm_in, hipStream_
 int launch_skinny(SrcKind src, const GemvArgs& a, hipStream_t st);
 int skinny_splits(int rows, int Kd);
 
-// Row kernels of the matrix-core path: one block per row.
+// Row kernels of the matrix-core path: one block per row (SwiGLU: per column group).
 struct RowArgs {
   int max_rows;
   const int32_t* count;     // device row count (nullable: max_rows)
@@ -179,6 +179,8 @@ struct AttnArgs {
   float scale;
   int n_split;              // grid splits; split sp covers positions [sp * split_len, + split_len)
   int split_len;            // tokens per split (multiple of 64; 0: ceil(n_ctx / n_split) per sequence)
+  const int32_t* items;     // work list from k_setup (b | split << 16), *n_items entries;
+  const int32_t* n_items;   // nullable: block y = split * B + b
   const float* q_prep;      // [rows][nq][hd] queries already normalised, rotated and scaled, with
                             // the new keys/values already in the cache (nullable: done here)
   float* part;              // [rows][nq][n_split][hd + 2]
@@ -249,6 +251,11 @@ struct SetupArgs {
   int32_t* committed;
   int32_t* bslot;
   int32_t* ar_pos;
+  // attention work list (longest first) for splits of split_len positions, sized
+  // for the longest context of the step (ingest + K - 1 draft positions)
+  int split_len;
+  int32_t* attn_items;      // [B * n_split]: b | split << 16
+  int32_t* attn_n_items;
   uint32_t* err;
 };
 void launch_setup(const SetupArgs& a, hipStream_t st);

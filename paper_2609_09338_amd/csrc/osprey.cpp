@@ -69,6 +69,7 @@ struct Ws {
   uint32_t* err;
   int32_t *ing_seq, *ing_pos, *ing_tok, *ing_tap, *n_rows, *cu, *last_row, *committed, *bslot;
   int32_t *ar_pos, *ar_tok;
+  int32_t *attn_items, *attn_n_items;   // attention work list of the current step
   float *x, *s, *gfb, *qkv, *o, *h;
   uint16_t *s_hi, *s_lo, *xa_hi, *xa_lo;   // matrix-core path inputs (bf16 hi / lo)
   float* attn_part;
@@ -135,6 +136,8 @@ size_t plan(const osprey_config& c, char* base, Ws* w) {
   W.bslot = (int32_t*)take(4L * D.B);
   W.ar_pos = (int32_t*)take(4L * D.B);
   W.ar_tok = (int32_t*)take(4L * D.B);
+  W.attn_items = (int32_t*)take(4L * D.B * kMaxSplit);
+  W.attn_n_items = (int32_t*)take(4);
   W.x = (float*)take(4L * D.Rmax * d);
   W.s = (float*)take(4L * D.Rmax * d);
   W.gfb = (float*)take(4L * D.B * d);
@@ -358,6 +361,8 @@ void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, c
     a.scale = 1.0f / std::sqrt((float)hd);
     a.n_split = sp.n_split;
     a.split_len = sp.split_len;
+    a.items = W.attn_items;
+    a.n_items = W.attn_n_items;
     a.part = W.attn_part;
     a.o = W.o;
     a.err = W.err;
@@ -503,6 +508,8 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     a.scale = 1.0f / std::sqrt((float)hd);
     a.n_split = sp.n_split;
     a.split_len = sp.split_len;
+    a.items = W.attn_items;
+    a.n_items = W.attn_n_items;
     a.part = W.attn_part;
     a.o = W.o;
     a.o_hi = W.xa_hi;
@@ -902,6 +909,10 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
   sa.bslot = W.bslot;
   sa.ar_pos = W.ar_pos;
   sa.err = W.err;
+  const SplitPlan split = plan_splits(h, ctx_max, ctx_total);
+  sa.split_len = split.split_len;
+  sa.attn_items = W.attn_items;
+  sa.attn_n_items = W.attn_n_items;
   launch_setup(sa, h->stream);
 
   // ---- ingest: tap projection (Eq. 1) then the body over every new row ------------------
@@ -918,7 +929,6 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
   gt.y = W.s;
   gt.ldy = c.d_model;
   gt.split_buf = W.split;
-  const SplitPlan split = plan_splits(h, ctx_max, ctx_total);
   if (gemm_use_mfma(c.dtype, (int)rows)) {
     int ks_taps;
     if (rows <= kLmMaxRows) {

@@ -1,5 +1,6 @@
 // Row kernels of the matrix-core path (passes of several rows): they close one
-// product and prepare the next one's input.  One block per row:
+// product and prepare the next one's input.  One block per row (SwiGLU, which is
+// elementwise: a row's columns spread over several blocks):
 //   * add the K-split partial sums of the product in split order (fixed order,
 //     so results do not depend on scheduling),
 //   * apply the residual, RMSNorm with gain, or SwiGLU in fp32,
@@ -98,11 +99,12 @@ __global__ void __launch_bounds__(kRowThreads) k_rows_resid_norm(RowArgs a) {
   norm_out(a, r, ss, sm);
 }
 
+// Elementwise: the columns of a row are spread over gridDim.y blocks.
 __global__ void __launch_bounds__(kRowThreads) k_rows_swiglu(RowArgs a) {
   const int r = blockIdx.x;
   const int rows = a.count ? min(*a.count, a.max_rows) : a.max_rows;
   if (r >= rows) return;
-  for (int c = threadIdx.x * 4; c < a.W; c += kRowThreads * 4) {
+  for (int c = (blockIdx.y * kRowThreads + threadIdx.x) * 4; c < a.W; c += gridDim.y * kRowThreads * 4) {
     const float4 g = sum_parts4(a, r, c);
     const float4 u = sum_parts4(a, r, a.W + c);
     const float4 h = make_float4(g.x / (1.0f + __expf(-g.x)) * u.x, g.y / (1.0f + __expf(-g.y)) * u.y,
@@ -118,7 +120,8 @@ void launch_rows_resid_norm(const RowArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(k_rows_resid_norm, dim3(a.max_rows), dim3(kRowThreads), 0, st, a);
 }
 void launch_rows_swiglu(const RowArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(k_rows_swiglu, dim3(a.max_rows), dim3(kRowThreads), 0, st, a);
+  const int per_row = (a.W + kRowThreads * 4 - 1) / (kRowThreads * 4);   // one column group per block
+  hipLaunchKernelGGL(k_rows_swiglu, dim3(a.max_rows, per_row), dim3(kRowThreads), 0, st, a);
 }
 
 }  // namespace osp

@@ -70,6 +70,39 @@ __global__ void __launch_bounds__(kSetupThreads) k_setup(SetupArgs a) {
     a.cu[a.B] = total;
     a.n_rows[0] = total;
   }
+  // ---- attention work list: every split but the last of each sequence covers
+  //      split_len positions; those come first (sequence-major), then the last
+  //      splits by decreasing length, so the longest blocks start first --------------
+  if (a.attn_items) {
+    __shared__ int s_last[kSetupThreads];
+    const int nmax = act ? len + n + (a.K > 0 ? a.K - 1 : 0) : 0;
+    const int ns = act ? (nmax + a.split_len - 1) / a.split_len : 0;
+    const int nfull = ns > 0 ? ns - 1 : 0;
+    const int last = act ? nmax - nfull * a.split_len : -1;
+    s_last[b] = last;
+    int finc = nfull;
+#pragma unroll
+    for (int s = 1; s < 64; s <<= 1) {
+      const int o = __shfl_up(finc, s, OSP_WAVE);
+      if (lane >= s) finc += o;
+    }
+    __syncthreads();
+    if (lane == 63) s_tot[wave] = finc;
+    __syncthreads();
+    int fbefore = 0, ftotal = 0;
+    for (int w = 0; w < kSetupThreads / 64; ++w) {
+      if (w < wave) fbefore += s_tot[w];
+      ftotal += s_tot[w];
+    }
+    if (act) {
+      const int f0 = fbefore + finc - nfull;
+      for (int sp = 0; sp < nfull; ++sp) a.attn_items[f0 + sp] = b | (sp << 16);
+      int rank = 0;
+      for (int o = 0; o < a.B; ++o) rank += (s_last[o] > last || (s_last[o] == last && o < b)) ? 1 : 0;
+      a.attn_items[ftotal + rank] = b | (nfull << 16);
+    }
+    if (b == 0) a.attn_n_items[0] = ftotal + a.B;
+  }
 }
 
 void launch_setup(const SetupArgs& a, hipStream_t st) {
