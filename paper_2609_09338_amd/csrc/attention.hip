@@ -119,6 +119,8 @@ struct Page {
   }
 };
 
+constexpr int kMaxSplitAttn = 64;   // context splits per row (bound; the host keeps to it)
+
 // Element `off` of the projections: the sum of the K-split partials (in split
 // order) on the matrix-core path, else the plain row.
 OSP_DEV float qkv_at(const AttnArgs& a, long off) {
@@ -649,39 +651,58 @@ __global__ void __launch_bounds__(256) k_rows_qkv(AttnArgs a, float* q_out) {
   }
 }
 
-// One wavefront per (row, head): lane t reads split t's (max, sum); the output
-// elements are accumulated over splits with all loads independent.
-__global__ void __launch_bounds__(64) k_attn_combine(AttnArgs a) {
+// One block per (row, head).  Every thread requests its share of the split outputs
+// at once (dimension tid % hd, splits tid / hd, + 256 / hd, ...) while wavefront 0
+// reads the splits' (max, sum); the weights exp(m_s - M) / L come through LDS and the
+// thread groups are added in LDS, in a fixed order.
+template <int HD>
+__global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
+  constexpr int G = 256 / HD;              // thread groups (splits interleaved)
+  constexpr int PER = kMaxSplitAttn / G;   // splits per thread (bound)
+  __shared__ float s_f[kMaxSplitAttn];
+  __shared__ float s_part[G][HD];
   const int r = blockIdx.x, h = blockIdx.y;
   const int rows = a.rows.count ? min(*a.rows.count, a.rows.max_rows) : a.rows.max_rows;
   if (r >= rows) return;
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int e = tid % HD, grp = tid / HD;
   // splits that hold any position visible to this row (later ones were not written)
-  const int hd = a.hd, ns = min(a.n_split, a.rows.pos[r] / a.split_len + 1);
-  const float* pp = a.part + ((long)r * a.nq + h) * a.n_split * (hd + 2);
-  const float m = lane < ns ? pp[lane * (hd + 2)] : -INFINITY;
-  const float lsum = lane < ns ? pp[lane * (hd + 2) + 1] : 0.f;
-  const float M = wave_max(m);
-  const float f = (m > -INFINITY) ? __expf(m - M) : 0.f;
-  const float L = wave_sum(lsum * f);
-  const float inv = L > 0.f ? 1.0f / L : 0.f;
-  const long obase = (long)r * a.nq * hd + h * hd;
-  for (int e = lane; e < hd; e += 64) {
-    float O = 0.f;
-    for (int s0 = 0; s0 < ns; s0 += 8) {
-      float v[8];
+  const int ns = min(a.n_split, a.rows.pos[r] / a.split_len + 1);
+  const float* pp = a.part + ((long)r * a.nq + h) * a.n_split * (HD + 2);
+  float v[PER];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = s0 + i < ns ? pp[(s0 + i) * (hd + 2) + 2 + e] : 0.f;
+  for (int i = 0; i < PER; ++i) {
+    const int sp = grp + G * i;
+    v[i] = sp < ns ? pp[(long)sp * (HD + 2) + 2 + e] : 0.f;
+  }
+  if (tid < 64) {
+    const float m = lane < ns ? pp[(long)lane * (HD + 2)] : -INFINITY;
+    const float lsum = lane < ns ? pp[(long)lane * (HD + 2) + 1] : 0.f;
+    const float M = wave_max(m);
+    const float f = (m > -INFINITY) ? __expf(m - M) : 0.f;
+    const float L = wave_sum(lsum * f);
+    s_f[lane] = L > 0.f ? f / L : 0.f;
+  }
+  __syncthreads();
+  float O = 0.f;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) O += v[i] * __shfl(f, (s0 + i) & 63, OSP_WAVE);
-    }
-    const float y = O * inv;
+  for (int i = 0; i < PER; ++i) {
+    const int sp = grp + G * i;
+    if (sp < ns) O += v[i] * s_f[sp];
+  }
+  s_part[grp][e] = O;
+  __syncthreads();
+  if (tid < HD) {
+    float y = 0.f;
+#pragma unroll
+    for (int g2 = 0; g2 < G; ++g2) y += s_part[g2][tid];
+    const long o = (long)r * a.nq * HD + h * HD + tid;
     if (a.o_hi) {
       const bf16_t yh = f32_to_bf16(y);
-      a.o_hi[obase + e] = yh;
-      a.o_lo[obase + e] = f32_to_bf16(y - bf16_to_f32(yh));
+      a.o_hi[o] = yh;
+      a.o_lo[o] = f32_to_bf16(y - bf16_to_f32(yh));
     } else {
-      a.o[obase + e] = y;
+      a.o[o] = y;
     }
   }
 }
@@ -722,7 +743,8 @@ void launch_rows_qkv(int kvdtype, const AttnArgs& a, float* q_out, hipStream_t s
 }
 
 void launch_attn_combine(const AttnArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(k_attn_combine, dim3(a.rows.max_rows, a.nq), dim3(64), 0, st, a);
+  if (a.hd == 128) hipLaunchKernelGGL(k_attn_combine<128>, dim3(a.rows.max_rows, a.nq), dim3(256), 0, st, a);
+  else hipLaunchKernelGGL(k_attn_combine<64>, dim3(a.rows.max_rows, a.nq), dim3(256), 0, st, a);
 }
 
 }  // namespace osp

@@ -29,6 +29,16 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
   const float* part = a.part + (long)b * a.nblk * 4;
   const float T = a.temp[b];
   const float u = a.u[(long)b * a.K + a.k];
+  // the hidden state fed back to the next step does not depend on the pick: read it
+  // now, with the records, so its load is not one more round trip at the end
+  constexpr int kFbPer = 4;            // d <= kSampleThreads * 4 * kFbPer
+  const int xr = a.gather ? a.gather[b] : b;
+  float4 fb[kFbPer];
+#pragma unroll
+  for (int q = 0; q < kFbPer; ++q) {
+    const int c = (tid + q * kSampleThreads) * 4;
+    fb[q] = c < a.d ? *reinterpret_cast<const float4*>(a.x + (long)xr * a.d + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
   // ---- this thread's contiguous records, all loads issued together ----------------
   const int i0 = tid * kPer;
   float bm[kPer], bs[kPer];
@@ -147,10 +157,11 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
     a.ar_tok[b] = d;
     a.ar_pos[b] = a.committed[b] + a.k;
   }
-  const int xr = a.gather ? a.gather[b] : b;
-  for (int c = tid * 4; c < a.d; c += kSampleThreads * 4)
-    *reinterpret_cast<float4*>(a.gfb + (long)b * a.d + c) =
-        *reinterpret_cast<const float4*>(a.x + (long)xr * a.d + c);
+#pragma unroll
+  for (int q = 0; q < kFbPer; ++q) {
+    const int c = (tid + q * kSampleThreads) * 4;
+    if (c < a.d) *reinterpret_cast<float4*>(a.gfb + (long)b * a.d + c) = fb[q];
+  }
 }
 
 void launch_sample(const SampleArgs& a, hipStream_t st) {
