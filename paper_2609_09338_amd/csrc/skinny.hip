@@ -37,7 +37,7 @@ typedef float sk_f32x4 __attribute__((ext_vector_type(4)));
 constexpr int kSkWaves = 8;
 constexpr int kSkThreads = kSkWaves * 64;
 constexpr int kSkUnit = 256;              // weight columns per streamed unit
-constexpr int kSkDepth = 3;               // register ring of units
+constexpr int kSkDepthMax = 3;            // register ring of units (64 rows: 2)
 constexpr int kSkTmaxHead = 5;            // tiles per wavefront (bound): LM head
 constexpr int kSkTmaxProj = 1;            // projections: one tile, K split across blocks
 
@@ -59,6 +59,8 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
   constexpr int TMAX = EPI == SK_LOGITS ? kSkTmaxHead : kSkTmaxProj;
   constexpr int NU = TMAX * NCH;          // units per phase (bound)
   constexpr bool EXACT = SRC == SK_TAPS;  // bf16 inputs: no lo part
+  // ring depth: 64-row passes hold 80 accumulators and need the registers
+  constexpr int kSkDepth = MT == 4 ? 2 : kSkDepthMax;
   __shared__ __attribute__((aligned(16))) bf16_t xh[ROWS * PITCH];
   __shared__ __attribute__((aligned(16))) bf16_t xl[EXACT ? 8 : ROWS * PITCH];
   __shared__ float s_inv[SRC == SK_NORM ? ROWS : 1];
@@ -197,16 +199,24 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) {
           const sk_bf16x8 bw = *reinterpret_cast<const sk_bf16x8*>(&w[ks]);
+          // all A fragments of this K step are requested before the first product, so
+          // one LDS latency covers the step's 2 MT products instead of one each
+          sk_bf16x8 ah[MT], al[MT];
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
             const int off = (mt * 16 + wrow) * PITCH + kl + 32 * ks;
-            const sk_bf16x8 ah = *reinterpret_cast<const sk_bf16x8*>(xh + off);
-            acc[j][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bw, acc[j][mt], 0, 0, 0);
-            if constexpr (!EXACT) {
-              const sk_bf16x8 al = *reinterpret_cast<const sk_bf16x8*>(xl + off);
-              acc[j][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bw, acc[j][mt], 0, 0, 0);
-            }
+            ah[mt] = *reinterpret_cast<const sk_bf16x8*>(xh + off);
+            if constexpr (!EXACT) al[mt] = *reinterpret_cast<const sk_bf16x8*>(xl + off);
           }
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            acc[j][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[mt], bw, acc[j][mt], 0, 0, 0);
+            if constexpr (!EXACT) acc[j][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[mt], bw, acc[j][mt], 0, 0, 0);
+          }
+          // keep that order: the scheduler, near the register limit, would otherwise
+          // put a wait on each read right before its product
+          __builtin_amdgcn_sched_group_barrier(0x100, EXACT ? MT : 2 * MT, 0);   // LDS reads
+          __builtin_amdgcn_sched_group_barrier(0x008, EXACT ? MT : 2 * MT, 0);   // MFMAs
         }
       }
     }
