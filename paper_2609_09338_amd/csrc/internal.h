@@ -25,6 +25,8 @@ enum SrcKind {
   SRC_TAPS = 3,   // X[r][c] = taps[tap_row[r]*ldt + c] (weight dtype)
   SRC_PREP = 4,   // matrix-core passes: X[r][c] prepared as bf16 hi + lo pairs,
                   // c < seg from (xs_hi, xs_lo) row r, else (xa_hi, xa_lo) row gather[r] or r
+  SRC_SWIGLU = 5, // matrix-core passes of <= 64 rows: X[r][c] = silu(g) u with g, u the sums of
+                  // the gate/up K-split partials part_in[k][r][c] and part_in[k][r][Kd + c]
 };
 enum EpiKind {
   EPI_STORE = 0,   // y[r][n] = acc
@@ -77,6 +79,11 @@ struct GemvArgs {
   const uint16_t* xa_hi;
   const uint16_t* xa_lo;
   int ld_xa;
+  // SRC_SWIGLU inputs: gate/up partial sums, split k row r at part_in + k * part_in_split + r * ld_in
+  const float* part_in;
+  int ks_in;
+  long part_in_split;
+  int ld_in;
   uint32_t* err;
 };
 constexpr int kMaxKSplit = 16;
@@ -108,7 +115,8 @@ LmPlan lm_head_plan(int rows, int N, int n_cu);
 void launch_lm_head(const GemvArgs& a, const LmPlan& p, bool norm_in, hipStream_t st);
 
 // Projections of passes of at most kLmMaxRows rows on the same streaming kernel:
-// src SRC_PREP (pairs; [xs ; xa] when seg > 0) or SRC_TAPS; with w1 set, the up
+// src SRC_PREP (pairs; [xs ; xa] when seg > 0), SRC_TAPS, or SRC_SWIGLU (the down
+// projection forms silu(gate) * up from the gate/up partials itself); with w1 set, the up
 // matrix supplies rows [N, 2N).  Writes K-split partial sums to
 // split_buf[split][max_rows][N or 2N]; returns the number of splits.
 int launch_skinny(SrcKind src, const GemvArgs& a, hipStream_t st);

@@ -75,6 +75,7 @@ struct Ws {
   float* attn_part;
   float* split;
   float* split_s;     // K-split partials of passes of at most kLmMaxRows rows
+  float* split_s2;    // a second such buffer (the down projection reads gate/up partials)
   float* logits;
   float* lm_part;
   int32_t* drafts;
@@ -163,6 +164,7 @@ size_t plan(const osprey_config& c, char* base, Ws* w) {
     need = std::max<long>(need, skinny_splits(rs, c.d_model) * 2L * c.d_ffn);
     need = std::max<long>(need, skinny_splits(rs, c.d_ffn) * d);
     W.split_s = (float*)take(4L * rs * need);
+    W.split_s2 = (float*)take(4L * rs * need);
   }
   W.logits = (float*)take(4L * D.B * D.Km * c.vocab_draft);
   W.lm_part = (float*)take(16L * D.B * D.lm_nblk_max);
@@ -544,8 +546,10 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     rs.W = F;
     rs.ldp = 2 * F;
     rs.ks = gemm(SRC_PREP, EPI_SWIGLU, gu);
-    launch_rows_swiglu(rs, h->stream);
-    // down projection; residual + the next layer's input norm (final norm after the last)
+    // down projection; residual + the next layer's input norm (final norm after the last).
+    // Passes of up to 16 rows form silu(gate) * up while staging the down projection's
+    // inputs (each block re-reads the gate/up partials of its K range, which only stays
+    // cheaper than a separate row kernel for few rows).
     GemvArgs gd = gb;
     gd.ld_xa = F;
     gd.Kd = F;
@@ -554,7 +558,19 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     RowArgs rd = ra;
     rd.W = d;
     rd.ldp = d;
-    rd.ks = gemm(SRC_PREP, EPI_STORE, gd);
+    if (skinny && rows.max_rows <= 16) {
+      gd.part_in = part;
+      gd.ks_in = rs.ks;
+      gd.part_in_split = (long)rows.max_rows * 2 * F;
+      gd.ld_in = 2 * F;
+      gd.split_buf = W.split_s2;
+      rd.part = W.split_s2;
+      rd.ks = launch_skinny(SRC_SWIGLU, gd, h->stream);
+    } else {
+      launch_rows_swiglu(rs, h->stream);
+      rd.ks = gemm(SRC_PREP, EPI_STORE, gd);
+      rd.part = part;
+    }
     rd.gamma = l + 1 < c.n_layers ? h->layers[l + 1].in_norm : h->w.final_norm;
     launch_rows_resid_norm(rd, h->stream);
   }

@@ -41,7 +41,7 @@ constexpr int kSkDepthMax = 3;            // register ring of units (64 rows: 2)
 constexpr int kSkTmaxHead = 5;            // tiles per wavefront (bound): LM head
 constexpr int kSkTmaxProj = 1;            // projections: one tile, K split across blocks
 
-enum SkSrc { SK_PREP = 0, SK_NORM = 1, SK_TAPS = 2 };
+enum SkSrc { SK_PREP = 0, SK_NORM = 1, SK_TAPS = 2, SK_SWIGLU = 3 };
 enum SkEpi { SK_LOGITS = 0, SK_PART = 1 };
 
 // Input columns resident per block and phase: 64 rows x 512 or 32 rows x 1024
@@ -162,6 +162,30 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
           } else if constexpr (SRC == SK_TAPS) {
             h = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16_t*>(a.taps) +
                                                 (long)a.tap_row[r] * a.ldt + c);
+          } else if constexpr (SRC == SK_SWIGLU) {
+            // SwiGLU of the gate/up products: their K-split partials added in split order
+            const float* pr = a.part_in + (long)r * a.ld_in + c;
+            float g[8], u[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) { g[e] = 0.f; u[e] = 0.f; }
+            for (int k = 0; k < a.ks_in; ++k) {
+              const float* pk = pr + (long)k * a.part_in_split;
+              const float4 g0 = *reinterpret_cast<const float4*>(pk);
+              const float4 g1 = *reinterpret_cast<const float4*>(pk + 4);
+              const float4 u0 = *reinterpret_cast<const float4*>(pk + a.Kd);
+              const float4 u1 = *reinterpret_cast<const float4*>(pk + a.Kd + 4);
+              g[0] += g0.x; g[1] += g0.y; g[2] += g0.z; g[3] += g0.w;
+              g[4] += g1.x; g[5] += g1.y; g[6] += g1.z; g[7] += g1.w;
+              u[0] += u0.x; u[1] += u0.y; u[2] += u0.z; u[3] += u0.w;
+              u[4] += u1.x; u[5] += u1.y; u[6] += u1.z; u[7] += u1.w;
+            }
+            float y[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) y[e] = g[e] / (1.0f + __expf(-g[e])) * u[e];
+            split_bf16x2(y[0], y[1], h.x, l.x);
+            split_bf16x2(y[2], y[3], h.y, l.y);
+            split_bf16x2(y[4], y[5], h.z, l.z);
+            split_bf16x2(y[6], y[7], h.w, l.w);
           } else if (c < a.seg) {
             const long o = (long)r * a.ld_xs + c;
             h = *reinterpret_cast<const uint4*>(a.xs_hi + o);
@@ -415,6 +439,7 @@ int launch_skinny(SrcKind src, const GemvArgs& a, hipStream_t st) {
   const int ks = (a.Kd + kc - 1) / kc;
   const dim3 grid((((NR + 15) / 16) + kSkWaves - 1) / kSkWaves, ks);
   if (src == SRC_TAPS) sk_launch<SK_TAPS, SK_PART>(mt, grid, a, 1, kc, st);
+  else if (src == SRC_SWIGLU) sk_launch<SK_SWIGLU, SK_PART>(mt, grid, a, 1, kc, st);
   else sk_launch<SK_PREP, SK_PART>(mt, grid, a, 1, kc, st);
   return ks;
 }
