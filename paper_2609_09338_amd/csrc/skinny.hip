@@ -132,23 +132,25 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
   for (int ph = 0; ph < nphase; ++ph) {
     const int k0 = k_lo + ph * KC;
     if (ph > 0) __syncthreads();
-    // ---- inputs of this phase into LDS (rows past R and columns past k_hi are zero);
-    //      each thread requests a batch of 16-byte pieces before storing any, so the
-    //      copy costs a couple of L2 round trips instead of one per piece ----------------
-    constexpr int ITEMS = ROWS * (KC / 8) / kSkThreads;
-    // (the 64-row LM head holds 80 accumulators: no room for a batch there)
-    constexpr int BATCH = (MT == 4 && EPI == SK_LOGITS) ? 1 : (ITEMS < 4 ? ITEMS : 4);
-    static_assert(ITEMS * kSkThreads == ROWS * (KC / 8) && ITEMS % BATCH == 0, "staging split");
+    // ---- inputs of this phase into LDS: rows r < R and the columns this block reads
+    //      (the projections' K range, or the whole phase); columns past k_hi are zero.
+    //      Rows past R are left as they are: they only feed outputs that are dropped.
+    //      Each thread requests a batch of 16-byte pieces before storing any, so the
+    //      copy costs a round trip or two instead of one per piece ------------------------
+    const int span8 = (EPI == SK_PART ? kc : KC) / 8;      // 16-byte pieces per row
+    const int nitems = R * span8;
+    // (the LM head holds 20 MT accumulators: smaller batches for more rows)
+    constexpr int BATCH = EPI == SK_LOGITS ? (MT == 4 ? 1 : (MT == 2 ? 2 : 4)) : 4;
 #pragma unroll 1
-    for (int b0 = 0; b0 < ITEMS; b0 += BATCH) {
+    for (int b0 = 0; b0 < nitems; b0 += BATCH * kSkThreads) {
       uint4 hv[BATCH], lv[BATCH];
 #pragma unroll
       for (int q = 0; q < BATCH; ++q) {
-        const int i = tid + (b0 + q) * kSkThreads;
-        const int r = i / (KC / 8), col = (i - r * (KC / 8)) * 8;
+        const int i = b0 + tid + q * kSkThreads;
+        const int r = i / span8, col = (i - r * span8) * 8;
         const int c = k0 + col;
         uint4 h = make_uint4(0u, 0u, 0u, 0u), l = h;
-        if (r < R && c < k_hi) {
+        if (i < nitems && c < k_hi) {
           if constexpr (SRC == SK_NORM) {
             const float* xr = a.xin + (long)(a.gather ? a.gather[r] : r) * a.ldx + c;
             const float4 v0 = *reinterpret_cast<const float4*>(xr);
@@ -201,10 +203,12 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
       }
 #pragma unroll
       for (int q = 0; q < BATCH; ++q) {
-        const int i = tid + (b0 + q) * kSkThreads;
-        const int r = i / (KC / 8), col = (i - r * (KC / 8)) * 8;
-        *reinterpret_cast<uint4*>(xh + r * PITCH + col) = hv[q];
-        if constexpr (!EXACT) *reinterpret_cast<uint4*>(xl + r * PITCH + col) = lv[q];
+        const int i = b0 + tid + q * kSkThreads;
+        const int r = i / span8, col = (i - r * span8) * 8;
+        if (i < nitems) {
+          *reinterpret_cast<uint4*>(xh + r * PITCH + col) = hv[q];
+          if constexpr (!EXACT) *reinterpret_cast<uint4*>(xl + r * PITCH + col) = lv[q];
+        }
       }
     }
     __syncthreads();
