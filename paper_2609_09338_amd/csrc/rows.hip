@@ -23,12 +23,19 @@ OSP_DEV void store_pair4(uint16_t* hi, uint16_t* lo, long o, float4 v) {
   *reinterpret_cast<uint2*>(lo + o) = make_uint2(l[0], l[1]);
 }
 
-// Sum over the K splits of columns [c, c + 4) of row r (offset col0 within the row).
+// Sum over the K splits of columns [col, col + 4) of row r, in split order; the loads
+// of four splits are requested together.
 OSP_DEV float4 sum_parts4(const RowArgs& a, int r, int col) {
   float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int k = 0; k < a.ks; ++k) {
-    const float4 v = *reinterpret_cast<const float4*>(a.part + ((long)k * a.max_rows + r) * a.ldp + col);
-    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  const float* p = a.part + (long)r * a.ldp + col;
+  const long stride = (long)a.max_rows * a.ldp;
+  for (int k0 = 0; k0 < a.ks; k0 += 4) {
+    float4 v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      v[q] = k0 + q < a.ks ? *reinterpret_cast<const float4*>(p + (k0 + q) * stride) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) { s.x += v[q].x; s.y += v[q].y; s.z += v[q].z; s.w += v[q].w; }
   }
   return s;
 }

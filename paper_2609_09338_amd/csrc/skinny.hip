@@ -170,16 +170,25 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
             float g[8], u[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) { g[e] = 0.f; u[e] = 0.f; }
-            for (int k = 0; k < a.ks_in; ++k) {
-              const float* pk = pr + (long)k * a.part_in_split;
-              const float4 g0 = *reinterpret_cast<const float4*>(pk);
-              const float4 g1 = *reinterpret_cast<const float4*>(pk + 4);
-              const float4 u0 = *reinterpret_cast<const float4*>(pk + a.Kd);
-              const float4 u1 = *reinterpret_cast<const float4*>(pk + a.Kd + 4);
-              g[0] += g0.x; g[1] += g0.y; g[2] += g0.z; g[3] += g0.w;
-              g[4] += g1.x; g[5] += g1.y; g[6] += g1.z; g[7] += g1.w;
-              u[0] += u0.x; u[1] += u0.y; u[2] += u0.z; u[3] += u0.w;
-              u[4] += u1.x; u[5] += u1.y; u[6] += u1.z; u[7] += u1.w;
+            for (int k0 = 0; k0 < a.ks_in; k0 += 2) {      // two splits' loads at a time
+              float4 gv[2][2], uv[2][2];
+#pragma unroll
+              for (int q = 0; q < 2; ++q) {
+                const bool in = k0 + q < a.ks_in;
+                const float* pk = pr + (long)(k0 + q) * a.part_in_split;
+                const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+                gv[q][0] = in ? *reinterpret_cast<const float4*>(pk) : z;
+                gv[q][1] = in ? *reinterpret_cast<const float4*>(pk + 4) : z;
+                uv[q][0] = in ? *reinterpret_cast<const float4*>(pk + a.Kd) : z;
+                uv[q][1] = in ? *reinterpret_cast<const float4*>(pk + a.Kd + 4) : z;
+              }
+#pragma unroll
+              for (int q = 0; q < 2; ++q) {
+                g[0] += gv[q][0].x; g[1] += gv[q][0].y; g[2] += gv[q][0].z; g[3] += gv[q][0].w;
+                g[4] += gv[q][1].x; g[5] += gv[q][1].y; g[6] += gv[q][1].z; g[7] += gv[q][1].w;
+                u[0] += uv[q][0].x; u[1] += uv[q][0].y; u[2] += uv[q][0].z; u[3] += uv[q][0].w;
+                u[4] += uv[q][1].x; u[5] += uv[q][1].y; u[6] += uv[q][1].z; u[7] += uv[q][1].w;
+              }
             }
             float y[8];
 #pragma unroll
