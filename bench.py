@@ -184,7 +184,7 @@ def run_cpu_baseline(w, seconds: float):
     dr = OH.build_drafter(w)
     t0 = time.perf_counter()
     tokens, iters = 0, 0
-    seq_iters = OH.run_sequence_timed(w, 0, 64, seconds, drafter=dr)
+    seq_iters = OH.run_sequence_timed(w, 0, 512, seconds, drafter=dr)
     for it in seq_iters:
         tokens += it.result.accept_len + 1
         iters += 1

@@ -62,15 +62,16 @@ def start_sequence(w, drafter: Drafter, b: int, n_iters: int) -> Sequence:
 
 def run_sequence_timed(w, b: int, n_max: int, seconds: float,
                        drafter: Optional[Drafter] = None) -> List[Iteration]:
-    """Iterations of sequence b until `seconds` have elapsed (at least one)."""
+    """Iterations of sequence b until `seconds` have elapsed (at least one); the
+    records keep no logit rows (a long timed run would otherwise hold gigabytes)."""
     import time
     t0 = time.perf_counter()
     return run_sequence(w, b, n_max, drafter=drafter,
-                        stop=lambda: time.perf_counter() - t0 > seconds)
+                        stop=lambda: time.perf_counter() - t0 > seconds, lean=True)
 
 
 def run_sequence(w, b: int, n_iters: int, drafter: Optional[Drafter] = None,
-                 residual_fn=None, stop=None) -> List[Iteration]:
+                 residual_fn=None, stop=None, lean: bool = False) -> List[Iteration]:
     drafter = drafter or build_drafter(w)
     seq = start_sequence(w, drafter, b, n_iters)
     ctx = int(synth.context_lengths(w)[b])
@@ -85,7 +86,8 @@ def run_sequence(w, b: int, n_iters: int, drafter: Optional[Drafter] = None,
         tl = synth.target_logits(w, logits, drafter.d2t, synth.target_noise(w, it, b))
         res = verify(tl, logits, drafter.d2t, drafts, T, synth.u_accept(w, it)[b],
                      float(synth.u_bonus(w, it)[b]), residual_fn=residual_fn)
-        out.append(Iteration(pre, new_tokens.copy(), committed, drafts, rows, logits, tl, res))
+        out.append(Iteration(pre, new_tokens.copy(), committed, drafts, rows,
+                             None if lean else logits, None if lean else tl, res))
         drafter.rollback(seq, committed)
         new_tokens = res.tokens[: res.accept_len + 1].copy()
         if stop is not None and stop():
