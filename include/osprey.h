@@ -161,6 +161,18 @@ typedef struct {
                                   them untouched until osprey_verify has run. */
 } osprey_step_args;
 
+/* Drafter temperature.  The rule checks each draft against the distribution it
+ * was actually drawn from: q_k = softmax(l_k / T_d) carried to target ids, with T_d
+ * the draft temperature of the request, while p_k = softmax(target row / T).
+ * T_d = 0 is greedy drafting, the top-1 chain of the paper's serving setup
+ * (Section 4, inference settings; serving configuration in the appendix on
+ * adaptation): q_k is one-hot at the drafter's argmax row (lowest row on ties),
+ * draft k is accepted iff u_k < p_k(d_k), and a rejected position is redrawn
+ * from p_a with d_a removed (target-only acceptance).  Draft with
+ * osprey_draft_step at temperature T_d (0 for greedy) and pass the same values
+ * as draft_temperature here.  With T == 0 the rule is the greedy prefix match
+ * whatever T_d is. */
+
 /* Arguments of osprey_verify (stateful: the drafts and drafter rows of the last
  * draft_step on exactly these slots in this order with this K).  The target's
  * logits are for the K + 1 positions after the committed prefix followed by
@@ -175,12 +187,15 @@ typedef struct {
   int32_t K;
   const int32_t* slots;         /* (host) [batch] */
   const float* target_logits;   /* [batch][K + 1][V_T] fp32 */
-  const float* temperature;     /* [batch] (the same T as the draft step) */
+  const float* temperature;     /* [batch] the target's temperature T (>= 0) */
   const float* u_accept;        /* [batch][K] */
   const float* u_bonus;         /* [batch] */
   int32_t* accept_len;          /* [batch] out */
   uint8_t* accept_mask;         /* [batch][K] out */
   int32_t* out_tokens;          /* [batch][K + 1] out */
+  const float* draft_temperature; /* [batch] temperature the drafts were drawn at (the
+                                  draft_step's `temperature`), or NULL: the same as
+                                  `temperature`.  See "Drafter temperature" below. */
 } osprey_verify_args;
 
 /* Arguments of osprey_verify_rows: the same rule on caller-supplied drafts and
@@ -197,6 +212,7 @@ typedef struct {
   int32_t* accept_len;
   uint8_t* accept_mask;
   int32_t* out_tokens;
+  const float* draft_temperature;  /* [batch] or NULL (= temperature), as in osprey_verify_args */
 } osprey_verify_rows_args;
 
 /* Host-only check of a configuration.  Returns OSPREY_OK or the first problem. */

@@ -77,15 +77,16 @@ def run_sequence(w, b: int, n_iters: int, drafter: Optional[Drafter] = None,
     ctx = int(synth.context_lengths(w)[b])
     new_tokens = synth.prompt_tokens(w, b, ctx)[ctx - 1:ctx].astype(np.int64)
     T = w.temperature(b)
+    Td = w.draft_temperature(b)
     out = []
     for it in range(n_iters):
         pre = seq.length
         taps = synth.taps(w, it, b, w.K + 1)[: len(new_tokens)]
         ud = synth.u_draft(w, it)[b]
-        drafts, logits, rows, committed = drafter.draft(seq, new_tokens, taps, w.K, T, ud)
+        drafts, logits, rows, committed = drafter.draft(seq, new_tokens, taps, w.K, Td, ud)
         tl = synth.target_logits(w, logits, drafter.d2t, synth.target_noise(w, it, b))
         res = verify(tl, logits, drafter.d2t, drafts, T, synth.u_accept(w, it)[b],
-                     float(synth.u_bonus(w, it)[b]), residual_fn=residual_fn)
+                     float(synth.u_bonus(w, it)[b]), residual_fn=residual_fn, T_draft=Td)
         out.append(Iteration(pre, new_tokens.copy(), committed, drafts, rows,
                              None if lean else logits, None if lean else tl, res))
         drafter.rollback(seq, committed)

@@ -11,6 +11,14 @@ replacement is drawn from the normalised residual max(0, p_a - q_a); if every
 draft is accepted a bonus token is drawn from p_K.  At temperature 0 both
 distributions are one-hot at their argmax, which makes this a greedy prefix
 match followed by the target's argmax.
+
+The drafter may draw its drafts at a temperature of its own (T_draft) while the
+target is sampled at T.  The rule is unchanged: q is the distribution the
+drafts were actually drawn from.  With T_draft = 0 (greedy drafting: the
+top-1 chain of the paper's serving setup, Section 4 "Inference settings and
+metrics" and the serving configuration of the adaptation appendix) q is
+one-hot at the drafter's argmax, so draft k is accepted with probability
+p_k(d_k) and a rejected position is redrawn from p_a with d_a removed.
 """
 from __future__ import annotations
 
@@ -43,8 +51,10 @@ def drafter_probs_on_target(draft_logits: np.ndarray, d2t: np.ndarray, V_T: int,
 
 def verify(target_logits: np.ndarray, draft_logits: np.ndarray, d2t: np.ndarray,
            drafts: np.ndarray, T: float, u_accept: np.ndarray, u_bonus: float,
-           residual_fn=None) -> VerifyResult:
-    """target_logits [K+1, V_T]; draft_logits [K, V_d]; drafts [K] target ids."""
+           residual_fn=None, T_draft=None) -> VerifyResult:
+    """target_logits [K+1, V_T]; draft_logits [K, V_d]; drafts [K] target ids.
+    T is the target's temperature, T_draft the drafter's (None: the same as T)."""
+    Td = T if T_draft is None else float(T_draft)
     tl = np.asarray(target_logits, dtype=np.float64)
     K = len(drafts)
     V_T = tl.shape[1]
@@ -56,7 +66,7 @@ def verify(target_logits: np.ndarray, draft_logits: np.ndarray, d2t: np.ndarray,
     q_rows = []
     while a < K:
         p = sampling.probs(tl[a], T)
-        q = drafter_probs_on_target(draft_logits[a], d2t, V_T, T)
+        q = drafter_probs_on_target(draft_logits[a], d2t, V_T, Td)
         q_rows.append(q)
         d = int(drafts[a])
         pd, qd = p[d], q[d]

@@ -48,7 +48,8 @@ class osprey_verify_args(C.Structure):
     _fields_ = [("batch", C.c_int32), ("K", C.c_int32), ("slots", C.POINTER(C.c_int32)),
                 ("target_logits", C.c_void_p), ("temperature", C.c_void_p),
                 ("u_accept", C.c_void_p), ("u_bonus", C.c_void_p), ("accept_len", C.c_void_p),
-                ("accept_mask", C.c_void_p), ("out_tokens", C.c_void_p)]
+                ("accept_mask", C.c_void_p), ("out_tokens", C.c_void_p),
+                ("draft_temperature", C.c_void_p)]
 
 
 class osprey_verify_rows_args(C.Structure):
@@ -56,7 +57,7 @@ class osprey_verify_rows_args(C.Structure):
                 ("draft_logits", C.c_void_p), ("draft_tokens", C.c_void_p),
                 ("temperature", C.c_void_p), ("u_accept", C.c_void_p), ("u_bonus", C.c_void_p),
                 ("accept_len", C.c_void_p), ("accept_mask", C.c_void_p),
-                ("out_tokens", C.c_void_p)]
+                ("out_tokens", C.c_void_p), ("draft_temperature", C.c_void_p)]
 
 
 _P = C.c_void_p

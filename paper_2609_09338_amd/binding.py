@@ -192,7 +192,7 @@ class Drafter:
         _check(_lib().osprey_draft_step(self.h, C.byref(a)))
 
     def verify(self, slots, K: int, target_logits, temperature, u_accept, u_bonus,
-               accept_len, accept_mask, out_tokens) -> None:
+               accept_len, accept_mask, out_tokens, draft_temperature=None) -> None:
         torch, c = self.torch, self.cfg
         B = len(slots)
         _need(target_logits, B * (K + 1) * c.vocab_target, torch.float32, "target_logits")
@@ -202,6 +202,7 @@ class Drafter:
         _need(accept_len, B, torch.int32, "accept_len")
         _need(accept_mask, B * K, torch.uint8, "accept_mask")
         _need(out_tokens, B * (K + 1), torch.int32, "out_tokens")
+        _need(draft_temperature, B, torch.float32, "draft_temperature")
         a = L.osprey_verify_args()
         a.batch = B
         a.K = K
@@ -214,10 +215,12 @@ class Drafter:
         a.accept_len = _ptr(accept_len)
         a.accept_mask = _ptr(accept_mask)
         a.out_tokens = _ptr(out_tokens)
+        a.draft_temperature = _ptr(draft_temperature)
         _check(_lib().osprey_verify(self.h, C.byref(a)))
 
     def verify_rows(self, K: int, target_logits, draft_logits, draft_tokens, temperature,
-                    u_accept, u_bonus, accept_len, accept_mask, out_tokens) -> None:
+                    u_accept, u_bonus, accept_len, accept_mask, out_tokens,
+                    draft_temperature=None) -> None:
         torch, c = self.torch, self.cfg
         B = int(target_logits.shape[0])
         _need(target_logits, B * (K + 1) * c.vocab_target, torch.float32, "target_logits")
@@ -229,6 +232,7 @@ class Drafter:
         _need(accept_len, B, torch.int32, "accept_len")
         _need(accept_mask, B * K, torch.uint8, "accept_mask")
         _need(out_tokens, B * (K + 1), torch.int32, "out_tokens")
+        _need(draft_temperature, B, torch.float32, "draft_temperature")
         a = L.osprey_verify_rows_args()
         a.batch = B
         a.K = K
@@ -241,6 +245,7 @@ class Drafter:
         a.accept_len = _ptr(accept_len)
         a.accept_mask = _ptr(accept_mask)
         a.out_tokens = _ptr(out_tokens)
+        a.draft_temperature = _ptr(draft_temperature)
         _check(_lib().osprey_verify_rows(self.h, C.byref(a)))
 
     # -- diagnostics ------------------------------------------------------------------

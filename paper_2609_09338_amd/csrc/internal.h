@@ -277,7 +277,8 @@ struct VerifyArgs {
   long ld_draft_b;          // rows per sequence in draft
   const int32_t* drafts;    // row b at drafts + b*ld_drafts
   int ld_drafts;
-  const float* temp;
+  const float* temp;        // [B] target temperature T
+  const float* temp_d;      // [B] temperature the drafts were drawn at (0: greedy, q one-hot)
   const float* u_acc;       // [B][K]
   const float* u_bonus;     // [B]
   const int32_t* d2t;
@@ -287,7 +288,7 @@ struct VerifyArgs {
   int nchunk_t, nchunk_d;
   float* part;              // [B][(K+1)*nchunk_t + K*nchunk_d][4]
   double* res_part;         // [B][nchunk_t][2]: residual and p sums per chunk
-  int32_t* vstate;          // [B][4]: a, argmax of p_a (T = 0), flags
+  int32_t* vstate;          // [B][4]: a, argmax of p_a, one-hot drafter row of q_a (T_d = 0)
   double* vstat;            // [B][4]: M_a, S_a (target), m_a, s_a (draft)
   uint32_t* counters;       // [2*B] last-arriver counters
   int32_t* accept_len;

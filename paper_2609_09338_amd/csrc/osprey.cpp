@@ -1013,6 +1013,7 @@ OSPREY_API int osprey_verify(osprey_handle* h, const osprey_verify_args* a) {
   v.drafts = h->W.drafts;
   v.ld_drafts = h->D.Km;
   v.temp = a->temperature;
+  v.temp_d = a->draft_temperature ? a->draft_temperature : a->temperature;
   v.u_acc = a->u_accept;
   v.u_bonus = a->u_bonus;
   v.accept_len = a->accept_len;
@@ -1048,6 +1049,7 @@ OSPREY_API int osprey_verify_rows(osprey_handle* h, const osprey_verify_rows_arg
   v.drafts = a->draft_tokens;
   v.ld_drafts = a->K;
   v.temp = a->temperature;
+  v.temp_d = a->draft_temperature ? a->draft_temperature : a->temperature;
   v.u_acc = a->u_accept;
   v.u_bonus = a->u_bonus;
   v.accept_len = a->accept_len;

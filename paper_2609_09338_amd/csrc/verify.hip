@@ -3,7 +3,10 @@
 //
 // Row convention per sequence: drafts d_0..d_{K-1} with drafter logit rows
 // q_0..q_{K-1} (over drafter rows, mapped to target ids by d2t / t2d); target
-// logit rows p_0..p_K over target ids.
+// logit rows p_0..p_K over target ids.  p is the softmax of the target row at the
+// request's temperature T, q that of the drafter row at the temperature the drafts
+// were drawn at (T_d; T_d = 0: one-hot at the drafter row's lowest argmax, which
+// reduces acceptance to u_k < p_k(d_k) and the residual to p_a without d_a).
 //
 //   k_vstats  (B x jobs)   per chunk of every target and drafter row: max,
 //                          lowest argmax and sum exp((l - max)/T)
@@ -87,7 +90,7 @@ __global__ void __launch_bounds__(kVThreads) k_vstats(VerifyArgs a) {
     if (v[q] > m) { m = v[q]; am = i0 + lane + q * 64; }   // ascending ids: first hit is lowest
   const float M = wave_max(m);
   const int A = wave_min_i((m == M && m > -INFINITY) ? am : 0x7fffffff);
-  const float T = a.temp[b];
+  const float T = j < nt ? a.temp[b] : a.temp_d[b];
   double se = 0.0;   // float64 sums: exactness of the 10^5-entry CDFs that follow
   if (T > 0.f && M > -INFINITY) {
 #pragma unroll
@@ -141,14 +144,14 @@ __global__ void __launch_bounds__(kVThreads) k_vaccept(VerifyArgs a) {
   const int nt = (K + 1) * a.nchunk_t;
   const int nj = nt + K * a.nchunk_d;
   const float* part = a.part + (long)b * nj * 4;
-  const float T = a.temp[b];
+  const float T = a.temp[b], Td = a.temp_d[b];
   const int nrows = (K + 1) + (T > 0.f ? K : 0);
   for (int q = wave; q < nrows; q += kVThreads / 64) {
     float M;
     double S;
     int am;
     if (q <= K) merge_row(part + (long)q * a.nchunk_t * 4, a.nchunk_t, T, M, S, am);
-    else merge_row(part + ((long)nt + (long)(q - K - 1) * a.nchunk_d) * 4, a.nchunk_d, T, M, S, am);
+    else merge_row(part + ((long)nt + (long)(q - K - 1) * a.nchunk_d) * 4, a.nchunk_d, Td, M, S, am);
     if (lane == 0) { s_M[q] = M; s_S[q] = S; s_am[q] = am; }
   }
   __syncthreads();
@@ -167,8 +170,12 @@ __global__ void __launch_bounds__(kVThreads) k_vaccept(VerifyArgs a) {
       const float tv = tl[d];
       double qd = 0.0;
       if (s >= 0) {
-        const float ls = a.draft[((long)b * a.ld_draft_b + k) * a.V_d + s];
-        if (ls > -INFINITY) qd = (double)__expf((ls - s_M[K + 1 + k]) / T) / s_S[K + 1 + k];
+        if (Td > 0.f) {
+          const float ls = a.draft[((long)b * a.ld_draft_b + k) * a.V_d + s];
+          if (ls > -INFINITY) qd = (double)__expf((ls - s_M[K + 1 + k]) / Td) / s_S[K + 1 + k];
+        } else {
+          qd = s == s_am[K + 1 + k] ? 1.0 : 0.0;   // greedy drafting: q one-hot
+        }
       }
       const double pd = (double)__expf((tv - s_M[k]) / T) / s_S[k];
       const double r = qd > 0.0 ? fmin(1.0, pd / qd) : (pd > 0.0 ? 1.0 : 0.0);
@@ -193,7 +200,9 @@ __global__ void __launch_bounds__(kVThreads) k_vaccept(VerifyArgs a) {
     a.vstat[b * 4 + 1] = s_S[A];
     const bool dq = A < K && T > 0.f;
     a.vstat[b * 4 + 2] = dq ? s_M[K + 1 + A] : 0.0;
-    a.vstat[b * 4 + 3] = dq ? s_S[K + 1 + A] : 1.0;
+    a.vstat[b * 4 + 3] = (dq && Td > 0.f) ? s_S[K + 1 + A] : 1.0;
+    // greedy drafting: the drafter row q_a is one-hot at (-1: no drafter row / a = K)
+    a.vstate[b * 4 + 2] = (dq && !(Td > 0.f)) ? s_am[K + 1 + A] : -1;
   }
 }
 
@@ -203,19 +212,14 @@ struct ResidRow {
   const float* tl;   // target row a
   const float* dl;   // drafter row a (nullptr when a = K)
   const int32_t* t2d;
-  float Mt, Md, T;
+  float Mt, Md, T, Td;
   double iSt, iSd;   // 1 / normalisers
-  OSP_DEV void eval(int v, double& w, double& p) const {
-    p = (double)__expf((tl[v] - Mt) / T) * iSt;
-    double q = 0.0;
-    if (dl) {
-      const int s = t2d[v];
-      if (s >= 0) {
-        const float l = dl[s];
-        if (l > -INFINITY) q = (double)__expf((l - Md) / T) * iSd;
-      }
-    }
-    w = fmax(p - q, 0.0);
+  int onehot;        // Td = 0: the drafter row q_a is one-hot at (else -1)
+  // q_a(v) from the drafter row entry s = t2d[v] (-1: none) and its logit l
+  OSP_DEV double q_of(int s, float l) const {
+    if (!dl || s < 0) return 0.0;
+    if (!(Td > 0.f)) return s == onehot ? 1.0 : 0.0;
+    return l > -INFINITY ? (double)__expf((l - Md) / Td) * iSd : 0.0;
   }
   // Residual weights (which = 0) or target probabilities (which = 1) of the kVPer
   // ids i0 + q*stride, q < kVPer (0 past V_T); all loads of a phase are issued together.
@@ -231,11 +235,11 @@ struct ResidRow {
     }
     float dv[kVPer];
 #pragma unroll
-    for (int q = 0; q < kVPer; ++q) dv[q] = sidx[q] >= 0 ? dl[sidx[q]] : -INFINITY;
+    for (int q = 0; q < kVPer; ++q) dv[q] = (sidx[q] >= 0 && Td > 0.f) ? dl[sidx[q]] : -INFINITY;
 #pragma unroll
     for (int q = 0; q < kVPer; ++q) {
       const double p = tv[q] > -INFINITY ? (double)__expf((tv[q] - Mt) / T) * iSt : 0.0;
-      const double qq = dv[q] > -INFINITY ? (double)__expf((dv[q] - Md) / T) * iSd : 0.0;
+      const double qq = q_of(sidx[q], dv[q]);
       out[q] = which ? p : fmax(p - qq, 0.0);
     }
   }
@@ -252,6 +256,8 @@ OSP_DEV ResidRow resid_row(const VerifyArgs& a, int b) {
   r.Md = (float)a.vstat[b * 4 + 2];
   r.iSd = 1.0 / a.vstat[b * 4 + 3];
   r.T = a.temp[b];
+  r.Td = a.temp_d[b];
+  r.onehot = a.vstate[b * 4 + 2];
   return r;
 }
 
@@ -278,12 +284,12 @@ __global__ void __launch_bounds__(kVThreads) k_vresid(VerifyArgs a) {
   }
   float dv[kVPer];
 #pragma unroll
-  for (int q = 0; q < kVPer; ++q) dv[q] = sidx[q] >= 0 ? rr.dl[sidx[q]] : -INFINITY;
+  for (int q = 0; q < kVPer; ++q) dv[q] = (sidx[q] >= 0 && rr.Td > 0.f) ? rr.dl[sidx[q]] : -INFINITY;
   double sw = 0.0, sp = 0.0;
 #pragma unroll
   for (int q = 0; q < kVPer; ++q) {
     const double p = tv[q] > -INFINITY ? (double)__expf((tv[q] - rr.Mt) / rr.T) * rr.iSt : 0.0;
-    const double qq = dv[q] > -INFINITY ? (double)__expf((dv[q] - rr.Md) / rr.T) * rr.iSd : 0.0;
+    const double qq = rr.q_of(sidx[q], dv[q]);
     sw += fmax(p - qq, 0.0);
     sp += p;
   }

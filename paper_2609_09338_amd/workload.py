@@ -37,7 +37,8 @@ class Setup:
     blocks: List[np.ndarray]
     n_iters: int
     device: object
-    temperature: object      # [B] float32 device tensor
+    temperature: object      # [B] float32 device tensor: the target's temperature
+    draft_temperature: object  # [B] float32: the temperature drafts are drawn at
 
 
 def capacity(w, ctx: int, n_iters: int) -> int:
@@ -67,7 +68,9 @@ def make_drafter(w, n_iters: int, device="cuda:0", weights=None) -> Setup:
     dr = Drafter(cfg, tw, torch.from_numpy(d2t).to(device))
     temp = torch.tensor([w.temperature(b) for b in range(w.batch)], dtype=torch.float32,
                         device=device)
-    s = Setup(w, dr, ctx, blocks, n_iters, device, temp)
+    temp_d = torch.tensor([w.draft_temperature(b) for b in range(w.batch)], dtype=torch.float32,
+                          device=device)
+    s = Setup(w, dr, ctx, blocks, n_iters, device, temp, temp_d)
     return s
 
 
@@ -95,7 +98,7 @@ def reset_sequences(s: Setup) -> None:
                 taps.append(t)
             new_tokens = torch.from_numpy(np.concatenate(toks).astype(np.int32)).to(s.device)
             tp = to_dev(np.concatenate(taps), w, s.device)
-            dr.draft_step(sl, 0, tp, s.temperature[sl], n_new=[rows[b] for b in sl],
+            dr.draft_step(sl, 0, tp, s.draft_temperature[sl], n_new=[rows[b] for b in sl],
                           new_tokens=new_tokens, taps_stride=0)
 
 
@@ -144,12 +147,12 @@ def draft(s: Setup, it: int, inp: IterInputs, out: IterOutputs) -> None:
     w = s.w
     slots = list(range(w.batch))
     if it == 0:
-        s.drafter.draft_step(slots, w.K, inp.taps, s.temperature, inp.u_draft,
+        s.drafter.draft_step(slots, w.K, inp.taps, s.draft_temperature, inp.u_draft,
                              n_new=[1] * w.batch, new_tokens=inp.new_tokens,
                              taps_stride=w.K + 1, draft_tokens=out.drafts,
                              draft_logits=out.logits)
     else:
-        s.drafter.draft_step(slots, w.K, inp.taps, s.temperature, inp.u_draft,
+        s.drafter.draft_step(slots, w.K, inp.taps, s.draft_temperature, inp.u_draft,
                              taps_stride=w.K + 1, draft_tokens=out.drafts,
                              draft_logits=out.logits)
 
@@ -157,7 +160,8 @@ def draft(s: Setup, it: int, inp: IterInputs, out: IterOutputs) -> None:
 def verify(s: Setup, inp: IterInputs, target_logits, out: IterOutputs) -> None:
     w = s.w
     s.drafter.verify(list(range(w.batch)), w.K, target_logits, s.temperature, inp.u_accept,
-                     inp.u_bonus, out.accept_len, out.mask, out.tokens)
+                     inp.u_bonus, out.accept_len, out.mask, out.tokens,
+                     draft_temperature=s.draft_temperature)
 
 
 def synthetic_target(s: Setup, it: int, draft_logits, d2t: Optional[np.ndarray] = None):

@@ -51,6 +51,7 @@ class Workload:
     ctx_hi: int = 128          # contexts ~ U[ctx_lo, ctx_hi] per sequence
     prefill: str = "kv"        # "kv": synthetic post-RoPE KV; "ingest": prompt run through the drafter
     temps: Tuple[float, ...] = (0.0,)   # temperature of request b is temps[b % len(temps)]
+    draft_temps: Tuple[float, ...] = ()  # drafter's temperature per request (empty: = temps)
     sigma: float = 1.0         # std of the noise added to form target logits
     vocab_map: str = "identity"  # "identity" | "inject" | "partial"
     expansion: str = "normal"  # "zero" | "normal": the c-slot columns of W~_qkv
@@ -72,6 +73,12 @@ class Workload:
 
     def temperature(self, b: int) -> float:
         return float(self.temps[b % len(self.temps)])
+
+    def draft_temperature(self, b: int) -> float:
+        """Temperature the drafter samples request b at (0: greedy drafting)."""
+        if not self.draft_temps:
+            return self.temperature(b)
+        return float(self.draft_temps[b % len(self.draft_temps)])
 
 
 # ---------------------------------------------------------------------------
@@ -98,6 +105,11 @@ WORKLOADS: Dict[str, Workload] = {
     "c4": Workload(name="c4", cfg_id=4, vocab_draft=151936, vocab_target=200064,
                    target_hidden=3072, batch=32, K=5, ctx_lo=8192, ctx_hi=8192, temps=(0.7,),
                    sigma=1.5, vocab_map="inject", shuffle_blocks=True, **_QWEN_DRAFTER),
+    # The Qwen3-8B-shaped step with greedy (top-1) drafting verified against a target
+    # sampled at T = 1: the serving setup the paper reports (top-1 chains).
+    "c2g": Workload(name="c2g", cfg_id=6, vocab_draft=151936, vocab_target=151936,
+                    target_hidden=4096, batch=1, K=7, ctx_lo=2048, ctx_hi=2048, temps=(1.0,),
+                    draft_temps=(0.0,), sigma=1.0, **_QWEN_DRAFTER),
     # Throughput-bound decode: batch 64, ragged contexts, mixed greedy / T = 1.
     "c5": Workload(name="c5", cfg_id=5, vocab_draft=151936, vocab_target=151936,
                    target_hidden=4096, batch=64, K=7, ctx_lo=512, ctx_hi=4096,
@@ -119,6 +131,13 @@ PARITY: Dict[str, Workload] = {
                           vocab_target=4099, target_hidden=256, batch=4, K=6, ctx_lo=31,
                           ctx_hi=65, temps=(1.0,), sigma=1.0, vocab_map="partial",
                           shuffle_blocks=True),
+    # greedy drafting against sampled, greedy and sharply sampled targets
+    "p_greedy_draft": Workload(name="p_greedy_draft", cfg_id=15, dtype="bf16", n_layers=2,
+                               d_model=256, n_q_heads=4, n_kv_heads=2, head_dim=64, d_ffn=768,
+                               vocab_draft=5003, vocab_target=4099, target_hidden=320,
+                               batch=4, K=5, ctx_lo=9, ctx_hi=40, temps=(1.0, 0.1, 0.0, 0.7),
+                               draft_temps=(0.0, 0.0, 0.0, 0.3), sigma=0.05,
+                               vocab_map="partial", shuffle_blocks=True),
     "p_inject": Workload(name="p_inject", cfg_id=14, dtype="bf16", n_layers=1, d_model=256,
                          n_q_heads=4, n_kv_heads=1, head_dim=128, d_ffn=512, vocab_draft=3001,
                          vocab_target=4513, target_hidden=192, batch=2, K=3, ctx_lo=1, ctx_hi=16,

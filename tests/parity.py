@@ -12,9 +12,10 @@ can be from the oracle's:
   8 (delta/T) sqrt(sum_{i<=j} w_i^2) + 1e-9 S of a breakpoint C_{j-1} or C_j
   (w = oracle weights): the drafter's logit errors shift the cumulative sums
   by about (delta/T) sqrt(sum w^2) when the errors are independent.
-* acceptance u_k < r_k: |u_k - r_k| < 1e-5 + 4 (delta/T) r_k (delta = 0 when
-  both sides read the same drafter logits).
-* residual / bonus draw: the draw point is within 8 (delta/T) sqrt(sum q^2) +
+* acceptance u_k < r_k: |u_k - r_k| < 1e-5 + 4 (delta/T_d) r_k (delta = 0 when
+  both sides read the same drafter logits; T_d the drafter's temperature, no
+  drafter term when T_d = 0: q is then one-hot and r_k = p_k(d_k)).
+* residual / bonus draw: the draw point is within 8 (delta/T_d) sqrt(sum q^2) +
   1e-8 of a breakpoint (absolute probability units).
 """
 from __future__ import annotations
@@ -68,23 +69,26 @@ def residual_flag(w: np.ndarray, q: np.ndarray, u: float, delta: float, T: float
     return margin < err
 
 
-def verify_flags(res, target_logits, draft_logits, d2t, drafts, T, u_acc, u_bonus, delta=0.0):
-    """True if any decision of this verification is within its flag window."""
+def verify_flags(res, target_logits, draft_logits, d2t, drafts, T, u_acc, u_bonus, delta=0.0,
+                 T_draft=None):
+    """True if any decision of this verification is within its flag window
+    (T the target's temperature, T_draft the drafter's; None: T)."""
     from oracle.verify import drafter_probs_on_target
     K = len(drafts)
+    Td = T if T_draft is None else float(T_draft)
     if T == 0.0:
         # the oracle's decisions are exact comparisons of identical fp32 inputs
         return False
     for k in range(min(res.accept_len + 1, K)):
-        if accept_flag(u_acc[k], res.ratios[k], delta, T):
+        if accept_flag(u_acc[k], res.ratios[k], delta, Td):
             return True
     a = res.accept_len
     tl = np.asarray(target_logits, dtype=np.float64)
     p = sampling.probs(tl[a], T)
     if a < K:
-        q = drafter_probs_on_target(draft_logits[a], d2t, tl.shape[1], T)
+        q = drafter_probs_on_target(draft_logits[a], d2t, tl.shape[1], Td)
         w = np.maximum(p - q, 0.0)
         if w.sum() <= 0:
             w = p
-        return residual_flag(w, q, u_bonus, delta, T)
+        return residual_flag(w, q, u_bonus, delta, Td)
     return residual_flag(p, np.zeros_like(p), u_bonus, 0.0, T)

@@ -39,10 +39,17 @@ def _say(*a):
 # ----------------------------------------------------------------------------------------
 # verify_rows: same inputs on both sides
 # ----------------------------------------------------------------------------------------
-@pytest.mark.parametrize("name,V_d,V_T,vmap", [("small_partial", 997, 811, "partial"),
-                                               ("inject", 3001, 4513, "inject"),
-                                               ("large_identity", 151936, 151936, "identity")])
-def test_verify_rows_matches_oracle(name, V_d, V_T, vmap):
+@pytest.mark.parametrize("name,V_d,V_T,vmap,dmode", [
+    ("small_partial", 997, 811, "partial", "same"),
+    ("inject", 3001, 4513, "inject", "same"),
+    ("large_identity", 151936, 151936, "identity", "same"),
+    ("small_partial_greedy_draft", 997, 811, "partial", "mixed"),
+    ("inject_greedy_draft", 3001, 4513, "inject", "mixed"),
+    ("large_identity_greedy_draft", 151936, 151936, "identity", "greedy")])
+def test_verify_rows_matches_oracle(name, V_d, V_T, vmap, dmode):
+    """dmode: drafts drawn at the target's temperature ("same"), greedily ("greedy":
+    q one-hot, target-only acceptance) or at a mix of greedy, equal and other
+    drafter temperatures ("mixed")."""
     _require_gpu()
     from paper_2609_09338_amd import workload as WL
     _say(f"[verify_rows] {name}")
@@ -55,6 +62,13 @@ def test_verify_rows_matches_oracle(name, V_d, V_T, vmap):
     rng = np.random.default_rng(42)
     B, K = w.batch, w.K
     temps = np.array([[0.0, 0.7, 1.0, 1.3][b % 4] for b in range(B)], dtype=np.float32)
+    if dmode == "same":
+        temps_d = temps.copy()
+    elif dmode == "greedy":
+        temps_d = np.zeros(B, dtype=np.float32)
+    else:
+        temps_d = np.array([[0.0, 0.0, 1.0, 0.5][(b // 2) % 4] for b in range(B)],
+                           dtype=np.float32)
     sig = np.array([[0.05, 0.5, 1.0, 3.0][(b // 4) % 4] for b in range(B)])
     dl = (rng.standard_normal((B, K, V_d)) * 1.5).astype(np.float32)
     dl[:, :, d2t < 0] = -np.inf
@@ -62,7 +76,7 @@ def test_verify_rows_matches_oracle(name, V_d, V_T, vmap):
     drafts = np.zeros((B, K), dtype=np.int32)
     for b in range(B):
         for k in range(K):
-            drafts[b, k] = d2t[OS.pick(dl[b, k], float(temps[b]), float(u_d[b, k]))]
+            drafts[b, k] = d2t[OS.pick(dl[b, k], float(temps_d[b]), float(u_d[b, k]))]
     noise = rng.standard_normal((B, K + 1, V_T)).astype(np.float32)
     tl = np.zeros((B, K + 1, V_T), dtype=np.float32)
     for b in range(B):
@@ -75,19 +89,22 @@ def test_verify_rows_matches_oracle(name, V_d, V_T, vmap):
     al = torch.empty(B, dtype=torch.int32, device=dev)
     mk = torch.empty((B, K), dtype=torch.uint8, device=dev)
     ot = torch.empty((B, K + 1), dtype=torch.int32, device=dev)
-    s.drafter.verify_rows(K, T(tl), T(dl), T(drafts), T(temps), T(u_a), T(u_b), al, mk, ot)
+    s.drafter.verify_rows(K, T(tl), T(dl), T(drafts), T(temps), T(u_a), T(u_b), al, mk, ot,
+                          draft_temperature=None if dmode == "same" else T(temps_d))
     torch.cuda.synchronize()
     assert s.drafter.device_errors() == 0
     al, mk, ot = al.cpu().numpy(), mk.cpu().numpy(), ot.cpu().numpy()
     flagged = 0
     accepted = 0
     for b in range(B):
-        r = o_verify(tl[b], dl[b], d2t, drafts[b], float(temps[b]), u_a[b], float(u_b[b]))
+        r = o_verify(tl[b], dl[b], d2t, drafts[b], float(temps[b]), u_a[b], float(u_b[b]),
+                     T_draft=float(temps_d[b]))
         same = (al[b] == r.accept_len and np.array_equal(mk[b], r.mask)
                 and np.array_equal(ot[b], r.tokens))
         if not same:
             assert parity.verify_flags(r, tl[b], dl[b], d2t, drafts[b], float(temps[b]), u_a[b],
-                                       float(u_b[b])), (b, al[b], r.accept_len, ot[b], r.tokens)
+                                       float(u_b[b]), T_draft=float(temps_d[b])), \
+                (b, al[b], r.accept_len, ot[b], r.tokens)
             flagged += 1
         accepted += r.accept_len
     assert flagged <= 2
@@ -131,7 +148,7 @@ def _run_parity(w, n_iters, seqs, tol):
                               out.tokens.cpu().numpy())
         for b in sorted(live):
             rec = ref[b][it]
-            T = w.temperature(b)
+            T, Td = w.temperature(b), w.draft_temperature(b)
             ok = True
             for k in range(w.K):
                 delta = _delta(g_logits[b, k], rec.draft_logits[k])
@@ -139,7 +156,7 @@ def _run_parity(w, n_iters, seqs, tol):
                 assert delta <= tol, (w.name, b, it, k, delta)
                 if g_drafts[b, k] != rec.drafts[k]:
                     u = float(synth.u_draft(w, it)[b, k])
-                    assert parity.draw_flag(rec.draft_logits[k], T, u, delta), \
+                    assert parity.draw_flag(rec.draft_logits[k], Td, u, delta), \
                         (w.name, b, it, k, g_drafts[b, k], rec.drafts[k])
                     ok = False
                     break
@@ -151,7 +168,7 @@ def _run_parity(w, n_iters, seqs, tol):
                     delta = max(_delta(g_logits[b, k], rec.draft_logits[k]) for k in range(w.K))
                     assert parity.verify_flags(rec.result, rec.target_logits, rec.draft_logits,
                                                d2t, rec.drafts, T, synth.u_accept(w, it)[b],
-                                               float(synth.u_bonus(w, it)[b]), delta), \
+                                               float(synth.u_bonus(w, it)[b]), delta, T_draft=Td), \
                         (w.name, b, it, g_a[b], rec.result.accept_len, g_tok[b], rec.result.tokens)
                     ok = False
             stats["compared"] += 1
@@ -165,7 +182,8 @@ def _run_parity(w, n_iters, seqs, tol):
     return stats
 
 
-@pytest.mark.parametrize("name", ["p_tiny_f32", "p_qwen_small", "p_partial", "p_inject"])
+@pytest.mark.parametrize("name", ["p_tiny_f32", "p_qwen_small", "p_partial", "p_inject",
+                                  "p_greedy_draft"])
 def test_iterations_match_oracle(name):
     _require_gpu()
     w = synth.get(name)
@@ -239,8 +257,8 @@ def test_runs_are_deterministic_and_page_order_free():
 # ----------------------------------------------------------------------------------------
 # full-size workloads, sampled sequences (the GPU runs the whole batch)
 # ----------------------------------------------------------------------------------------
-@pytest.mark.parametrize("name,seqs,iters", [("c2", [0], 2), ("c3", [7], 2), ("c4", [31], 1),
-                                             ("c5", [62, 63], 2)])
+@pytest.mark.parametrize("name,seqs,iters", [("c2", [0], 2), ("c2g", [0], 2), ("c3", [7], 2),
+                                             ("c4", [31], 1), ("c5", [62, 63], 2)])
 def test_full_size_sampled_sequences_match_oracle(name, seqs, iters):
     """Benchmark-size shapes in the launch configuration the benchmark uses; the oracle
     follows the sampled sequences one by one (sequences of a batch are independent)."""

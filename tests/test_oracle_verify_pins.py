@@ -13,7 +13,11 @@ consequences rather than against itself:
 * the acceptance frequency of draft k is sum_v min(p_k, q_k);
 * q = p accepts everything; K = 0 is plain sampling from p_0; target ids that
   no drafter row reaches have q = 0 and are still reachable through the
-  residual.
+  residual;
+* greedy drafting against a sampled target (q one-hot): lossless by
+  chi-square, acceptance frequency p_k(d_k), a rejected position redrawn from
+  p_k without d_k (closed forms), and a planted mistake (treating greedy drafts
+  as sampled at the target's temperature) is rejected.
 """
 import numpy as np
 import pytest
@@ -168,3 +172,95 @@ def test_unreachable_target_ids_have_zero_q_and_come_from_residual():
         d = d2t[sampling.pick(dl, 1.0, rng.random())]
         r = verify(tl, dl[None], d2t, np.array([d]), 1.0, rng.random(1), rng.random())
         assert r.accept_len == 0 and r.tokens[0] == 9 and r.residual_used
+
+
+# ----------------------------------------------------------------------------------------
+# Greedy drafting (drafter temperature 0) verified against a sampled target: q is
+# one-hot at the drafter's argmax, so the rule reduces to target-only acceptance.
+# ----------------------------------------------------------------------------------------
+def _greedy_counts(p_logits, q_logits, T, n, seed, T_draft=0.0):
+    """Greedy drafts (argmax of each drafter row) verified at target temperature T
+    with the drafter temperature T_draft; histograms of the first committed token,
+    of the second one when d_0 was accepted, and of the replacement when d_0 was
+    rejected, plus the number of accepted d_0."""
+    rng = np.random.default_rng(seed)
+    K, V = q_logits.shape
+    d2t = np.arange(V)
+    drafts = np.array([sampling.argmax_lowest(q_logits[k]) for k in range(K)])
+    first = np.zeros(V, dtype=np.int64)
+    second = np.zeros(V, dtype=np.int64)
+    repl = np.zeros(V, dtype=np.int64)
+    acc0 = 0
+    for _ in range(n):
+        r = verify(p_logits, q_logits, d2t, drafts, T, rng.random(K), rng.random(),
+                   T_draft=T_draft)
+        first[r.tokens[0]] += 1
+        if r.accept_len >= 1:
+            acc0 += 1
+            second[r.tokens[1]] += 1
+        else:
+            repl[r.tokens[0]] += 1
+    return drafts, first, second, repl, acc0
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_greedy_drafting_is_lossless(seed):
+    rng = np.random.default_rng(200 + seed)
+    V, K, T = 10, 2, 1.0
+    p_logits = _rand_logits(rng, (K + 1, V), 1.5)
+    q_logits = _rand_logits(rng, (K, V), 1.5)
+    _, first, second, _, _ = _greedy_counts(p_logits, q_logits, T, 30000, seed)
+    assert _chi2_p(first, sampling.probs(p_logits[0], T)) > 1e-4
+    assert _chi2_p(second, sampling.probs(p_logits[1], T)) > 1e-4
+
+
+def test_greedy_drafting_accepts_with_target_probability_and_redraws_without_draft():
+    """Closed forms of the one-hot case: P(accept d_0) = p_0(d_0), and a rejected
+    position is redrawn from p_0 with d_0 removed and renormalised."""
+    rng = np.random.default_rng(210)
+    V, K, T, n = 8, 1, 0.8, 40000
+    p_logits = _rand_logits(rng, (K + 1, V), 1.0)
+    q_logits = p_logits[:K] + _rand_logits(rng, (K, V), 0.3)   # a drafter close to the target
+    drafts, _, _, repl, acc0 = _greedy_counts(p_logits, q_logits, T, n, 5)
+    p0 = sampling.probs(p_logits[0], T)
+    d = int(drafts[0])
+    assert 0.05 < p0[d] < 0.95            # the case is not degenerate
+    assert stats.binomtest(acc0, n, p0[d]).pvalue > 1e-4
+    expect = p0.copy()
+    expect[d] = 0.0
+    assert repl[d] == 0
+    assert _chi2_p(repl, expect / expect.sum()) > 1e-4
+
+
+def test_greedy_drafting_test_rejects_sampled_q_for_greedy_drafts():
+    """Power check: verifying greedy drafts as if they had been sampled at the
+    target's temperature (q = softmax instead of one-hot) is not lossless."""
+    rng = np.random.default_rng(220)
+    V, K, T = 10, 2, 1.0
+    p_logits = _rand_logits(rng, (K + 1, V), 1.5)
+    q_logits = _rand_logits(rng, (K, V), 1.5)
+    _, first, _, _, _ = _greedy_counts(p_logits, q_logits, T, 30000, 6, T_draft=T)
+    assert _chi2_p(first, sampling.probs(p_logits[0], T)) < 1e-6
+
+
+def test_drafter_temperature_defaults_and_greedy_target():
+    """T_draft = None is T_draft = T; a greedy target (T = 0) gives the greedy
+    prefix rule whatever the drafter's temperature."""
+    rng = np.random.default_rng(230)
+    V, K = 9, 4
+    d2t = np.arange(V)
+    for _ in range(200):
+        tl = _rand_logits(rng, (K + 1, V))
+        dl = _rand_logits(rng, (K, V))
+        drafts = rng.integers(0, V, K)
+        j = int(rng.integers(0, K + 1))
+        drafts[:j] = np.argmax(tl, axis=1)[:j]        # a matching prefix of random length
+        ua, ub = rng.random(K), rng.random()
+        for T in (0.0, 0.7):
+            a = verify(tl, dl, d2t, drafts, T, ua, ub)
+            b = verify(tl, dl, d2t, drafts, T, ua, ub, T_draft=T)
+            assert a.accept_len == b.accept_len and np.array_equal(a.tokens, b.tokens)
+        g = verify(tl, dl, d2t, drafts, 0.0, ua, ub)
+        for Td in (0.0, 1.3):
+            x = verify(tl, dl, d2t, drafts, 0.0, ua, ub, T_draft=Td)
+            assert x.accept_len == g.accept_len and np.array_equal(x.tokens, g.tokens)
