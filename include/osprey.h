@@ -270,13 +270,17 @@ int osprey_verify_rows(osprey_handle* h, const osprey_verify_rows_args* a);
  * bit 3 a KV write beyond the slot's pages, bit 4 a draft id outside [0, V_T). */
 int osprey_device_errors(osprey_handle* h, uint32_t* flags);
 
-/* Kernel timing for roofline reports.  When enabled, the library records HIP
- * events around every launch of the named kernel family on its stream;
- * osprey_kernel_time synchronises and returns the summed duration (ms) and the
- * number of launches since the last reset.  Families: 0 = LM head (final norm +
- * vocabulary GEMV + softmax statistics), 1 = attention (split pass), 2 = verify
- * (all four kernels), 3 = a whole draft_step, 4 = expanded-QKV GEMV. */
-int osprey_kernel_timing(osprey_handle* h, int32_t enable);
+/* Kernel timing for roofline reports.  `families` is a bit mask: bit f enables HIP
+ * event timing of family f on the handle's stream (0 disables; every call clears
+ * the records).  Families: 0 = LM head (final norm + vocabulary GEMV + softmax
+ * statistics), 1 = attention (split pass), 2 = verify (all four kernels), 3 = a
+ * whole draft_step, 4 = expanded-QKV GEMV.  Each event adds a few microseconds of
+ * idle time to the stream, so time few families at once.  A timed LM head runs
+ * 8 times back to back between its events (the same outputs again), so its events'
+ * overhead is shared by 8 launches.  osprey_kernel_time synchronises and returns
+ * the summed duration (ms) and the number of launches since the last
+ * osprey_kernel_timing call. */
+int osprey_kernel_timing(osprey_handle* h, int32_t families);
 int osprey_kernel_time(osprey_handle* h, int32_t family, double* total_ms, int64_t* launches);
 
 /* Change the stream subsequent calls are enqueued on. */

@@ -254,8 +254,12 @@ class Drafter:
         _check(_lib().osprey_device_errors(self.h, C.byref(f)))
         return int(f.value)
 
-    def kernel_timing(self, enable: bool) -> None:
-        _check(_lib().osprey_kernel_timing(self.h, 1 if enable else 0))
+    def kernel_timing(self, families=()) -> None:
+        """Event timing of the given kernel families (KERNEL_*); () disables it."""
+        mask = 0
+        for f in families:
+            mask |= 1 << int(f)
+        _check(_lib().osprey_kernel_timing(self.h, mask))
 
     def kernel_time(self, family: int):
         ms, n = C.c_double(), C.c_int64()

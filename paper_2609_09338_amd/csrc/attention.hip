@@ -237,7 +237,7 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   const int p_lo = sp * a.split_len;
   if (p_lo >= n_ctx) return;           // beyond this sequence: the combine reads no partial here
   const int p_hi = min(n_ctx, p_lo + a.split_len);
-  const int slot = a.bslot[b];
+  const int slot = a.slot0 >= 0 ? a.slot0 : a.bslot[b];
   const int nblocks = a.slot_nblocks[slot];
   const int32_t* bt = a.block_table + (long)slot * a.max_blocks;
   TKV* kvb = reinterpret_cast<TKV*>(a.kv);
@@ -421,6 +421,19 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
   const int g = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int row = lane & 15, grp = lane >> 4;
+  // The slot first (an argument for a batch of one), so that the page-table entries of
+  // a whole split, the slot's page count and the row positions are requested together
+  // and the first page follows after one round trip.
+  const int slot = a.slot0 >= 0 ? a.slot0 : a.bslot[b];
+  const int32_t* bt = a.block_table + (long)slot * a.max_blocks;
+  const int pg_lo = sp * a.split_len / PG;   // split_len is a multiple of a page
+  // this wavefront's pages: split pages wave, wave + 4, ... (at most 64: the host keeps
+  // split_len <= 4096), their page-table entries one per lane
+  const int pid = pg_lo + wave + 4 * lane;
+  const int n_pg_full = a.split_len / PG;
+  const int n_mine_full = min(64, n_pg_full > wave ? (n_pg_full - wave + 3) / 4 : 0);
+  const int bt_any = (lane < n_mine_full && pid < a.max_blocks) ? bt[pid] : -1;
+  const int nblocks = a.slot_nblocks[slot];
   int r_beg, r_end;
   if (a.cu) { r_beg = a.cu[b]; r_end = a.cu[b + 1]; } else { r_beg = b; r_end = b + 1; }
   const int rows_total = a.rows.count ? min(*a.rows.count, a.rows.max_rows) : a.rows.max_rows;
@@ -433,24 +446,15 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
   const int p_lo = sp * a.split_len;
   if (p_lo >= n_ctx) return;           // beyond this sequence: the combine reads no partial here
   const int p_hi = min(n_ctx, p_lo + a.split_len);
-  const int slot = a.bslot[b];
-  const int nblocks = a.slot_nblocks[slot];
-  const int32_t* bt = a.block_table + (long)slot * a.max_blocks;
   bf16_t* kvb = reinterpret_cast<bf16_t*>(a.kv);
   const long blk_elems = kv_block_elems(a.n_layers, a.nkv, a.kv_block, HD);
   const long k_off = (((long)a.layer * 2 + 0) * a.nkv + g) * a.kv_block * HD;
   const long v_off = (((long)a.layer * 2 + 1) * a.nkv + g) * a.kv_block * HD;
 
-  // this wavefront's pages: split pages wave, wave + 4, ... (at most 64: the host keeps
-  // split_len <= 4096), their page-table entries one per lane (-1: beyond the slot's pages)
-  const int pg_lo = p_lo / PG;
+  // the pages that hold positions of this split (-1: beyond the slot's pages)
   const int n_pg = p_hi > p_lo ? (p_hi - p_lo + PG - 1) / PG : 0;
   const int n_mine = min(64, n_pg > wave ? (n_pg - wave + 3) / 4 : 0);
-  int bt_reg;
-  {
-    const int pid = pg_lo + wave + 4 * lane;
-    bt_reg = (lane < n_mine && pid < nblocks) ? bt[pid] : -1;
-  }
+  const int bt_reg = (lane < n_mine && pid < nblocks) ? bt_any : -1;
   auto load_page = [&](MPage<HD>& pg, int i) {
     const int phys = __shfl(bt_reg, i, OSP_WAVE);
     if (phys >= 0) {
@@ -628,7 +632,7 @@ __global__ void __launch_bounds__(256) k_rows_qkv(AttnArgs a, float* q_out) {
   }
   const int g = hh - a.nq;
   const int b = a.rows.seq ? a.rows.seq[r] : r;
-  const int slot = a.bslot[b];
+  const int slot = a.slot0 >= 0 ? a.slot0 : a.bslot[b];
   const int blk = pos / a.kv_block;
   if (blk >= a.slot_nblocks[slot]) { if (lane == 0) atomicOr(a.err, 1u << 3); return; }
   const long ko = (long)r * a.qkv_w + (long)(a.nq + g) * HD;
@@ -669,15 +673,19 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
   // splits that hold any position visible to this row (later ones were not written)
   const int ns = min(a.n_split, a.rows.pos[r] / a.split_len + 1);
   const float* pp = a.part + ((long)r * a.nq + h) * a.n_split * (HD + 2);
+  // every split's values are requested before the row position arrives; those of
+  // splits past ns (not written for this row) are discarded by selection
   float v[PER];
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     const int sp = grp + G * i;
-    v[i] = sp < ns ? pp[(long)sp * (HD + 2) + 2 + e] : 0.f;
+    v[i] = sp < a.n_split ? pp[(long)sp * (HD + 2) + 2 + e] : 0.f;
   }
   if (tid < 64) {
-    const float m = lane < ns ? pp[(long)lane * (HD + 2)] : -INFINITY;
-    const float lsum = lane < ns ? pp[(long)lane * (HD + 2) + 1] : 0.f;
+    const float m_any = lane < a.n_split ? pp[(long)lane * (HD + 2)] : -INFINITY;
+    const float l_any = lane < a.n_split ? pp[(long)lane * (HD + 2) + 1] : 0.f;
+    const float m = lane < ns ? m_any : -INFINITY;
+    const float lsum = lane < ns ? l_any : 0.f;
     const float M = wave_max(m);
     const float f = (m > -INFINITY) ? __expf(m - M) : 0.f;
     const float L = wave_sum(lsum * f);

@@ -40,6 +40,10 @@ template <> struct WRaw<bf16_t> {
   uint4 v;
   OSP_DEV void load(const bf16_t* p) { v = *reinterpret_cast<const uint4*>(p); }
   OSP_DEV void zero() { v = make_uint4(0u, 0u, 0u, 0u); }
+  OSP_DEV float get(int e) const {
+    const uint32_t w = e < 2 ? v.x : e < 4 ? v.y : e < 6 ? v.z : v.w;
+    return (e & 1) ? bf16_hi(w) : bf16_lo(w);
+  }
   OSP_DEV float dot(const float* x, float s) const {
     s = fmaf(bf16_lo(v.x), x[0], s); s = fmaf(bf16_hi(v.x), x[1], s);
     s = fmaf(bf16_lo(v.y), x[2], s); s = fmaf(bf16_hi(v.y), x[3], s);
@@ -52,6 +56,7 @@ template <> struct WRaw<float> {
   float4 v;
   OSP_DEV void load(const float* p) { v = *reinterpret_cast<const float4*>(p); }
   OSP_DEV void zero() { v = make_float4(0.f, 0.f, 0.f, 0.f); }
+  OSP_DEV float get(int e) const { return e == 0 ? v.x : e == 1 ? v.y : e == 2 ? v.z : v.w; }
   OSP_DEV float dot(const float* x, float s) const {
     s = fmaf(v.x, x[0], s); s = fmaf(v.y, x[1], s); s = fmaf(v.z, x[2], s); s = fmaf(v.w, x[3], s);
     return s;
@@ -107,6 +112,10 @@ OSP_DEV void norm_x(const GemvArgs& a, int col, float inv_rms, float* v) {
   for (int e = 0; e < VEC; ++e) v[e] = v[e] * inv_rms * g[e];
 }
 
+// Column of the gain vector that input column `col` uses (negative: not normalised).
+template <int SRC>
+OSP_DEV int gain_col(const GemvArgs& a, int col) { return SRC == SRC_QKV ? col - a.d_norm : col; }
+
 // 1 / sqrt(mean(x^2) + eps) of the normalised segment of row rr, by one wavefront.
 template <typename TW, int SRC>
 OSP_DEV float row_inv_rms(const GemvArgs& a, int rr, int lane) {
@@ -125,13 +134,16 @@ OSP_DEV float row_inv_rms(const GemvArgs& a, int rr, int lane) {
 }
 
 // Register budget: the streaming kernels want >= 4 wavefronts per SIMD (<= 128 VGPRs)
-// so that enough loads are in flight; small-row variants fit that budget.
-template <int RB, int NW, int XV> struct GemvOcc {
-  static constexpr int value = (RB * NW * XV <= 8 && RB * XV <= 4) ? 4 : 1;
+// so that enough loads are in flight; small-row variants fit that budget.  Normalised
+// inputs also hold the first step's weights and the gains across the norm: they get
+// 2 wavefronts per SIMD (their grids never place more there).
+template <int RB, int NW, int XV, bool NORMED> struct GemvOcc {
+  static constexpr int value = (RB * NW * XV <= 8 && RB * XV <= 4) ? (NORMED ? 2 : 4) : 1;
 };
 
 template <typename TW, int SRC, int EPI, int RB, int NW, int XV, bool CACHED>
-__global__ void __launch_bounds__(kGemvThreads, (GemvOcc<RB, NW, XV>::value))
+__global__ void __launch_bounds__(kGemvThreads,
+                                  (GemvOcc<RB, NW, XV, (SRC == SRC_NORM || SRC == SRC_QKV)>::value))
 k_gemv(GemvArgs a, int rows_per_wave) {
   constexpr int VEC = Vec<TW>::N;
   constexpr int NWV = (EPI == EPI_SWIGLU) ? 2 * NW : NW;
@@ -152,12 +164,43 @@ k_gemv(GemvArgs a, int rows_per_wave) {
   const int nvec = a.Kd / VEC;                 // 16-byte vectors per weight row
   constexpr bool cached = CACHED;              // the whole input row fits in registers
 
+  // Weights of one step: rows n0 .. n0 + NW (gate and up for SwiGLU), vectors jb + lane + 64 u.
+  auto load_w = [&](WRaw<TW> (&wr)[NWV][XV], int n0, int jb) {
+#pragma unroll
+    for (int i = 0; i < NWV; ++i) {
+      const int n = n0 + (i % NW);
+#pragma unroll
+      for (int u = 0; u < XV; ++u) {
+        const int j = jb + lane + OSP_WAVE * u;
+        if (n < n_hi && j < nvec)
+          wr[i][u].load(((EPI == EPI_SWIGLU && i >= NW) ? w1 : w0) + (long)n * a.Kd + j * VEC);
+        else
+          wr[i][u].zero();
+      }
+    }
+  };
+  // The first step's weights do not depend on the input rows: they are requested
+  // before the rows, their norm and the gains, so that those latencies overlap.
+  WRaw<TW> wr[NWV][XV];
+  load_w(wr, n_lo, 0);
+  bool have_w = true;
+
   for (int r0 = 0; r0 < rows; r0 += RB) {
     float xc[RB][XV][VEC];                     // this lane's input values (cached mode)
     float inv_rms[RB];
 #pragma unroll
     for (int r = 0; r < RB; ++r) inv_rms[r] = 1.f;
     if constexpr (cached) {
+      // gains of this lane's columns, requested with the rows
+      WRaw<TW> gr[XV];
+      if constexpr (NORMED) {
+#pragma unroll
+        for (int u = 0; u < XV; ++u) {
+          const int gc = gain_col<SRC>(a, (lane + OSP_WAVE * u) * VEC);
+          if (gc >= 0 && gc < a.d_norm) gr[u].load(reinterpret_cast<const TW*>(a.gamma) + gc);
+          else gr[u].zero();
+        }
+      }
 #pragma unroll
       for (int r = 0; r < RB; ++r) {
         bool isn[XV];
@@ -172,6 +215,20 @@ k_gemv(GemvArgs a, int rows_per_wave) {
 #pragma unroll
               for (int e = 0; e < VEC; ++e) ss += xc[r][u][e] * xc[r][u][e];
             }
+            if constexpr (SRC == SRC_QKV) {
+              // layer 0: x = embed[token] for the residual, each vector written by one
+              // wavefront (the one whose index matches it modulo the working wavefronts)
+              if (a.embed && a.x_out && isn[u]) {
+                const int jn = j - a.d_norm / VEC;
+                if (jn % ((a.N + rows_per_wave - 1) / rows_per_wave) == gw) {
+                  float* xo = a.x_out + (long)(r0 + r) * a.ldx + jn * VEC;
+#pragma unroll
+                  for (int e = 0; e < VEC; e += 4)
+                    *reinterpret_cast<float4*>(xo + e) =
+                        make_float4(xc[r][u][e], xc[r][u][e + 1], xc[r][u][e + 2], xc[r][u][e + 3]);
+                }
+              }
+            }
           } else {
 #pragma unroll
             for (int e = 0; e < VEC; ++e) xc[r][u][e] = 0.f;
@@ -182,7 +239,10 @@ k_gemv(GemvArgs a, int rows_per_wave) {
           inv_rms[r] = 1.0f / sqrtf(ss / (float)a.d_norm + a.eps);
 #pragma unroll
           for (int u = 0; u < XV; ++u)
-            if (isn[u]) norm_x<TW, SRC, VEC>(a, (lane + OSP_WAVE * u) * VEC, inv_rms[r], xc[r][u]);
+            if (isn[u]) {
+#pragma unroll
+              for (int e = 0; e < VEC; ++e) xc[r][u][e] = xc[r][u][e] * inv_rms[r] * gr[u].get(e);
+            }
         }
       }
     } else if constexpr (NORMED) {
@@ -190,8 +250,9 @@ k_gemv(GemvArgs a, int rows_per_wave) {
       for (int r = 0; r < RB; ++r)
         if (r0 + r < rows) inv_rms[r] = row_inv_rms<TW, SRC>(a, r0 + r, lane);
     }
-    // layer 0 of the expanded QKV: one wavefront writes x = embed[token] for the residual
-    if constexpr (SRC == SRC_QKV) {
+    // layer 0 of the expanded QKV (rows not held in registers): one wavefront writes
+    // x = embed[token] for the residual
+    if constexpr (SRC == SRC_QKV && !cached) {
       if (a.embed && a.x_out && gw == 0) {
         for (int r = 0; r < RB && r0 + r < rows; ++r) {
           int t = a.tok[r0 + r];
@@ -218,26 +279,21 @@ k_gemv(GemvArgs a, int rows_per_wave) {
     for (int n0 = n_lo; n0 < n_hi; n0 += NW) {
       const int idx = lane >> SH;
       const int vi = idx / RB, rsel = idx - vi * RB;
+      const bool owner = (lane & ((1 << SH) - 1)) == 0;
+      const int rr = r0 + rsel;
+      const int n = n0 + vi;
       int mapped = 1;
       if constexpr (EPI == EPI_LOGITS)   // prefetch the vocabulary map of this step's rows
         mapped = (n0 + vi < n_hi) ? a.d2t[n0 + vi] : -1;
+      float y_old = 0.f;                 // the residual value this lane updates, read early
+      if constexpr (EPI == EPI_RESID)
+        if (owner && rr < rows && n < n_hi) y_old = a.y[(long)rr * a.ldy + n];
       float acc[V];
 #pragma unroll
       for (int i = 0; i < V; ++i) acc[i] = 0.f;
       for (int jb = 0; jb < nvec; jb += OSP_WAVE * XV) {
-        WRaw<TW> wr[NWV][XV];
-#pragma unroll
-        for (int i = 0; i < NWV; ++i) {
-          const int n = n0 + (i % NW);
-#pragma unroll
-          for (int u = 0; u < XV; ++u) {
-            const int j = jb + lane + OSP_WAVE * u;
-            if (n < n_hi && j < nvec)
-              wr[i][u].load(((EPI == EPI_SWIGLU && i >= NW) ? w1 : w0) + (long)n * a.Kd + j * VEC);
-            else
-              wr[i][u].zero();
-          }
-        }
+        if (!have_w) load_w(wr, n0, jb);
+        have_w = false;
         if constexpr (!cached) {
 #pragma unroll
           for (int r = 0; r < RB; ++r)
@@ -266,9 +322,6 @@ k_gemv(GemvArgs a, int rows_per_wave) {
       }
       // ---- reduce across lanes: lane l ends with value index l >> SH --------------------
       const float tot = transpose_reduce<LOGV>(acc, lane);
-      const bool owner = (lane & ((1 << SH) - 1)) == 0;
-      const int rr = r0 + rsel;
-      const int n = n0 + vi;
       if constexpr (EPI == EPI_SWIGLU) {
         // gate rows are values [0, NW), up rows [NW, 2 NW)
         const int up_lane = ((vi + NW) * RB + rsel) << SH;
@@ -292,10 +345,7 @@ k_gemv(GemvArgs a, int rows_per_wave) {
           }
         }
       } else {
-        if (owner && rr < rows && n < n_hi) {
-          float* yp = a.y + (long)rr * a.ldy + n;
-          if constexpr (EPI == EPI_RESID) *yp += tot; else *yp = tot;
-        }
+        if (owner && rr < rows && n < n_hi) a.y[(long)rr * a.ldy + n] = y_old + tot;
       }
     }
     if constexpr (EPI == EPI_LOGITS) {

@@ -164,6 +164,7 @@ struct AttnArgs {
   RowMeta rows;
   const int32_t* cu;        // [B+1] rows of sequence b are [cu[b], cu[b+1]) (nullable: [b, b+1))
   const int32_t* bslot;     // [B] slot of sequence b
+  int slot0;                // the slot of sequence 0 when B == 1 (no load); -1: bslot
   int B;
   int rows_per_seq;         // host bound on the rows of one sequence in this pass
   const float* qkv;         // [rows][qkv_w] raw projections (split 0 of qkv_ks partials)

@@ -126,16 +126,28 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
       s_before = run;
     }
     __syncthreads();
-    // ---- scan the chosen range's logits with one wavefront ----------------------------
+    // ---- scan the chosen range's logits with one wavefront; the first kScanPre x 64 of
+    //      them are requested at once (a range holds 16 T <= 128 logits) -------------------
     if (wave == 0) {
+      constexpr int kScanPre = 2;
       const int r0 = s_blk * a.blk_rows;
       const int r1 = min(r0 + a.blk_rows, a.V);
       const float* lg = a.logits + (long)b * a.ld_logits;
+      float pre[kScanPre];
+#pragma unroll
+      for (int q = 0; q < kScanPre; ++q) {
+        const int i = r0 + q * OSP_WAVE + lane;
+        pre[q] = i < r1 ? lg[i] : -INFINITY;
+      }
       double run = s_before;
       int last_pos = -1, found = -1;
-      for (int c0 = r0; c0 < r1; c0 += OSP_WAVE) {
+      for (int c0 = r0, q = 0; c0 < r1; c0 += OSP_WAVE, ++q) {
         const int i = c0 + lane;
-        const float li = i < r1 ? lg[i] : -INFINITY;
+        float li = -INFINITY;
+#pragma unroll
+        for (int p = 0; p < kScanPre; ++p)
+          if (p == q) li = pre[p];
+        if (q >= kScanPre) li = i < r1 ? lg[i] : -INFINITY;
         const float w = li > -INFINITY ? __expf((li - M) / T) : 0.f;
         const float inc = wave_incl_scan<float>(w);
         const unsigned long long hit = __ballot(w > 0.f && run + (double)inc > target);
