@@ -138,6 +138,16 @@ PARITY: Dict[str, Workload] = {
                                batch=4, K=5, ctx_lo=9, ctx_hi=40, temps=(1.0, 0.1, 0.0, 0.7),
                                draft_temps=(0.0, 0.0, 0.0, 0.3), sigma=0.05,
                                vocab_map="partial", shuffle_blocks=True),
+    # single sequences (batch 1): the one-launch body of autoregressive steps
+    "p_single64": Workload(name="p_single64", cfg_id=16, dtype="bf16", n_layers=2, d_model=256,
+                           n_q_heads=8, n_kv_heads=2, head_dim=64, d_ffn=640, vocab_draft=4001,
+                           vocab_target=4001, target_hidden=128, batch=1, K=6, ctx_lo=23,
+                           ctx_hi=23, temps=(1.0,), sigma=0.5, shuffle_blocks=True),
+    "p_single128": Workload(name="p_single128", cfg_id=17, dtype="bf16", n_layers=3, d_model=384,
+                            n_q_heads=4, n_kv_heads=2, head_dim=128, d_ffn=1152, vocab_draft=3001,
+                            vocab_target=4513, target_hidden=192, batch=1, K=5, ctx_lo=47,
+                            ctx_hi=47, temps=(0.0,), sigma=0.05, vocab_map="inject",
+                            shuffle_blocks=True),
     "p_inject": Workload(name="p_inject", cfg_id=14, dtype="bf16", n_layers=1, d_model=256,
                          n_q_heads=4, n_kv_heads=1, head_dim=128, d_ffn=512, vocab_draft=3001,
                          vocab_target=4513, target_hidden=192, batch=2, K=3, ctx_lo=1, ctx_hi=16,

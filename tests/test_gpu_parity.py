@@ -183,7 +183,7 @@ def _run_parity(w, n_iters, seqs, tol):
 
 
 @pytest.mark.parametrize("name", ["p_tiny_f32", "p_qwen_small", "p_partial", "p_inject",
-                                  "p_greedy_draft"])
+                                  "p_greedy_draft", "p_single64", "p_single128"])
 def test_iterations_match_oracle(name):
     _require_gpu()
     w = synth.get(name)
