@@ -110,6 +110,15 @@ WORKLOADS: Dict[str, Workload] = {
     "c2g": Workload(name="c2g", cfg_id=6, vocab_draft=151936, vocab_target=151936,
                     target_hidden=4096, batch=1, K=7, ctx_lo=2048, ctx_hi=2048, temps=(1.0,),
                     draft_temps=(0.0,), sigma=1.0, **_QWEN_DRAFTER),
+    # The paper's own drafter shape (2 layers of pruned Qwen3-4B: d 2560, 32 / 8 heads x 128,
+    # FFN 9728; its size is pinned by the table of draft sizes) for the Qwen3-8B target,
+    # served as the paper serves it: a greedy (top-1) chain of 5 draft steps, target
+    # temperature 0; a target close to the drafter (sigma 0.05) stands in for a trained one.
+    "osprey_2l": Workload(name="osprey_2l", cfg_id=7, dtype="bf16", n_layers=2, d_model=2560,
+                          n_q_heads=32, n_kv_heads=8, head_dim=128, d_ffn=9728,
+                          vocab_draft=151936, vocab_target=151936, target_hidden=4096, batch=1,
+                          K=5, ctx_lo=2048, ctx_hi=2048, temps=(0.0,), draft_temps=(0.0,),
+                          sigma=0.05),
     # Throughput-bound decode: batch 64, ragged contexts, mixed greedy / T = 1.
     "c5": Workload(name="c5", cfg_id=5, vocab_draft=151936, vocab_target=151936,
                    target_hidden=4096, batch=64, K=7, ctx_lo=512, ctx_hi=4096,

@@ -258,7 +258,8 @@ def test_runs_are_deterministic_and_page_order_free():
 # full-size workloads, sampled sequences (the GPU runs the whole batch)
 # ----------------------------------------------------------------------------------------
 @pytest.mark.parametrize("name,seqs,iters", [("c2", [0], 2), ("c2g", [0], 2), ("c3", [7], 2),
-                                             ("c4", [31], 1), ("c5", [62, 63], 2)])
+                                             ("c4", [31], 1), ("c5", [62, 63], 2),
+                                             ("osprey_2l", [0], 2)])
 def test_full_size_sampled_sequences_match_oracle(name, seqs, iters):
     """Benchmark-size shapes in the launch configuration the benchmark uses; the oracle
     follows the sampled sequences one by one (sequences of a batch are independent)."""
