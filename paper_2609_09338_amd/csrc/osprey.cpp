@@ -529,8 +529,14 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     a.o_hi = W.xa_hi;
     a.o_lo = W.xa_lo;
     a.err = W.err;
-    launch_rows_qkv(c.dtype, a, W.o, h->stream);
-    a.q_prep = W.o;
+    // Several rows per sequence: one row kernel prepares q (norm, RoPE, scale) and
+    // appends k / v once, instead of every split block of the sequence doing it.  One
+    // row per sequence (draft steps): the attention blocks sum the QKV partials and
+    // prepare their own queries, one launch fewer per layer.
+    if (rows_per_seq > 1) {
+      launch_rows_qkv(c.dtype, a, W.o, h->stream);
+      a.q_prep = W.o;
+    }
     t = h->t_begin(1);
     launch_attention(c.dtype, a, h->stream);
     h->t_end(t);
