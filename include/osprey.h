@@ -170,8 +170,10 @@ typedef struct {
  * draft k is accepted iff u_k < p_k(d_k), and a rejected position is redrawn
  * from p_a with d_a removed (target-only acceptance).  Draft with
  * osprey_draft_step at temperature T_d (0 for greedy) and pass the same values
- * as draft_temperature here.  With T == 0 the rule is the greedy prefix match
- * whatever T_d is. */
+ * as draft_temperature here: osprey_verify takes each drafter row's max and
+ * normaliser from the draft step (computed there at its temperature) and reads
+ * the drafter's logits only at the drafted entries and in row a.  With T == 0 the rule is the
+ * greedy prefix match whatever T_d is. */
 
 /* Arguments of osprey_verify (stateful: the drafts and drafter rows of the last
  * draft_step on exactly these slots in this order with this K).  The target's

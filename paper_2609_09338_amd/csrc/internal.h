@@ -205,6 +205,15 @@ void launch_rows_qkv(int kvdtype, const AttnArgs& a, float* q_out, hipStream_t s
 void launch_attn_combine(const AttnArgs& a, hipStream_t st);
 
 // Sampling from the LM-head block statistics.
+// Statistics of one drafter logit row at the temperature its draft was drawn at:
+// S = sum exp((l - M) / T_d) over mapped rows (T_d = 0: unused), M the max and am the
+// lowest argmax row (-1: every row masked).
+struct QStat {
+  double S;
+  float M;
+  int am;
+};
+
 struct SampleArgs {
   int B;
   int k;                    // draft step index
@@ -228,6 +237,8 @@ struct SampleArgs {
   const int32_t* gather;    // row of g for sequence b (nullable: b)
   int d;
   float* gfb;               // [B][d] fed-back hidden state
+  QStat* qstat;             // [B][ld_qstat]: row statistics of step k at column k (nullable)
+  int ld_qstat;
 };
 void launch_sample(const SampleArgs& a, hipStream_t st);
 
@@ -287,7 +298,11 @@ struct VerifyArgs {
   int V_T, V_d;
   int chunk;                // elements per partial block
   int nchunk_t, nchunk_d;
-  float* part;              // [B][(K+1)*nchunk_t + K*nchunk_d][4]
+  float* part;              // [B][(K+1)*nchunk_t + (qstat ? 0 : K*nchunk_d)][4]
+  // drafter row statistics kept by the draft step's sampling kernel ([B][ld_qstat],
+  // column k); nullptr: computed here from the drafter rows
+  const QStat* qstat;
+  int ld_qstat;
   double* res_part;         // [B][nchunk_t][2]: residual and p sums per chunk
   int32_t* vstate;          // [B][4]: a, argmax of p_a, one-hot drafter row of q_a (T_d = 0)
   double* vstat;            // [B][4]: M_a, S_a (target), m_a, s_a (draft)

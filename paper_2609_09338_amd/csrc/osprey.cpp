@@ -78,6 +78,7 @@ struct Ws {
   float* split_s2;    // a second such buffer (the down projection reads gate/up partials)
   float* logits;
   float* lm_part;
+  QStat* qstat;       // drafter row statistics of the last chain, [B][Km]
   int32_t* drafts;
   float* u_zero;
   float* v_part;
@@ -168,6 +169,7 @@ size_t plan(const osprey_config& c, char* base, Ws* w) {
   }
   W.logits = (float*)take(4L * D.B * D.Km * c.vocab_draft);
   W.lm_part = (float*)take(16L * D.B * D.lm_nblk_max);
+  W.qstat = (QStat*)take(sizeof(QStat) * D.B * D.Km);
   W.drafts = (int32_t*)take(4L * D.B * D.Km);
   W.u_zero = (float*)take(4L * D.B * D.Km);
   W.v_part = (float*)take(16L * D.B * ((D.Km + 1) * D.nchunk_t + D.Km * D.nchunk_d));
@@ -682,6 +684,8 @@ void run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, cons
   s.gather = gather;
   s.d = c.d_model;
   s.gfb = W.gfb;
+  s.qstat = W.qstat;
+  s.ld_qstat = h->D.Km;
   launch_sample(s, h->stream);
 }
 
@@ -1031,6 +1035,8 @@ OSPREY_API int osprey_verify(osprey_handle* h, const osprey_verify_args* a) {
   v.target = a->target_logits;
   v.draft = h->last_logits;
   v.ld_draft_b = h->last_ld_b;
+  v.qstat = h->W.qstat;
+  v.ld_qstat = h->D.Km;
   v.drafts = h->W.drafts;
   v.ld_drafts = h->D.Km;
   v.temp = a->temperature;

@@ -8,7 +8,8 @@
 // that point is found from the range sums (float64 prefix), then that range's
 // logits are scanned.  The row is mapped to a target id through d2t; the token,
 // its position and the last-layer hidden state (fed back as the next step's
-// conditioning input) are written for the next autoregressive step.
+// conditioning input) are written for the next autoregressive step, and the row's
+// (S, M, lowest argmax) for the verification of the chain.
 #include "common.h"
 #include "internal.h"
 
@@ -79,6 +80,7 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
   }
   const float M = m;
   int row;
+  double S = 0.0;
   if (T <= 0.f || M == -INFINITY) {
     row = am;
   } else {
@@ -93,6 +95,7 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
     }
     double incl, tot;
     const double excl = block_scan<kSampleThreads, double>(loc, s_scan, incl, tot);
+    S = tot;
     const double target = (double)u * tot;
     if (tid == 0) { s_blk = -1; s_row = -1; }
     __syncthreads();
@@ -168,6 +171,8 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
     if (a.drafts_out) a.drafts_out[(long)b * a.K + a.k] = d;
     a.ar_tok[b] = d;
     a.ar_pos[b] = a.committed[b] + a.k;
+    // the row's statistics, for the verification of this draft
+    if (a.qstat) a.qstat[(long)b * a.ld_qstat + a.k] = QStat{S, M, am == 0x7fffffff ? -1 : am};
   }
 #pragma unroll
   for (int q = 0; q < kFbPer; ++q) {

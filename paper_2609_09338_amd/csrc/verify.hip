@@ -9,7 +9,9 @@
 // reduces acceptance to u_k < p_k(d_k) and the residual to p_a without d_a).
 //
 //   k_vstats  (B x jobs)   per chunk of every target and drafter row: max,
-//                          lowest argmax and sum exp((l - max)/T)
+//                          lowest argmax and sum exp((l - max)/T) (stateful
+//                          verify: target rows only; the drafter rows' were kept
+//                          by the draft step's sampling kernel)
 //   k_vaccept (B)          merges chunks in order; accepts d_k while
 //                          u_k < min(1, p_k(d_k)/q_k(d_k)) (T = 0: d_k equals
 //                          the target argmax); writes a, the mask and d_0..d_{a-1}
@@ -60,7 +62,7 @@ __global__ void __launch_bounds__(kVThreads) k_vstats(VerifyArgs a) {
   const int lane = threadIdx.x & 63;
   const int j = blockIdx.y * (kVThreads / 64) + (threadIdx.x >> 6);
   const int nt = (a.K + 1) * a.nchunk_t;
-  const int nj = nt + a.K * a.nchunk_d;
+  const int nj = nt + (a.qstat ? 0 : a.K * a.nchunk_d);
   if (j >= nj) return;
   const float* row;
   int V, c;
@@ -142,10 +144,18 @@ __global__ void __launch_bounds__(kVThreads) k_vaccept(VerifyArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int K = a.K;
   const int nt = (K + 1) * a.nchunk_t;
-  const int nj = nt + K * a.nchunk_d;
+  const int nj = nt + (a.qstat ? 0 : K * a.nchunk_d);
   const float* part = a.part + (long)b * nj * 4;
   const float T = a.temp[b], Td = a.temp_d[b];
-  const int nrows = (K + 1) + (T > 0.f ? K : 0);
+  // drafter rows: the statistics the sampling kernel kept, or merged chunks
+  const bool kept = a.qstat != nullptr;
+  if (kept && T > 0.f && tid < K) {
+    const QStat qs = a.qstat[(long)b * a.ld_qstat + tid];
+    s_M[K + 1 + tid] = qs.M;
+    s_S[K + 1 + tid] = qs.S;
+    s_am[K + 1 + tid] = qs.am;
+  }
+  const int nrows = (K + 1) + (T > 0.f && !kept ? K : 0);
   for (int q = wave; q < nrows; q += kVThreads / 64) {
     float M;
     double S;
@@ -419,7 +429,7 @@ __global__ void __launch_bounds__(kVThreads) k_vfinal(VerifyArgs a) {
 }
 
 void launch_verify(const VerifyArgs& a, hipStream_t st) {
-  const int nj = (a.K + 1) * a.nchunk_t + a.K * a.nchunk_d;
+  const int nj = (a.K + 1) * a.nchunk_t + (a.qstat ? 0 : a.K * a.nchunk_d);
   hipLaunchKernelGGL(k_vstats, dim3(a.B, (nj + kVThreads / 64 - 1) / (kVThreads / 64)), dim3(kVThreads), 0, st, a);
   hipLaunchKernelGGL(k_vaccept, dim3(a.B), dim3(kVThreads), 0, st, a);
   hipLaunchKernelGGL(k_vresid, dim3(a.B, a.nchunk_t), dim3(kVThreads), 0, st, a);
