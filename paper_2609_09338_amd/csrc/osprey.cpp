@@ -193,6 +193,15 @@ int validate(const osprey_config* c) {
   if (c->vocab_draft < 1 || c->vocab_target < 1) return fail(OSPREY_E_SHAPE, "vocabularies must be non-empty");
   if (c->target_hidden < 8 || c->target_hidden % 8) return fail(OSPREY_E_SHAPE, "target_hidden %d must be a positive multiple of 8", c->target_hidden);
   if (c->n_taps < 1 || c->n_taps > 16) return fail(OSPREY_E_SHAPE, "n_taps %d not in [1, 16]", c->n_taps);
+  // weight matrices are read through 32-bit byte offsets: each must stay under 1 GiB
+  {
+    const long qkv = (long)(c->n_q_heads + 2 * c->n_kv_heads) * c->head_dim;
+    const long mats[] = {(long)c->vocab_draft * c->d_model, (long)c->d_model * c->n_taps * c->target_hidden,
+                         qkv * 2 * c->d_model, (long)c->d_model * c->n_q_heads * c->head_dim,
+                         (long)c->d_ffn * c->d_model};
+    for (long m : mats)
+      if (m * 4 > 0x7fffffffL) return fail(OSPREY_E_UNSUPPORTED, "a weight matrix of %ld values is over 1 GiB in bf16", m);
+  }
   if (c->dtype != OSPREY_F32 && c->dtype != OSPREY_BF16) return fail(OSPREY_E_INVALID, "dtype %d", c->dtype);
   if (c->qk_norm != 0 && c->qk_norm != 1) return fail(OSPREY_E_INVALID, "qk_norm must be 0 or 1");
   if (!(c->rms_eps > 0.f) || !(c->rope_theta > 1.f)) return fail(OSPREY_E_INVALID, "rms_eps must be > 0 and rope_theta > 1");

@@ -22,8 +22,12 @@
 // only).  Two MFMAs per product keep about 16 significant bits of every input,
 // so the result stays close to fp32.
 //
-// Inputs: prepared pairs (two segments [xs ; xa] for the expanded QKV), fp32 rows
-// normalised here (LM head after the vector body), or bf16 taps rows.
+// Inputs: prepared pairs (two segments [xs ; xa] for the expanded QKV), one fp32
+// row normalised here (LM head after the batch-1 vector body), or bf16 taps rows.
+// The single normalised row is staged whole, once, before the stream starts: its
+// loads are issued ahead of the first weight units (a load waits for every load
+// issued before it), and the K phases then follow one another with no barrier or
+// input copy.
 #include "common.h"
 #include "internal.h"
 
@@ -63,7 +67,6 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
   constexpr int kSkDepth = MT == 4 ? 2 : kSkDepthMax;
   __shared__ __attribute__((aligned(16))) bf16_t xh[ROWS * PITCH];
   __shared__ __attribute__((aligned(16))) bf16_t xl[EXACT ? 8 : ROWS * PITCH];
-  __shared__ float s_inv[SRC == SK_NORM ? ROWS : 1];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wrow = lane & 15, grp = lane >> 4;
@@ -78,6 +81,8 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
   const int k_lo = EPI == SK_PART ? blockIdx.y * kc : 0;
   const int k_hi = EPI == SK_PART ? min(a.Kd, k_lo + kc) : a.Kd;
   const int nch = EPI == SK_PART ? kc / kSkUnit : NCH;  // units per tile and phase
+  // LM head blocks with no tile at all leave at once (block-uniform, before any barrier)
+  if (EPI == SK_LOGITS && blockIdx.x * kSkWaves * T >= nt16) return;
 
   sk_f32x4 acc[TMAX][MT];
 #pragma unroll
@@ -100,37 +105,75 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
   };
   const int nphase = (k_hi - k_lo + KC - 1) / KC;
   const int nu = ntiles * nch;                          // units per phase
+  // single normalised row: thread t stages columns [8t, 8t + 8) (Kd <= 8 x 512), read
+  // before the weights are requested (addresses clamped into the row; pieces past Kd
+  // are neither summed nor stored)
+  float4 nx0, nx1;
+  uint4 ng;
+  if constexpr (SRC == SK_NORM) {
+    const float* xr = a.xin + (long)(a.gather ? a.gather[0] : 0) * a.ldx;
+    const int c = min(tid * 8, a.Kd - 8);
+    nx0 = *reinterpret_cast<const float4*>(xr + c);
+    nx1 = *reinterpret_cast<const float4*>(xr + c + 4);
+    ng = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16_t*>(a.gamma) + c);
+  }
   uint4 ring[kSkDepth][8];
-  // the first units of a phase are requested before its inputs are staged
+  // units whose columns start at or past k_hi (the last phase of a K that is not a
+  // multiple of KC) are neither loaded nor multiplied
+  auto real = [&](int k0, int u) { return u < nu && k0 + (u % nch) * kSkUnit < k_hi; };
+  // the first units of a phase are requested before its inputs are staged.  The
+  // single normalised row requests them with no condition (the addresses are clamped;
+  // a unit that is not real is never used), so that the waits on its input loads need
+  // not assume an unknown number of loads in between; elsewhere a unit past the block's
+  // range could be a whole unit of another block's weights
   auto prefetch_phase = [&](int k0) {
 #pragma unroll
     for (int u = 0; u + 1 < kSkDepth; ++u)
-      if (u < nu) load_unit(ring[u], k0, u);
+      if (SRC == SK_NORM || real(k0, u)) load_unit(ring[u], k0, u);
   };
   prefetch_phase(k_lo);
-  // LM head: which of this lane's columns map to a target id (one per tile)
-  int live[TMAX];
+  // LM head: the map entries of this lane's columns (one per tile), read from a clamped
+  // address with no condition: a value tested where it is loaded would make the
+  // wavefront wait there for every load issued before it (the weights)
+  int dmap[TMAX];
 #pragma unroll
-  for (int j = 0; j < TMAX; ++j) {
-    const int n = (t0 + j) * 16 + wrow;
-    live[j] = (EPI == SK_LOGITS && j < ntiles && n < a.N) ? (a.d2t[n] >= 0) : 0;
-  }
+  for (int j = 0; j < TMAX; ++j)
+    dmap[j] = EPI == SK_LOGITS ? a.d2t[min((t0 + j) * 16 + wrow, a.N - 1)] : 0;
   if constexpr (SRC == SK_NORM) {
-    // RMS of every input row (one wavefront per row)
-    for (int r = wave; r < R; r += kSkWaves) {
-      const float* xr = a.xin + (long)(a.gather ? a.gather[r] : r) * a.ldx;
-      float ss = 0.f;
-      for (int c = lane * 4; c < a.Kd; c += 64 * 4) {
-        const float4 v = *reinterpret_cast<const float4*>(xr + c);
-        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-      }
-      ss = wave_sum(ss);
-      if (lane == 0) s_inv[r] = 1.0f / sqrtf(ss / (float)a.Kd + a.eps);
+    // RMS of the row (wavefront sums, then the block's in a fixed order), then the
+    // normalised row as hi / lo pairs at LDS columns [0, Kd)
+    __shared__ float s_ss[kSkWaves];
+    const int c = tid * 8;
+    const bool in = c < a.Kd;
+    float ss = 0.f;
+    if (in)
+      ss = nx0.x * nx0.x + nx0.y * nx0.y + nx0.z * nx0.z + nx0.w * nx0.w +
+           nx1.x * nx1.x + nx1.y * nx1.y + nx1.z * nx1.z + nx1.w * nx1.w;
+    ss = wave_sum(ss);
+    if (lane == 0) s_ss[wave] = ss;
+    __syncthreads();
+    float tot = 0.f;
+#pragma unroll
+    for (int w = 0; w < kSkWaves; ++w) tot += s_ss[w];
+    const float inv = 1.0f / sqrtf(tot / (float)a.Kd + a.eps);
+    if (!in && c < nphase * KC) {   // columns of the last phase past Kd meet zeros
+      *reinterpret_cast<uint4*>(xh + c) = make_uint4(0u, 0u, 0u, 0u);
+      *reinterpret_cast<uint4*>(xl + c) = make_uint4(0u, 0u, 0u, 0u);
+    }
+    if (in) {
+      uint4 h, l;
+      split_bf16x2(nx0.x * inv * bf16_lo(ng.x), nx0.y * inv * bf16_hi(ng.x), h.x, l.x);
+      split_bf16x2(nx0.z * inv * bf16_lo(ng.y), nx0.w * inv * bf16_hi(ng.y), h.y, l.y);
+      split_bf16x2(nx1.x * inv * bf16_lo(ng.z), nx1.y * inv * bf16_hi(ng.z), h.z, l.z);
+      split_bf16x2(nx1.z * inv * bf16_lo(ng.w), nx1.w * inv * bf16_hi(ng.w), h.w, l.w);
+      *reinterpret_cast<uint4*>(xh + c) = h;
+      *reinterpret_cast<uint4*>(xl + c) = l;
     }
     __syncthreads();
   }
   for (int ph = 0; ph < nphase; ++ph) {
     const int k0 = k_lo + ph * KC;
+    if constexpr (SRC != SK_NORM) {
     if (ph > 0) __syncthreads();
     // ---- inputs of this phase into LDS: rows r < R and the columns this block reads
     //      (the projections' K range, or the whole phase); columns past k_hi are zero.
@@ -151,17 +194,7 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
         const int c = k0 + col;
         uint4 h = make_uint4(0u, 0u, 0u, 0u), l = h;
         if (i < nitems && c < k_hi) {
-          if constexpr (SRC == SK_NORM) {
-            const float* xr = a.xin + (long)(a.gather ? a.gather[r] : r) * a.ldx + c;
-            const float4 v0 = *reinterpret_cast<const float4*>(xr);
-            const float4 v1 = *reinterpret_cast<const float4*>(xr + 4);
-            const uint4 g = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16_t*>(a.gamma) + c);
-            const float inv = s_inv[r];
-            split_bf16x2(v0.x * inv * bf16_lo(g.x), v0.y * inv * bf16_hi(g.x), h.x, l.x);
-            split_bf16x2(v0.z * inv * bf16_lo(g.y), v0.w * inv * bf16_hi(g.y), h.y, l.y);
-            split_bf16x2(v1.x * inv * bf16_lo(g.z), v1.y * inv * bf16_hi(g.z), h.z, l.z);
-            split_bf16x2(v1.z * inv * bf16_lo(g.w), v1.w * inv * bf16_hi(g.w), h.w, l.w);
-          } else if constexpr (SRC == SK_TAPS) {
+          if constexpr (SRC == SK_TAPS) {
             h = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16_t*>(a.taps) +
                                                 (long)a.tap_row[r] * a.ldt + c);
           } else if constexpr (SRC == SK_SWIGLU) {
@@ -221,12 +254,15 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
       }
     }
     __syncthreads();
+    }
 
     // ---- stream this wavefront's units: tile j = u / NCH, columns (u % NCH) * 256 ----
 #pragma unroll
     for (int u = 0; u < NU; ++u) {
-      if (u < nu) {
-        if (u + kSkDepth - 1 < nu) load_unit(ring[(u + kSkDepth - 1) % kSkDepth], k0, u + kSkDepth - 1);
+      // (a unit that is not real still requests the one kSkDepth - 1 places ahead, which
+      // may be)
+      if (real(k0, u + kSkDepth - 1)) load_unit(ring[(u + kSkDepth - 1) % kSkDepth], k0, u + kSkDepth - 1);
+      if (real(k0, u)) {
         // keep each unit's work in place: hoisting later units' LDS reads or loads
         // above this point only raises register pressure
         __builtin_amdgcn_sched_barrier(0);
@@ -241,7 +277,9 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
           sk_bf16x8 ah[MT], al[MT];
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
-            const int off = (mt * 16 + wrow) * PITCH + kl + 32 * ks;
+            // (the single normalised row: every lane reads row 0 at its column in the
+            // whole row; the outputs of rows 1..15 are dropped)
+            const int off = SRC == SK_NORM ? k0 + kl + 32 * ks : (mt * 16 + wrow) * PITCH + kl + 32 * ks;
             ah[mt] = *reinterpret_cast<const sk_bf16x8*>(xh + off);
             if constexpr (!EXACT) al[mt] = *reinterpret_cast<const sk_bf16x8*>(xl + off);
           }
@@ -297,7 +335,7 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const float lv = live[j] ? acc[j][mt][e] : -INFINITY;
+            const float lv = (n < a.N && dmap[j] >= 0) ? acc[j][mt][e] : -INFINITY;
             acc[j][mt][e] = lv;
             if (mt * 16 + 4 * grp + e < R && n < a.N) yc[(long)(mt * 16 + e) * a.ld_logits] = lv;
           }
@@ -421,7 +459,10 @@ static void sk_launch(int mt, dim3 grid, const GemvArgs& a, int T, int kc, hipSt
 }
 
 void launch_lm_head(const GemvArgs& a, const LmPlan& p, bool norm_in, hipStream_t st) {
-  if (norm_in) sk_launch<SK_NORM, SK_LOGITS>(p.mt, dim3(p.grid), a, p.T, 0, st);
+  // the fp32 input is normalised in the head for one row only (batch 1), of at most
+  // 8 x kSkThreads columns
+  if (norm_in && (a.max_rows != 1 || a.Kd > 8 * kSkThreads)) std::abort();
+  if (norm_in) sk_launch<SK_NORM, SK_LOGITS>(1, dim3(p.grid), a, p.T, 0, st);
   else sk_launch<SK_PREP, SK_LOGITS>(p.mt, dim3(p.grid), a, p.T, 0, st);
 }
 
