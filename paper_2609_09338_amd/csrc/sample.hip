@@ -34,28 +34,29 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
   // now, with the records, so its load is not one more round trip at the end
   constexpr int kFbPer = 4;            // d <= kSampleThreads * 4 * kFbPer
   const int xr = a.gather ? a.gather[b] : b;
-  // (every load below is unconditional, from a clamped address, and masked where it
-  // is used: a load under a condition is followed by a wait for it, and for all loads
-  // issued before it)
   float4 fb[kFbPer];
 #pragma unroll
   for (int q = 0; q < kFbPer; ++q) {
-    const int c = min((tid + q * kSampleThreads) * 4, a.d - 4);
-    fb[q] = *reinterpret_cast<const float4*>(a.x + (long)xr * a.d + c);
+    const int c = (tid + q * kSampleThreads) * 4;
+    fb[q] = c < a.d ? *reinterpret_cast<const float4*>(a.x + (long)xr * a.d + c) : make_float4(0.f, 0.f, 0.f, 0.f);
   }
   // ---- this thread's contiguous records, all loads issued together ----------------
   const int i0 = tid * kPer;
-  float4 rec[kPer];
-#pragma unroll
-  for (int q = 0; q < kPer; ++q) rec[q] = *reinterpret_cast<const float4*>(part + min(i0 + q, a.nblk - 1) * 4);
   float bm[kPer], bs[kPer];
   int ba[kPer];
 #pragma unroll
   for (int q = 0; q < kPer; ++q) {
-    const bool in = i0 + q < a.nblk;
-    bm[q] = in ? rec[q].x : -INFINITY;
-    bs[q] = in ? rec[q].y : 0.f;
-    ba[q] = in ? __float_as_int(rec[q].z) : -1;
+    const int i = i0 + q;
+    if (i < a.nblk) {
+      const float4 r = *reinterpret_cast<const float4*>(part + i * 4);
+      bm[q] = r.x;
+      bs[q] = r.y;
+      ba[q] = __float_as_int(r.z);
+    } else {
+      bm[q] = -INFINITY;
+      bs[q] = 0.f;
+      ba[q] = -1;
+    }
   }
   // ---- global max and lowest argmax ------------------------------------------------
   float m = -INFINITY;
