@@ -66,7 +66,8 @@ struct GemvArgs {
   // logits epilogue
   const int32_t* d2t;       // [N]
   const float* temp;        // [B] temperature per sequence
-  const int32_t* row_seq;   // batch index of output row r (nullable: r)
+  const int32_t* row_seq;   // batch index of output row r (nullable: r; the matrix-core LM head
+                            // takes row r as sequence r)
   long ld_logits;           // stride between rows of y for logits
   float* part;              // [rows][nblk][4]: max, sumexp, argmax, unused
   int nblk;

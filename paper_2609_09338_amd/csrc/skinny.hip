@@ -139,6 +139,13 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
 #pragma unroll
   for (int j = 0; j < TMAX; ++j)
     dmap[j] = EPI == SK_LOGITS ? a.d2t[min((t0 + j) * 16 + wrow, a.N - 1)] : 0;
+  // ... and the temperatures of the lane's output rows 16 mt + 4 grp + e (row r of the
+  // pass is sequence r), requested now so that the epilogue does not wait for them
+  constexpr int NTK = EPI == SK_LOGITS ? 4 * MT : 1;
+  float tk[NTK];
+#pragma unroll
+  for (int k = 0; k < NTK; ++k)
+    tk[k] = EPI == SK_LOGITS ? a.temp[min((k / 4) * 16 + 4 * grp + (k % 4), R - 1)] : 0.f;
   if constexpr (SRC == SK_NORM) {
     // RMS of the row (wavefront sums, then the block's in a fixed order), then the
     // normalised row as hi / lo pairs at LDS columns [0, Kd)
@@ -393,12 +400,13 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
     for (int k = 0; k < V; ++k) {
       const float Mk = __shfl(rv[0], (lane & ~15) | lane_of_row(k), OSP_WAVE);
       const int m = (k / 4) * 16 + 4 * grp + (k % 4);
-      const float Tk = m < R ? a.temp[a.row_seq ? a.row_seq[m] : m] : 0.f;
+      const float Tk = m < R ? tk[k] : 0.f;
       float sum = 0.f;
       if (Tk > 0.f && Mk > -INFINITY) {
+        const float iT = 1.0f / Tk;
 #pragma unroll
         for (int j = 0; j < TMAX; ++j)
-          if (j < ntiles && acc[j][k / 4][k % 4] > -INFINITY) sum += __expf((acc[j][k / 4][k % 4] - Mk) / Tk);
+          if (j < ntiles && acc[j][k / 4][k % 4] > -INFINITY) sum += __expf((acc[j][k / 4][k % 4] - Mk) * iT);
       }
       sv[k] = sum;
     }
