@@ -1,0 +1,99 @@
+"""Lossless verification of a draft tree (test infrastructure: only tests,
+the smoke check and the benchmark's CPU baseline call this module).
+
+The paper serves its drafter through speculative decoding with a top-k
+parameter (Section 4, inference settings: top-k 1, i.e. chains); with top-k
+> 1 every node of the draft carries the drafter's k most likely tokens as
+children, and the target scores all of them in one pass (dynamic draft trees,
+discussed among the related drafters).  The children of a node are not
+samples from a distribution but deterministic candidates, so the lossless
+rule is the target-only one of greedy drafting (the drafter distribution is
+one-hot at each candidate), applied to the candidates in turn:
+
+  at node n with target distribution p, for children c_1, c_2, ... in order:
+    accept c_i iff u_{c_i} < p'(t_{c_i}), where p' is p with the tokens of the
+    children already rejected at n removed and renormalised;
+    on acceptance continue from c_i (its own target row), else remove t_{c_i}.
+  When no child is accepted, the next token is drawn from p' by inverse CDF
+  with u_bonus.
+
+Each step samples exactly from p: accepting c_1 with probability p(t_1), else
+drawing from p without t_1, is the same as drawing from p, and so on for the
+later candidates.  At T = 0 p is one-hot at the lowest argmax: the walk
+follows the child whose token is the target's argmax, and the bonus is that
+argmax.  With one child per node this is the chain rule with greedy drafts.
+
+Tree layout: nodes 0..N-1 in topological order (a parent before its
+children), parents[i] = -1 for children of the root, else the parent's index;
+children are tried in index order.  target_logits row 0 is the root (the
+position after the committed prefix), row i + 1 node i.  Node i's uniform is
+u_accept[i], used when node i is tried.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+from . import sampling
+
+
+@dataclass
+class TreeResult:
+    accept_len: int           # accepted nodes on the path
+    path: np.ndarray          # [accept_len] node indices, root's child first
+    tokens: np.ndarray        # [accept_len + 1]: the path's tokens, then the bonus
+    removed: np.ndarray       # tokens rejected at the last node (removed from p)
+    last: int                 # node the bonus is drawn at (-1: the root)
+
+
+def children_of(parents: np.ndarray, n: int) -> np.ndarray:
+    """Children of node n (-1: the root) in index order."""
+    return np.flatnonzero(np.asarray(parents) == n)
+
+
+def verify_tree(target_logits: np.ndarray, tokens: np.ndarray, parents: np.ndarray, T: float,
+                u_accept: np.ndarray, u_bonus: float) -> TreeResult:
+    tl = np.asarray(target_logits, dtype=np.float64)
+    tokens = np.asarray(tokens, dtype=np.int64)
+    parents = np.asarray(parents, dtype=np.int64)
+    cur = -1
+    path = []
+    while True:
+        row = tl[cur + 1]
+        kids = children_of(parents, cur)
+        removed = []
+        nxt = -1
+        if T == 0.0:
+            star = sampling.argmax_lowest(row)
+            for c in kids:
+                if tokens[c] == star:
+                    nxt = int(c)
+                    break
+        else:
+            p = sampling.probs(row, T)
+            for c in kids:
+                t = int(tokens[c])
+                if t in removed:
+                    continue                  # p'(t) = 0: never accepted
+                left = 1.0 - sum(p[r] for r in removed)
+                if left > 0.0 and float(u_accept[c]) < p[t] / left:
+                    nxt = int(c)
+                    break
+                removed.append(t)
+        if nxt < 0:
+            break
+        path.append(nxt)
+        cur = nxt
+    row = tl[cur + 1]
+    if T == 0.0:
+        bonus = sampling.argmax_lowest(row)
+    else:
+        w = sampling.probs(row, T)
+        w[np.asarray(removed, dtype=np.int64)] = 0.0
+        if np.sum(w) <= 0.0:                  # every token with mass was a rejected child
+            w = sampling.probs(row, T)
+        bonus = sampling.pick_weights(w, float(u_bonus))
+    out = np.array([tokens[i] for i in path] + [bonus], dtype=np.int64)
+    return TreeResult(len(path), np.array(path, dtype=np.int64), out,
+                      np.array(removed, dtype=np.int64), cur)
