@@ -174,9 +174,47 @@ def run_gpu(args):
                     kt[name] = s.drafter.kernel_time(fam)
             s.drafter.kernel_timing(())
         res["kernels"] = kt
+        res["tree_verify"] = time_tree_verify(s, w)
     assert s.drafter.device_errors() == 0
     res["ctx_mean"] = float(np.mean(s.ctx))
     return w, res
+
+
+TREE_NODES, TREE_TOPK = 15, 4
+
+
+def time_tree_verify(s, w, reps: int = 20):
+    """Draft-tree verification (osprey_verify_tree) on synthetic 15-node, top-4 trees
+    for every sequence of the batch at the workload's target vocabulary: per-call time
+    from HIP events on the library's stream, against the bytes it must read (every
+    target row once for its statistics, the last node's row again for the bonus)."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2609_09338_amd import binding as BD
+    B, N, V = w.batch, TREE_NODES, w.vocab_target
+    dev = s.device
+    par, tok, tl = zip(*(synth.tree_inputs(b, V, N, TREE_TOPK, 0.3) for b in range(B)))
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(np.stack(a))).to(dev)
+    g = np.random.default_rng(7)
+    args = (T(tl), T(tok), T(par), torch.tensor([w.temperature(b) for b in range(B)], dtype=torch.float32, device=dev),
+            torch.from_numpy((g.integers(0, 1 << 24, (B, N)) * 2.0 ** -24).astype(np.float32)).to(dev),
+            torch.from_numpy((g.integers(0, 1 << 24, B) * 2.0 ** -24).astype(np.float32)).to(dev),
+            torch.empty(B, dtype=torch.int32, device=dev), torch.empty((B, N), dtype=torch.int32, device=dev),
+            torch.empty((B, N + 1), dtype=torch.int32, device=dev))
+    s.drafter.verify_tree(*args)
+    s.drafter.kernel_timing((BD.KERNEL_VERIFY,))
+    for _ in range(reps):
+        s.drafter.verify_tree(*args)
+    torch.cuda.synchronize()
+    ms, n = s.drafter.kernel_time(BD.KERNEL_VERIFY)
+    s.drafter.kernel_timing(())
+    us = ms * 1e3 / max(n, 1)
+    nbytes = B * (N + 2) * V * 4
+    return dict(nodes=N, topk=TREE_TOPK, batch=B, us_per_call=round(us, 2), bytes_per_call=nbytes,
+                achieved_gbs=round(nbytes / (us * 1e-6) / 1e9, 1),
+                frac=round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4))
 
 
 def run_cpu_baseline(w, seconds: float):
@@ -253,6 +291,7 @@ def main():
         line["ar_step_algorithmic_bytes"] = int(sb["total"])
         ar_us = ds_ms * 1e3 / max(ds_n, 1) / w.K
         line["draft_token_hbm_frac"] = round(sb["total"] / (ar_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+        line["tree_verify"] = r["tree_verify"]
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = run_cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(line), flush=True)

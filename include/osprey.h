@@ -217,6 +217,38 @@ typedef struct {
   const float* draft_temperature;  /* [batch] or NULL (= temperature), as in osprey_verify_args */
 } osprey_verify_rows_args;
 
+/* Draft trees (top-k > 1).  The paper serves with a top-k parameter of 1 (chains;
+ * Section 4, inference settings); with top-k > 1 each node of the draft carries
+ * the drafter's k most likely tokens as children (dynamic draft trees, among the
+ * related drafters the paper discusses), and the target scores every node in one
+ * pass.  Children are deterministic candidates, not samples, so the lossless rule
+ * is target-only acceptance (as for greedy chains, "Drafter temperature" below)
+ * applied to the children in turn: at a node with target distribution p, child c
+ * is accepted iff u_accept[c] < p'(token_c), with p' = p without the tokens of the
+ * children already rejected there, renormalised; the walk continues from an
+ * accepted child; when none is accepted the next token is drawn from p' by
+ * inverse CDF with u_bonus.  T = 0: the walk follows the child whose token is the
+ * target's argmax (lowest id on ties), and the bonus is that argmax.
+ *
+ * Nodes 0..n_nodes-1 are in topological order: parents[i] = -1 for a child of the
+ * root, otherwise an index < i; a parent outside [-1, i) makes node i unreachable
+ * (device error bit 5).  Children are tried in index order.  Row 0 of
+ * target_logits is the root (the position after the committed prefix), row i + 1
+ * node i.  Limits: 0 <= n_nodes <= 64. */
+typedef struct {
+  int32_t batch;
+  int32_t n_nodes;
+  const float* target_logits;   /* [batch][n_nodes + 1][V_T] fp32 */
+  const int32_t* tokens;        /* [batch][n_nodes] target ids */
+  const int32_t* parents;       /* [batch][n_nodes] */
+  const float* temperature;     /* [batch] the target's temperature (>= 0) */
+  const float* u_accept;        /* [batch][n_nodes] node i's uniform, used when it is tried */
+  const float* u_bonus;         /* [batch] */
+  int32_t* accept_len;          /* [batch] out: accepted nodes on the path */
+  int32_t* accept_path;         /* [batch][n_nodes] out: the path's node indices, then -1 */
+  int32_t* out_tokens;          /* [batch][n_nodes + 1] out: the path's tokens, the bonus, then -1 */
+} osprey_verify_tree_args;
+
 /* Host-only check of a configuration.  Returns OSPREY_OK or the first problem. */
 int osprey_config_validate(const osprey_config* cfg);
 
@@ -266,10 +298,15 @@ int osprey_verify(osprey_handle* h, const osprey_verify_args* a);
 /* Stateless verification of caller-supplied drafts (see osprey_verify_rows_args). */
 int osprey_verify_rows(osprey_handle* h, const osprey_verify_rows_args* a);
 
+/* Stateless verification of a caller-supplied draft tree (see
+ * osprey_verify_tree_args).  No slot state is involved. */
+int osprey_verify_tree(osprey_handle* h, const osprey_verify_tree_args* a);
+
 /* Synchronise, read and clear the device error flags (host out):
  * bit 0 an ingest row count outside [1, max new rows] (pending without verify),
  * bit 1 a token id outside [0, V_T), bit 2 a sequence beyond its KV pages,
- * bit 3 a KV write beyond the slot's pages, bit 4 a draft id outside [0, V_T). */
+ * bit 3 a KV write beyond the slot's pages, bit 4 a draft id outside [0, V_T),
+ * bit 5 a tree node whose parent is not an earlier node or the root. */
 int osprey_device_errors(osprey_handle* h, uint32_t* flags);
 
 /* Kernel timing for roofline reports.  `families` is a bit mask: bit f enables HIP

@@ -60,6 +60,13 @@ class osprey_verify_rows_args(C.Structure):
                 ("out_tokens", C.c_void_p), ("draft_temperature", C.c_void_p)]
 
 
+class osprey_verify_tree_args(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("n_nodes", C.c_int32), ("target_logits", C.c_void_p),
+                ("tokens", C.c_void_p), ("parents", C.c_void_p), ("temperature", C.c_void_p),
+                ("u_accept", C.c_void_p), ("u_bonus", C.c_void_p), ("accept_len", C.c_void_p),
+                ("accept_path", C.c_void_p), ("out_tokens", C.c_void_p)]
+
+
 _P = C.c_void_p
 _H = C.c_void_p
 SIGNATURES = {
@@ -75,6 +82,7 @@ SIGNATURES = {
     "osprey_draft_step": (C.c_int, [_H, C.POINTER(osprey_step_args)]),
     "osprey_verify": (C.c_int, [_H, C.POINTER(osprey_verify_args)]),
     "osprey_verify_rows": (C.c_int, [_H, C.POINTER(osprey_verify_rows_args)]),
+    "osprey_verify_tree": (C.c_int, [_H, C.POINTER(osprey_verify_tree_args)]),
     "osprey_device_errors": (C.c_int, [_H, C.POINTER(C.c_uint32)]),
     "osprey_kernel_timing": (C.c_int, [_H, C.c_int32]),
     "osprey_kernel_time": (C.c_int, [_H, C.c_int32, C.POINTER(C.c_double),

@@ -248,6 +248,37 @@ class Drafter:
         a.draft_temperature = _ptr(draft_temperature)
         _check(_lib().osprey_verify_rows(self.h, C.byref(a)))
 
+    def verify_tree(self, target_logits, tokens, parents, temperature, u_accept, u_bonus,
+                    accept_len, accept_path, out_tokens) -> None:
+        """Lossless verification of a draft tree (osprey_verify_tree): target_logits
+        [B, N + 1, V_T], tokens / parents / u_accept [B, N], outputs accept_len [B],
+        accept_path [B, N], out_tokens [B, N + 1]."""
+        torch, c = self.torch, self.cfg
+        B = int(target_logits.shape[0])
+        N = int(target_logits.shape[1]) - 1
+        _need(target_logits, B * (N + 1) * c.vocab_target, torch.float32, "target_logits")
+        _need(tokens, B * N, torch.int32, "tokens")
+        _need(parents, B * N, torch.int32, "parents")
+        _need(temperature, B, torch.float32, "temperature")
+        _need(u_accept, B * N, torch.float32, "u_accept")
+        _need(u_bonus, B, torch.float32, "u_bonus")
+        _need(accept_len, B, torch.int32, "accept_len")
+        _need(accept_path, B * N, torch.int32, "accept_path")
+        _need(out_tokens, B * (N + 1), torch.int32, "out_tokens")
+        a = L.osprey_verify_tree_args()
+        a.batch = B
+        a.n_nodes = N
+        a.target_logits = _ptr(target_logits)
+        a.tokens = _ptr(tokens)
+        a.parents = _ptr(parents)
+        a.temperature = _ptr(temperature)
+        a.u_accept = _ptr(u_accept)
+        a.u_bonus = _ptr(u_bonus)
+        a.accept_len = _ptr(accept_len)
+        a.accept_path = _ptr(accept_path)
+        a.out_tokens = _ptr(out_tokens)
+        _check(_lib().osprey_verify_tree(self.h, C.byref(a)))
+
     # -- diagnostics ------------------------------------------------------------------
     def device_errors(self) -> int:
         f = C.c_uint32()

@@ -311,6 +311,13 @@ struct VerifyArgs {
   int32_t* accept_len;
   uint8_t* accept_mask;
   int32_t* out_tokens;
+  // draft trees (nullable: chain verification).  K is then the number of nodes, the
+  // target has K + 1 rows per sequence (root, then node i at row i + 1), and there are
+  // no drafter rows.
+  const int32_t* tree_tok;  // [B][K] node tokens (target ids)
+  const int32_t* tree_par;  // [B][K] parents (-1: the root)
+  int32_t* tree_path;       // [B][K] out: the accepted path's nodes, then -1
+  int32_t* tree_removed;    // [B][kMaxTreeNodes] tokens rejected at the node the bonus is drawn at
   // state update (stateful verify); nullable
   const int32_t* bslot;
   int32_t* pend_n;
@@ -319,6 +326,8 @@ struct VerifyArgs {
   uint32_t* err;
 };
 void launch_verify(const VerifyArgs& a, hipStream_t st);
+constexpr int kMaxTreeNodes = 64;
+void launch_verify_tree(const VerifyArgs& a, hipStream_t st);
 
 // KV helpers.
 void launch_kv_append(int kvdtype, void* kv, const void* k, const void* v, int n_layers, int n,

@@ -86,6 +86,7 @@ struct Ws {
   int32_t* vstate;
   double* vstat;
   uint32_t* counters;
+  int32_t* tree_removed;
 };
 
 struct Dims {
@@ -172,7 +173,10 @@ size_t plan(const osprey_config& c, char* base, Ws* w) {
   W.qstat = (QStat*)take(sizeof(QStat) * D.B * D.Km);
   W.drafts = (int32_t*)take(4L * D.B * D.Km);
   W.u_zero = (float*)take(4L * D.B * D.Km);
-  W.v_part = (float*)take(16L * D.B * ((D.Km + 1) * D.nchunk_t + D.Km * D.nchunk_d));
+  // chain rows ((Km + 1) target and Km drafter rows) or a draft tree's kMaxTreeNodes + 1 rows
+  W.v_part = (float*)take(16L * D.B * std::max<long>((D.Km + 1) * D.nchunk_t + D.Km * D.nchunk_d,
+                                                     (kMaxTreeNodes + 1L) * D.nchunk_t));
+  W.tree_removed = (int32_t*)take(4L * D.B * kMaxTreeNodes);
   W.v_res = (double*)take(16L * D.B * D.nchunk_t);
   W.vstate = (int32_t*)take(16L * D.B);
   W.vstat = (double*)take(32L * D.B);
@@ -1093,6 +1097,35 @@ OSPREY_API int osprey_verify_rows(osprey_handle* h, const osprey_verify_rows_arg
   v.out_tokens = a->out_tokens;
   int t = h->t_begin(2);
   launch_verify(v, h->stream);
+  h->t_end(t);
+  return hip_last();
+}
+
+OSPREY_API int osprey_verify_tree(osprey_handle* h, const osprey_verify_tree_args* a) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (!a) return fail(OSPREY_E_INVALID, "args is NULL");
+  if (a->batch < 1 || a->batch > h->cfg.max_batch) return fail(OSPREY_E_INVALID, "batch %d not in [1, %d]", a->batch, h->cfg.max_batch);
+  if (a->n_nodes < 0 || a->n_nodes > kMaxTreeNodes)
+    return fail(OSPREY_E_INVALID, "n_nodes %d not in [0, %d]", a->n_nodes, kMaxTreeNodes);
+  if (!a->target_logits || !a->temperature || !a->u_bonus || !a->accept_len || !a->out_tokens ||
+      (a->n_nodes > 0 && (!a->tokens || !a->parents || !a->u_accept || !a->accept_path)))
+    return fail(OSPREY_E_INVALID, "a verify_tree pointer is NULL");
+  VerifyArgs v{};
+  fill_verify_common(h, v, a->batch, a->n_nodes);
+  v.target = a->target_logits;
+  v.temp = a->temperature;
+  v.temp_d = a->temperature;
+  v.u_acc = a->u_accept;
+  v.u_bonus = a->u_bonus;
+  v.accept_len = a->accept_len;
+  v.out_tokens = a->out_tokens;
+  v.tree_tok = a->tokens;
+  v.tree_par = a->parents;
+  v.tree_path = a->accept_path;
+  v.tree_removed = h->W.tree_removed;
+  int t = h->t_begin(2);
+  launch_verify_tree(v, h->stream);
   h->t_end(t);
   return hip_last();
 }

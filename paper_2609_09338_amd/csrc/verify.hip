@@ -21,6 +21,13 @@
 //                          in ascending target ids -> the token at index a;
 //                          stateful verify also records the a + 1 committed
 //                          tokens as the slot's pending ingest
+//
+// Draft trees (deterministic top-k children, accepted in turn with the target's
+// probability renormalised over the children not yet rejected; the bonus from the
+// target without the rejected tokens): k_vstats over the K + 1 target rows, then
+//   k_tree_walk (B)        row statistics, every node's target probability in its
+//                          parent's row, the walk from the root; the last node's
+//                          row and rejected tokens go to k_vresid / k_vfinal
 #include "common.h"
 #include "internal.h"
 
@@ -62,7 +69,7 @@ __global__ void __launch_bounds__(kVThreads) k_vstats(VerifyArgs a) {
   const int lane = threadIdx.x & 63;
   const int j = blockIdx.y * (kVThreads / 64) + (threadIdx.x >> 6);
   const int nt = (a.K + 1) * a.nchunk_t;
-  const int nj = nt + (a.qstat ? 0 : a.K * a.nchunk_d);
+  const int nj = nt + (a.qstat || a.tree_par ? 0 : a.K * a.nchunk_d);
   if (j >= nj) return;
   const float* row;
   int V, c;
@@ -225,6 +232,18 @@ struct ResidRow {
   float Mt, Md, T, Td;
   double iSt, iSd;   // 1 / normalisers
   int onehot;        // Td = 0: the drafter row q_a is one-hot at (else -1)
+  const int32_t* rem;   // draft trees: tokens removed from p (nrem of them); chains: nrem < 0
+  int nrem;
+  OSP_DEV bool removed(int v) const {
+    bool r = false;
+    for (int i = 0; i < nrem; ++i) r |= rem[i] == v;
+    return r;
+  }
+  // residual weight of target id v with target probability p (drafter row entry s, logit l)
+  OSP_DEV double resid(double p, int v, int s, float l) const {
+    if (nrem >= 0) return removed(v) ? 0.0 : p;
+    return fmax(p - q_of(s, l), 0.0);
+  }
   // q_a(v) from the drafter row entry s = t2d[v] (-1: none) and its logit l
   OSP_DEV double q_of(int s, float l) const {
     if (!dl || s < 0) return 0.0;
@@ -249,8 +268,7 @@ struct ResidRow {
 #pragma unroll
     for (int q = 0; q < kVPer; ++q) {
       const double p = tv[q] > -INFINITY ? (double)__expf((tv[q] - Mt) / T) * iSt : 0.0;
-      const double qq = q_of(sidx[q], dv[q]);
-      out[q] = which ? p : fmax(p - qq, 0.0);
+      out[q] = which ? p : resid(p, i0 + q * stride, sidx[q], dv[q]);
     }
   }
 };
@@ -259,7 +277,9 @@ OSP_DEV ResidRow resid_row(const VerifyArgs& a, int b) {
   ResidRow r;
   const int A = a.vstate[b * 4 + 0];
   r.tl = a.target + ((long)b * (a.K + 1) + A) * a.V_T;
-  r.dl = A < a.K ? a.draft + ((long)b * a.ld_draft_b + A) * a.V_d : nullptr;
+  r.dl = (A < a.K && !a.tree_par) ? a.draft + ((long)b * a.ld_draft_b + A) * a.V_d : nullptr;
+  r.rem = a.tree_par ? a.tree_removed + (long)b * kMaxTreeNodes : nullptr;
+  r.nrem = a.tree_par ? a.vstate[b * 4 + 3] : -1;
   r.t2d = a.t2d;
   r.Mt = (float)a.vstat[b * 4 + 0];
   r.iSt = 1.0 / a.vstat[b * 4 + 1];
@@ -299,8 +319,7 @@ __global__ void __launch_bounds__(kVThreads) k_vresid(VerifyArgs a) {
 #pragma unroll
   for (int q = 0; q < kVPer; ++q) {
     const double p = tv[q] > -INFINITY ? (double)__expf((tv[q] - rr.Mt) / rr.T) * rr.iSt : 0.0;
-    const double qq = rr.q_of(sidx[q], dv[q]);
-    sw += fmax(p - qq, 0.0);
+    sw += rr.resid(p, i0 + q * kVThreads, sidx[q], dv[q]);
     sp += p;
   }
   // fixed-order block sums in float64
@@ -418,7 +437,8 @@ __global__ void __launch_bounds__(kVThreads) k_vfinal(VerifyArgs a) {
     tok = s_tok;
   }
   if (tid == 0) {
-    a.out_tokens[(long)b * (a.K + 1) + A] = tok;
+    // (draft trees: the bonus follows the accepted path)
+    a.out_tokens[(long)b * (a.K + 1) + (a.tree_par ? a.accept_len[b] : A)] = tok;
     if (a.bslot) {
       const int slot = a.bslot[b];
       a.pend_n[slot] = A + 1;
@@ -426,6 +446,100 @@ __global__ void __launch_bounds__(kVThreads) k_vfinal(VerifyArgs a) {
         a.pend_tok[(long)slot * a.pend_ld + k] = a.out_tokens[(long)b * (a.K + 1) + k];
     }
   }
+}
+
+// One block per sequence.  Every node's token, parent, uniform and target logit in its
+// parent's row are read at once (thread c: node c), the K + 1 row statistics merged
+// in parallel (one wavefront per row); one thread then walks the tree from the root:
+// the children of a node follow it in index order, so the walk ends within K steps.
+__global__ void __launch_bounds__(kVThreads) k_tree_walk(VerifyArgs a) {
+  __shared__ float s_M[kMaxTreeNodes + 1];
+  __shared__ double s_S[kMaxTreeNodes + 1];
+  __shared__ int s_am[kMaxTreeNodes + 1];
+  __shared__ int s_tok[kMaxTreeNodes], s_par[kMaxTreeNodes], s_path[kMaxTreeNodes];
+  __shared__ float s_lt[kMaxTreeNodes], s_u[kMaxTreeNodes];
+  __shared__ int s_rem[kMaxTreeNodes];
+  __shared__ int s_A, s_nrem;
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int N = a.K;
+  const float T = a.temp[b];
+  if (tid < N) {
+    int t = a.tree_tok[(long)b * N + tid];
+    int p = a.tree_par[(long)b * N + tid];
+    if (p < -1 || p >= tid) { atomicOr(a.err, 1u << 5); p = -2; }      // unreachable
+    if (t < 0 || t >= a.V_T) { atomicOr(a.err, 1u << 4); t = 0; p = -2; }
+    s_tok[tid] = t;
+    s_par[tid] = p;
+    s_u[tid] = a.u_acc[(long)b * N + tid];
+    s_lt[tid] = a.target[((long)b * (N + 1) + max(p, -1) + 1) * a.V_T + t];
+  }
+  const float* part = a.part + (long)b * (N + 1) * a.nchunk_t * 4;
+  for (int q = wave; q <= N; q += kVThreads / 64) {
+    float M;
+    double S;
+    int am;
+    merge_row(part + (long)q * a.nchunk_t * 4, a.nchunk_t, T, M, S, am);
+    if (lane == 0) { s_M[q] = M; s_S[q] = S; s_am[q] = am; }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int* rem = s_rem;
+    int cur = -1, A = 0, nrem = 0;
+    for (;;) {
+      const int row = cur + 1;
+      int nxt = -1;
+      double left = 1.0;                 // target mass not yet removed at this node
+      nrem = 0;
+      for (int c = cur + 1; c < N && nxt < 0; ++c) {
+        if (s_par[c] != cur) continue;
+        const int t = s_tok[c];
+        if (!(T > 0.f)) {
+          if (t == s_am[row]) nxt = c;
+          continue;
+        }
+        bool dup = false;
+        for (int r = 0; r < nrem; ++r) dup |= rem[r] == t;
+        if (dup) continue;               // already rejected here: p'(t) = 0
+        const double pt = s_lt[c] > -INFINITY ? (double)__expf((s_lt[c] - s_M[row]) / T) / s_S[row] : 0.0;
+        if (left > 0.0 && (double)s_u[c] < pt / left) {
+          nxt = c;
+        } else {
+          rem[nrem++] = t;
+          left -= pt;
+        }
+      }
+      if (nxt < 0) break;
+      s_path[A++] = nxt;
+      cur = nxt;
+    }
+    s_A = A;
+    s_nrem = T > 0.f ? nrem : 0;
+    const int row = cur + 1;
+    a.accept_len[b] = A;
+    a.vstate[b * 4 + 0] = row;
+    a.vstate[b * 4 + 1] = s_am[row];
+    a.vstate[b * 4 + 2] = -1;
+    a.vstate[b * 4 + 3] = T > 0.f ? nrem : 0;
+    a.vstat[b * 4 + 0] = s_M[row];
+    a.vstat[b * 4 + 1] = s_S[row];
+    a.vstat[b * 4 + 2] = 0.0;
+    a.vstat[b * 4 + 3] = 1.0;
+  }
+  __syncthreads();
+  const int A = s_A;
+  if (tid < s_nrem) a.tree_removed[(long)b * kMaxTreeNodes + tid] = s_rem[tid];
+  for (int i = tid; i < N; i += kVThreads) a.tree_path[(long)b * N + i] = i < A ? s_path[i] : -1;
+  for (int i = tid; i <= N; i += kVThreads)
+    if (i != A) a.out_tokens[(long)b * (N + 1) + i] = i < A ? s_tok[s_path[i]] : -1;
+}
+
+void launch_verify_tree(const VerifyArgs& a, hipStream_t st) {
+  const int nj = (a.K + 1) * a.nchunk_t;
+  hipLaunchKernelGGL(k_vstats, dim3(a.B, (nj + kVThreads / 64 - 1) / (kVThreads / 64)), dim3(kVThreads), 0, st, a);
+  hipLaunchKernelGGL(k_tree_walk, dim3(a.B), dim3(kVThreads), 0, st, a);
+  hipLaunchKernelGGL(k_vresid, dim3(a.B, a.nchunk_t), dim3(kVThreads), 0, st, a);
+  hipLaunchKernelGGL(k_vfinal, dim3(a.B), dim3(kVThreads), 0, st, a);
 }
 
 void launch_verify(const VerifyArgs& a, hipStream_t st) {

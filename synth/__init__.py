@@ -393,3 +393,44 @@ def target_logits(w: Workload, draft_logits, d2t, noise):
         base[k, :] = m.mean()
         base[k, d2t[mapped]] = m
     return (base + w.sigma * np.asarray(noise, dtype=np.float64)).astype(np.float32)
+
+
+def tree_inputs(seed: int, V_T: int, n_nodes: int, topk: int, sigma: float):
+    """A synthetic draft tree in the shape dynamic draft trees take, and target
+    logits for it (inputs only; no verification arithmetic).
+
+    Nodes are grown level by level: every frontier node gets up to `topk`
+    children, and up to `topk` of the new nodes (chosen at random) form the next
+    frontier, until there are n_nodes (parents before children).  Each row (root,
+    then node i) has drafter-like logits N(0, 1.5); the children of a row carry
+    its top-ranked tokens, best first, and the target row is those logits plus
+    sigma * N(0, 1), so that the target often agrees with the first children.
+    Returns parents [N] int32, tokens [N] int32, target logits [N + 1, V_T] fp32."""
+    g = np.random.default_rng([0x7EE, seed])
+    parents = []
+    frontier = [-1]
+    while len(parents) < n_nodes:
+        new = []
+        for f in frontier:
+            for _ in range(topk):
+                if len(parents) < n_nodes:
+                    parents.append(f)
+                    new.append(len(parents) - 1)
+        if not new:
+            break
+        frontier = sorted(g.permutation(new)[:topk].tolist())
+    parents = np.array(parents, dtype=np.int32)
+    dl = g.standard_normal((n_nodes + 1, V_T)) * 1.5
+    tokens = np.zeros(n_nodes, dtype=np.int32)
+    rank, best = {}, {}
+    for i, p in enumerate(parents):
+        p = int(p)
+        r = rank.get(p, 0)
+        rank[p] = r + 1
+        if p not in best:          # the row's topk best tokens, best first
+            row = dl[p + 1]
+            top = np.argpartition(-row, min(topk, V_T - 1))[:topk + 1]
+            best[p] = top[np.argsort(-row[top], kind="stable")]
+        tokens[i] = int(best[p][r])
+    tl = dl + sigma * g.standard_normal((n_nodes + 1, V_T))
+    return parents, tokens, tl.astype(np.float32)

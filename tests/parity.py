@@ -92,3 +92,39 @@ def verify_flags(res, target_logits, draft_logits, d2t, drafts, T, u_acc, u_bonu
             w = p
         return residual_flag(w, q, u_bonus, delta, Td)
     return residual_flag(p, np.zeros_like(p), u_bonus, 0.0, T)
+
+
+def tree_flags(res, target_logits, tokens, parents, T, u_acc, u_bonus) -> bool:
+    """True if a decision of this tree verification is within its flag window: a
+    tried child's uniform within 1e-5 of its renormalised probability p'(t), or the
+    bonus draw point within 1e-6 of the total of a breakpoint (the GPU's target
+    probabilities come from fp32 exponentials and chunk sums).  At T = 0 both sides
+    compare the same fp32 logits: no flags."""
+    from oracle.tree import children_of
+    if T == 0.0:
+        return False
+    tl = np.asarray(target_logits, dtype=np.float64)
+    cur = -1
+    path = list(res.path) + [None]
+    for nxt in path:
+        p = sampling.probs(tl[cur + 1], T)
+        removed = []
+        for c in children_of(parents, cur):
+            t = int(tokens[c])
+            if t in removed:
+                continue
+            left = 1.0 - sum(p[r] for r in removed)
+            if left > 0.0 and abs(float(u_acc[c]) - p[t] / left) < 1e-5:
+                return True
+            if nxt is not None and c == nxt:
+                break
+            removed.append(t)
+        if nxt is None:
+            w = p.copy()
+            w[np.asarray(removed, dtype=np.int64)] = 0.0
+            if w.sum() <= 0:
+                return True
+            _, margin, run = cdf_margin(w, u_bonus)
+            return margin < 1e-6 * run[-1] + 1e-12
+        cur = int(nxt)
+    return False
