@@ -97,3 +97,76 @@ def verify_tree(target_logits: np.ndarray, tokens: np.ndarray, parents: np.ndarr
     out = np.array([tokens[i] for i in path] + [bonus], dtype=np.int64)
     return TreeResult(len(path), np.array(path, dtype=np.int64), out,
                       np.array(removed, dtype=np.int64), cur)
+
+
+# ---------------------------------------------------------------------------------------
+# Drafting a tree (dynamic draft trees with top-k children; the paper's serving setup
+# uses top-k 1, i.e. chains)
+# ---------------------------------------------------------------------------------------
+@dataclass
+class DraftTree:
+    tokens: np.ndarray        # [N] target ids, topological order (generation order)
+    parents: np.ndarray       # [N] -1: child of the root
+    scores: np.ndarray        # [N] cumulative log-probability of the node's path
+    depths: np.ndarray        # [N] 1 for the root's children
+    cand_scores: np.ndarray   # scores of every candidate, in generation order
+
+
+def top_rows(logits: np.ndarray, k: int) -> np.ndarray:
+    """The k drafter rows with the largest logits, best first, ties to the lower row;
+    masked rows (-inf) only when fewer than k rows are finite."""
+    l = np.asarray(logits, dtype=np.float64)
+    order = np.lexsort((np.arange(l.size), -l))      # by logit descending, then row
+    return order[:k]
+
+
+def log_probs(logits: np.ndarray) -> np.ndarray:
+    """log softmax at temperature 1 (the drafter's confidence); -inf rows stay -inf."""
+    l = np.asarray(logits, dtype=np.float64)
+    m = np.max(l)
+    return l - m - np.log(np.sum(np.exp(l - m)))
+
+
+def draft_tree(drafter, seq, tokens, taps, topk: int, depth: int, n_nodes: int) -> DraftTree:
+    """Ingest the committed tokens, then grow the tree.
+
+    The root is the last committed row; its k most likely rows (scores log p at
+    temperature 1) are the depth-1 candidates.  For depth d = 2 .. `depth` every
+    node of the frontier (the k best candidates of the previous depth; depth 1: all
+    of them) runs through the drafter at position committed + (its depth - 1), with
+    its parent's hidden state as the conditioning input, attending to the committed
+    context and to its own ancestors (each branch has its own copy of the cache
+    beyond the context); its k most likely rows become candidates with the parent's
+    score plus their log probability.  Finally the n_nodes best candidates (score,
+    then generation order) form the tree, listed in generation order."""
+    import copy
+    g_root = drafter.ingest(seq, tokens, taps)
+    L = seq.length
+    cands = []      # (token, parent candidate index, score, depth)
+    lp = log_probs(drafter.logits(g_root))
+    for r in top_rows(drafter.logits(g_root), topk):
+        cands.append((int(drafter.d2t[r]), -1, float(lp[r]), 1))
+    state = {}      # candidate index -> (branch cache, hidden state g)
+    frontier = list(range(len(cands)))
+    for d in range(2, depth + 1):
+        new = []
+        for f in frontier:
+            tok, par, sc, dep = cands[f]
+            base, g_par = (seq, g_root) if par < 0 else state[par]
+            br = copy.deepcopy(base)
+            g = drafter.forward_row(br, tok, g_par, L + dep - 1)
+            state[f] = (br, g)
+            l = drafter.logits(g)
+            lpf = log_probs(l)
+            for r in top_rows(l, topk):
+                new.append(len(cands))
+                cands.append((int(drafter.d2t[r]), f, sc + float(lpf[r]), dep + 1))
+        order = sorted(new, key=lambda i: (-cands[i][2], i))
+        frontier = sorted(order[:topk])
+    allsc = np.array([c[2] for c in cands])
+    pick = sorted(sorted(range(len(cands)), key=lambda i: (-cands[i][2], i))[:n_nodes])
+    index = {c: j for j, c in enumerate(pick)}
+    toks = np.array([cands[i][0] for i in pick], dtype=np.int64)
+    pars = np.array([index[cands[i][1]] if cands[i][1] >= 0 else -1 for i in pick], dtype=np.int64)
+    return DraftTree(toks, pars, np.array([cands[i][2] for i in pick]),
+                     np.array([cands[i][3] for i in pick], dtype=np.int64), allsc)

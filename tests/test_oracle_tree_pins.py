@@ -193,3 +193,85 @@ def test_empty_tree_samples_the_root():
         r = verify_tree(tl, np.zeros(0, np.int64), np.zeros(0, np.int64), 1.0, np.zeros(0), u)
         assert r.accept_len == 0
         assert int(r.tokens[0]) == sampling.pick(tl[0], 1.0, u)
+
+
+# ----------------------------------------------------------------------------------------
+# tree drafting
+# ----------------------------------------------------------------------------------------
+def _tiny_drafter(dtype="bf16"):
+    import synth
+    from oracle.drafter import Drafter, Sequence
+    w = synth.Workload(name="tree_pin", cfg_id=131, dtype=dtype, n_layers=2, d_model=64,
+                       n_q_heads=4, n_kv_heads=2, head_dim=16, d_ffn=96, vocab_draft=61,
+                       vocab_target=61, target_hidden=24, batch=1, K=3, prefill="ingest",
+                       gains="normal")
+    dr = Drafter(w, synth.make_weights(w), synth.make_d2t(w))
+    rng = np.random.default_rng(4)
+    toks = rng.integers(0, w.vocab_target, 9)
+    taps = rng.standard_normal((9, 3 * w.target_hidden))
+    return w, dr, Sequence, toks, taps
+
+
+def test_tree_with_one_child_per_node_is_the_greedy_chain():
+    from oracle.tree import draft_tree
+    w, dr, Sequence, toks, taps = _tiny_drafter()
+    for K in (1, 3, 5):
+        s1, s2 = Sequence(w, 64), Sequence(w, 64)
+        t = draft_tree(dr, s1, toks, taps, 1, K, K)
+        drafts, _, _, _ = dr.draft(s2, toks, taps, K, 0.0, np.zeros(K))
+        assert list(t.tokens) == list(drafts)
+        assert list(t.parents) == list(range(-1, K - 1))
+
+
+def test_tree_nodes_match_independent_path_replays():
+    """Every selected node's score is the sum of log-probabilities along its path,
+    recomputed by replaying the path through a fresh copy of the committed cache,
+    and its children are among the top-k rows of the replayed logits; the
+    selection is the n best candidates and contains every selected node's parent."""
+    import copy
+    from oracle.tree import draft_tree, log_probs, top_rows
+    w, dr, Sequence, toks, taps = _tiny_drafter()
+    topk, depth, n = 3, 4, 12
+    seq = Sequence(w, 64)
+    t = draft_tree(dr, seq, toks, taps, topk, depth, n)
+    base = Sequence(w, 64)
+    g0 = dr.ingest(base, toks, taps)
+    L = base.length
+    inv = {int(dr.d2t[r]): r for r in range(w.vocab_draft) if dr.d2t[r] >= 0}
+    for i in range(n):
+        path = [i]
+        while t.parents[path[-1]] >= 0:
+            path.append(int(t.parents[path[-1]]))
+        path = path[::-1]
+        br = copy.deepcopy(base)
+        g, score = g0, 0.0
+        for j, node in enumerate(path):
+            l = dr.logits(g)
+            r = inv[int(t.tokens[node])]
+            assert r in top_rows(l, topk)
+            score += log_probs(l)[r]
+            if j + 1 < len(path):
+                g = dr.forward_row(br, int(t.tokens[node]), g, L + j)
+        assert abs(score - t.scores[i]) < 1e-9
+        assert t.depths[i] == len(path)
+    best = np.sort(t.cand_scores)[::-1][:n]
+    assert np.allclose(np.sort(t.scores)[::-1], best)
+    assert all(p < i for i, p in enumerate(t.parents))
+
+
+def test_tree_is_independent_of_taps_with_zero_expansion():
+    """Eq. 3: with the c-slot columns zero the tree does not depend on the taps."""
+    import synth
+    from oracle.drafter import Drafter, Sequence
+    from oracle.tree import draft_tree
+    w = synth.Workload(name="tree_zero", cfg_id=132, dtype="bf16", n_layers=1, d_model=64,
+                       n_q_heads=2, n_kv_heads=1, head_dim=32, d_ffn=64, vocab_draft=53,
+                       vocab_target=53, target_hidden=16, batch=1, K=3, prefill="ingest",
+                       expansion="zero")
+    dr = Drafter(w, synth.make_weights(w), synth.make_d2t(w))
+    rng = np.random.default_rng(8)
+    toks = rng.integers(0, w.vocab_target, 6)
+    a = draft_tree(dr, Sequence(w, 32), toks, rng.standard_normal((6, 48)), 3, 3, 8)
+    b = draft_tree(dr, Sequence(w, 32), toks, rng.standard_normal((6, 48)) * 5, 3, 3, 8)
+    assert list(a.tokens) == list(b.tokens) and list(a.parents) == list(b.parents)
+    assert np.array_equal(a.scores, b.scores)
