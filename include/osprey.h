@@ -249,6 +249,30 @@ typedef struct {
   int32_t* out_tokens;          /* [batch][n_nodes + 1] out: the path's tokens, the bonus, then -1 */
 } osprey_verify_tree_args;
 
+/* Arguments of osprey_draft_tree: growing a draft tree instead of a chain.  The root
+ * is each sequence's last committed row; its topk most likely drafter rows are the
+ * depth-1 candidates, scored by their log-probability at temperature 1 (the drafter's
+ * confidence).  At every further depth the frontier (the topk best candidates of the
+ * previous depth; depth 1: all of them) runs through the drafter, each node at
+ * position committed + its depth - 1 with its parent's hidden state as the
+ * conditioning input (Section 3.4), attending to the committed context and to its own
+ * ancestors only; its topk most likely rows become candidates scored with the
+ * parent's score plus their log-probability.  The n_nodes best candidates (higher
+ * score, then generation order) form the tree, listed in generation order (parents
+ * before children) for osprey_verify_tree.  Ties in the drafter's logits go to the
+ * lower row.  Limits: 2 <= topk <= min(8, max_k), 1 <= depth <= 8,
+ * n_nodes <= min(64, topk + (depth - 1) topk^2); bf16 weights. */
+typedef struct {
+  int32_t topk;
+  int32_t depth;
+  int32_t n_nodes;
+  int32_t* tokens;              /* [batch][n_nodes] out: target ids */
+  int32_t* parents;             /* [batch][n_nodes] out: -1 for the root's children, else an
+                                   earlier node */
+  double* scores;               /* [batch][n_nodes] out, optional (NULL: not written): each
+                                   node's score, the sum of the log-probabilities on its path */
+} osprey_tree_args;
+
 /* Host-only check of a configuration.  Returns OSPREY_OK or the first problem. */
 int osprey_config_validate(const osprey_config* cfg);
 
@@ -291,6 +315,13 @@ int osprey_seq_length(osprey_handle* h, int32_t slot, int32_t* length);
 /* Ingest the new rows and propose K drafts per sequence (see osprey_step_args).
  * State: READY (explicit) or VERIFIED (pending) -> DRAFTED (K >= 1) / READY (K == 0). */
 int osprey_draft_step(osprey_handle* h, const osprey_step_args* a);
+
+/* Ingest the new rows (as osprey_draft_step, with a->K = 0) and grow a draft tree
+ * (see osprey_tree_args).  The tree's keys and values never enter the slot's pages:
+ * the slot ends READY with the ingested rows committed, and the next call ingests the
+ * tokens osprey_verify_tree accepted (explicit new_tokens).  State: READY or VERIFIED
+ * -> READY. */
+int osprey_draft_tree(osprey_handle* h, const osprey_step_args* a, const osprey_tree_args* t);
 
 /* Verify the last drafts (see osprey_verify_args).  State: DRAFTED -> VERIFIED. */
 int osprey_verify(osprey_handle* h, const osprey_verify_args* a);

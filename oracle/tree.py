@@ -110,6 +110,8 @@ class DraftTree:
     scores: np.ndarray        # [N] cumulative log-probability of the node's path
     depths: np.ndarray        # [N] 1 for the root's children
     cand_scores: np.ndarray   # scores of every candidate, in generation order
+    min_gap: float = np.inf   # smallest margin of any selection (top-k logits, frontier,
+                              # final): where a computation in another precision may differ
 
 
 def top_rows(logits: np.ndarray, k: int) -> np.ndarray:
@@ -140,10 +142,18 @@ def draft_tree(drafter, seq, tokens, taps, topk: int, depth: int, n_nodes: int) 
     score plus their log probability.  Finally the n_nodes best candidates (score,
     then generation order) form the tree, listed in generation order."""
     import copy
+    gaps = []
+
+    def gap(values, k):           # margin between the k-th and (k+1)-th largest values
+        v = np.sort(np.asarray(values, dtype=np.float64)[np.isfinite(values)])[::-1]
+        if len(v) > k:
+            gaps.append(v[k - 1] - v[k])
+
     g_root = drafter.ingest(seq, tokens, taps)
     L = seq.length
     cands = []      # (token, parent candidate index, score, depth)
     lp = log_probs(drafter.logits(g_root))
+    gap(drafter.logits(g_root), topk)
     for r in top_rows(drafter.logits(g_root), topk):
         cands.append((int(drafter.d2t[r]), -1, float(lp[r]), 1))
     state = {}      # candidate index -> (branch cache, hidden state g)
@@ -158,15 +168,20 @@ def draft_tree(drafter, seq, tokens, taps, topk: int, depth: int, n_nodes: int) 
             state[f] = (br, g)
             l = drafter.logits(g)
             lpf = log_probs(l)
+            gap(l, topk)
             for r in top_rows(l, topk):
                 new.append(len(cands))
                 cands.append((int(drafter.d2t[r]), f, sc + float(lpf[r]), dep + 1))
         order = sorted(new, key=lambda i: (-cands[i][2], i))
+        if d < depth:
+            gap([cands[i][2] for i in new], topk)
         frontier = sorted(order[:topk])
     allsc = np.array([c[2] for c in cands])
+    gap(allsc, n_nodes)
     pick = sorted(sorted(range(len(cands)), key=lambda i: (-cands[i][2], i))[:n_nodes])
     index = {c: j for j, c in enumerate(pick)}
     toks = np.array([cands[i][0] for i in pick], dtype=np.int64)
     pars = np.array([index[cands[i][1]] if cands[i][1] >= 0 else -1 for i in pick], dtype=np.int64)
     return DraftTree(toks, pars, np.array([cands[i][2] for i in pick]),
-                     np.array([cands[i][3] for i in pick], dtype=np.int64), allsc)
+                     np.array([cands[i][3] for i in pick], dtype=np.int64), allsc,
+                     min(gaps) if gaps else np.inf)

@@ -67,6 +67,11 @@ class osprey_verify_tree_args(C.Structure):
                 ("accept_path", C.c_void_p), ("out_tokens", C.c_void_p)]
 
 
+class osprey_tree_args(C.Structure):
+    _fields_ = [("topk", C.c_int32), ("depth", C.c_int32), ("n_nodes", C.c_int32),
+                ("tokens", C.c_void_p), ("parents", C.c_void_p), ("scores", C.c_void_p)]
+
+
 _P = C.c_void_p
 _H = C.c_void_p
 SIGNATURES = {
@@ -83,6 +88,7 @@ SIGNATURES = {
     "osprey_verify": (C.c_int, [_H, C.POINTER(osprey_verify_args)]),
     "osprey_verify_rows": (C.c_int, [_H, C.POINTER(osprey_verify_rows_args)]),
     "osprey_verify_tree": (C.c_int, [_H, C.POINTER(osprey_verify_tree_args)]),
+    "osprey_draft_tree": (C.c_int, [_H, C.POINTER(osprey_step_args), C.POINTER(osprey_tree_args)]),
     "osprey_device_errors": (C.c_int, [_H, C.POINTER(C.c_uint32)]),
     "osprey_kernel_timing": (C.c_int, [_H, C.c_int32]),
     "osprey_kernel_time": (C.c_int, [_H, C.c_int32, C.POINTER(C.c_double),

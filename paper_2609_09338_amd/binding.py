@@ -191,6 +191,42 @@ class Drafter:
         a.draft_logits = _ptr(draft_logits)
         _check(_lib().osprey_draft_step(self.h, C.byref(a)))
 
+    def draft_tree(self, slots, topk: int, depth: int, n_nodes: int, taps, temperature,
+                   tokens, parents, n_new, new_tokens, taps_stride: int = 0,
+                   scores=None) -> None:
+        """Ingest the new rows and grow a draft tree (osprey_draft_tree); tokens and
+        parents [B, n_nodes] int32 outputs, scores [B, n_nodes] float64 (optional)."""
+        torch, c = self.torch, self.cfg
+        B = len(slots)
+        tap_w = c.n_taps * c.target_hidden
+        rows = B * taps_stride if taps_stride > 0 else int(sum(n_new))
+        _need(taps, rows * tap_w, self._wdtype, "taps")
+        _need(temperature, B, torch.float32, "temperature")
+        _need(new_tokens, int(sum(n_new)), torch.int32, "new_tokens")
+        _need(tokens, B * n_nodes, torch.int32, "tokens")
+        _need(parents, B * n_nodes, torch.int32, "parents")
+        if scores is not None:
+            _need(scores, B * n_nodes, torch.float64, "scores")
+        a = L.osprey_step_args()
+        a.batch = B
+        a.K = 0
+        sl = _i32_array(slots)
+        a.slots = C.cast(sl, C.POINTER(C.c_int32))
+        nn = _i32_array(n_new)
+        a.n_new = C.cast(nn, C.POINTER(C.c_int32))
+        a.new_tokens = _ptr(new_tokens)
+        a.taps = _ptr(taps)
+        a.taps_stride = taps_stride
+        a.temperature = _ptr(temperature)
+        t = L.osprey_tree_args()
+        t.topk = topk
+        t.depth = depth
+        t.n_nodes = n_nodes
+        t.tokens = _ptr(tokens)
+        t.parents = _ptr(parents)
+        t.scores = _ptr(scores) if scores is not None else None
+        _check(_lib().osprey_draft_tree(self.h, C.byref(a), C.byref(t)))
+
     def verify(self, slots, K: int, target_logits, temperature, u_accept, u_bonus,
                accept_len, accept_mask, out_tokens, draft_temperature=None) -> None:
         torch, c = self.torch, self.cfg

@@ -618,7 +618,8 @@ __global__ void __launch_bounds__(256) k_rows_qkv(AttnArgs a, float* q_out) {
   const int lane = threadIdx.x & 63;
   const int hh = blockIdx.y * 4 + (threadIdx.x >> 6);
   if (hh >= a.nq + a.nkv) return;
-  const int pos = a.rows.pos[r];
+  // (a draft-tree row: its own position for RoPE; rows.pos bounds the context read)
+  const int pos = a.tree_pos ? a.tree_pos[r] : a.rows.pos[r];
   if (hh < a.nq) {
     const long qo = (long)r * a.qkv_w + (long)hh * HD;
     float q1 = lane < HALF ? qkv_at(a, qo + lane) : 0.f, q2 = lane < HALF ? qkv_at(a, qo + lane + HALF) : 0.f;
@@ -631,16 +632,30 @@ __global__ void __launch_bounds__(256) k_rows_qkv(AttnArgs a, float* q_out) {
     return;
   }
   const int g = hh - a.nq;
-  const int b = a.rows.seq ? a.rows.seq[r] : r;
-  const int slot = a.slot0 >= 0 ? a.slot0 : a.bslot[b];
-  const int blk = pos / a.kv_block;
-  if (blk >= a.slot_nblocks[slot]) { if (lane == 0) atomicOr(a.err, 1u << 3); return; }
   const long ko = (long)r * a.qkv_w + (long)(a.nq + g) * HD;
   const long vo = (long)r * a.qkv_w + (long)(a.nq + a.nkv + g) * HD;
   float k1 = lane < HALF ? qkv_at(a, ko + lane) : 0.f, k2 = lane < HALF ? qkv_at(a, ko + lane + HALF) : 0.f;
   const float v1 = lane < HALF ? qkv_at(a, vo + lane) : 0.f;
   const float v2 = lane < HALF ? qkv_at(a, vo + lane + HALF) : 0.f;
   norm_rope<TKV, HD>(a, a.k_norm, pos, lane, k1, k2);
+  if (a.tree_node) {
+    // draft tree: into the tree cache at the node's slot, [layer][k | v][kv head][dim]
+    if (a.tree_node[r] < 0 || a.tree_node[r] >= a.tree_slots) { if (lane == 0) atomicOr(a.err, 1u << 3); return; }
+    TKV* tk = reinterpret_cast<TKV*>(a.tree_kv);
+    const long kb = ((((long)a.tree_node[r] * a.n_layers + a.layer) * 2 + 0) * a.nkv + g) * HD;
+    const long vb = kb + (long)a.nkv * HD;
+    if (lane < HALF) {
+      store_from_f32(tk, kb + lane, k1);
+      store_from_f32(tk, kb + lane + HALF, k2);
+      store_from_f32(tk, vb + lane, v1);
+      store_from_f32(tk, vb + lane + HALF, v2);
+    }
+    return;
+  }
+  const int b = a.rows.seq ? a.rows.seq[r] : r;
+  const int slot = a.slot0 >= 0 ? a.slot0 : a.bslot[b];
+  const int blk = pos / a.kv_block;
+  if (blk >= a.slot_nblocks[slot]) { if (lane == 0) atomicOr(a.err, 1u << 3); return; }
   TKV* kvb = reinterpret_cast<TKV*>(a.kv);
   const long base = (long)a.block_table[(long)slot * a.max_blocks + blk] *
                     kv_block_elems(a.n_layers, a.nkv, a.kv_block, HD);
@@ -681,11 +696,14 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
     const int sp = grp + G * i;
     v[i] = sp < a.n_split ? pp[(long)sp * (HD + 2) + 2 + e] : 0.f;
   }
+  // (a draft-tree row: the last split is its attention over its ancestors and itself)
+  const int extra = a.tree_node ? a.n_split - 1 : -1;
   if (tid < 64) {
     const float m_any = lane < a.n_split ? pp[(long)lane * (HD + 2)] : -INFINITY;
     const float l_any = lane < a.n_split ? pp[(long)lane * (HD + 2) + 1] : 0.f;
-    const float m = lane < ns ? m_any : -INFINITY;
-    const float lsum = lane < ns ? l_any : 0.f;
+    const bool use = lane < ns || lane == extra;
+    const float m = use ? m_any : -INFINITY;
+    const float lsum = use ? l_any : 0.f;
     const float M = wave_max(m);
     const float f = (m > -INFINITY) ? __expf(m - M) : 0.f;
     const float L = wave_sum(lsum * f);
@@ -696,7 +714,7 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     const int sp = grp + G * i;
-    if (sp < ns) O += v[i] * s_f[sp];
+    if (sp < ns || sp == extra) O += v[i] * s_f[sp];
   }
   s_part[grp][e] = O;
   __syncthreads();

@@ -198,8 +198,19 @@ struct AttnArgs {
   uint16_t* o_hi;           // matrix-core path: o as bf16 hi / lo pairs instead (nullable)
   uint16_t* o_lo;
   uint32_t* err;
+  // draft-tree passes (nullable): every row is a frontier node with one row per
+  // sequence; rows.pos holds the last committed position (the split attention reads the
+  // committed context only), tree_pos the node's own position (RoPE); its keys/values go
+  // to the tree cache at slot tree_node[r] instead of the pages, and split n_split - 1 is
+  // attention over tree_anc[r] (its ancestors' slots, then its own; -1 padded)
+  const int32_t* tree_node;
+  const int32_t* tree_anc;  // [rows][kMaxTreeDepth]
+  const int32_t* tree_pos;
+  void* tree_kv;            // [slot][n_layers][2][nkv][hd], cache dtype
+  int tree_slots;           // slots of tree_kv
 };
 void launch_attention(int kvdtype, const AttnArgs& a, hipStream_t st);
+void launch_tree_attn(int kvdtype, const AttnArgs& a, hipStream_t st);
 // Matrix-core path: per row, sum the QKV split partials, normalise and rotate q
 // and k, write q * (1/sqrt(hd)) to q_out and the new k, v into the cache.
 void launch_rows_qkv(int kvdtype, const AttnArgs& a, float* q_out, hipStream_t st);
@@ -328,6 +339,51 @@ struct VerifyArgs {
 void launch_verify(const VerifyArgs& a, hipStream_t st);
 constexpr int kMaxTreeNodes = 64;
 void launch_verify_tree(const VerifyArgs& a, hipStream_t st);
+
+// Draft-tree growth (see tree.hip).
+constexpr int kMaxTopk = 8;           // children per node
+constexpr int kMaxTreeDepth = 8;      // depths
+constexpr int kMaxTreeProc = 64;      // frontier nodes run through the drafter per sequence
+constexpr int kMaxCand = 512;         // candidates per sequence (>= 8 + 7 x 64)
+constexpr int kTkBlocks = 64;         // blocks per LM-head row in the candidate pass
+struct TreeArgs {
+  int B, k, depth, pass, n_nodes;
+  int V;                    // LM-head rows
+  const int32_t* d2t;
+  const float* logits;      // rows of this pass at logits + r * ld_logits
+  long ld_logits;
+  float* cand_v;            // [rows][kTkBlocks][kMaxTopk] best (logit, row) pairs per block
+  int32_t* cand_r;
+  const float* rec;         // LM-head records [rows][nblk][4] at temperature 1
+  int nblk;
+  // candidates per sequence [B][kMaxCand], generation order
+  int32_t* c_tok;
+  int32_t* c_par;
+  double* c_score;
+  int32_t* c_depth;
+  int32_t* c_slot;          // tree-cache slot once run through the drafter (else -1)
+  int32_t* n_cand;          // [B]
+  int32_t* front;           // [B][kMaxTopk] the candidates of the current pass's rows
+  // the next pass's rows b * k + j
+  int32_t* r_tok;
+  int32_t* r_pos;
+  int32_t* r_attpos;
+  int32_t* r_node;
+  int32_t* r_anc;           // [rows][kMaxTreeDepth]
+  int32_t* r_bslot;
+  float* r_s;               // [rows][d] conditioning input: the parent's hidden state
+  const float* x;           // this pass's body output rows (root pass: the ingest rows)
+  int d;
+  const int32_t* last_row;
+  const int32_t* committed;
+  const int32_t* bslot;
+  int32_t* out_tok;         // [B][n_nodes]
+  int32_t* out_par;
+  double* out_score;            // optional
+};
+void launch_tree_topk(const TreeArgs& a, int rows, hipStream_t st);
+void launch_tree_step(const TreeArgs& a, hipStream_t st);
+void launch_tree_final(const TreeArgs& a, hipStream_t st);
 
 // KV helpers.
 void launch_kv_append(int kvdtype, void* kv, const void* k, const void* v, int n_layers, int n,

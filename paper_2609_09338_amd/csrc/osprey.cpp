@@ -87,6 +87,15 @@ struct Ws {
   double* vstat;
   uint32_t* counters;
   int32_t* tree_removed;
+  // draft-tree growth
+  void* tree_kv;              // [B * kMaxTreeProc][n_layers][2][nkv][hd], cache dtype
+  float* tree_cv;             // [B * kMaxTopk][kTkBlocks][kMaxTopk]
+  int32_t* tree_cr;
+  int32_t *c_tok, *c_par, *c_depth, *c_slot, *n_cand, *front;   // [B][kMaxCand] / [B] / [B][kMaxTopk]
+  double* c_score;
+  int32_t *r_tok, *r_pos, *r_attpos, *r_node, *r_anc, *r_bslot;  // [B * kMaxTopk] (r_anc x kMaxTreeDepth)
+  float* r_s;                 // [B * kMaxTopk][d]
+  float* ones;                // [B * kMaxTopk] temperature 1 for the tree's LM-head records
 };
 
 struct Dims {
@@ -169,7 +178,7 @@ size_t plan(const osprey_config& c, char* base, Ws* w) {
     W.split_s2 = (float*)take(4L * rs * need);
   }
   W.logits = (float*)take(4L * D.B * D.Km * c.vocab_draft);
-  W.lm_part = (float*)take(16L * D.B * D.lm_nblk_max);
+  W.lm_part = (float*)take(16L * D.B * kMaxTopk * D.lm_nblk_max);   // (draft trees: B x k rows)
   W.qstat = (QStat*)take(sizeof(QStat) * D.B * D.Km);
   W.drafts = (int32_t*)take(4L * D.B * D.Km);
   W.u_zero = (float*)take(4L * D.B * D.Km);
@@ -177,6 +186,28 @@ size_t plan(const osprey_config& c, char* base, Ws* w) {
   W.v_part = (float*)take(16L * D.B * std::max<long>((D.Km + 1) * D.nchunk_t + D.Km * D.nchunk_d,
                                                      (kMaxTreeNodes + 1L) * D.nchunk_t));
   W.tree_removed = (int32_t*)take(4L * D.B * kMaxTreeNodes);
+  {
+    const long el = c.dtype == OSPREY_BF16 ? 2 : 4;
+    const long rows = (long)D.B * kMaxTopk;
+    W.tree_kv = take(el * D.B * kMaxTreeProc * c.n_layers * 2 * c.n_kv_heads * c.head_dim);
+    W.tree_cv = (float*)take(4L * rows * kTkBlocks * kMaxTopk);
+    W.tree_cr = (int32_t*)take(4L * rows * kTkBlocks * kMaxTopk);
+    W.c_tok = (int32_t*)take(4L * D.B * kMaxCand);
+    W.c_par = (int32_t*)take(4L * D.B * kMaxCand);
+    W.c_depth = (int32_t*)take(4L * D.B * kMaxCand);
+    W.c_slot = (int32_t*)take(4L * D.B * kMaxCand);
+    W.c_score = (double*)take(8L * D.B * kMaxCand);
+    W.n_cand = (int32_t*)take(4L * D.B);
+    W.front = (int32_t*)take(4L * D.B * kMaxTopk);
+    W.r_tok = (int32_t*)take(4L * rows);
+    W.r_pos = (int32_t*)take(4L * rows);
+    W.r_attpos = (int32_t*)take(4L * rows);
+    W.r_node = (int32_t*)take(4L * rows);
+    W.r_bslot = (int32_t*)take(4L * rows);
+    W.r_anc = (int32_t*)take(4L * rows * kMaxTreeDepth);
+    W.r_s = (float*)take(4L * rows * d);
+    W.ones = (float*)take(4L * rows);
+  }
   W.v_res = (double*)take(16L * D.B * D.nchunk_t);
   W.vstate = (int32_t*)take(16L * D.B);
   W.vstat = (double*)take(32L * D.B);
@@ -309,11 +340,11 @@ int hip_last() {
 struct SplitPlan {
   int n_split, split_len;
 };
-SplitPlan plan_splits(const osprey_handle* h, long ctx_max, long ctx_total) {
+SplitPlan plan_splits(const osprey_handle* h, long ctx_max, long ctx_total, int max_split = kMaxSplit) {
   const long target_blocks = 320;
   long len = (ctx_total * h->cfg.n_kv_heads + target_blocks - 1) / target_blocks;
   len = std::min<long>(std::max<long>(len, 64), kEvenSplitLen);
-  len = std::max<long>(len, (ctx_max + kMaxSplit - 1) / kMaxSplit);
+  len = std::max<long>(len, (ctx_max + max_split - 1) / max_split);
   len = std::min<long>(len, kMaxSplitLen);
   len = (len + 15) / 16 * 16;
   SplitPlan p;
@@ -448,8 +479,17 @@ void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, c
 // SwiGLU) and write the next product's input as bf16 hi / lo pairs; the last one
 // leaves RMSNorm_final(x) for the LM head.  `s_src` holds the conditioning rows,
 // or is null when they are the tap projection's `ks_taps` partial sums.
+// A draft-tree pass: the rows are frontier nodes, one per (sequence, branch).
+struct TreePass {
+  const int32_t* node;      // [rows] tree-cache slot
+  const int32_t* anc;       // [rows][kMaxTreeDepth] ancestors' slots, then the node's
+  const int32_t* pos;       // [rows] the node's position (RoPE)
+  const int32_t* bslot;     // [rows] the sequence's cache slot (its committed context)
+};
+
 void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, const float* s_src,
-                 int ks_taps, const SplitPlan& sp, int rows_per_seq, int slot0) {
+                 int ks_taps, const SplitPlan& sp, int rows_per_seq, int slot0,
+                 const TreePass* tree = nullptr) {
   const osprey_config& c = h->cfg;
   const Ws& W = h->W;
   // passes of at most kLmMaxRows rows stream the weights once with the inputs
@@ -508,8 +548,8 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     AttnArgs a{};
     a.rows = rows;
     a.cu = cu;
-    a.bslot = W.bslot;
-    a.slot0 = B == 1 ? slot0 : -1;
+    a.bslot = tree ? tree->bslot : W.bslot;
+    a.slot0 = (B == 1 && !tree) ? slot0 : -1;
     a.B = B;
     a.rows_per_seq = rows_per_seq;
     a.qkv = part;
@@ -536,9 +576,18 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     a.scale = 1.0f / std::sqrt((float)hd);
     a.n_split = sp.n_split;
     a.split_len = sp.split_len;
-    // the longest-first work list only matters for several sequences
-    a.items = B == 1 ? nullptr : W.attn_items;
-    a.n_items = B == 1 ? nullptr : W.attn_n_items;
+    // the longest-first work list only matters for several sequences (it lists the
+    // step's sequences, not a tree pass's branches)
+    a.items = (B == 1 || tree) ? nullptr : W.attn_items;
+    a.n_items = (B == 1 || tree) ? nullptr : W.attn_n_items;
+    if (tree) {
+      a.tree_node = tree->node;
+      a.tree_anc = tree->anc;
+      a.tree_pos = tree->pos;
+      a.tree_kv = W.tree_kv;
+      a.tree_slots = h->D.B * kMaxTreeProc;
+      a.n_split = sp.n_split + 1;    // the last split: attention over the node's ancestors
+    }
     a.part = W.attn_part;
     a.o = W.o;
     a.o_hi = W.xa_hi;
@@ -548,13 +597,14 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     // appends k / v once, instead of every split block of the sequence doing it.  One
     // row per sequence (draft steps): the attention blocks sum the QKV partials and
     // prepare their own queries, one launch fewer per layer.
-    if (rows_per_seq > 1) {
+    if (rows_per_seq > 1 || tree) {
       launch_rows_qkv(c.dtype, a, W.o, h->stream);
       a.q_prep = W.o;
     }
     t = h->t_begin(1);
     launch_attention(c.dtype, a, h->stream);
     h->t_end(t);
+    if (tree) launch_tree_attn(c.dtype, a, h->stream);
     launch_attn_combine(a, h->stream);
     // O projection; residual + post-attention RMSNorm
     GemvArgs go = gb;
@@ -702,6 +752,47 @@ void run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, cons
   launch_sample(s, h->stream);
 }
 
+// LM head over `rows` rows of a draft-tree pass (gathered from the ingest rows for the
+// root), logits row r at W.logits + r V, records at temperature 1.  Returns the records
+// per row.
+int run_head_tree(osprey_handle* h, int rows, const int32_t* gather) {
+  const osprey_config& c = h->cfg;
+  const Ws& W = h->W;
+  const bool prepared = gemm_use_mfma(c.dtype, rows);
+  const LmPlan lp = lm_head_plan(std::min(rows, kLmMaxRows), c.vocab_draft, h->n_cu);
+  GemvArgs g{};
+  g.xin = W.x;
+  g.ldx = c.d_model;
+  g.xa_hi = W.xa_hi;
+  g.xa_lo = W.xa_lo;
+  g.ld_xa = c.d_model;
+  g.gamma = h->w.final_norm;
+  g.eps = c.rms_eps;
+  g.d_norm = c.d_model;
+  g.Kd = c.d_model;
+  g.w0 = h->w.lm_head;
+  g.N = c.vocab_draft;
+  g.ld_logits = c.vocab_draft;
+  g.d2t = h->w.d2t;
+  g.nblk = lp.nblk;
+  for (int r0 = 0; r0 < rows; r0 += kLmMaxRows) {
+    GemvArgs p = g;
+    p.max_rows = std::min(kLmMaxRows, rows - r0);
+    if (gather) {
+      p.gather = gather + r0;
+    } else {
+      p.xa_hi = W.xa_hi + (long)r0 * c.d_model;
+      p.xa_lo = W.xa_lo + (long)r0 * c.d_model;
+      p.xin = W.x + (long)r0 * c.d_model;
+    }
+    p.y = W.logits + (long)r0 * c.vocab_draft;
+    p.temp = W.ones + r0;
+    p.part = W.lm_part + (long)r0 * lp.nblk * 4;
+    launch_lm_head(p, lp, !prepared, h->stream);
+  }
+  return lp.nblk;
+}
+
 void fill_verify_common(osprey_handle* h, VerifyArgs& v, int B, int K) {
   const osprey_config& c = h->cfg;
   v.B = B;
@@ -807,12 +898,15 @@ OSPREY_API int osprey_draft_init(const osprey_config* cfg, const osprey_weights*
       hipMemcpy(W.rope_sin, sn.data(), 4 * sn.size(), hipMemcpyHostToDevice) != hipSuccess)
     return bail(fail(OSPREY_E_DEVICE, "uploading tables failed"));
   const long B = h->D.B;
+  // temperature 1 for the LM-head records of draft-tree passes
+  launch_fill_i32(reinterpret_cast<int32_t*>(W.ones), 0x3f800000, B * kMaxTopk, h->stream);
   if (hipMemset(W.slot_len, 0, 4 * B) != hipSuccess || hipMemset(W.pend_n, 0, 4 * B) != hipSuccess ||
       hipMemset(W.slot_nblocks, 0, 4 * B) != hipSuccess ||
       hipMemset(W.block_table, 0, 4L * B * h->D.max_blocks) != hipSuccess ||
       hipMemset(W.pend_tok, 0, 4L * B * (cfg->max_k + 1)) != hipSuccess ||
       hipMemset(W.err, 0, 16) != hipSuccess ||
       hipMemset(W.u_zero, 0, 4L * B * h->D.Km) != hipSuccess ||
+      hipMemset(W.n_cand, 0, 4L * B) != hipSuccess ||
       hipMemset(W.counters, 0, 8 * B) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
     return bail(fail(OSPREY_E_DEVICE, "clearing the workspace failed"));
   *out = h;
@@ -886,16 +980,19 @@ OSPREY_API int osprey_seq_length(osprey_handle* h, int32_t slot, int32_t* length
   return ok();
 }
 
-OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
-  int rc = check_handle(h);
-  if (rc) return rc;
-  if (!a) return fail(OSPREY_E_INVALID, "args is NULL");
+namespace {
+
+// Validation, row layout and ingest of a draft call: the new rows of every sequence
+// through the tap projection (Eq. 1) and the body.  K: the chain's drafts (the setup
+// kernel's autoregressive positions); extra: positions past the ingest the call will
+// use (chain: K - 1; tree: its depth).
+int step_ingest(osprey_handle* h, const osprey_step_args* a, int K, int extra, SplitPlan& split,
+                bool& pending, int& tt, int max_split = kMaxSplit) {
+  int rc;
   const osprey_config& c = h->cfg;
-  const int B = a->batch, K = a->K;
-  if (B < 1 || B > c.max_batch) return fail(OSPREY_E_INVALID, "batch %d not in [1, %d]", B, c.max_batch);
-  if (K < 0 || K > c.max_k) return fail(OSPREY_E_INVALID, "K %d not in [0, %d]", K, c.max_k);
+  const int B = a->batch;
   if (!a->slots || !a->taps || !a->temperature) return fail(OSPREY_E_INVALID, "slots, taps and temperature must be non-NULL");
-  const bool pending = a->n_new == nullptr;
+  pending = a->n_new == nullptr;
   if (!pending && !a->new_tokens) return fail(OSPREY_E_INVALID, "new_tokens is NULL in explicit mode");
   if (a->taps_stride < 0) return fail(OSPREY_E_INVALID, "taps_stride < 0");
   if (pending && a->taps_stride == 0) return fail(OSPREY_E_INVALID, "pending mode needs taps_stride > 0");
@@ -919,7 +1016,7 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
       if (n < 1) return fail(OSPREY_E_INVALID, "n_new[%d] = %d < 1", b, n);
       if (a->taps_stride > 0 && n > a->taps_stride) return fail(OSPREY_E_INVALID, "n_new[%d] = %d > taps_stride", b, n);
     }
-    const long need = s.len_max + n + std::max(K - 1, 0);
+    const long need = s.len_max + n + extra;
     if (need > (long)s.nblocks * c.kv_block || need > c.max_seq_len)
       return fail(OSPREY_E_CAPACITY, "slot %d: up to %ld positions exceed its %d pages / max_seq_len", slot, need, s.nblocks);
     rows += n;
@@ -932,7 +1029,11 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
     return fail(OSPREY_E_CAPACITY, "%ld new rows exceed max_new_rows", rows);
 
   const Ws& W = h->W;
-  int tt = h->t_begin(3);
+  split = plan_splits(h, ctx_max, ctx_total, max_split);
+  if (split.n_split > max_split)
+    return fail(OSPREY_E_UNSUPPORTED, "a context of %ld positions needs %d splits (at most %d)", ctx_max,
+                split.n_split, max_split);
+  tt = h->t_begin(3);
   // ---- row layout of the ingest ---------------------------------------------------------
   SetupArgs sa{};
   sa.B = B;
@@ -963,7 +1064,6 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
   sa.bslot = W.bslot;
   sa.ar_pos = W.ar_pos;
   sa.err = W.err;
-  const SplitPlan split = plan_splits(h, ctx_max, ctx_total);
   sa.split_len = split.split_len;
   sa.attn_items = W.attn_items;
   sa.attn_n_items = W.attn_n_items;
@@ -996,6 +1096,35 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
     launch_gemv(c.dtype, SRC_TAPS, EPI_STORE, gt, h->stream);
     run_body(h, ing, W.cu, B, W.s, true, split, max_new, a->slots[0]);
   }
+  return OSPREY_OK;
+}
+
+// Slot bookkeeping after a draft call: the ingested rows are committed.
+void step_commit(osprey_handle* h, const osprey_step_args* a, bool pending, int K) {
+  for (int b = 0; b < a->batch; ++b) {
+    SlotHost& s = h->slots[a->slots[b]];
+    const int n = pending ? s.drafted_k + 1 : a->n_new[b];
+    s.len_max += n;
+    s.state = K >= 1 ? S_DRAFTED : S_READY;
+    s.drafted_k = K;
+  }
+}
+
+}  // namespace
+
+OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (!a) return fail(OSPREY_E_INVALID, "args is NULL");
+  const osprey_config& c = h->cfg;
+  const int B = a->batch, K = a->K;
+  if (B < 1 || B > c.max_batch) return fail(OSPREY_E_INVALID, "batch %d not in [1, %d]", B, c.max_batch);
+  if (K < 0 || K > c.max_k) return fail(OSPREY_E_INVALID, "K %d not in [0, %d]", K, c.max_k);
+  SplitPlan split;
+  bool pending;
+  int tt;
+  if ((rc = step_ingest(h, a, K, std::max(K - 1, 0), split, pending, tt))) return rc;
+  const Ws& W = h->W;
 
   // ---- K autoregressive draft steps ---------------------------------------------------------
   float* logits = a->draft_logits ? a->draft_logits : W.logits;
@@ -1013,18 +1142,92 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
   }
   h->t_end(tt);
   if ((rc = hip_last())) return rc;
-  for (int b = 0; b < B; ++b) {
-    SlotHost& s = h->slots[a->slots[b]];
-    const int n = pending ? s.drafted_k + 1 : a->n_new[b];
-    s.len_max += n;
-    s.state = K >= 1 ? S_DRAFTED : S_READY;
-    s.drafted_k = K;
-  }
+  step_commit(h, a, pending, K);
   h->last_B = B;
   h->last_K = K;
   h->last_slots.assign(a->slots, a->slots + B);
   h->last_logits = logits;
   h->last_ld_b = ld_b;
+  return ok();
+}
+
+OSPREY_API int osprey_draft_tree(osprey_handle* h, const osprey_step_args* a, const osprey_tree_args* t) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (!a || !t) return fail(OSPREY_E_INVALID, "args is NULL");
+  const osprey_config& c = h->cfg;
+  const int B = a->batch, k = t->topk, D = t->depth, N = t->n_nodes;
+  if (B < 1 || B > c.max_batch) return fail(OSPREY_E_INVALID, "batch %d not in [1, %d]", B, c.max_batch);
+  if (a->K != 0) return fail(OSPREY_E_INVALID, "a draft tree takes K = 0 in its step arguments (K %d)", a->K);
+  if (c.dtype != OSPREY_BF16) return fail(OSPREY_E_UNSUPPORTED, "draft trees need bf16 weights (the matrix-core body)");
+  const int kmax = std::min(kMaxTopk, std::max(c.max_k, 1));
+  if (k < 2 || k > kmax) return fail(OSPREY_E_INVALID, "topk %d not in [2, %d] (top-k 1 is a chain: osprey_draft_step)", k, kmax);
+  if (D < 1 || D > kMaxTreeDepth) return fail(OSPREY_E_INVALID, "depth %d not in [1, %d]", D, kMaxTreeDepth);
+  const int n_cand = k + (D - 1) * k * k;
+  if (N < 1 || N > std::min(kMaxTreeNodes, n_cand))
+    return fail(OSPREY_E_INVALID, "n_nodes %d not in [1, %d]", N, std::min(kMaxTreeNodes, n_cand));
+  if (!t->tokens || !t->parents) return fail(OSPREY_E_INVALID, "tree outputs are NULL");
+  if (c.vocab_draft > kTkBlocks * 256 * 16) return fail(OSPREY_E_UNSUPPORTED, "vocab_draft %d too large for trees", c.vocab_draft);
+  SplitPlan split;
+  bool pending;
+  int tt;
+  if ((rc = step_ingest(h, a, 0, D - 1, split, pending, tt, kMaxSplit - 1))) return rc;
+  const Ws& W = h->W;
+  TreeArgs ta{};
+  ta.B = B;
+  ta.k = k;
+  ta.depth = D;
+  ta.n_nodes = N;
+  ta.V = c.vocab_draft;
+  ta.d2t = h->w.d2t;
+  ta.logits = W.logits;
+  ta.ld_logits = c.vocab_draft;
+  ta.cand_v = W.tree_cv;
+  ta.cand_r = W.tree_cr;
+  ta.rec = W.lm_part;
+  ta.c_tok = W.c_tok;
+  ta.c_par = W.c_par;
+  ta.c_score = W.c_score;
+  ta.c_depth = W.c_depth;
+  ta.c_slot = W.c_slot;
+  ta.n_cand = W.n_cand;
+  ta.front = W.front;
+  ta.r_tok = W.r_tok;
+  ta.r_pos = W.r_pos;
+  ta.r_attpos = W.r_attpos;
+  ta.r_node = W.r_node;
+  ta.r_anc = W.r_anc;
+  ta.r_bslot = W.r_bslot;
+  ta.r_s = W.r_s;
+  ta.x = W.x;
+  ta.d = c.d_model;
+  ta.last_row = W.last_row;
+  ta.committed = W.committed;
+  ta.bslot = W.bslot;
+  ta.out_tok = t->tokens;
+  ta.out_par = t->parents;
+  ta.out_score = t->scores;
+  // the root: the last ingest row of every sequence
+  ta.pass = 0;
+  ta.nblk = run_head_tree(h, B, W.last_row);
+  launch_tree_topk(ta, B, h->stream);
+  launch_tree_step(ta, h->stream);
+  // every further depth: the frontier's B k rows through the body and the LM head
+  const int rows = B * k;
+  for (int p = 1; p < D; ++p) {
+    RowMeta rm{nullptr, W.r_attpos, W.r_tok, nullptr, rows};
+    TreePass tp{W.r_node, W.r_anc, W.r_pos, W.r_bslot};
+    run_body_mr(h, rm, nullptr, rows, W.r_s, 1, split, 1, -1, &tp);
+    ta.pass = p;
+    ta.nblk = run_head_tree(h, rows, nullptr);
+    launch_tree_topk(ta, rows, h->stream);
+    launch_tree_step(ta, h->stream);
+  }
+  launch_tree_final(ta, h->stream);
+  h->t_end(tt);
+  if ((rc = hip_last())) return rc;
+  step_commit(h, a, pending, 0);
+  h->last_B = 0;
   return ok();
 }
 

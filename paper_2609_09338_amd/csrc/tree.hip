@@ -1,0 +1,328 @@
+// Growing a draft tree (top-k > 1; the paper serves chains, top-k 1, Section 4):
+// every node of the frontier runs through the drafter, its k most likely rows become
+// candidates scored by the cumulative log-probability of their path (temperature 1),
+// the k best candidates of a depth form the next frontier, and the n best candidates
+// of all depths form the tree.
+//
+//   k_tree_topk  (rows x 64)  the k best (logit, row) pairs of each 1/64 of an LM-head
+//                             row (larger logit first, lower row on ties)
+//   k_tree_step  (B)          per sequence: the rows' k best pairs and log-normalisers
+//                             (LM-head records at temperature 1), the new candidates,
+//                             the next frontier and the next pass's rows: token, position,
+//                             node slot, ancestors' slots, conditioning row (the parent's
+//                             hidden state) and cache slot
+//   k_tree_final (B)          the n best candidates in generation order, parents
+//                             re-indexed
+//   k_tree_attn  (rows x nq)  attention of a frontier row over its ancestors' and its own
+//                             keys/values (the tree cache), as one more split partial for
+//                             the merge kernel
+#include "common.h"
+#include "internal.h"
+
+namespace osp {
+
+constexpr int kTkThreads = 256;
+constexpr int kTkPer = 16;        // logits per thread and block: a row of up to 64 x 4096
+
+OSP_DEV bool tk_better(float v1, int r1, float v2, int r2) { return v1 > v2 || (v1 == v2 && r1 < r2); }
+
+// Wavefront-wide best (value, row) pair.
+OSP_DEV void wave_best(float& v, int& r) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const float ov = __shfl_xor(v, m, OSP_WAVE);
+    const int orow = __shfl_xor(r, m, OSP_WAVE);
+    if (tk_better(ov, orow, v, r)) { v = ov; r = orow; }
+  }
+}
+
+__global__ void __launch_bounds__(kTkThreads) k_tree_topk(TreeArgs a) {
+  __shared__ float s_v[kTkThreads / OSP_WAVE][kMaxTopk];
+  __shared__ int s_r[kTkThreads / OSP_WAVE][kMaxTopk];
+  const int row = blockIdx.x, blk = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int K = a.k;
+  const int chunk = (a.V + kTkBlocks - 1) / kTkBlocks;
+  const int i0 = blk * chunk, i1 = min(a.V, i0 + chunk);
+  const float* lg = a.logits + (long)row * a.ld_logits;
+  float v[kTkPer];
+  int idx[kTkPer];
+#pragma unroll
+  for (int q = 0; q < kTkPer; ++q) {
+    const int i = i0 + tid + q * kTkThreads;
+    const float l = lg[min(i, a.V - 1)];          // clamped address, masked below
+    v[q] = i < i1 ? l : -INFINITY;
+    idx[q] = i < i1 ? i : 0x7fffffff;
+  }
+  // the wavefront's K best: K rounds of a wavefront arg-best, the winner removed
+  for (int t = 0; t < K; ++t) {
+    float bv = -INFINITY;
+    int br = 0x7fffffff;
+#pragma unroll
+    for (int q = 0; q < kTkPer; ++q)
+      if (tk_better(v[q], idx[q], bv, br)) { bv = v[q]; br = idx[q]; }
+    float wv = bv;
+    int wr = br;
+    wave_best(wv, wr);
+#pragma unroll
+    for (int q = 0; q < kTkPer; ++q)
+      if (idx[q] == wr && wr != 0x7fffffff) { v[q] = -INFINITY; idx[q] = 0x7fffffff; }
+    if (lane == 0) { s_v[wave][t] = wv; s_r[wave][t] = wr; }
+  }
+  __syncthreads();
+  if (wave == 0) {
+    const int nc = (kTkThreads / OSP_WAVE) * K;
+    float cv = lane < nc ? s_v[lane / K][lane % K] : -INFINITY;
+    int cr = lane < nc ? s_r[lane / K][lane % K] : 0x7fffffff;
+    const long o = ((long)row * kTkBlocks + blk) * kMaxTopk;
+    for (int t = 0; t < K; ++t) {
+      float wv = cv;
+      int wr = cr;
+      wave_best(wv, wr);
+      if (cr == wr && wr != 0x7fffffff) { cv = -INFINITY; cr = 0x7fffffff; }
+      if (lane == 0) { a.cand_v[o + t] = wv; a.cand_r[o + t] = wr; }
+    }
+  }
+}
+
+// Candidate c is better than candidate e: larger score, lower index on ties.
+OSP_DEV bool cand_better(double s1, int i1, double s2, int i2) { return s1 > s2 || (s1 == s2 && i1 < i2); }
+
+__global__ void __launch_bounds__(kTkThreads) k_tree_step(TreeArgs a) {
+  __shared__ float s_cv[kMaxTopk][kMaxTopk];
+  __shared__ int s_cr[kMaxTopk][kMaxTopk];
+  __shared__ double s_lse[kMaxTopk];
+  __shared__ double s_sc[kMaxTopk * kMaxTopk];
+  __shared__ int s_sel[kMaxTopk];
+  __shared__ int s_src[kMaxTopk];
+  __shared__ int s_prev[kMaxTopk];
+  __shared__ int s_ntok[kMaxTopk * kMaxTopk], s_ndep[kMaxTopk * kMaxTopk];
+  __shared__ int s_n0;
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int K = a.k, p = a.pass;
+  const int nfr = p == 0 ? 1 : K;                 // rows of this pass that are sequence b's
+  const int row0 = p == 0 ? b : b * K;
+  const long cb = (long)b * kMaxCand;
+  if (tid < K) s_prev[tid] = p == 0 ? -1 : a.front[b * kMaxTopk + tid];
+  if (tid == 0) s_n0 = p == 0 ? 0 : a.n_cand[b];   // (read before anyone writes it below)
+  if (tid < K) { s_sel[tid] = tid; s_src[tid] = p == 0 ? 0 : tid; }   // (overwritten below)
+  // ---- each row's K best (logit, row) pairs and its log-normaliser M + log S --------------
+  for (int j = wave; j < nfr; j += kTkThreads / OSP_WAVE) {
+    const int r = row0 + j;
+    // LM-head records of the row (temperature 1): max and rescaled sums
+    const float* rec = a.rec + (long)r * a.nblk * 4;
+    float m = -INFINITY;
+    for (int c = lane; c < a.nblk; c += OSP_WAVE) m = fmaxf(m, rec[c * 4]);
+    const float M = wave_max(m);
+    double s = 0.0;
+    for (int c = lane; c < a.nblk; c += OSP_WAVE) {
+      const float mc = rec[c * 4];
+      if (mc > -INFINITY) s += (double)rec[c * 4 + 1] * (double)__expf(mc - M);
+    }
+    const double S = wave_sum_d(s);
+    // the blocks' candidates: kTkBlocks x K pairs, lane l holds pairs l, l + 64, ...
+    constexpr int NPL = kTkBlocks * kMaxTopk / OSP_WAVE;
+    float cv[NPL];
+    int cr[NPL];
+#pragma unroll
+    for (int q = 0; q < NPL; ++q) {
+      const int e = lane + q * OSP_WAVE;            // pair e = block e / kMaxTopk, rank e % kMaxTopk
+      const bool in = e % kMaxTopk < K;
+      const long o = ((long)r * kTkBlocks) * kMaxTopk + e;
+      cv[q] = in ? a.cand_v[o] : -INFINITY;
+      cr[q] = in ? a.cand_r[o] : 0x7fffffff;
+    }
+    for (int t = 0; t < K; ++t) {
+      float bv = -INFINITY;
+      int br = 0x7fffffff;
+#pragma unroll
+      for (int q = 0; q < NPL; ++q)
+        if (tk_better(cv[q], cr[q], bv, br)) { bv = cv[q]; br = cr[q]; }
+      float wv = bv;
+      int wr = br;
+      wave_best(wv, wr);
+#pragma unroll
+      for (int q = 0; q < NPL; ++q)
+        if (cr[q] == wr && wr != 0x7fffffff) { cv[q] = -INFINITY; cr[q] = 0x7fffffff; }
+      if (lane == 0) { s_cv[j][t] = wv; s_cr[j][t] = wr; }
+    }
+    if (lane == 0) s_lse[j] = (double)M + log(S);
+  }
+  __syncthreads();
+  // ---- the new candidates (row j, rank t) in generation order -----------------------------
+  const int n0 = s_n0;
+  const int nnew = nfr * K;
+  if (tid < nnew) {
+    const int j = tid / K, t = tid % K;
+    const int par = s_prev[j];
+    const int c = n0 + tid;
+    const int rr = s_cr[j][t];
+    const bool ok = rr >= 0 && rr < a.V;
+    const double sc = (par >= 0 ? a.c_score[cb + par] : 0.0) + ((double)s_cv[j][t] - s_lse[j]);
+    const int tok = ok ? a.d2t[rr] : -1;
+    const int dep = (par >= 0 ? a.c_depth[cb + par] : 0) + 1;
+    a.c_tok[cb + c] = tok;
+    a.c_par[cb + c] = par;
+    a.c_score[cb + c] = sc;
+    a.c_depth[cb + c] = dep;
+    s_sc[tid] = sc;
+    s_ntok[tid] = tok;                              // (read back below from LDS: another
+    s_ndep[tid] = dep;                              // wavefront's global writes may not be)
+  }
+  if (tid == 0) a.n_cand[b] = n0 + nnew;
+  __syncthreads();
+  if (p + 1 >= a.depth) {                         // the last pass: no next frontier
+    if (tid < nnew) a.c_slot[cb + n0 + tid] = -1;
+    return;
+  }
+  // ---- the next frontier: the K best new candidates, then in generation order -------------
+  if (tid < nnew) {
+    int rank = 0;
+    for (int e = 0; e < nnew; ++e) rank += cand_better(s_sc[e], e, s_sc[tid], tid) ? 1 : 0;
+    int pos = K;
+    if (rank < K) {
+      pos = 0;            // place among the selected, by generation order
+      for (int e = 0; e < tid; ++e) {
+        int re = 0;
+        for (int f = 0; f < nnew; ++f) re += cand_better(s_sc[f], f, s_sc[e], e) ? 1 : 0;
+        pos += re < K ? 1 : 0;
+      }
+    }
+    if (pos < K) {        // (a score that is not a number ranks nowhere)
+      s_sel[pos] = tid;                             // (new candidate n0 + tid)
+      s_src[pos] = tid / K;                         // the frontier row of its parent
+      // (each new candidate's slot is written once, by its own thread)
+      a.c_slot[cb + n0 + tid] = b * kMaxTreeProc + p * K + pos;
+    } else {
+      a.c_slot[cb + n0 + tid] = -1;
+    }
+  }
+  __syncthreads();
+  // ---- the next pass's rows ---------------------------------------------------------------
+  if (tid < K) {
+    const int j = tid;
+    const int e0 = s_sel[j];                        // index among the new candidates
+    const int c = n0 + e0;
+    const int slot = b * kMaxTreeProc + p * K + j;  // run through the drafter in pass p + 1
+    a.front[b * kMaxTopk + j] = c;
+    const int r = b * K + j;
+    const int L = a.committed[b];
+    a.r_tok[r] = max(s_ntok[e0], 0);
+    a.r_pos[r] = L + s_ndep[e0] - 1;
+    a.r_attpos[r] = L - 1;
+    a.r_node[r] = slot;
+    a.r_bslot[r] = a.bslot[b];
+    // ancestors' slots (earlier passes' frontier nodes), the root's child first, then
+    // the node itself
+    int chain[kMaxTreeDepth];
+    int n = 0;
+    chain[n++] = slot;
+    for (int e = s_prev[e0 / K]; e >= 0 && e < kMaxCand && n < kMaxTreeDepth; e = a.c_par[cb + e])
+      chain[n++] = a.c_slot[cb + e];
+    for (int i = 0; i < kMaxTreeDepth; ++i) a.r_anc[r * kMaxTreeDepth + i] = i < n ? chain[n - 1 - i] : -1;
+  }
+  // ---- conditioning rows: the parent's hidden state (root: the last ingest row) ------------
+  for (int j = 0; j < K; ++j) {
+    const int src = p == 0 ? a.last_row[b] : b * K + s_src[j];
+    for (int i = tid; i < a.d; i += kTkThreads) a.r_s[(long)(b * K + j) * a.d + i] = a.x[(long)src * a.d + i];
+  }
+}
+
+__global__ void __launch_bounds__(kTkThreads) k_tree_final(TreeArgs a) {
+  __shared__ double s_sc[kMaxCand];
+  __shared__ int s_keep[kMaxCand];
+  __shared__ int s_pos[kMaxCand];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const long cb = (long)b * kMaxCand;
+  const int n = min(a.n_cand[b], kMaxCand);
+  const int N = min(a.n_nodes, n);
+  for (int c = tid; c < n; c += kTkThreads) s_sc[c] = a.c_score[cb + c];
+  __syncthreads();
+  for (int c = tid; c < n; c += kTkThreads) {
+    int rank = 0;
+    for (int e = 0; e < n; ++e) rank += cand_better(s_sc[e], e, s_sc[c], c) ? 1 : 0;
+    s_keep[c] = rank < N ? 1 : 0;
+  }
+  __syncthreads();
+  for (int c = tid; c < n; c += kTkThreads) {
+    int pos = 0;
+    for (int e = 0; e < c; ++e) pos += s_keep[e];
+    s_pos[c] = pos;
+  }
+  __syncthreads();
+  for (int c = tid; c < n; c += kTkThreads) {
+    if (!s_keep[c] || s_pos[c] >= a.n_nodes) continue;
+    const int i = s_pos[c];
+    const int par = a.c_par[cb + c];
+    a.out_tok[(long)b * a.n_nodes + i] = a.c_tok[cb + c];
+    // (the parent scores at least as high and comes earlier: it is kept too)
+    a.out_par[(long)b * a.n_nodes + i] = par >= 0 ? (s_keep[par] ? s_pos[par] : -2) : -1;
+    if (a.out_score) a.out_score[(long)b * a.n_nodes + i] = s_sc[c];
+  }
+  for (int i = N + tid; i < a.n_nodes; i += kTkThreads) {
+    a.out_tok[(long)b * a.n_nodes + i] = -1;
+    a.out_par[(long)b * a.n_nodes + i] = -2;
+    if (a.out_score) a.out_score[(long)b * a.n_nodes + i] = -INFINITY;
+  }
+}
+
+// One wavefront per (row, query head): online softmax over the ancestors' and the row's
+// own keys/values in the tree cache; the result is the partial of split n_split - 1.
+template <typename TKV, int HD>
+__global__ void __launch_bounds__(64) k_tree_attn(AttnArgs a) {
+  constexpr int DPL = HD / OSP_WAVE;              // head dims per lane
+  const int r = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+  const int g = h / (a.nq / a.nkv);
+  const float* q = a.q_prep + ((long)r * a.nq + h) * HD;
+  float qv[DPL], o[DPL];
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) { qv[e] = q[lane * DPL + e]; o[e] = 0.f; }
+  const TKV* kv = reinterpret_cast<const TKV*>(a.tree_kv);
+  float m = -INFINITY, l = 0.f;
+  for (int i = 0; i < kMaxTreeDepth; ++i) {
+    const int slot = a.tree_anc[r * kMaxTreeDepth + i];
+    if (slot < 0 || slot >= a.tree_slots) break;
+    const long kb = ((((long)slot * a.n_layers + a.layer) * 2 + 0) * a.nkv + g) * HD + lane * DPL;
+    const long vb = ((((long)slot * a.n_layers + a.layer) * 2 + 1) * a.nkv + g) * HD + lane * DPL;
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) s += qv[e] * load_f32(kv, kb + e);
+    s = wave_sum(s);
+    const float mn = fmaxf(m, s);
+    const float f = __expf(m - mn), w = __expf(s - mn);
+    l = l * f + w;
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) o[e] = o[e] * f + w * load_f32(kv, vb + e);
+    m = mn;
+  }
+  float* pp = a.part + (((long)r * a.nq + h) * a.n_split + (a.n_split - 1)) * (HD + 2);
+  if (lane == 0) { pp[0] = m; pp[1] = l; }
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) pp[2 + lane * DPL + e] = o[e];
+}
+
+void launch_tree_topk(const TreeArgs& a, int rows, hipStream_t st) {
+  hipLaunchKernelGGL(k_tree_topk, dim3(rows, kTkBlocks), dim3(kTkThreads), 0, st, a);
+}
+
+void launch_tree_step(const TreeArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(k_tree_step, dim3(a.B), dim3(kTkThreads), 0, st, a);
+}
+
+void launch_tree_final(const TreeArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(k_tree_final, dim3(a.B), dim3(kTkThreads), 0, st, a);
+}
+
+void launch_tree_attn(int kvdtype, const AttnArgs& a, hipStream_t st) {
+  const dim3 grid(a.rows.max_rows, a.nq);
+  if (kvdtype == 1) {
+    if (a.hd == 128) hipLaunchKernelGGL((k_tree_attn<bf16_t, 128>), grid, dim3(64), 0, st, a);
+    else hipLaunchKernelGGL((k_tree_attn<bf16_t, 64>), grid, dim3(64), 0, st, a);
+  } else {
+    if (a.hd == 128) hipLaunchKernelGGL((k_tree_attn<float, 128>), grid, dim3(64), 0, st, a);
+    else hipLaunchKernelGGL((k_tree_attn<float, 64>), grid, dim3(64), 0, st, a);
+  }
+}
+
+}  // namespace osp

@@ -117,3 +117,93 @@ def test_verify_tree_duplicate_and_invalid_parent():
         assert al[b] == r.accept_len and list(ap[b][:r.accept_len]) == list(r.path), b
         assert list(ot[b][:r.accept_len + 1]) == list(r.tokens), b
         assert 2 not in list(ap[b])          # the duplicate sibling is never accepted
+
+
+# ----------------------------------------------------------------------------------------
+# growing trees (osprey_draft_tree) against the oracle's tree growth
+# ----------------------------------------------------------------------------------------
+def _path_keys(tokens, parents):
+    """Each node's path from the root as a tuple of tokens (identifies a node across
+    two trees whose generation orders differ)."""
+    keys = []
+    for i in range(len(tokens)):
+        k, j = [], i
+        while j >= 0:
+            k.append(int(tokens[j]))
+            j = int(parents[j])
+        keys.append(tuple(k[::-1]))
+    return keys
+
+
+@pytest.mark.parametrize("wl,topk,depth,n_nodes", [("p_qwen_small", 3, 4, 12),
+                                                   ("p_single128", 4, 3, 15),
+                                                   ("p_partial", 2, 5, 9),
+                                                   ("p_greedy_draft", 5, 2, 30)])
+def test_draft_tree_matches_oracle(wl, topk, depth, n_nodes):
+    """Two tree steps per sequence: the first ingests the last prompt token, the
+    second the tokens that following each tree's first children for two levels
+    commits, plus one more (the same on both sides).  The GPU tree must be valid
+    (parents earlier, the root's children first at depth 1), its scores within 2e-2
+    of the oracle's on every node both trees hold, and the trees (tokens, parents)
+    identical unless one of the oracle's selections had a margin below four times
+    that measured score error (a near tie that another rounding may break)."""
+    _require_gpu()
+    from oracle import harness as OH
+    from oracle.tree import draft_tree as o_draft_tree
+    from paper_2609_09338_amd import workload as WL
+    _say(f"[draft_tree] {wl} topk {topk} depth {depth} nodes {n_nodes}")
+    w = synth.PARITY[wl]
+    s = WL.make_drafter(w, 3)
+    WL.reset_sequences(s)
+    dr = OH.build_drafter(w)
+    B, dev = w.batch, s.device
+    seqs = [OH.start_sequence(w, dr, b, 3) for b in range(B)]
+    new_tok = [np.array([synth.prompt_tokens(w, b, int(s.ctx[b]))[-1]], dtype=np.int64)
+               for b in range(B)]
+    flagged = compared = 0
+    max_err = 0.0
+    for step in range(2):
+        taps = np.stack([synth.taps(w, step, b, w.K + 1) for b in range(B)])
+        n_new = [len(t) for t in new_tok]
+        tok_d = torch.from_numpy(np.concatenate(new_tok).astype(np.int32)).to(dev)
+        tk = torch.full((B, n_nodes), -7, dtype=torch.int32, device=dev)
+        pr = torch.full((B, n_nodes), -7, dtype=torch.int32, device=dev)
+        sc = torch.full((B, n_nodes), 7.0, dtype=torch.float64, device=dev)
+        s.drafter.draft_tree(list(range(B)), topk, depth, n_nodes, WL.to_dev(taps, w, dev),
+                             s.temperature, tk, pr, n_new=n_new, new_tokens=tok_d,
+                             taps_stride=w.K + 1, scores=sc)
+        torch.cuda.synchronize()
+        assert s.drafter.device_errors() == 0
+        tk, pr, sc = tk.cpu().numpy(), pr.cpu().numpy(), sc.cpu().numpy()
+        nxt = []
+        for b in range(B):
+            t = o_draft_tree(dr, seqs[b], new_tok[b], taps[b][: n_new[b]].astype(np.float64),
+                             topk, depth, n_nodes)
+            compared += 1
+            # a valid tree: parents earlier, scores non-increasing along every path
+            assert all(-1 <= pr[b, i] < i for i in range(n_nodes)), pr[b]
+            assert all(pr[b, i] < 0 or sc[b, i] <= sc[b, pr[b, i]] for i in range(n_nodes))
+            assert np.all(tk[b] >= 0) and np.all(tk[b] < w.vocab_target)
+            gk = dict(zip(_path_keys(tk[b], pr[b]), sc[b]))
+            ok = dict(zip(_path_keys(t.tokens, t.parents), t.scores))
+            common = set(gk) & set(ok)
+            assert common, (wl, step, b)
+            err = max(abs(gk[k] - ok[k]) for k in common)
+            assert err <= 2e-2, (wl, step, b, err)
+            max_err = max(max_err, err)
+            if not (np.array_equal(tk[b], t.tokens) and np.array_equal(pr[b], t.parents)):
+                assert t.min_gap < 4.0 * err + 1e-9, (wl, step, b, tk[b], t.tokens, pr[b],
+                                                       t.parents, t.min_gap, err)
+                flagged += 1
+            # commit: the first child of each node for two levels, then the root's first child
+            path, cur = [], -1
+            while len(path) < 2:
+                kids = np.flatnonzero(t.parents == cur)
+                if len(kids) == 0:
+                    break
+                cur = int(kids[0])
+                path.append(int(t.tokens[cur]))
+            nxt.append(np.array(path + [int(t.tokens[0])], dtype=np.int64))
+        new_tok = nxt
+    _say(f"[draft_tree] {wl}: compared {compared} flagged {flagged} max score error {max_err:.3g}")
+    assert flagged <= max(1, compared // 5)
