@@ -175,6 +175,9 @@ def run_gpu(args):
             s.drafter.kernel_timing(())
         res["kernels"] = kt
         res["tree_verify"] = time_tree_verify(s, w)
+        if w.dtype == "bf16" and w.K >= TREE_TOPK:
+            rewind()
+            res["tree_draft"] = time_tree_draft(s, w, float(np.mean(s.ctx)))
     assert s.drafter.device_errors() == 0
     res["ctx_mean"] = float(np.mean(s.ctx))
     return w, res
@@ -214,6 +217,53 @@ def time_tree_verify(s, w, reps: int = 20):
     nbytes = B * (N + 2) * V * 4
     return dict(nodes=N, topk=TREE_TOPK, batch=B, us_per_call=round(us, 2), bytes_per_call=nbytes,
                 achieved_gbs=round(nbytes / (us * 1e-6) / 1e9, 1),
+                frac=round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4))
+
+
+TREE_DEPTH = 4
+
+
+def time_tree_draft(s, w, ctx_mean: float, reps: int = 10):
+    """Draft-tree growth (osprey_draft_tree: ingest of one token per sequence, then a
+    top-4, depth-4 tree of 15 nodes) for every sequence of the batch: per-call time
+    from HIP events on the library's stream, against its algorithmic bytes (per depth
+    every drafter weight and each sequence's context keys/values once, plus W_c for the
+    ingest and the logits written).  Each call starts from the same committed prefix."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2609_09338_amd import binding as BD
+    B, N, k, D = w.batch, TREE_NODES, TREE_TOPK, TREE_DEPTH
+    dev = s.device
+    taps = torch.zeros((B, w.tap_width), dtype=torch.bfloat16, device=dev)
+    tok = torch.from_numpy(np.array([synth.prompt_tokens(w, b, int(s.ctx[b]))[-1]
+                                     for b in range(B)], dtype=np.int32)).to(dev)
+    tk = torch.empty((B, N), dtype=torch.int32, device=dev)
+    pr = torch.empty((B, N), dtype=torch.int32, device=dev)
+
+    def call():
+        for b in range(B):
+            s.drafter.seq_truncate(b, int(s.ctx[b]) - 1)
+        s.drafter.draft_tree(list(range(B)), k, D, N, taps, s.temperature, tk, pr,
+                             n_new=[1] * B, new_tokens=tok)
+
+    call()
+    s.drafter.kernel_timing((BD.KERNEL_DRAFT_STEP,))
+    for _ in range(reps):
+        call()
+    torch.cuda.synchronize()
+    ms, n = s.drafter.kernel_time(BD.KERNEL_DRAFT_STEP)
+    s.drafter.kernel_timing(())
+    for b in range(B):
+        s.drafter.seq_truncate(b, int(s.ctx[b]) - 1)
+    us = ms * 1e3 / max(n, 1)
+    el = 2 if w.dtype == "bf16" else 4
+    sb = step_bytes(w, ctx_mean)
+    nbytes = int(D * sb["total"] + w.tap_width * w.d_model * el
+                 + B * w.vocab_draft * 4 * (1 + (D - 1) * k))
+    return dict(nodes=N, topk=k, depth=D, batch=B, us_per_call=round(us, 2),
+                bytes_per_call=nbytes, achieved_gbs=round(nbytes / (us * 1e-6) / 1e9, 1),
                 frac=round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4))
 
 
@@ -292,6 +342,8 @@ def main():
         ar_us = ds_ms * 1e3 / max(ds_n, 1) / w.K
         line["draft_token_hbm_frac"] = round(sb["total"] / (ar_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
         line["tree_verify"] = r["tree_verify"]
+        if "tree_draft" in r:
+            line["tree_draft"] = r["tree_draft"]
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = run_cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(line), flush=True)

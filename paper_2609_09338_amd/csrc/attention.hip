@@ -674,12 +674,66 @@ __global__ void __launch_bounds__(256) k_rows_qkv(AttnArgs a, float* q_out) {
 // at once (dimension tid % hd, splits tid / hd, + 256 / hd, ...) while wavefront 0
 // reads the splits' (max, sum); the weights exp(m_s - M) / L come through LDS and the
 // thread groups are added in LDS, in a fixed order.
+// A draft-tree row's attention over its ancestors' and its own keys/values in the tree
+// cache (one wavefront): the (max, sum, unnormalised output) of one more split.  Every
+// ancestor's key and value are requested at once (slots clamped into the cache; the
+// -1 padding masked afterwards), then scored and summed.
+template <int HD>
+OSP_DEV void tree_partial(const AttnArgs& a, int r, int h, int lane, float& m, float& l, float* s_o) {
+  constexpr int DPL = HD / OSP_WAVE;              // head dims per lane
+  const int g = h / (a.nq / a.nkv);
+  const float* q = a.q_prep + ((long)r * a.nq + h) * HD;
+  const bf16_t* kv = reinterpret_cast<const bf16_t*>(a.tree_kv);
+  const int my = lane < kMaxTreeDepth ? a.tree_anc[r * kMaxTreeDepth + lane] : -1;
+  float qv[DPL];
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) qv[e] = q[lane * DPL + e];
+  float kx[kMaxTreeDepth][DPL], vx[kMaxTreeDepth][DPL];
+  bool ok[kMaxTreeDepth];
+  bool run = true;                                // leading valid slots only
+#pragma unroll
+  for (int i = 0; i < kMaxTreeDepth; ++i) {
+    const int slot = __shfl(my, i, OSP_WAVE);
+    run = run && slot >= 0 && slot < a.tree_slots;
+    ok[i] = run;
+    const long kb = ((((long)(run ? slot : 0) * a.n_layers + a.layer) * 2 + 0) * a.nkv + g) * HD + lane * DPL;
+    const long vb = kb + (long)a.nkv * HD;
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) { kx[i][e] = load_f32(kv, kb + e); vx[i][e] = load_f32(kv, vb + e); }
+  }
+  float sc[kMaxTreeDepth];
+  m = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < kMaxTreeDepth; ++i) {
+    float d = 0.f;
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) d += qv[e] * kx[i][e];
+    d = wave_sum(d);
+    sc[i] = ok[i] ? d : -INFINITY;
+    m = fmaxf(m, sc[i]);
+  }
+  float o[DPL];
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) o[e] = 0.f;
+  l = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxTreeDepth; ++i) {
+    const float w = ok[i] ? __expf(sc[i] - m) : 0.f;
+    l += w;
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) o[e] += w * vx[i][e];
+  }
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) s_o[lane * DPL + e] = o[e];
+}
+
 template <int HD>
 __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
   constexpr int G = 256 / HD;              // thread groups (splits interleaved)
   constexpr int PER = kMaxSplitAttn / G;   // splits per thread (bound)
   __shared__ float s_f[kMaxSplitAttn];
   __shared__ float s_part[G][HD];
+  __shared__ float s_to[HD];               // a draft-tree row's partial over its ancestors
   const int r = blockIdx.x, h = blockIdx.y;
   const int rows = a.rows.count ? min(*a.rows.count, a.rows.max_rows) : a.rows.max_rows;
   if (r >= rows) return;
@@ -696,11 +750,18 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
     const int sp = grp + G * i;
     v[i] = sp < a.n_split ? pp[(long)sp * (HD + 2) + 2 + e] : 0.f;
   }
-  // (a draft-tree row: the last split is its attention over its ancestors and itself)
-  const int extra = a.tree_node ? a.n_split - 1 : -1;
+  // (a draft-tree row: one more split after the context's, its attention over its
+  // ancestors and itself)
+  const bool tree = a.tree_node != nullptr;
+  const int extra = tree ? a.n_split : -1;
   if (tid < 64) {
-    const float m_any = lane < a.n_split ? pp[(long)lane * (HD + 2)] : -INFINITY;
-    const float l_any = lane < a.n_split ? pp[(long)lane * (HD + 2) + 1] : 0.f;
+    float m_any = lane < a.n_split ? pp[(long)lane * (HD + 2)] : -INFINITY;
+    float l_any = lane < a.n_split ? pp[(long)lane * (HD + 2) + 1] : 0.f;
+    if (tree) {
+      float tm, tl;
+      tree_partial<HD>(a, r, h, lane, tm, tl, s_to);
+      if (lane == extra) { m_any = tm; l_any = tl; }
+    }
     const bool use = lane < ns || lane == extra;
     const float m = use ? m_any : -INFINITY;
     const float lsum = use ? l_any : 0.f;
@@ -714,8 +775,9 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     const int sp = grp + G * i;
-    if (sp < ns || sp == extra) O += v[i] * s_f[sp];
+    if (sp < ns) O += v[i] * s_f[sp];
   }
+  if (tree && grp == 0) O += s_to[e] * s_f[extra];
   s_part[grp][e] = O;
   __syncthreads();
   if (tid < HD) {

@@ -198,19 +198,19 @@ struct AttnArgs {
   uint16_t* o_hi;           // matrix-core path: o as bf16 hi / lo pairs instead (nullable)
   uint16_t* o_lo;
   uint32_t* err;
-  // draft-tree passes (nullable): every row is a frontier node with one row per
-  // sequence; rows.pos holds the last committed position (the split attention reads the
-  // committed context only), tree_pos the node's own position (RoPE); its keys/values go
-  // to the tree cache at slot tree_node[r] instead of the pages, and split n_split - 1 is
-  // attention over tree_anc[r] (its ancestors' slots, then its own; -1 padded)
+  // draft-tree passes (nullable): the rows are frontier nodes, cu groups each
+  // sequence's rows (they share its context pages); rows.pos holds the last committed
+  // position (the split attention reads the committed context only), tree_pos the
+  // node's own position (RoPE); its keys/values go to the tree cache at slot
+  // tree_node[r] instead of the pages, and the combine adds the row's attention over
+  // tree_anc[r] (its ancestors' slots, then its own; -1 padded) as one more split
   const int32_t* tree_node;
   const int32_t* tree_anc;  // [rows][kMaxTreeDepth]
   const int32_t* tree_pos;
-  void* tree_kv;            // [slot][n_layers][2][nkv][hd], cache dtype
+  void* tree_kv;            // [slot][n_layers][2][nkv][hd], bf16
   int tree_slots;           // slots of tree_kv
 };
 void launch_attention(int kvdtype, const AttnArgs& a, hipStream_t st);
-void launch_tree_attn(int kvdtype, const AttnArgs& a, hipStream_t st);
 // Matrix-core path: per row, sum the QKV split partials, normalise and rotate q
 // and k, write q * (1/sqrt(hd)) to q_out and the new k, v into the cache.
 void launch_rows_qkv(int kvdtype, const AttnArgs& a, float* q_out, hipStream_t st);
@@ -370,7 +370,7 @@ struct TreeArgs {
   int32_t* r_attpos;
   int32_t* r_node;
   int32_t* r_anc;           // [rows][kMaxTreeDepth]
-  int32_t* r_bslot;
+  int32_t* r_cu;            // [B + 1] the rows of sequence b: [b k, (b + 1) k)
   float* r_s;               // [rows][d] conditioning input: the parent's hidden state
   const float* x;           // this pass's body output rows (root pass: the ingest rows)
   int d;

@@ -93,7 +93,8 @@ struct Ws {
   int32_t* tree_cr;
   int32_t *c_tok, *c_par, *c_depth, *c_slot, *n_cand, *front;   // [B][kMaxCand] / [B] / [B][kMaxTopk]
   double* c_score;
-  int32_t *r_tok, *r_pos, *r_attpos, *r_node, *r_anc, *r_bslot;  // [B * kMaxTopk] (r_anc x kMaxTreeDepth)
+  int32_t *r_tok, *r_pos, *r_attpos, *r_node, *r_anc;  // [B * kMaxTopk] (r_anc x kMaxTreeDepth)
+  int32_t* r_cu;                                       // [B + 1]
   float* r_s;                 // [B * kMaxTopk][d]
   float* ones;                // [B * kMaxTopk] temperature 1 for the tree's LM-head records
 };
@@ -203,7 +204,7 @@ size_t plan(const osprey_config& c, char* base, Ws* w) {
     W.r_pos = (int32_t*)take(4L * rows);
     W.r_attpos = (int32_t*)take(4L * rows);
     W.r_node = (int32_t*)take(4L * rows);
-    W.r_bslot = (int32_t*)take(4L * rows);
+    W.r_cu = (int32_t*)take(4L * (D.B + 1));
     W.r_anc = (int32_t*)take(4L * rows * kMaxTreeDepth);
     W.r_s = (float*)take(4L * rows * d);
     W.ones = (float*)take(4L * rows);
@@ -484,7 +485,7 @@ struct TreePass {
   const int32_t* node;      // [rows] tree-cache slot
   const int32_t* anc;       // [rows][kMaxTreeDepth] ancestors' slots, then the node's
   const int32_t* pos;       // [rows] the node's position (RoPE)
-  const int32_t* bslot;     // [rows] the sequence's cache slot (its committed context)
+  const int32_t* bslot;     // [B] each sequence's cache slot (its committed context)
 };
 
 void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, const float* s_src,
@@ -586,7 +587,6 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
       a.tree_pos = tree->pos;
       a.tree_kv = W.tree_kv;
       a.tree_slots = h->D.B * kMaxTreeProc;
-      a.n_split = sp.n_split + 1;    // the last split: attention over the node's ancestors
     }
     a.part = W.attn_part;
     a.o = W.o;
@@ -604,7 +604,6 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     t = h->t_begin(1);
     launch_attention(c.dtype, a, h->stream);
     h->t_end(t);
-    if (tree) launch_tree_attn(c.dtype, a, h->stream);
     launch_attn_combine(a, h->stream);
     // O projection; residual + post-attention RMSNorm
     GemvArgs go = gb;
@@ -1197,7 +1196,7 @@ OSPREY_API int osprey_draft_tree(osprey_handle* h, const osprey_step_args* a, co
   ta.r_attpos = W.r_attpos;
   ta.r_node = W.r_node;
   ta.r_anc = W.r_anc;
-  ta.r_bslot = W.r_bslot;
+  ta.r_cu = W.r_cu;
   ta.r_s = W.r_s;
   ta.x = W.x;
   ta.d = c.d_model;
@@ -1216,8 +1215,8 @@ OSPREY_API int osprey_draft_tree(osprey_handle* h, const osprey_step_args* a, co
   const int rows = B * k;
   for (int p = 1; p < D; ++p) {
     RowMeta rm{nullptr, W.r_attpos, W.r_tok, nullptr, rows};
-    TreePass tp{W.r_node, W.r_anc, W.r_pos, W.r_bslot};
-    run_body_mr(h, rm, nullptr, rows, W.r_s, 1, split, 1, -1, &tp);
+    TreePass tp{W.r_node, W.r_anc, W.r_pos, W.bslot};
+    run_body_mr(h, rm, W.r_cu, B, W.r_s, 1, split, k, -1, &tp);
     ta.pass = p;
     ta.nblk = run_head_tree(h, rows, nullptr);
     launch_tree_topk(ta, rows, h->stream);

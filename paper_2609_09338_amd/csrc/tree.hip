@@ -9,13 +9,12 @@
 //   k_tree_step  (B)          per sequence: the rows' k best pairs and log-normalisers
 //                             (LM-head records at temperature 1), the new candidates,
 //                             the next frontier and the next pass's rows: token, position,
-//                             node slot, ancestors' slots, conditioning row (the parent's
-//                             hidden state) and cache slot
+//                             node slot, ancestors' slots and conditioning row (the
+//                             parent's hidden state)
 //   k_tree_final (B)          the n best candidates in generation order, parents
 //                             re-indexed
-//   k_tree_attn  (rows x nq)  attention of a frontier row over its ancestors' and its own
-//                             keys/values (the tree cache), as one more split partial for
-//                             the merge kernel
+// A frontier row's attention over its ancestors' and its own keys/values (the tree
+// cache) is one more split of the context attention, added by the split combine.
 #include "common.h"
 #include "internal.h"
 
@@ -97,6 +96,7 @@ __global__ void __launch_bounds__(kTkThreads) k_tree_step(TreeArgs a) {
   __shared__ int s_src[kMaxTopk];
   __shared__ int s_prev[kMaxTopk];
   __shared__ int s_ntok[kMaxTopk * kMaxTopk], s_ndep[kMaxTopk * kMaxTopk];
+  __shared__ int s_rank[kMaxTopk * kMaxTopk];
   __shared__ int s_n0;
   const int b = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -180,16 +180,16 @@ __global__ void __launch_bounds__(kTkThreads) k_tree_step(TreeArgs a) {
   if (tid < nnew) {
     int rank = 0;
     for (int e = 0; e < nnew; ++e) rank += cand_better(s_sc[e], e, s_sc[tid], tid) ? 1 : 0;
+    s_rank[tid] = rank;
+  }
+  __syncthreads();
+  if (tid < nnew) {
     int pos = K;
-    if (rank < K) {
+    if (s_rank[tid] < K) {
       pos = 0;            // place among the selected, by generation order
-      for (int e = 0; e < tid; ++e) {
-        int re = 0;
-        for (int f = 0; f < nnew; ++f) re += cand_better(s_sc[f], f, s_sc[e], e) ? 1 : 0;
-        pos += re < K ? 1 : 0;
-      }
+      for (int e = 0; e < tid; ++e) pos += s_rank[e] < K ? 1 : 0;
     }
-    if (pos < K) {        // (a score that is not a number ranks nowhere)
+    if (pos < K) {        // (scores that are not numbers could put more than K below rank K)
       s_sel[pos] = tid;                             // (new candidate n0 + tid)
       s_src[pos] = tid / K;                         // the frontier row of its parent
       // (each new candidate's slot is written once, by its own thread)
@@ -212,7 +212,10 @@ __global__ void __launch_bounds__(kTkThreads) k_tree_step(TreeArgs a) {
     a.r_pos[r] = L + s_ndep[e0] - 1;
     a.r_attpos[r] = L - 1;
     a.r_node[r] = slot;
-    a.r_bslot[r] = a.bslot[b];
+    if (j == 0) {                                   // the next pass's rows of sequence b
+      a.r_cu[b] = b * K;
+      if (b == a.B - 1) a.r_cu[a.B] = a.B * K;
+    }
     // ancestors' slots (earlier passes' frontier nodes), the root's child first, then
     // the node itself
     int chain[kMaxTreeDepth];
@@ -267,41 +270,6 @@ __global__ void __launch_bounds__(kTkThreads) k_tree_final(TreeArgs a) {
   }
 }
 
-// One wavefront per (row, query head): online softmax over the ancestors' and the row's
-// own keys/values in the tree cache; the result is the partial of split n_split - 1.
-template <typename TKV, int HD>
-__global__ void __launch_bounds__(64) k_tree_attn(AttnArgs a) {
-  constexpr int DPL = HD / OSP_WAVE;              // head dims per lane
-  const int r = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
-  const int g = h / (a.nq / a.nkv);
-  const float* q = a.q_prep + ((long)r * a.nq + h) * HD;
-  float qv[DPL], o[DPL];
-#pragma unroll
-  for (int e = 0; e < DPL; ++e) { qv[e] = q[lane * DPL + e]; o[e] = 0.f; }
-  const TKV* kv = reinterpret_cast<const TKV*>(a.tree_kv);
-  float m = -INFINITY, l = 0.f;
-  for (int i = 0; i < kMaxTreeDepth; ++i) {
-    const int slot = a.tree_anc[r * kMaxTreeDepth + i];
-    if (slot < 0 || slot >= a.tree_slots) break;
-    const long kb = ((((long)slot * a.n_layers + a.layer) * 2 + 0) * a.nkv + g) * HD + lane * DPL;
-    const long vb = ((((long)slot * a.n_layers + a.layer) * 2 + 1) * a.nkv + g) * HD + lane * DPL;
-    float s = 0.f;
-#pragma unroll
-    for (int e = 0; e < DPL; ++e) s += qv[e] * load_f32(kv, kb + e);
-    s = wave_sum(s);
-    const float mn = fmaxf(m, s);
-    const float f = __expf(m - mn), w = __expf(s - mn);
-    l = l * f + w;
-#pragma unroll
-    for (int e = 0; e < DPL; ++e) o[e] = o[e] * f + w * load_f32(kv, vb + e);
-    m = mn;
-  }
-  float* pp = a.part + (((long)r * a.nq + h) * a.n_split + (a.n_split - 1)) * (HD + 2);
-  if (lane == 0) { pp[0] = m; pp[1] = l; }
-#pragma unroll
-  for (int e = 0; e < DPL; ++e) pp[2 + lane * DPL + e] = o[e];
-}
-
 void launch_tree_topk(const TreeArgs& a, int rows, hipStream_t st) {
   hipLaunchKernelGGL(k_tree_topk, dim3(rows, kTkBlocks), dim3(kTkThreads), 0, st, a);
 }
@@ -312,17 +280,6 @@ void launch_tree_step(const TreeArgs& a, hipStream_t st) {
 
 void launch_tree_final(const TreeArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(k_tree_final, dim3(a.B), dim3(kTkThreads), 0, st, a);
-}
-
-void launch_tree_attn(int kvdtype, const AttnArgs& a, hipStream_t st) {
-  const dim3 grid(a.rows.max_rows, a.nq);
-  if (kvdtype == 1) {
-    if (a.hd == 128) hipLaunchKernelGGL((k_tree_attn<bf16_t, 128>), grid, dim3(64), 0, st, a);
-    else hipLaunchKernelGGL((k_tree_attn<bf16_t, 64>), grid, dim3(64), 0, st, a);
-  } else {
-    if (a.hd == 128) hipLaunchKernelGGL((k_tree_attn<float, 128>), grid, dim3(64), 0, st, a);
-    else hipLaunchKernelGGL((k_tree_attn<float, 64>), grid, dim3(64), 0, st, a);
-  }
 }
 
 }  // namespace osp
