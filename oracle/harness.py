@@ -10,8 +10,9 @@ Per sequence b:
 * iteration 0 ingests prompt token ctx-1; iteration i > 0 ingests the a+1
   tokens committed by iteration i-1; the conditioning rows are the first
   n_new rows of `synth.taps(w, i, b, K + 1)`;
-* K drafts are proposed, the synthetic target logits are formed from the
-  drafter's logits (`synth.target_logits`), and verify decides.
+* K drafts are proposed (a chain of K steps, or one block for workloads that
+  draft in blocks), the synthetic target logits are formed from the drafter's
+  logits (`synth.target_logits`), and verify decides.
 """
 from __future__ import annotations
 
@@ -21,6 +22,7 @@ from typing import Dict, List, Optional
 import numpy as np
 
 import synth
+from .block import draft_block
 from .drafter import Drafter, Sequence
 from .verify import VerifyResult, verify
 
@@ -83,7 +85,11 @@ def run_sequence(w, b: int, n_iters: int, drafter: Optional[Drafter] = None,
         pre = seq.length
         taps = synth.taps(w, it, b, w.K + 1)[: len(new_tokens)]
         ud = synth.u_draft(w, it)[b]
-        drafts, logits, rows, committed = drafter.draft(seq, new_tokens, taps, w.K, Td, ud)
+        if w.drafting == "block":
+            drafts, logits, rows, committed = draft_block(drafter, seq, new_tokens, taps, w.K, Td,
+                                                          ud, synth.mask_token(w))
+        else:
+            drafts, logits, rows, committed = drafter.draft(seq, new_tokens, taps, w.K, Td, ud)
         tl = synth.target_logits(w, logits, drafter.d2t, synth.target_noise(w, it, b))
         res = verify(tl, logits, drafter.d2t, drafts, T, synth.u_accept(w, it)[b],
                      float(synth.u_bonus(w, it)[b]), residual_fn=residual_fn, T_draft=Td)

@@ -59,6 +59,7 @@ class Workload:
     kv_block: int = 16
     shuffle_blocks: bool = False
     variant: int = 0
+    drafting: str = "chain"    # "chain": K autoregressive steps; "block": one block pass
 
     def with_(self, **kw) -> "Workload":
         return dataclasses.replace(self, **kw)
@@ -79,6 +80,11 @@ class Workload:
         if not self.draft_temps:
             return self.temperature(b)
         return float(self.draft_temps[b % len(self.draft_temps)])
+
+
+def mask_token(w: "Workload") -> int:
+    """The placeholder token of block drafting: the last target id."""
+    return w.vocab_target - 1
 
 
 # ---------------------------------------------------------------------------
@@ -123,6 +129,19 @@ WORKLOADS: Dict[str, Workload] = {
     "c5": Workload(name="c5", cfg_id=5, vocab_draft=151936, vocab_target=151936,
                    target_hidden=4096, batch=64, K=7, ctx_lo=512, ctx_hi=4096,
                    temps=(0.0, 1.0), sigma=1.0, shuffle_blocks=True, **_QWEN_DRAFTER),
+    # Block drafting (the EAGLE-style interface of the DFlash ablation) with the c2 drafter:
+    # 7 proposals from one pass over the anchor and 6 mask rows.
+    "c2b": Workload(name="c2b", cfg_id=8, vocab_draft=151936, vocab_target=151936,
+                    target_hidden=4096, batch=1, K=7, ctx_lo=2048, ctx_hi=2048, temps=(1.0,),
+                    sigma=1.0, drafting="block", **_QWEN_DRAFTER),
+    # The ablation's own shape: a four-block Llama-shaped drafter (d 2048, 32 / 8 heads x
+    # 64, FFN 8192, no QK-norm, RoPE theta 5e5) for the Qwen3-8B target, blocks of 16
+    # (15 proposals).
+    "dflash_4l": Workload(name="dflash_4l", cfg_id=9, dtype="bf16", n_layers=4, d_model=2048,
+                          n_q_heads=32, n_kv_heads=8, head_dim=64, d_ffn=8192, qk_norm=0,
+                          rope_theta=5.0e5, vocab_draft=151936, vocab_target=151936,
+                          target_hidden=4096, batch=1, K=15, ctx_lo=2048, ctx_hi=2048,
+                          temps=(1.0,), sigma=1.0, drafting="block"),
 }
 
 # Parity shapes: the benchmark architectures at sizes the oracle finishes in
@@ -161,6 +180,17 @@ PARITY: Dict[str, Workload] = {
                          n_q_heads=4, n_kv_heads=1, head_dim=128, d_ffn=512, vocab_draft=3001,
                          vocab_target=4513, target_hidden=192, batch=2, K=3, ctx_lo=1, ctx_hi=16,
                          temps=(0.7,), sigma=1.5, vocab_map="inject", shuffle_blocks=True),
+    # block drafting: Llama-shaped body (no QK-norm), several sequences, mixed temperatures
+    "p_block": Workload(name="p_block", cfg_id=18, dtype="bf16", n_layers=2, d_model=256,
+                        n_q_heads=4, n_kv_heads=2, head_dim=64, d_ffn=640, qk_norm=0,
+                        rope_theta=5.0e5, vocab_draft=4001, vocab_target=4001,
+                        target_hidden=128, batch=3, K=7, ctx_lo=9, ctx_hi=40,
+                        temps=(1.0, 0.0, 0.7), sigma=0.5, shuffle_blocks=True, drafting="block"),
+    "p_block_single": Workload(name="p_block_single", cfg_id=19, dtype="bf16", n_layers=2,
+                               d_model=384, n_q_heads=4, n_kv_heads=2, head_dim=128, d_ffn=1152,
+                               vocab_draft=3001, vocab_target=4513, target_hidden=192, batch=1,
+                               K=5, ctx_lo=47, ctx_hi=47, temps=(1.0,), sigma=0.3,
+                               vocab_map="inject", shuffle_blocks=True, drafting="block"),
 }
 
 
