@@ -314,7 +314,8 @@ def main():
                                f"V_d={w.vocab_draft}, V_T={w.vocab_target}, taps 3x{w.target_hidden}, "
                                f"batch {w.batch}, context {w.ctx_lo}"
                                + (f"-{w.ctx_hi}" if w.ctx_hi != w.ctx_lo else "")
-                               + f", K={w.K}, T={list(w.temps)}",
+                               + f", K={w.K}, T={list(w.temps)}"
+                               + (", block drafting" if w.drafting == "block" else ""),
                    "batch": w.batch, "K": w.K},
         "mean_accepted_drafts": round(r["mean_accept"], 3),
         "tokens_timed": r["tokens"],
@@ -328,7 +329,9 @@ def main():
         line["us_per_verify"] = round(vf_ms * 1e3 / max(vf_n, 1), 2)
         lm_ms, lm_n = kt["lm_head"]
         lm_us = lm_ms * 1e3 / max(lm_n, 1)
-        bytes_launch = lm_head_bytes(w, w.batch)
+        block = w.drafting == "block"
+        # (block drafting: one head launch over every sequence's K block rows)
+        bytes_launch = lm_head_bytes(w, w.batch * (w.K if block else 1))
         ach = bytes_launch / (lm_us * 1e-6) / 1e9
         line["roofline"] = {"bound": "hbm", "kernel": "LM head (final RMSNorm + vocabulary GEMV "
                             "+ masked logits + softmax block statistics)",
@@ -338,9 +341,19 @@ def main():
                             "bytes_per_launch": bytes_launch, "us_per_launch": round(lm_us, 3),
                             "launches": lm_n, "timing": "HIP events on the library stream, "
                             "8 back-to-back launches per event pair"}
-        line["ar_step_algorithmic_bytes"] = int(sb["total"])
-        ar_us = ds_ms * 1e3 / max(ds_n, 1) / w.K
-        line["draft_token_hbm_frac"] = round(sb["total"] / (ar_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+        if block:
+            # a block call: the ingest pass (tap projection, body, context) and the block
+            # pass (body, context), one LM head over the block rows, the logits written
+            el = 2 if w.dtype == "bf16" else 4
+            call = (w.tap_width * w.d_model * el + 2 * (sb["body"] + sb["kv"]) + sb["lm"]
+                    + w.batch * w.K * w.vocab_draft * 4)
+            call_us = ds_ms * 1e3 / max(ds_n, 1)
+            line["draft_call_algorithmic_bytes"] = int(call)
+            line["draft_call_hbm_frac"] = round(call / (call_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+        else:
+            line["ar_step_algorithmic_bytes"] = int(sb["total"])
+            ar_us = ds_ms * 1e3 / max(ds_n, 1) / w.K
+            line["draft_token_hbm_frac"] = round(sb["total"] / (ar_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
         line["tree_verify"] = r["tree_verify"]
         if "tree_draft" in r:
             line["tree_draft"] = r["tree_draft"]

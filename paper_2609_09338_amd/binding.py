@@ -161,7 +161,9 @@ class Drafter:
     # -- the step ---------------------------------------------------------------------
     def draft_step(self, slots, K: int, taps, temperature, u_draft=None, n_new=None,
                    new_tokens=None, taps_stride: int = 0, draft_tokens=None,
-                   draft_logits=None) -> None:
+                   draft_logits=None, mask_token=None) -> None:
+        """Ingest the new rows and propose K drafts: a chain of K steps
+        (osprey_draft_step), or one block (osprey_draft_block) when mask_token is given."""
         torch, c = self.torch, self.cfg
         B = len(slots)
         tap_w = c.n_taps * c.target_hidden
@@ -189,7 +191,10 @@ class Drafter:
         a.u_draft = _ptr(u_draft)
         a.draft_tokens = _ptr(draft_tokens)
         a.draft_logits = _ptr(draft_logits)
-        _check(_lib().osprey_draft_step(self.h, C.byref(a)))
+        if mask_token is None:
+            _check(_lib().osprey_draft_step(self.h, C.byref(a)))
+        else:
+            _check(_lib().osprey_draft_block(self.h, C.byref(a), int(mask_token)))
 
     def draft_tree(self, slots, topk: int, depth: int, n_nodes: int, taps, temperature,
                    tokens, parents, n_new, new_tokens, taps_stride: int = 0,

@@ -95,6 +95,9 @@ struct Ws {
   double* c_score;
   int32_t *r_tok, *r_pos, *r_attpos, *r_node, *r_anc;  // [B * kMaxTopk] (r_anc x kMaxTreeDepth)
   int32_t* r_cu;                                       // [B + 1]
+  // block drafting: the block pass's rows [B * Km]
+  int32_t *b_seq, *b_tok, *b_pos, *b_skip, *b_cu;
+  float *b_temp, *b_s;
   float* r_s;                 // [B * kMaxTopk][d]
   float* ones;                // [B * kMaxTopk] temperature 1 for the tree's LM-head records
 };
@@ -179,7 +182,8 @@ size_t plan(const osprey_config& c, char* base, Ws* w) {
     W.split_s2 = (float*)take(4L * rs * need);
   }
   W.logits = (float*)take(4L * D.B * D.Km * c.vocab_draft);
-  W.lm_part = (float*)take(16L * D.B * kMaxTopk * D.lm_nblk_max);   // (draft trees: B x k rows)
+  // (draft trees: B x k rows; blocks: B x K rows)
+  W.lm_part = (float*)take(16L * D.B * std::max<long>(kMaxTopk, D.Km) * D.lm_nblk_max);
   W.qstat = (QStat*)take(sizeof(QStat) * D.B * D.Km);
   W.drafts = (int32_t*)take(4L * D.B * D.Km);
   W.u_zero = (float*)take(4L * D.B * D.Km);
@@ -208,6 +212,16 @@ size_t plan(const osprey_config& c, char* base, Ws* w) {
     W.r_anc = (int32_t*)take(4L * rows * kMaxTreeDepth);
     W.r_s = (float*)take(4L * rows * d);
     W.ones = (float*)take(4L * rows);
+  }
+  {
+    const long rows = (long)D.B * D.Km;
+    W.b_seq = (int32_t*)take(4L * rows);
+    W.b_tok = (int32_t*)take(4L * rows);
+    W.b_pos = (int32_t*)take(4L * rows);
+    W.b_skip = (int32_t*)take(4L * rows);
+    W.b_temp = (float*)take(4L * rows);
+    W.b_cu = (int32_t*)take(4L * (D.B + 1));
+    W.b_s = (float*)take(4L * rows * d);
   }
   W.v_res = (double*)take(16L * D.B * D.nchunk_t);
   W.vstate = (int32_t*)take(16L * D.B);
@@ -490,7 +504,8 @@ struct TreePass {
 
 void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, const float* s_src,
                  int ks_taps, const SplitPlan& sp, int rows_per_seq, int slot0,
-                 const TreePass* tree = nullptr) {
+                 const TreePass* tree = nullptr, const int32_t* kv_skip = nullptr,
+                 bool keep_s = false) {
   const osprey_config& c = h->cfg;
   const Ws& W = h->W;
   // passes of at most kLmMaxRows rows stream the weights once with the inputs
@@ -523,6 +538,7 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     p.embed = h->w.embed;
     p.tok = rows.tok;
     p.vocab_embed = c.vocab_target;
+    p.s_out = keep_s ? W.s : nullptr;
     launch_rows_prep(p, h->stream);
   }
   GemvArgs gb{};
@@ -550,6 +566,7 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     a.rows = rows;
     a.cu = cu;
     a.bslot = tree ? tree->bslot : W.bslot;
+    a.kv_skip = kv_skip;
     a.slot0 = (B == 1 && !tree) ? slot0 : -1;
     a.B = B;
     a.rows_per_seq = rows_per_seq;
@@ -751,10 +768,11 @@ void run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, cons
   launch_sample(s, h->stream);
 }
 
-// LM head over `rows` rows of a draft-tree pass (gathered from the ingest rows for the
-// root), logits row r at W.logits + r V, records at temperature 1.  Returns the records
-// per row.
-int run_head_tree(osprey_handle* h, int rows, const int32_t* gather) {
+// LM head over `rows` rows (gathered through `gather`, else rows 0.. of the body's
+// output), logits row r at y + r V, softmax records at the rows' temperatures `temp`
+// (W.lm_part, nblk per row).  Draft trees: rows of a pass at temperature 1 into
+// W.logits; blocks: a block's rows into the draft logits.  Returns the head's plan.
+LmPlan run_head_rows(osprey_handle* h, int rows, const int32_t* gather, const float* temp, float* y) {
   const osprey_config& c = h->cfg;
   const Ws& W = h->W;
   const bool prepared = gemm_use_mfma(c.dtype, rows);
@@ -774,22 +792,31 @@ int run_head_tree(osprey_handle* h, int rows, const int32_t* gather) {
   g.ld_logits = c.vocab_draft;
   g.d2t = h->w.d2t;
   g.nblk = lp.nblk;
-  for (int r0 = 0; r0 < rows; r0 += kLmMaxRows) {
-    GemvArgs p = g;
-    p.max_rows = std::min(kLmMaxRows, rows - r0);
-    if (gather) {
-      p.gather = gather + r0;
-    } else {
-      p.xa_hi = W.xa_hi + (long)r0 * c.d_model;
-      p.xa_lo = W.xa_lo + (long)r0 * c.d_model;
-      p.xin = W.x + (long)r0 * c.d_model;
+  const int t = h->t_begin(0);
+  const int reps = t >= 0 ? kTimedRepeats : 1;
+  for (int rep = 0; rep < reps; ++rep) {
+    for (int r0 = 0; r0 < rows; r0 += kLmMaxRows) {
+      GemvArgs p = g;
+      p.max_rows = std::min(kLmMaxRows, rows - r0);
+      if (gather) {
+        p.gather = gather + r0;
+      } else {
+        p.xa_hi = W.xa_hi + (long)r0 * c.d_model;
+        p.xa_lo = W.xa_lo + (long)r0 * c.d_model;
+        p.xin = W.x + (long)r0 * c.d_model;
+      }
+      p.y = y + (long)r0 * c.vocab_draft;
+      p.temp = temp + r0;
+      p.part = W.lm_part + (long)r0 * lp.nblk * 4;
+      launch_lm_head(p, lp, !prepared, h->stream);
     }
-    p.y = W.logits + (long)r0 * c.vocab_draft;
-    p.temp = W.ones + r0;
-    p.part = W.lm_part + (long)r0 * lp.nblk * 4;
-    launch_lm_head(p, lp, !prepared, h->stream);
   }
-  return lp.nblk;
+  h->t_end(t, reps);
+  return lp;
+}
+
+int run_head_tree(osprey_handle* h, int rows, const int32_t* gather) {
+  return run_head_rows(h, rows, gather, h->W.ones, h->W.logits).nblk;
 }
 
 void fill_verify_common(osprey_handle* h, VerifyArgs& v, int B, int K) {
@@ -982,11 +1009,12 @@ OSPREY_API int osprey_seq_length(osprey_handle* h, int32_t slot, int32_t* length
 namespace {
 
 // Validation, row layout and ingest of a draft call: the new rows of every sequence
-// through the tap projection (Eq. 1) and the body.  K: the chain's drafts (the setup
+// through the tap projection (Eq. 1) and the body (keep_s: their conditioning inputs
+// also kept in fp32 at W.s, as the vector path leaves them).  K: the chain's drafts (the setup
 // kernel's autoregressive positions); extra: positions past the ingest the call will
 // use (chain: K - 1; tree: its depth).
 int step_ingest(osprey_handle* h, const osprey_step_args* a, int K, int extra, SplitPlan& split,
-                bool& pending, int& tt, int max_split = kMaxSplit) {
+                bool& pending, int& tt, int max_split = kMaxSplit, bool keep_s = false) {
   int rc;
   const osprey_config& c = h->cfg;
   const int B = a->batch;
@@ -1090,7 +1118,7 @@ int step_ingest(osprey_handle* h, const osprey_step_args* a, int K, int extra, S
     } else {
       ks_taps = launch_gemm(SRC_TAPS, EPI_STORE, gt, h->stream);
     }
-    run_body_mr(h, ing, W.cu, B, nullptr, ks_taps, split, max_new, a->slots[0]);
+    run_body_mr(h, ing, W.cu, B, nullptr, ks_taps, split, max_new, a->slots[0], nullptr, nullptr, keep_s);
   } else {
     launch_gemv(c.dtype, SRC_TAPS, EPI_STORE, gt, h->stream);
     run_body(h, ing, W.cu, B, W.s, true, split, max_new, a->slots[0]);
@@ -1147,6 +1175,79 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
   h->last_slots.assign(a->slots, a->slots + B);
   h->last_logits = logits;
   h->last_ld_b = ld_b;
+  return ok();
+}
+
+OSPREY_API int osprey_draft_block(osprey_handle* h, const osprey_step_args* a, int32_t mask_token) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (!a) return fail(OSPREY_E_INVALID, "args is NULL");
+  const osprey_config& c = h->cfg;
+  const int B = a->batch, K = a->K;
+  if (B < 1 || B > c.max_batch) return fail(OSPREY_E_INVALID, "batch %d not in [1, %d]", B, c.max_batch);
+  if (K < 2 || K > c.max_k) return fail(OSPREY_E_INVALID, "K %d not in [2, %d] (one proposal is osprey_draft_step's first)", K, c.max_k);
+  if (c.dtype != OSPREY_BF16) return fail(OSPREY_E_UNSUPPORTED, "block drafting needs bf16 weights (the matrix-core body)");
+  if (mask_token < 0 || mask_token >= c.vocab_target)
+    return fail(OSPREY_E_INVALID, "mask_token %d not in [0, %d)", mask_token, c.vocab_target);
+  SplitPlan split;
+  bool pending;
+  int tt;
+  if ((rc = step_ingest(h, a, K, K - 1, split, pending, tt, kMaxSplit, true))) return rc;
+  const Ws& W = h->W;
+  // ---- the block pass: every sequence's anchor and K - 1 mask rows ----------------------
+  BlockArgs ba{};
+  ba.B = B;
+  ba.K = K;
+  ba.d = c.d_model;
+  ba.mask = mask_token;
+  ba.last_row = W.last_row;
+  ba.ing_tok = W.ing_tok;
+  ba.committed = W.committed;
+  ba.s = W.s;
+  ba.temp = a->temperature;
+  ba.r_seq = W.b_seq;
+  ba.r_tok = W.b_tok;
+  ba.r_pos = W.b_pos;
+  ba.r_skip = W.b_skip;
+  ba.r_temp = W.b_temp;
+  ba.r_cu = W.b_cu;
+  ba.r_s = W.b_s;
+  launch_block_rows(ba, h->stream);
+  const int rows = B * K;
+  RowMeta rm{W.b_seq, W.b_pos, W.b_tok, nullptr, rows};
+  run_body_mr(h, rm, W.b_cu, B, W.b_s, 1, split, K, a->slots[0], nullptr, W.b_skip);
+  // ---- LM head over the block's rows, then one pick per (sequence, proposal) ------------
+  float* logits = a->draft_logits ? a->draft_logits : W.logits;
+  const LmPlan lp = run_head_rows(h, rows, nullptr, W.b_temp, logits);
+  SampleArgs sm{};
+  sm.block = 1;
+  sm.B = B;
+  sm.K = K;
+  sm.logits = logits;
+  sm.ld_logits = (long)K * c.vocab_draft;
+  sm.V = c.vocab_draft;
+  sm.part = W.lm_part;
+  sm.nblk = lp.nblk;
+  sm.blk_rows = lp.blk_rows;
+  sm.temp = a->temperature;
+  sm.u = a->u_draft ? a->u_draft : W.u_zero;
+  sm.d2t = h->w.d2t;
+  sm.drafts = W.drafts;
+  sm.ld_drafts = h->D.Km;
+  sm.drafts_out = a->draft_tokens;
+  sm.committed = W.committed;
+  sm.d = 0;
+  sm.qstat = W.qstat;
+  sm.ld_qstat = h->D.Km;
+  launch_sample(sm, h->stream);
+  h->t_end(tt);
+  if ((rc = hip_last())) return rc;
+  step_commit(h, a, pending, K);
+  h->last_B = B;
+  h->last_K = K;
+  h->last_slots.assign(a->slots, a->slots + B);
+  h->last_logits = logits;
+  h->last_ld_b = K;
   return ok();
 }
 

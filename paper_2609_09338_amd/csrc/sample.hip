@@ -27,9 +27,11 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
   __shared__ double s_before;
   __shared__ int s_blk, s_row;
 
-  const float* part = a.part + (long)b * a.nblk * 4;
+  const int k = a.block ? (int)blockIdx.y : a.k;  // (block drafting: proposal k of sequence b)
+  const int prow = a.block ? b * a.K + k : b;     // its records' and logits' row
+  const float* part = a.part + (long)prow * a.nblk * 4;
   const float T = a.temp[b];
-  const float u = a.u[(long)b * a.K + a.k];
+  const float u = a.u[(long)b * a.K + k];
   // the hidden state fed back to the next step does not depend on the pick: read it
   // now, with the records, so its load is not one more round trip at the end
   constexpr int kFbPer = 4;            // d <= kSampleThreads * 4 * kFbPer
@@ -135,7 +137,7 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
       constexpr int kScanPre = 2;
       const int r0 = s_blk * a.blk_rows;
       const int r1 = min(r0 + a.blk_rows, a.V);
-      const float* lg = a.logits + (long)b * a.ld_logits;
+      const float* lg = a.logits + (long)b * a.ld_logits + (a.block ? (long)k * a.V : 0L);
       float pre[kScanPre];
 #pragma unroll
       for (int q = 0; q < kScanPre; ++q) {
@@ -167,12 +169,14 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
   row = min(max(row, 0), a.V - 1);
   const int d = a.d2t[row];
   if (tid == 0) {
-    a.drafts[(long)b * a.ld_drafts + a.k] = d;
-    if (a.drafts_out) a.drafts_out[(long)b * a.K + a.k] = d;
-    a.ar_tok[b] = d;
-    a.ar_pos[b] = a.committed[b] + a.k;
+    a.drafts[(long)b * a.ld_drafts + k] = d;
+    if (a.drafts_out) a.drafts_out[(long)b * a.K + k] = d;
+    if (!a.block) {
+      a.ar_tok[b] = d;
+      a.ar_pos[b] = a.committed[b] + k;
+    }
     // the row's statistics, for the verification of this draft
-    if (a.qstat) a.qstat[(long)b * a.ld_qstat + a.k] = QStat{S, M, am == 0x7fffffff ? -1 : am};
+    if (a.qstat) a.qstat[(long)b * a.ld_qstat + k] = QStat{S, M, am == 0x7fffffff ? -1 : am};
   }
 #pragma unroll
   for (int q = 0; q < kFbPer; ++q) {
@@ -182,7 +186,7 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
 }
 
 void launch_sample(const SampleArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(k_sample, dim3(a.B), dim3(kSampleThreads), 0, st, a);
+  hipLaunchKernelGGL(k_sample, dim3(a.B, a.block ? a.K : 1), dim3(kSampleThreads), 0, st, a);
 }
 
 }  // namespace osp

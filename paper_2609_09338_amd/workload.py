@@ -146,15 +146,16 @@ def alloc_outputs(s: Setup) -> IterOutputs:
 def draft(s: Setup, it: int, inp: IterInputs, out: IterOutputs) -> None:
     w = s.w
     slots = list(range(w.batch))
+    mask = synth.mask_token(w) if w.drafting == "block" else None
     if it == 0:
         s.drafter.draft_step(slots, w.K, inp.taps, s.draft_temperature, inp.u_draft,
                              n_new=[1] * w.batch, new_tokens=inp.new_tokens,
                              taps_stride=w.K + 1, draft_tokens=out.drafts,
-                             draft_logits=out.logits)
+                             draft_logits=out.logits, mask_token=mask)
     else:
         s.drafter.draft_step(slots, w.K, inp.taps, s.draft_temperature, inp.u_draft,
                              taps_stride=w.K + 1, draft_tokens=out.drafts,
-                             draft_logits=out.logits)
+                             draft_logits=out.logits, mask_token=mask)
 
 
 def verify(s: Setup, inp: IterInputs, target_logits, out: IterOutputs) -> None:

@@ -6,8 +6,10 @@
 * whole draft -> verify iterations on the parity workloads (ragged
   vocabularies, partial and injective vocabulary maps, shuffled KV pages,
   contexts straddling page boundaries, greedy and sampled requests in one
-  batch): drafter logits within 2e-2 (bf16) / 1e-4 (fp32), draft ids and
-  verification outcomes bit-exact unless flagged (see tests/parity.py);
+  batch), chains and blocks (the anchor and mask rows of block drafting, a
+  Llama-shaped body without QK-norm): drafter logits within 2e-2 (bf16) / 1e-4
+  (fp32), draft ids and verification outcomes bit-exact unless flagged (see
+  tests/parity.py);
 * the zero-initialised expansion (Eq. 3) on the GPU: logits independent of the
   taps, bit for bit.
 """
@@ -183,7 +185,8 @@ def _run_parity(w, n_iters, seqs, tol):
 
 
 @pytest.mark.parametrize("name", ["p_tiny_f32", "p_qwen_small", "p_partial", "p_inject",
-                                  "p_greedy_draft", "p_single64", "p_single128"])
+                                  "p_greedy_draft", "p_single64", "p_single128", "p_block",
+                                  "p_block_single"])
 def test_iterations_match_oracle(name):
     _require_gpu()
     w = synth.get(name)
@@ -259,7 +262,8 @@ def test_runs_are_deterministic_and_page_order_free():
 # ----------------------------------------------------------------------------------------
 @pytest.mark.parametrize("name,seqs,iters", [("c2", [0], 2), ("c2g", [0], 2), ("c3", [7], 2),
                                              ("c4", [31], 1), ("c5", [62, 63], 2),
-                                             ("osprey_2l", [0], 2)])
+                                             ("osprey_2l", [0], 2), ("c2b", [0], 2),
+                                             ("dflash_4l", [0], 2)])
 def test_full_size_sampled_sequences_match_oracle(name, seqs, iters):
     """Benchmark-size shapes in the launch configuration the benchmark uses; the oracle
     follows the sampled sequences one by one (sequences of a batch are independent)."""
