@@ -324,17 +324,20 @@ int osprey_draft_step(osprey_handle* h, const osprey_step_args* a);
 int osprey_draft_tree(osprey_handle* h, const osprey_step_args* a, const osprey_tree_args* t);
 
 /* Block drafting (the EAGLE-style target interface of the DFlash ablation, appendix):
- * ingest the new rows as osprey_draft_step does (the last new token of a sequence is
- * its block's anchor), then run one pass of the drafter over every anchor and K - 1
- * mask rows (token mask_token at positions committed .. committed + K - 2), each with
- * the anchor's conditioning input (the target feature is taken once at the anchor and
- * broadcast), attending causally to the cache; draft k is drawn from block row k's
- * logits (row 0: the anchor) at temperature[b] with u_draft[b][k], independently of
- * the other drafts.  The mask rows' cache entries lie past the committed length and
- * are rolled back like the chain's draft positions.  Arguments, outputs (draft_tokens,
- * draft_logits [batch][K][V_d]), state transitions and the following osprey_verify
- * are those of osprey_draft_step with K drafts.  Limits: 2 <= K <= max_k; bf16
- * weights; 0 <= mask_token < vocab_target (else OSPREY_E_INVALID, nothing enqueued). */
+ * the new rows are ingested as osprey_draft_step does (the last new token of a
+ * sequence is its block's anchor) and, in the same pass of the drafter, K - 1 mask
+ * rows follow each sequence's new rows (token mask_token at positions committed ..
+ * committed + K - 2), each with the anchor's conditioning input (the target feature
+ * is taken once at the anchor and broadcast), attending causally to the cache; draft
+ * k is drawn from block row k's logits (row 0: the anchor) at temperature[b] with
+ * u_draft[b][k], independently of the other drafts.  The mask rows' cache entries lie
+ * past the committed length and are rolled back like the chain's draft positions.
+ * Arguments, outputs (draft_tokens, draft_logits [batch][K][V_d]), state transitions
+ * and the following osprey_verify are those of osprey_draft_step with K drafts.
+ * A pass holds sum_b (n_b + K - 1) rows: the workspace must hold them (the config's
+ * max_new_rows >= batch x 2 max_k covers pending steps), else OSPREY_E_CAPACITY.
+ * Limits: 2 <= K <= max_k; bf16 weights; 0 <= mask_token < vocab_target (else
+ * OSPREY_E_INVALID, nothing enqueued). */
 int osprey_draft_block(osprey_handle* h, const osprey_step_args* a, int32_t mask_token);
 
 /* Verify the last drafts (see osprey_verify_args).  State: DRAFTED -> VERIFIED. */

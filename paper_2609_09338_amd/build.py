@@ -21,7 +21,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libosprey.so")
 SOURCES = ["gemv.hip", "gemv_taps.hip", "gemv_qkv.hip", "gemv_resid.hip", "gemv_swiglu.hip",
            "gemv_logits.hip", "gemm_mfma.hip", "skinny.hip", "rows.hip", "attention.hip", "sample.hip", "verify.hip",
-           "state.hip", "tree.hip", "block.hip", "osprey.cpp"]
+           "state.hip", "tree.hip", "osprey.cpp"]
 ARCH = "gfx950"
 
 

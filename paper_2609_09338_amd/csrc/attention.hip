@@ -632,7 +632,6 @@ __global__ void __launch_bounds__(256) k_rows_qkv(AttnArgs a, float* q_out) {
     return;
   }
   const int g = hh - a.nq;
-  if (a.kv_skip && a.kv_skip[r]) return;          // (already in the cache)
   const long ko = (long)r * a.qkv_w + (long)(a.nq + g) * HD;
   const long vo = (long)r * a.qkv_w + (long)(a.nq + a.nkv + g) * HD;
   float k1 = lane < HALF ? qkv_at(a, ko + lane) : 0.f, k2 = lane < HALF ? qkv_at(a, ko + lane + HALF) : 0.f;

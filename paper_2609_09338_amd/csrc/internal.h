@@ -140,7 +140,6 @@ struct RowArgs {
   const float* s_src;       // conditioning rows (nullable: summed from part)
   uint16_t* s_hi;
   uint16_t* s_lo;
-  float* s_out;             // the conditioning rows in fp32 as well (nullable)
   const void* embed;
   const int32_t* tok;
   int vocab_embed;
@@ -210,9 +209,6 @@ struct AttnArgs {
   const int32_t* tree_pos;
   void* tree_kv;            // [slot][n_layers][2][nkv][hd], bf16
   int tree_slots;           // slots of tree_kv
-  // rows whose keys/values are already in the cache (nullable): kv_skip[r] != 0
-  // leaves the cache untouched (a block's anchor, ingested before the block)
-  const int32_t* kv_skip;
 };
 void launch_attention(int kvdtype, const AttnArgs& a, hipStream_t st);
 // Matrix-core path: per row, sum the QKV split partials, normalise and rotate q
@@ -261,25 +257,6 @@ struct SampleArgs {
 };
 void launch_sample(const SampleArgs& a, hipStream_t st);
 
-// Block drafting: the rows of the block pass (sequence b's rows b K + j: the anchor,
-// then K - 1 mask rows), from the ingest's last row of every sequence.
-struct BlockArgs {
-  int B, K, d;
-  int32_t mask;             // mask token (target id)
-  const int32_t* last_row;  // [B] the anchor's ingest row
-  const int32_t* ing_tok;   // ingest rows' tokens
-  const int32_t* committed; // [B] committed length (the anchor at committed - 1)
-  const float* s;           // ingest rows' conditioning inputs [rows][d] fp32
-  const float* temp;        // [B]
-  int32_t* r_seq;           // [B K] the row's sequence (its cache slot)
-  int32_t* r_tok;
-  int32_t* r_pos;
-  int32_t* r_skip;
-  float* r_temp;
-  int32_t* r_cu;            // [B + 1]
-  float* r_s;               // [B K][d]
-};
-void launch_block_rows(const BlockArgs& a, hipStream_t st);
 
 // Step setup.
 constexpr int kMaxBatch = 256;
@@ -316,6 +293,14 @@ struct SetupArgs {
   int32_t* attn_items;      // [B * n_split]: b | split << 16
   int32_t* attn_n_items;
   uint32_t* err;
+  // block drafting (extra > 0): every sequence's rows are its new tokens, then `extra`
+  // mask rows at the following positions with the anchor's (last new row's) tap row;
+  // blk_gather[b (extra + 1) + k] is the anchor's row + k, blk_temp its temperature
+  int extra;
+  int32_t mask;
+  const float* temp;        // [B]
+  int32_t* blk_gather;
+  float* blk_temp;
 };
 void launch_setup(const SetupArgs& a, hipStream_t st);
 

@@ -95,9 +95,9 @@ struct Ws {
   double* c_score;
   int32_t *r_tok, *r_pos, *r_attpos, *r_node, *r_anc;  // [B * kMaxTopk] (r_anc x kMaxTreeDepth)
   int32_t* r_cu;                                       // [B + 1]
-  // block drafting: the block pass's rows [B * Km]
-  int32_t *b_seq, *b_tok, *b_pos, *b_skip, *b_cu;
-  float *b_temp, *b_s;
+  // block drafting: the block rows [B * Km] (the anchor's row + k) and temperatures
+  int32_t* b_gather;
+  float* b_temp;
   float* r_s;                 // [B * kMaxTopk][d]
   float* ones;                // [B * kMaxTopk] temperature 1 for the tree's LM-head records
 };
@@ -215,13 +215,8 @@ size_t plan(const osprey_config& c, char* base, Ws* w) {
   }
   {
     const long rows = (long)D.B * D.Km;
-    W.b_seq = (int32_t*)take(4L * rows);
-    W.b_tok = (int32_t*)take(4L * rows);
-    W.b_pos = (int32_t*)take(4L * rows);
-    W.b_skip = (int32_t*)take(4L * rows);
+    W.b_gather = (int32_t*)take(4L * rows);
     W.b_temp = (float*)take(4L * rows);
-    W.b_cu = (int32_t*)take(4L * (D.B + 1));
-    W.b_s = (float*)take(4L * rows * d);
   }
   W.v_res = (double*)take(16L * D.B * D.nchunk_t);
   W.vstate = (int32_t*)take(16L * D.B);
@@ -504,8 +499,7 @@ struct TreePass {
 
 void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, const float* s_src,
                  int ks_taps, const SplitPlan& sp, int rows_per_seq, int slot0,
-                 const TreePass* tree = nullptr, const int32_t* kv_skip = nullptr,
-                 bool keep_s = false) {
+                 const TreePass* tree = nullptr) {
   const osprey_config& c = h->cfg;
   const Ws& W = h->W;
   // passes of at most kLmMaxRows rows stream the weights once with the inputs
@@ -538,7 +532,6 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     p.embed = h->w.embed;
     p.tok = rows.tok;
     p.vocab_embed = c.vocab_target;
-    p.s_out = keep_s ? W.s : nullptr;
     launch_rows_prep(p, h->stream);
   }
   GemvArgs gb{};
@@ -566,7 +559,6 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     a.rows = rows;
     a.cu = cu;
     a.bslot = tree ? tree->bslot : W.bslot;
-    a.kv_skip = kv_skip;
     a.slot0 = (B == 1 && !tree) ? slot0 : -1;
     a.B = B;
     a.rows_per_seq = rows_per_seq;
@@ -1009,12 +1001,13 @@ OSPREY_API int osprey_seq_length(osprey_handle* h, int32_t slot, int32_t* length
 namespace {
 
 // Validation, row layout and ingest of a draft call: the new rows of every sequence
-// through the tap projection (Eq. 1) and the body (keep_s: their conditioning inputs
-// also kept in fp32 at W.s, as the vector path leaves them).  K: the chain's drafts (the setup
+// through the tap projection (Eq. 1) and the body.  K: the chain's drafts (the setup
 // kernel's autoregressive positions); extra: positions past the ingest the call will
-// use (chain: K - 1; tree: its depth).
+// use (chain: K - 1; tree: its depth).  block_mask >= 0 (block drafting): extra mask
+// rows (token block_mask, the anchor's tap row) follow every sequence's new rows in
+// the same pass.
 int step_ingest(osprey_handle* h, const osprey_step_args* a, int K, int extra, SplitPlan& split,
-                bool& pending, int& tt, int max_split = kMaxSplit, bool keep_s = false) {
+                bool& pending, int& tt, int max_split = kMaxSplit, int block_mask = -1) {
   int rc;
   const osprey_config& c = h->cfg;
   const int B = a->batch;
@@ -1046,7 +1039,7 @@ int step_ingest(osprey_handle* h, const osprey_step_args* a, int K, int extra, S
     const long need = s.len_max + n + extra;
     if (need > (long)s.nblocks * c.kv_block || need > c.max_seq_len)
       return fail(OSPREY_E_CAPACITY, "slot %d: up to %ld positions exceed its %d pages / max_seq_len", slot, need, s.nblocks);
-    rows += n;
+    rows += n + (block_mask >= 0 ? extra : 0);
     max_new = std::max(max_new, n);
     ctx_max = std::max(ctx_max, need);
     ctx_total += need;
@@ -1094,6 +1087,13 @@ int step_ingest(osprey_handle* h, const osprey_step_args* a, int K, int extra, S
   sa.split_len = split.split_len;
   sa.attn_items = W.attn_items;
   sa.attn_n_items = W.attn_n_items;
+  if (block_mask >= 0) {
+    sa.extra = extra;
+    sa.mask = block_mask;
+    sa.temp = a->temperature;
+    sa.blk_gather = W.b_gather;
+    sa.blk_temp = W.b_temp;
+  }
   launch_setup(sa, h->stream);
 
   // ---- ingest: tap projection (Eq. 1) then the body over every new row ------------------
@@ -1118,7 +1118,7 @@ int step_ingest(osprey_handle* h, const osprey_step_args* a, int K, int extra, S
     } else {
       ks_taps = launch_gemm(SRC_TAPS, EPI_STORE, gt, h->stream);
     }
-    run_body_mr(h, ing, W.cu, B, nullptr, ks_taps, split, max_new, a->slots[0], nullptr, nullptr, keep_s);
+    run_body_mr(h, ing, W.cu, B, nullptr, ks_taps, split, max_new + (block_mask >= 0 ? extra : 0), a->slots[0]);
   } else {
     launch_gemv(c.dtype, SRC_TAPS, EPI_STORE, gt, h->stream);
     run_body(h, ing, W.cu, B, W.s, true, split, max_new, a->slots[0]);
@@ -1192,33 +1192,13 @@ OSPREY_API int osprey_draft_block(osprey_handle* h, const osprey_step_args* a, i
   SplitPlan split;
   bool pending;
   int tt;
-  if ((rc = step_ingest(h, a, K, K - 1, split, pending, tt, kMaxSplit, true))) return rc;
+  // the ingest and the block in one pass: every sequence's new rows, then K - 1 mask rows
+  if ((rc = step_ingest(h, a, K, K - 1, split, pending, tt, kMaxSplit, mask_token))) return rc;
   const Ws& W = h->W;
-  // ---- the block pass: every sequence's anchor and K - 1 mask rows ----------------------
-  BlockArgs ba{};
-  ba.B = B;
-  ba.K = K;
-  ba.d = c.d_model;
-  ba.mask = mask_token;
-  ba.last_row = W.last_row;
-  ba.ing_tok = W.ing_tok;
-  ba.committed = W.committed;
-  ba.s = W.s;
-  ba.temp = a->temperature;
-  ba.r_seq = W.b_seq;
-  ba.r_tok = W.b_tok;
-  ba.r_pos = W.b_pos;
-  ba.r_skip = W.b_skip;
-  ba.r_temp = W.b_temp;
-  ba.r_cu = W.b_cu;
-  ba.r_s = W.b_s;
-  launch_block_rows(ba, h->stream);
   const int rows = B * K;
-  RowMeta rm{W.b_seq, W.b_pos, W.b_tok, nullptr, rows};
-  run_body_mr(h, rm, W.b_cu, B, W.b_s, 1, split, K, a->slots[0], nullptr, W.b_skip);
   // ---- LM head over the block's rows, then one pick per (sequence, proposal) ------------
   float* logits = a->draft_logits ? a->draft_logits : W.logits;
-  const LmPlan lp = run_head_rows(h, rows, nullptr, W.b_temp, logits);
+  const LmPlan lp = run_head_rows(h, rows, W.b_gather, W.b_temp, logits);
   SampleArgs sm{};
   sm.block = 1;
   sm.B = B;

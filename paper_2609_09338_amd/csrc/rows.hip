@@ -74,7 +74,6 @@ __global__ void __launch_bounds__(kRowThreads) k_rows_prep(RowArgs a) {
     const float4 v = a.s_src ? *reinterpret_cast<const float4*>(a.s_src + (long)r * a.W + c)
                              : sum_parts4(a, r, c);
     store_pair4(a.s_hi, a.s_lo, (long)r * a.W + c, v);
-    if (a.s_out) *reinterpret_cast<float4*>(a.s_out + (long)r * a.W + c) = v;
   }
   // token segment: x = embed[tok], then its normalised copy
   int t = a.tok[r];

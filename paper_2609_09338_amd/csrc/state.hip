@@ -28,21 +28,27 @@ __global__ void __launch_bounds__(kSetupThreads) k_setup(SetupArgs a) {
       n = min(max(n, 1), a.max_new);
     }
   }
-  // exclusive prefix of n over the batch (integer scan: wave scan + wave totals)
-  int inc = n;
+  // block drafting: the block's mask rows follow the sequence's new rows
+  const int m = act ? a.extra : 0;
+  // exclusive prefixes over the batch (integer scans: wave scan + wave totals) of the
+  // rows (n + m) and of the new rows alone (packed tap rows)
+  int inc = n + m, incn = n;
 #pragma unroll
   for (int s = 1; s < 64; s <<= 1) {
     const int o = __shfl_up(inc, s, OSP_WAVE);
-    if (lane >= s) inc += o;
+    const int on = __shfl_up(incn, s, OSP_WAVE);
+    if (lane >= s) { inc += o; incn += on; }
   }
-  if (lane == 63) s_tot[wave] = inc;
+  __shared__ int s_totn[4];
+  if (lane == 63) { s_tot[wave] = inc; s_totn[wave] = incn; }
   __syncthreads();
-  int before = 0, total = 0;
+  int before = 0, total = 0, beforen = 0;
   for (int w = 0; w < kSetupThreads / 64; ++w) {
-    if (w < wave) before += s_tot[w];
+    if (w < wave) { before += s_tot[w]; beforen += s_totn[w]; }
     total += s_tot[w];
   }
-  const int cu = before + inc - n;
+  const int cu = before + inc - (n + m);
+  const int cun = beforen + incn - n;
   if (act) {
     a.cu[b] = cu;
     a.last_row[b] = cu + n - 1;
@@ -51,7 +57,7 @@ __global__ void __launch_bounds__(kSetupThreads) k_setup(SetupArgs a) {
     a.ar_pos[b] = len + n;
     for (int j = 0; j < n; ++j) {
       const int r = cu + j;
-      int t = a.explicit_rows ? a.new_tokens[r] : a.pend_tok[(long)slot * a.pend_ld + j];
+      int t = a.explicit_rows ? a.new_tokens[cun + j] : a.pend_tok[(long)slot * a.pend_ld + j];
       if (t < 0 || t >= a.V_T) {
         atomicOr(a.err, 1u << 1);
         t = min(max(t, 0), a.V_T - 1);
@@ -59,7 +65,22 @@ __global__ void __launch_bounds__(kSetupThreads) k_setup(SetupArgs a) {
       a.ing_seq[r] = b;
       a.ing_pos[r] = len + j;
       a.ing_tok[r] = t;
-      a.ing_tap[r] = a.taps_stride > 0 ? b * a.taps_stride + j : r;
+      a.ing_tap[r] = a.taps_stride > 0 ? b * a.taps_stride + j : cun + j;
+    }
+    // the block's mask rows: the anchor's tap row (its conditioning input, broadcast)
+    const int anchor_tap = a.taps_stride > 0 ? b * a.taps_stride + n - 1 : cun + n - 1;
+    for (int j = 0; j < m; ++j) {
+      const int r = cu + n + j;
+      a.ing_seq[r] = b;
+      a.ing_pos[r] = len + n + j;
+      a.ing_tok[r] = a.mask;
+      a.ing_tap[r] = anchor_tap;
+    }
+    if (m > 0) {
+      for (int k = 0; k <= m; ++k) {
+        a.blk_gather[b * (m + 1) + k] = cu + n - 1 + k;
+        a.blk_temp[b * (m + 1) + k] = a.temp[b];
+      }
     }
     const int cap = a.slot_nblocks[slot] * a.kv_block;
     if (len + n + (a.K > 0 ? a.K - 1 : 0) > cap) atomicOr(a.err, 1u << 2);

@@ -63,7 +63,9 @@ def make_drafter(w, n_iters: int, device="cuda:0", weights=None) -> Setup:
                       qk_norm=w.qk_norm, rms_eps=w.rms_eps, rope_theta=w.rope_theta,
                       max_batch=w.batch, max_k=w.K, max_seq_len=max(caps),
                       kv_block=w.kv_block, kv_num_blocks=int(sum(nblk)),
-                      max_new_rows=max(prefill_rows, w.batch * (w.K + 1)))
+                      # (block drafting: new rows and the block's mask rows in one pass)
+                      max_new_rows=max(prefill_rows, w.batch * (w.K + 1),
+                                       w.batch * 2 * w.K if w.drafting == "block" else 0))
     tw = {k: to_dev(v, w, device) for k, v in weights.items()}
     dr = Drafter(cfg, tw, torch.from_numpy(d2t).to(device))
     temp = torch.tensor([w.temperature(b) for b in range(w.batch)], dtype=torch.float32,
