@@ -342,10 +342,11 @@ def main():
                             "launches": lm_n, "timing": "HIP events on the library stream, "
                             "8 back-to-back launches per event pair"}
         if block:
-            # a block call: the ingest pass (tap projection, body, context) and the block
-            # pass (body, context), one LM head over the block rows, the logits written
+            # a block call: one pass over the new and the block rows (tap projection, the
+            # body's weights and each sequence's context once), one LM head over the
+            # block rows, the logits written
             el = 2 if w.dtype == "bf16" else 4
-            call = (w.tap_width * w.d_model * el + 2 * (sb["body"] + sb["kv"]) + sb["lm"]
+            call = (w.tap_width * w.d_model * el + sb["body"] + sb["kv"] + sb["lm"]
                     + w.batch * w.K * w.vocab_draft * 4)
             call_us = ds_ms * 1e3 / max(ds_n, 1)
             line["draft_call_algorithmic_bytes"] = int(call)
