@@ -30,6 +30,12 @@
  * the normalised residual max(0, p - q), and a fully accepted chain gets a
  * bonus token from p_K.
  *
+ * Beyond the paper's top-1 chains: osprey_draft_tree and osprey_verify_tree grow
+ * and verify draft trees (top-k > 1, the dynamic draft trees the related work in
+ * the appendix names), and osprey_draft_block proposes K drafts from one pass over
+ * an anchor and mask rows (the EAGLE-style interface of the DFlash ablation in the
+ * appendix), verified by osprey_verify.
+ *
  * Conventions for every call:
  *  - Pointers are DEVICE pointers unless marked (host).
  *  - Every call is asynchronous on the handle's HIP stream, except
