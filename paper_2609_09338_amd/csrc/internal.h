@@ -388,10 +388,9 @@ struct TreeArgs {
   int d;
   const int32_t* last_row;
   const int32_t* committed;
-  const int32_t* bslot;
   int32_t* out_tok;         // [B][n_nodes]
   int32_t* out_par;
-  double* out_score;            // optional
+  double* out_score;        // [B][n_nodes] (nullable)
 };
 void launch_tree_topk(const TreeArgs& a, int rows, hipStream_t st);
 void launch_tree_step(const TreeArgs& a, hipStream_t st);

@@ -1283,7 +1283,6 @@ OSPREY_API int osprey_draft_tree(osprey_handle* h, const osprey_step_args* a, co
   ta.d = c.d_model;
   ta.last_row = W.last_row;
   ta.committed = W.committed;
-  ta.bslot = W.bslot;
   ta.out_tok = t->tokens;
   ta.out_par = t->parents;
   ta.out_score = t->scores;
