@@ -1247,7 +1247,9 @@ OSPREY_API int osprey_draft_tree(osprey_handle* h, const osprey_step_args* a, co
   if (N < 1 || N > std::min(kMaxTreeNodes, n_cand))
     return fail(OSPREY_E_INVALID, "n_nodes %d not in [1, %d]", N, std::min(kMaxTreeNodes, n_cand));
   if (!t->tokens || !t->parents) return fail(OSPREY_E_INVALID, "tree outputs are NULL");
-  if (c.vocab_draft > kTkBlocks * 256 * 16) return fail(OSPREY_E_UNSUPPORTED, "vocab_draft %d too large for trees", c.vocab_draft);
+  if (c.vocab_draft > kTkBlocks * 256 * 16 ||
+      lm_head_plan(std::min(B * k, kLmMaxRows), c.vocab_draft, h->n_cu).nblk > kTkMaxRecords)
+    return fail(OSPREY_E_UNSUPPORTED, "vocab_draft %d too large for trees", c.vocab_draft);
   SplitPlan split;
   bool pending;
   int tt;

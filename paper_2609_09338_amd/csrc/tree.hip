@@ -22,6 +22,7 @@ namespace osp {
 
 constexpr int kTkThreads = 256;
 constexpr int kTkPer = 16;        // logits per thread and block: a row of up to 64 x 4096
+constexpr int kTkRecLane = kTkMaxRecords / OSP_WAVE;   // LM-head records per lane
 
 OSP_DEV bool tk_better(float v1, int r1, float v2, int r2) { return v1 > v2 || (v1 == v2 && r1 < r2); }
 
@@ -104,22 +105,32 @@ __global__ void __launch_bounds__(kTkThreads) k_tree_step(TreeArgs a) {
   const int nfr = p == 0 ? 1 : K;                 // rows of this pass that are sequence b's
   const int row0 = p == 0 ? b : b * K;
   const long cb = (long)b * kMaxCand;
+  // this pass's rows' ancestor lists (read before the next pass's replace them)
+  __shared__ int s_anc[kMaxTopk][kMaxTreeDepth];
+  if (p > 0 && tid < K * kMaxTreeDepth)
+    s_anc[tid / kMaxTreeDepth][tid % kMaxTreeDepth] = a.r_anc[(long)b * K * kMaxTreeDepth + tid];
   if (tid < K) s_prev[tid] = p == 0 ? -1 : a.front[b * kMaxTopk + tid];
   if (tid == 0) s_n0 = p == 0 ? 0 : a.n_cand[b];   // (read before anyone writes it below)
   if (tid < K) { s_sel[tid] = tid; s_src[tid] = p == 0 ? 0 : tid; }   // (overwritten below)
   // ---- each row's K best (logit, row) pairs and its log-normaliser M + log S --------------
   for (int j = wave; j < nfr; j += kTkThreads / OSP_WAVE) {
     const int r = row0 + j;
-    // LM-head records of the row (temperature 1): max and rescaled sums
+    // LM-head records of the row (temperature 1): max and rescaled sums, every record
+    // of the lane requested at once (clamped addresses; lane l: records l, l + 64, ...)
     const float* rec = a.rec + (long)r * a.nblk * 4;
+    float2 rs[kTkRecLane];
+#pragma unroll
+    for (int q = 0; q < kTkRecLane; ++q)
+      rs[q] = *reinterpret_cast<const float2*>(rec + (long)min(lane + q * OSP_WAVE, a.nblk - 1) * 4);
     float m = -INFINITY;
-    for (int c = lane; c < a.nblk; c += OSP_WAVE) m = fmaxf(m, rec[c * 4]);
+#pragma unroll
+    for (int q = 0; q < kTkRecLane; ++q)
+      if (lane + q * OSP_WAVE < a.nblk) m = fmaxf(m, rs[q].x);
     const float M = wave_max(m);
     double s = 0.0;
-    for (int c = lane; c < a.nblk; c += OSP_WAVE) {
-      const float mc = rec[c * 4];
-      if (mc > -INFINITY) s += (double)rec[c * 4 + 1] * (double)__expf(mc - M);
-    }
+#pragma unroll
+    for (int q = 0; q < kTkRecLane; ++q)
+      if (lane + q * OSP_WAVE < a.nblk && rs[q].x > -INFINITY) s += (double)rs[q].y * (double)__expf(rs[q].x - M);
     const double S = wave_sum_d(s);
     // the blocks' candidates: kTkBlocks x K pairs, lane l holds pairs l, l + 64, ...
     constexpr int NPL = kTkBlocks * kMaxTopk / OSP_WAVE;
@@ -216,19 +227,27 @@ __global__ void __launch_bounds__(kTkThreads) k_tree_step(TreeArgs a) {
       a.r_cu[b] = b * K;
       if (b == a.B - 1) a.r_cu[a.B] = a.B * K;
     }
-    // ancestors' slots (earlier passes' frontier nodes), the root's child first, then
-    // the node itself
-    int chain[kMaxTreeDepth];
-    int n = 0;
-    chain[n++] = slot;
-    for (int e = s_prev[e0 / K]; e >= 0 && e < kMaxCand && n < kMaxTreeDepth; e = a.c_par[cb + e])
-      chain[n++] = a.c_slot[cb + e];
-    for (int i = 0; i < kMaxTreeDepth; ++i) a.r_anc[r * kMaxTreeDepth + i] = i < n ? chain[n - 1 - i] : -1;
+    // ancestors' slots, the root's child first, then the node itself: the parent's list
+    // (a row of this pass; root children: none) followed by the node's slot
+    const int pr = s_src[j];
+    int cnt = 0;
+#pragma unroll
+    for (int i = 0; i < kMaxTreeDepth; ++i)
+      if (p > 0 && cnt == i && s_anc[pr][i] >= 0) cnt = i + 1;
+#pragma unroll
+    for (int i = 0; i < kMaxTreeDepth; ++i)
+      a.r_anc[r * kMaxTreeDepth + i] = i < cnt ? s_anc[pr][i] : (i == cnt ? slot : -1);
   }
-  // ---- conditioning rows: the parent's hidden state (root: the last ingest row) ------------
-  for (int j = 0; j < K; ++j) {
+  // ---- conditioning rows: the parent's hidden state (root: the last ingest row); the
+  //      buffers do not overlap, so the loads of several iterations go out together -------
+  const int d4 = a.d / 4, nv = K * d4;
+  const float4* __restrict__ x4 = reinterpret_cast<const float4*>(a.x);
+  float4* __restrict__ s4 = reinterpret_cast<float4*>(a.r_s) + (long)b * K * d4;
+#pragma unroll 4
+  for (int i = tid; i < nv; i += kTkThreads) {
+    const int j = i / d4;
     const int src = p == 0 ? a.last_row[b] : b * K + s_src[j];
-    for (int i = tid; i < a.d; i += kTkThreads) a.r_s[(long)(b * K + j) * a.d + i] = a.x[(long)src * a.d + i];
+    s4[i] = x4[(long)src * d4 + (i - j * d4)];
   }
 }
 
