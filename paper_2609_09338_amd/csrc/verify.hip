@@ -118,11 +118,26 @@ __global__ void __launch_bounds__(kVThreads) k_vstats(VerifyArgs a) {
 
 // Merge the chunk statistics of one row with one wavefront: max M, lowest
 // argmax, S = sum exp((l - M)/T).  Fixed summation order.
+constexpr int kMergeLane = 2;   // chunk records per lane held in registers by merge_row
+
 OSP_DEV void merge_row(const float* p, int n, float T, float& M, double& S, int& am) {
   const int lane = threadIdx.x & 63;
+  // the lane's first kMergeLane records requested at once and kept for both passes
+  // (clamped addresses; vocabularies up to kMergeLane x 64 chunks), any further ones
+  // read in a loop
+  float4 rq[kMergeLane];
+#pragma unroll
+  for (int q = 0; q < kMergeLane; ++q)
+    rq[q] = *reinterpret_cast<const float4*>(p + (long)min(lane + q * 64, n - 1) * 4);
   float m = -INFINITY;
   int ai = 0x7fffffff;
-  for (int c = lane; c < n; c += 64) {
+#pragma unroll
+  for (int q = 0; q < kMergeLane; ++q) {
+    const float mc = rq[q].x;
+    const int ac = __float_as_int(rq[q].z);
+    if (lane + q * 64 < n && (mc > m || (mc == m && mc > -INFINITY && ac < ai))) { m = mc; ai = ac; }
+  }
+  for (int c = lane + kMergeLane * 64; c < n; c += 64) {
     const float mc = p[c * 4];
     const int ac = __float_as_int(p[c * 4 + 2]);
     if (mc > m || (mc == m && mc > -INFINITY && ac < ai)) { m = mc; ai = ac; }
@@ -131,11 +146,15 @@ OSP_DEV void merge_row(const float* p, int n, float T, float& M, double& S, int&
   am = wave_min_i((m == M && m > -INFINITY) ? ai : 0x7fffffff);
   if (am == 0x7fffffff) am = -1;
   double s = 0.0;
-  if (T > 0.f && M > -INFINITY)
-    for (int c = lane; c < n; c += 64) {
+  if (T > 0.f && M > -INFINITY) {
+#pragma unroll
+    for (int q = 0; q < kMergeLane; ++q)
+      if (lane + q * 64 < n && rq[q].x > -INFINITY) s += (double)rq[q].y * (double)__expf((rq[q].x - M) / T);
+    for (int c = lane + kMergeLane * 64; c < n; c += 64) {
       const float mc = p[c * 4];
       if (mc > -INFINITY) s += (double)p[c * 4 + 1] * (double)__expf((mc - M) / T);
     }
+  }
   S = wave_sum_d(s);
 }
 
