@@ -271,3 +271,45 @@ def test_full_size_sampled_sequences_match_oracle(name, seqs, iters):
     w = synth.get(name)
     stats = _run_parity(w, iters, seqs, 2e-2)
     assert stats["compared"] >= len(seqs)
+
+
+def test_block_with_packed_rows_matches_oracle():
+    """Block drafting in explicit mode with packed taps (taps_stride 0) and several new
+    tokens per sequence (3, 1, 2): the mask rows sit between the sequences' new rows,
+    so the packed token and tap rows and the block rows are indexed apart."""
+    _require_gpu()
+    from oracle.block import draft_block
+    from paper_2609_09338_amd import workload as WL
+    w = synth.get("p_block")
+    _say(f"[parity] {w.name}: packed explicit block")
+    s = WL.make_drafter(w, 2)
+    WL.reset_sequences(s)
+    dr = OH.build_drafter(w)
+    B, dev = w.batch, s.device
+    n_new = [3, 1, 2][:B]
+    rng = np.random.default_rng(31)
+    toks = [rng.integers(0, w.vocab_target - 1, n) for n in n_new]
+    taps = [synth.taps(w, 5, b, n) for b, n in enumerate(n_new)]
+    u = synth.u_draft(w, 0)
+    out = WL.alloc_outputs(s)
+    s.drafter.draft_step(list(range(B)), w.K, WL.to_dev(np.concatenate(taps), w, dev),
+                         s.draft_temperature, torch.from_numpy(u).to(dev), n_new=n_new,
+                         new_tokens=torch.from_numpy(np.concatenate(toks).astype(np.int32)).to(dev),
+                         taps_stride=0, draft_tokens=out.drafts, draft_logits=out.logits,
+                         mask_token=synth.mask_token(w))
+    torch.cuda.synchronize()
+    assert s.drafter.device_errors() == 0
+    g_logits, g_drafts = out.logits.cpu().numpy(), out.drafts.cpu().numpy()
+    flagged = 0
+    for b in range(B):
+        seq = OH.start_sequence(w, dr, b, 2)
+        Td = w.draft_temperature(b)
+        drafts, logits, _, _ = draft_block(dr, seq, toks[b], taps[b].astype(np.float64), w.K, Td,
+                                           u[b], synth.mask_token(w))
+        for k in range(w.K):
+            delta = _delta(g_logits[b, k], logits[k])
+            assert delta <= 2e-2, (b, k, delta)
+            if g_drafts[b, k] != drafts[k]:
+                assert parity.draw_flag(logits[k], Td, float(u[b, k]), delta), (b, k)
+                flagged += 1
+    assert flagged <= 1
