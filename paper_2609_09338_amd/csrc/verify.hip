@@ -87,16 +87,35 @@ __global__ void __launch_bounds__(kVThreads) k_vstats(VerifyArgs a) {
   }
   const int i0 = c * a.chunk, i1 = min(V, i0 + a.chunk);
   float v[kVWaveElems];
-#pragma unroll
-  for (int q = 0; q < kVWaveElems; ++q) {
-    const int i = i0 + lane + q * 64;
-    v[q] = i < i1 ? row[i] : -INFINITY;
-  }
   float m = -INFINITY;
   int am = 0x7fffffff;
+  // 16-byte loads (lane l: ids 4 l .. 4 l + 3 of every 256) when the row allows them: a
+  // vocabulary that is a multiple of 4 never splits a load at a chunk or row end
+  const bool vec = (V & 3) == 0 && (reinterpret_cast<uintptr_t>(row) & 15) == 0;
+  if (vec) {
 #pragma unroll
-  for (int q = 0; q < kVWaveElems; ++q)
-    if (v[q] > m) { m = v[q]; am = i0 + lane + q * 64; }   // ascending ids: first hit is lowest
+    for (int q = 0; q < kVWaveElems / 4; ++q) {
+      const int i = i0 + q * 256 + 4 * lane;
+      const float4 t = *reinterpret_cast<const float4*>(row + min(i, V - 4));   // clamped, masked below
+      const bool in = i < i1;
+      v[4 * q + 0] = in ? t.x : -INFINITY;
+      v[4 * q + 1] = in ? t.y : -INFINITY;
+      v[4 * q + 2] = in ? t.z : -INFINITY;
+      v[4 * q + 3] = in ? t.w : -INFINITY;
+    }
+#pragma unroll
+    for (int q = 0; q < kVWaveElems; ++q)   // ascending ids: first hit is lowest
+      if (v[q] > m) { m = v[q]; am = i0 + (q >> 2) * 256 + 4 * lane + (q & 3); }
+  } else {
+#pragma unroll
+    for (int q = 0; q < kVWaveElems; ++q) {
+      const int i = i0 + lane + q * 64;
+      v[q] = i < i1 ? row[i] : -INFINITY;
+    }
+#pragma unroll
+    for (int q = 0; q < kVWaveElems; ++q)
+      if (v[q] > m) { m = v[q]; am = i0 + lane + q * 64; }   // ascending ids: first hit is lowest
+  }
   const float M = wave_max(m);
   const int A = wave_min_i((m == M && m > -INFINITY) ? am : 0x7fffffff);
   const float T = j < nt ? a.temp[b] : a.temp_d[b];
