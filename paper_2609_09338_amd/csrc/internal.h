@@ -356,6 +356,7 @@ void launch_verify_tree(const VerifyArgs& a, hipStream_t st);
 constexpr int kMaxTopk = 8;           // children per node
 constexpr int kMaxTreeDepth = 8;      // depths
 constexpr int kMaxTreeProc = 64;      // frontier nodes run through the drafter per sequence
+constexpr int kTkRecordRows = 64;     // tree passes of at least this many rows select from the records
 constexpr int kTkMaxRecords = 2048;   // LM-head records per row a draft tree takes (V_d <= 2048 x 128)
 constexpr int kMaxCand = 512;         // candidates per sequence (>= 8 + 7 x 64)
 constexpr int kTkBlocks = 64;         // blocks per LM-head row in the candidate pass
@@ -366,9 +367,11 @@ struct TreeArgs {
   const float* logits;      // rows of this pass at logits + r * ld_logits
   long ld_logits;
   float* cand_v;            // [rows][kTkBlocks][kMaxTopk] best (logit, row) pairs per block
+                            // (nullptr: the step kernel selects from the records)
   int32_t* cand_r;
   const float* rec;         // LM-head records [rows][nblk][4] at temperature 1
   int nblk;
+  int blk_rows;              // logits per record
   // candidates per sequence [B][kMaxCand], generation order
   int32_t* c_tok;
   int32_t* c_par;

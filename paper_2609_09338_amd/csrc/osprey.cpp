@@ -807,8 +807,8 @@ LmPlan run_head_rows(osprey_handle* h, int rows, const int32_t* gather, const fl
   return lp;
 }
 
-int run_head_tree(osprey_handle* h, int rows, const int32_t* gather) {
-  return run_head_rows(h, rows, gather, h->W.ones, h->W.logits).nblk;
+LmPlan run_head_tree(osprey_handle* h, int rows, const int32_t* gather) {
+  return run_head_rows(h, rows, gather, h->W.ones, h->W.logits);
 }
 
 void fill_verify_common(osprey_handle* h, VerifyArgs& v, int B, int K) {
@@ -1290,8 +1290,16 @@ OSPREY_API int osprey_draft_tree(osprey_handle* h, const osprey_step_args* a, co
   ta.out_score = t->scores;
   // the root: the last ingest row of every sequence
   ta.pass = 0;
-  ta.nblk = run_head_tree(h, B, W.last_row);
-  launch_tree_topk(ta, B, h->stream);
+  // passes of many rows select their top-k from the LM-head records in the step kernel;
+  // few rows spread each row over kTkBlocks blocks of a separate pass first
+  auto select = [&](int rows, const LmPlan& lp) {
+    ta.nblk = lp.nblk;
+    ta.blk_rows = lp.blk_rows;
+    ta.cand_v = rows >= kTkRecordRows ? nullptr : W.tree_cv;
+    ta.cand_r = W.tree_cr;
+    if (ta.cand_v) launch_tree_topk(ta, rows, h->stream);
+  };
+  select(B, run_head_tree(h, B, W.last_row));
   launch_tree_step(ta, h->stream);
   // every further depth: the frontier's B k rows through the body and the LM head
   const int rows = B * k;
@@ -1300,8 +1308,7 @@ OSPREY_API int osprey_draft_tree(osprey_handle* h, const osprey_step_args* a, co
     TreePass tp{W.r_node, W.r_anc, W.r_pos, W.bslot};
     run_body_mr(h, rm, W.r_cu, B, W.r_s, 1, split, k, -1, &tp);
     ta.pass = p;
-    ta.nblk = run_head_tree(h, rows, nullptr);
-    launch_tree_topk(ta, rows, h->stream);
+    select(rows, run_head_tree(h, rows, nullptr));
     launch_tree_step(ta, h->stream);
   }
   launch_tree_final(ta, h->stream);

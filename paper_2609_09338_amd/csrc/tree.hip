@@ -88,6 +88,37 @@ __global__ void __launch_bounds__(kTkThreads) k_tree_topk(TreeArgs a) {
 // Candidate c is better than candidate e: larger score, lower index on ties.
 OSP_DEV bool cand_better(double s1, int i1, double s2, int i2) { return s1 > s2 || (s1 == s2 && i1 < i2); }
 
+constexpr int kTkRanges = 16;     // record ranges a record-guided selection reads (else the row)
+
+// This lane's kMaxTopk best (value, index) pairs, best first: insert one.
+OSP_DEV void top_insert(float (&bv)[kMaxTopk], int (&br)[kMaxTopk], float v, int r) {
+  if (!tk_better(v, r, bv[kMaxTopk - 1], br[kMaxTopk - 1])) return;
+#pragma unroll
+  for (int i = 0; i < kMaxTopk; ++i) {
+    if (tk_better(v, r, bv[i], br[i])) {
+      const float tv = bv[i];
+      const int tr = br[i];
+      bv[i] = v;
+      br[i] = r;
+      v = tv;
+      r = tr;
+    }
+  }
+}
+
+// The wavefront's best pair over the lanes' lists (wv, wr); the lane holding it drops it.
+OSP_DEV void wave_pop_best(float (&bv)[kMaxTopk], int (&br)[kMaxTopk], float& wv, int& wr) {
+  wv = bv[0];
+  wr = br[0];
+  wave_best(wv, wr);
+  if (br[0] == wr && bv[0] == wv && wr != 0x7fffffff) {
+#pragma unroll
+    for (int i = 0; i + 1 < kMaxTopk; ++i) { bv[i] = bv[i + 1]; br[i] = br[i + 1]; }
+    bv[kMaxTopk - 1] = -INFINITY;
+    br[kMaxTopk - 1] = 0x7fffffff;
+  }
+}
+
 __global__ void __launch_bounds__(kTkThreads) k_tree_step(TreeArgs a) {
   __shared__ float s_cv[kMaxTopk][kMaxTopk];
   __shared__ int s_cr[kMaxTopk][kMaxTopk];
@@ -98,6 +129,7 @@ __global__ void __launch_bounds__(kTkThreads) k_tree_step(TreeArgs a) {
   __shared__ int s_prev[kMaxTopk];
   __shared__ int s_ntok[kMaxTopk * kMaxTopk], s_ndep[kMaxTopk * kMaxTopk];
   __shared__ int s_rank[kMaxTopk * kMaxTopk];
+  __shared__ int s_rng[kMaxTopk][kTkRanges];
   __shared__ int s_n0;
   const int b = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -132,31 +164,91 @@ __global__ void __launch_bounds__(kTkThreads) k_tree_step(TreeArgs a) {
     for (int q = 0; q < kTkRecLane; ++q)
       if (lane + q * OSP_WAVE < a.nblk && rs[q].x > -INFINITY) s += (double)rs[q].y * (double)__expf(rs[q].x - M);
     const double S = wave_sum_d(s);
-    // the blocks' candidates: kTkBlocks x K pairs, lane l holds pairs l, l + 64, ...
-    constexpr int NPL = kTkBlocks * kMaxTopk / OSP_WAVE;
-    float cv[NPL];
-    int cr[NPL];
+    if (!a.cand_v) {
+      // record-guided (passes of many rows): the K best logits lie in ranges whose max
+      // reaches Mk, the K-th largest range max (the K ranges of largest max hold K values
+      // >= Mk, so the K-th best value is >= Mk); only those ranges are read
+      float bv[kMaxTopk];
+      int br[kMaxTopk];
 #pragma unroll
-    for (int q = 0; q < NPL; ++q) {
-      const int e = lane + q * OSP_WAVE;            // pair e = block e / kMaxTopk, rank e % kMaxTopk
-      const bool in = e % kMaxTopk < K;
-      const long o = ((long)r * kTkBlocks) * kMaxTopk + e;
-      cv[q] = in ? a.cand_v[o] : -INFINITY;
-      cr[q] = in ? a.cand_r[o] : 0x7fffffff;
-    }
-    for (int t = 0; t < K; ++t) {
-      float bv = -INFINITY;
-      int br = 0x7fffffff;
+      for (int i = 0; i < kMaxTopk; ++i) { bv[i] = -INFINITY; br[i] = 0x7fffffff; }
 #pragma unroll
-      for (int q = 0; q < NPL; ++q)
-        if (tk_better(cv[q], cr[q], bv, br)) { bv = cv[q]; br = cr[q]; }
-      float wv = bv;
-      int wr = br;
-      wave_best(wv, wr);
+      for (int q = 0; q < kTkRecLane; ++q)
+        if (lane + q * OSP_WAVE < a.nblk) top_insert(bv, br, rs[q].x, lane + q * OSP_WAVE);
+      float Mk = -INFINITY;
+      for (int t = 0; t < K; ++t) {
+        float wv;
+        int wr;
+        wave_pop_best(bv, br, wv, wr);
+        Mk = wv;
+      }
+      int n = 0;
 #pragma unroll
-      for (int q = 0; q < NPL; ++q)
-        if (cr[q] == wr && wr != 0x7fffffff) { cv[q] = -INFINITY; cr[q] = 0x7fffffff; }
-      if (lane == 0) { s_cv[j][t] = wv; s_cr[j][t] = wr; }
+      for (int q = 0; q < kTkRecLane; ++q) {
+        const int c = lane + q * OSP_WAVE;
+        const bool in = c < a.nblk && rs[q].x >= Mk;
+        const unsigned long long bal = __ballot(in);
+        const int at = n + __popcll(bal & ((1ull << lane) - 1ull));
+        if (in && at < kTkRanges) s_rng[j][at] = c;
+        n += __popcll(bal);
+      }
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int i = 0; i < kMaxTopk; ++i) { bv[i] = -INFINITY; br[i] = 0x7fffffff; }
+      const float* lg = a.logits + (long)r * a.ld_logits;
+      if (n <= kTkRanges) {
+        // every listed range's logits requested at once: lane l reads entries l and l + 64
+        float v0[kTkRanges], v1[kTkRanges];
+        int e0[kTkRanges];
+#pragma unroll
+        for (int i = 0; i < kTkRanges; ++i) {
+          e0[i] = (i < n ? s_rng[j][i] : 0) * a.blk_rows + lane;
+          v0[i] = lg[min(e0[i], a.V - 1)];                       // clamped addresses; entries
+          v1[i] = lg[min(e0[i] + OSP_WAVE, a.V - 1)];            // outside a range are skipped
+        }
+#pragma unroll
+        for (int i = 0; i < kTkRanges; ++i) {
+          if (i < n && lane < a.blk_rows && e0[i] < a.V) top_insert(bv, br, v0[i], e0[i]);
+          if (i < n && lane + OSP_WAVE < a.blk_rows && e0[i] + OSP_WAVE < a.V)
+            top_insert(bv, br, v1[i], e0[i] + OSP_WAVE);
+        }
+      } else {
+        // ties or masked rows put more ranges at Mk: the whole row
+        for (int i = lane; i < a.V; i += OSP_WAVE) top_insert(bv, br, lg[i], i);
+      }
+      for (int t = 0; t < K; ++t) {
+        float wv;
+        int wr;
+        wave_pop_best(bv, br, wv, wr);
+        if (lane == 0) { s_cv[j][t] = wv; s_cr[j][t] = wr; }
+      }
+    } else {
+      // the blocks' candidates: kTkBlocks x K pairs, lane l holds pairs l, l + 64, ...
+      constexpr int NPL = kTkBlocks * kMaxTopk / OSP_WAVE;
+      float cv[NPL];
+      int cr[NPL];
+#pragma unroll
+      for (int q = 0; q < NPL; ++q) {
+        const int e = lane + q * OSP_WAVE;            // pair e = block e / kMaxTopk, rank e % kMaxTopk
+        const bool in = e % kMaxTopk < K;
+        const long o = ((long)r * kTkBlocks) * kMaxTopk + e;
+        cv[q] = in ? a.cand_v[o] : -INFINITY;
+        cr[q] = in ? a.cand_r[o] : 0x7fffffff;
+      }
+      for (int t = 0; t < K; ++t) {
+        float bv = -INFINITY;
+        int br = 0x7fffffff;
+#pragma unroll
+        for (int q = 0; q < NPL; ++q)
+          if (tk_better(cv[q], cr[q], bv, br)) { bv = cv[q]; br = cr[q]; }
+        float wv = bv;
+        int wr = br;
+        wave_best(wv, wr);
+#pragma unroll
+        for (int q = 0; q < NPL; ++q)
+          if (cr[q] == wr && wr != 0x7fffffff) { cv[q] = -INFINITY; cr[q] = 0x7fffffff; }
+        if (lane == 0) { s_cv[j][t] = wv; s_cr[j][t] = wr; }
+      }
     }
     if (lane == 0) s_lse[j] = (double)M + log(S);
   }
