@@ -356,7 +356,7 @@ void launch_verify_tree(const VerifyArgs& a, hipStream_t st);
 constexpr int kMaxTopk = 8;           // children per node
 constexpr int kMaxTreeDepth = 8;      // depths
 constexpr int kMaxTreeProc = 64;      // frontier nodes run through the drafter per sequence
-constexpr int kTkRecordRows = 64;     // tree passes of at least this many rows select from the records
+constexpr int kTkRecordRows = 64;    // tree passes of at least this many rows select from the records
 constexpr int kTkMaxRecords = 2048;   // LM-head records per row a draft tree takes (V_d <= 2048 x 128)
 constexpr int kMaxCand = 512;         // candidates per sequence (>= 8 + 7 x 64)
 constexpr int kTkBlocks = 64;         // blocks per LM-head row in the candidate pass

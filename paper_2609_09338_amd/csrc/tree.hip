@@ -119,6 +119,29 @@ OSP_DEV void wave_pop_best(float (&bv)[kMaxTopk], int (&br)[kMaxTopk], float& wv
   }
 }
 
+// K rounds of the wavefront's best (value, index) pair over the lanes' N pairs, each
+// winner dropped by its lane; lane 0 writes the winners to ov / orr when given.  Returns
+// the K-th winner's value.
+template <int N>
+OSP_DEV float wave_topk(const float (&v)[N], const int (&ix)[N], int K, float* ov, int* orr) {
+  unsigned long long gone = 0ull;
+  float last = -INFINITY;
+  for (int t = 0; t < K; ++t) {
+    float bv = -INFINITY;
+    int br = 0x7fffffff, bq = -1;
+#pragma unroll
+    for (int q = 0; q < N; ++q)
+      if (!((gone >> q) & 1ull) && tk_better(v[q], ix[q], bv, br)) { bv = v[q]; br = ix[q]; bq = q; }
+    float wv = bv;
+    int wr = br;
+    wave_best(wv, wr);
+    if (bq >= 0 && br == wr && wr != 0x7fffffff) gone |= 1ull << bq;
+    if (ov && (threadIdx.x & 63) == 0) { ov[t] = wv; orr[t] = wr; }
+    last = wv;
+  }
+  return last;
+}
+
 __global__ void __launch_bounds__(kTkThreads) k_tree_step(TreeArgs a) {
   __shared__ float s_cv[kMaxTopk][kMaxTopk];
   __shared__ int s_cr[kMaxTopk][kMaxTopk];
@@ -168,20 +191,15 @@ __global__ void __launch_bounds__(kTkThreads) k_tree_step(TreeArgs a) {
       // record-guided (passes of many rows): the K best logits lie in ranges whose max
       // reaches Mk, the K-th largest range max (the K ranges of largest max hold K values
       // >= Mk, so the K-th best value is >= Mk); only those ranges are read
-      float bv[kMaxTopk];
-      int br[kMaxTopk];
+      float mv[kTkRecLane];
+      int mi[kTkRecLane];
 #pragma unroll
-      for (int i = 0; i < kMaxTopk; ++i) { bv[i] = -INFINITY; br[i] = 0x7fffffff; }
-#pragma unroll
-      for (int q = 0; q < kTkRecLane; ++q)
-        if (lane + q * OSP_WAVE < a.nblk) top_insert(bv, br, rs[q].x, lane + q * OSP_WAVE);
-      float Mk = -INFINITY;
-      for (int t = 0; t < K; ++t) {
-        float wv;
-        int wr;
-        wave_pop_best(bv, br, wv, wr);
-        Mk = wv;
+      for (int q = 0; q < kTkRecLane; ++q) {
+        const bool in = lane + q * OSP_WAVE < a.nblk;
+        mv[q] = in ? rs[q].x : -INFINITY;
+        mi[q] = in ? lane + q * OSP_WAVE : 0x7fffffff;
       }
+      const float Mk = wave_topk(mv, mi, K, nullptr, nullptr);
       int n = 0;
 #pragma unroll
       for (int q = 0; q < kTkRecLane; ++q) {
@@ -193,34 +211,36 @@ __global__ void __launch_bounds__(kTkThreads) k_tree_step(TreeArgs a) {
         n += __popcll(bal);
       }
       __builtin_amdgcn_wave_barrier();
-#pragma unroll
-      for (int i = 0; i < kMaxTopk; ++i) { bv[i] = -INFINITY; br[i] = 0x7fffffff; }
       const float* lg = a.logits + (long)r * a.ld_logits;
       if (n <= kTkRanges) {
         // every listed range's logits requested at once: lane l reads entries l and l + 64
-        float v0[kTkRanges], v1[kTkRanges];
-        int e0[kTkRanges];
+        float lv[2 * kTkRanges];
+        int li[2 * kTkRanges];
 #pragma unroll
         for (int i = 0; i < kTkRanges; ++i) {
-          e0[i] = (i < n ? s_rng[j][i] : 0) * a.blk_rows + lane;
-          v0[i] = lg[min(e0[i], a.V - 1)];                       // clamped addresses; entries
-          v1[i] = lg[min(e0[i] + OSP_WAVE, a.V - 1)];            // outside a range are skipped
+          const int e0 = (i < n ? s_rng[j][i] : 0) * a.blk_rows + lane, e1 = e0 + OSP_WAVE;
+          const float l0 = lg[min(e0, a.V - 1)], l1 = lg[min(e1, a.V - 1)];   // clamped, masked below
+          const bool in0 = i < n && lane < a.blk_rows && e0 < a.V;
+          const bool in1 = i < n && lane + OSP_WAVE < a.blk_rows && e1 < a.V;
+          lv[2 * i] = in0 ? l0 : -INFINITY;
+          li[2 * i] = in0 ? e0 : 0x7fffffff;
+          lv[2 * i + 1] = in1 ? l1 : -INFINITY;
+          li[2 * i + 1] = in1 ? e1 : 0x7fffffff;
         }
-#pragma unroll
-        for (int i = 0; i < kTkRanges; ++i) {
-          if (i < n && lane < a.blk_rows && e0[i] < a.V) top_insert(bv, br, v0[i], e0[i]);
-          if (i < n && lane + OSP_WAVE < a.blk_rows && e0[i] + OSP_WAVE < a.V)
-            top_insert(bv, br, v1[i], e0[i] + OSP_WAVE);
-        }
+        wave_topk(lv, li, K, s_cv[j], s_cr[j]);
       } else {
         // ties or masked rows put more ranges at Mk: the whole row
+        float bv[kMaxTopk];
+        int br[kMaxTopk];
+#pragma unroll
+        for (int i = 0; i < kMaxTopk; ++i) { bv[i] = -INFINITY; br[i] = 0x7fffffff; }
         for (int i = lane; i < a.V; i += OSP_WAVE) top_insert(bv, br, lg[i], i);
-      }
-      for (int t = 0; t < K; ++t) {
-        float wv;
-        int wr;
-        wave_pop_best(bv, br, wv, wr);
-        if (lane == 0) { s_cv[j][t] = wv; s_cr[j][t] = wr; }
+        for (int t = 0; t < K; ++t) {
+          float wv;
+          int wr;
+          wave_pop_best(bv, br, wv, wr);
+          if (lane == 0) { s_cv[j][t] = wv; s_cr[j][t] = wr; }
+        }
       }
     } else {
       // the blocks' candidates: kTkBlocks x K pairs, lane l holds pairs l, l + 64, ...
