@@ -1,10 +1,10 @@
 """Elementwise building blocks of the drafter, in float64.
 
 These are the standard definitions of the pieces the drafter inherits from its
-source LM unchanged (Section 3.3: "MLP blocks, normalization layers, and other
-pretrained components are transferred without architectural changes"); the
-paper names the source (Qwen3-4B, Section 4) but not the formulas, so each is
-the Qwen3 definition.
+source LM unchanged (Section 3.3 keeps the feed-forward blocks, the norms and the
+other pretrained parts of the source model as they are); the paper names the
+source (Qwen3-4B, Section 4) but not the formulas, so each is the Qwen3
+definition.
 """
 from __future__ import annotations
 

@@ -112,6 +112,11 @@ class DraftTree:
     cand_scores: np.ndarray   # scores of every candidate, in generation order
     min_gap: float = np.inf   # smallest margin of any selection (top-k logits, frontier,
                               # final): where a computation in another precision may differ
+    # every selection the growth made, for locating near ties: (values of its best
+    # candidates in descending order, their path keys (tuples of target ids from the
+    # root), how many it kept, whether the order of the kept ones matters ("topk":
+    # children are generated in rank order) or only the cut ("cut"))
+    selections: list = None
 
 
 def top_rows(logits: np.ndarray, k: int) -> np.ndarray:
@@ -143,17 +148,31 @@ def draft_tree(drafter, seq, tokens, taps, topk: int, depth: int, n_nodes: int) 
     then generation order) form the tree, listed in generation order."""
     import copy
     gaps = []
+    selections = []
 
     def gap(values, k):           # margin between the k-th and (k+1)-th largest values
         v = np.sort(np.asarray(values, dtype=np.float64)[np.isfinite(values)])[::-1]
         if len(v) > k:
             gaps.append(v[k - 1] - v[k])
 
+    def record(values, keys, k, kind, extra=16):
+        values = np.asarray(values, dtype=np.float64)
+        order = np.lexsort((np.arange(values.size), -values))[: k + extra]
+        selections.append((values[order], [keys(int(i)) for i in order], k, kind))
+
+    def key_of(i):                # path key of candidate i: target ids from the root
+        out = []
+        while i >= 0:
+            out.append(cands[i][0])
+            i = cands[i][1]
+        return tuple(out[::-1])
+
     g_root = drafter.ingest(seq, tokens, taps)
     L = seq.length
     cands = []      # (token, parent candidate index, score, depth)
     lp = log_probs(drafter.logits(g_root))
     gap(drafter.logits(g_root), topk)
+    record(drafter.logits(g_root), lambda r: (int(drafter.d2t[r]),), topk, "topk")
     for r in top_rows(drafter.logits(g_root), topk):
         cands.append((int(drafter.d2t[r]), -1, float(lp[r]), 1))
     state = {}      # candidate index -> (branch cache, hidden state g)
@@ -169,19 +188,22 @@ def draft_tree(drafter, seq, tokens, taps, topk: int, depth: int, n_nodes: int) 
             l = drafter.logits(g)
             lpf = log_probs(l)
             gap(l, topk)
+            record(l, lambda r, f=f: key_of(f) + (int(drafter.d2t[r]),), topk, "topk")
             for r in top_rows(l, topk):
                 new.append(len(cands))
                 cands.append((int(drafter.d2t[r]), f, sc + float(lpf[r]), dep + 1))
         order = sorted(new, key=lambda i: (-cands[i][2], i))
         if d < depth:
             gap([cands[i][2] for i in new], topk)
+            record([cands[i][2] for i in new], lambda j, new=new: key_of(new[j]), topk, "cut")
         frontier = sorted(order[:topk])
     allsc = np.array([c[2] for c in cands])
     gap(allsc, n_nodes)
+    record(allsc, key_of, n_nodes, "cut")
     pick = sorted(sorted(range(len(cands)), key=lambda i: (-cands[i][2], i))[:n_nodes])
     index = {c: j for j, c in enumerate(pick)}
     toks = np.array([cands[i][0] for i in pick], dtype=np.int64)
     pars = np.array([index[cands[i][1]] if cands[i][1] >= 0 else -1 for i in pick], dtype=np.int64)
     return DraftTree(toks, pars, np.array([cands[i][2] for i in pick]),
                      np.array([cands[i][3] for i in pick], dtype=np.int64), allsc,
-                     min(gaps) if gaps else np.inf)
+                     min(gaps) if gaps else np.inf, selections)

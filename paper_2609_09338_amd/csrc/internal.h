@@ -112,8 +112,11 @@ struct LmPlan {
 constexpr int kLmMaxRows = 64;
 LmPlan lm_head_plan(int rows, int N, int n_cu);
 // norm_in: inputs are the fp32 rows xin (ldx, gathered), normalised with gamma / eps
-// in the kernel; else prepared pairs xa_hi / xa_lo.
-void launch_lm_head(const GemvArgs& a, const LmPlan& p, bool norm_in, hipStream_t st);
+// in the kernel (one row of at most 4096 columns: lm_head_norm_in_supported); else
+// prepared pairs xa_hi / xa_lo.  Returns false, launching nothing, for an unsupported
+// norm_in shape.
+bool lm_head_norm_in_supported(int rows, int Kd);
+bool launch_lm_head(const GemvArgs& a, const LmPlan& p, bool norm_in, hipStream_t st);
 
 // Projections of passes of at most kLmMaxRows rows on the same streaming kernel:
 // src SRC_PREP (pairs; [xs ; xa] when seg > 0), SRC_TAPS, or SRC_SWIGLU (the down

@@ -230,6 +230,9 @@ int validate(const osprey_config* c) {
   if (c->n_layers < 1 || c->n_layers > 64) return fail(OSPREY_E_INVALID, "n_layers %d not in [1, 64]", c->n_layers);
   if (c->d_model < 64 || c->d_model % 64) return fail(OSPREY_E_SHAPE, "d_model %d must be a positive multiple of 64", c->d_model);
   if (c->d_model > 4096) return fail(OSPREY_E_UNSUPPORTED, "d_model %d > 4096", c->d_model);
+  // (the batch-1 LM head normalises its row in the kernel: checked here, before any call)
+  if (!lm_head_norm_in_supported(1, c->d_model))
+    return fail(OSPREY_E_UNSUPPORTED, "d_model %d: the batch-1 LM head cannot normalise its row", c->d_model);
   if (c->d_ffn < 64 || c->d_ffn % 64) return fail(OSPREY_E_SHAPE, "d_ffn %d must be a positive multiple of 64", c->d_ffn);
   if (c->n_q_heads < 1 || c->n_kv_heads < 1 || c->n_q_heads % c->n_kv_heads)
     return fail(OSPREY_E_SHAPE, "n_kv_heads %d must divide n_q_heads %d", c->n_kv_heads, c->n_q_heads);
@@ -668,8 +671,8 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
 }
 
 // Final norm + LM head + block statistics, then the draft pick of step k.
-void run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, const float* temp,
-              const float* u, float* logits, long ld_b, int32_t* drafts_out) {
+int run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, const float* temp,
+             const float* u, float* logits, long ld_b, int32_t* drafts_out) {
   const osprey_config& c = h->cfg;
   const Ws& W = h->W;
   // bf16 heads run on the matrix cores at every batch size; the rows come prepared
@@ -725,7 +728,9 @@ void run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, cons
       p.y = g.y + (long)r0 * g.ld_logits;
       p.temp = temp + r0;
       p.part = W.lm_part + (long)r0 * nblk * 4;
-      launch_lm_head(p, lp, !prepared, h->stream);
+      if (!launch_lm_head(p, lp, !prepared, h->stream))
+        return fail(OSPREY_E_UNSUPPORTED, "LM head: %d rows of width %d cannot be normalised in the kernel",
+                    p.max_rows, p.Kd);
     }
   } else {
     launch_gemv(c.dtype, SRC_NORM, EPI_LOGITS, g, h->stream);
@@ -758,13 +763,15 @@ void run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, cons
   s.qstat = W.qstat;
   s.ld_qstat = h->D.Km;
   launch_sample(s, h->stream);
+  return OSPREY_OK;
 }
 
 // LM head over `rows` rows (gathered through `gather`, else rows 0.. of the body's
 // output), logits row r at y + r V, softmax records at the rows' temperatures `temp`
 // (W.lm_part, nblk per row).  Draft trees: rows of a pass at temperature 1 into
 // W.logits; blocks: a block's rows into the draft logits.  Returns the head's plan.
-LmPlan run_head_rows(osprey_handle* h, int rows, const int32_t* gather, const float* temp, float* y) {
+LmPlan run_head_rows(osprey_handle* h, int rows, const int32_t* gather, const float* temp, float* y,
+                     int& rc) {
   const osprey_config& c = h->cfg;
   const Ws& W = h->W;
   const bool prepared = gemm_use_mfma(c.dtype, rows);
@@ -800,15 +807,17 @@ LmPlan run_head_rows(osprey_handle* h, int rows, const int32_t* gather, const fl
       p.y = y + (long)r0 * c.vocab_draft;
       p.temp = temp + r0;
       p.part = W.lm_part + (long)r0 * lp.nblk * 4;
-      launch_lm_head(p, lp, !prepared, h->stream);
+      if (!launch_lm_head(p, lp, !prepared, h->stream))
+        rc = fail(OSPREY_E_UNSUPPORTED, "LM head: %d rows of width %d cannot be normalised in the kernel",
+                  p.max_rows, p.Kd);
     }
   }
   h->t_end(t, reps);
   return lp;
 }
 
-LmPlan run_head_tree(osprey_handle* h, int rows, const int32_t* gather) {
-  return run_head_rows(h, rows, gather, h->W.ones, h->W.logits);
+LmPlan run_head_tree(osprey_handle* h, int rows, const int32_t* gather, int& rc) {
+  return run_head_rows(h, rows, gather, h->W.ones, h->W.logits, rc);
 }
 
 void fill_verify_common(osprey_handle* h, VerifyArgs& v, int B, int K) {
@@ -1158,13 +1167,15 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
   const long ld_b = a->draft_logits ? K : h->D.Km;
   const float* u = a->u_draft ? a->u_draft : W.u_zero;
   if (K >= 1) {
-    run_head(h, B, 0, K, W.last_row, a->temperature, u, logits, ld_b, a->draft_tokens);
+    if ((rc = run_head(h, B, 0, K, W.last_row, a->temperature, u, logits, ld_b, a->draft_tokens)))
+      return rc;
     RowMeta ar{nullptr, W.ar_pos, W.ar_tok, nullptr, B};
     const bool ar_mr = gemm_use_mfma(c.dtype, B);
     for (int k = 1; k < K; ++k) {
       if (ar_mr) run_body_mr(h, ar, nullptr, B, W.gfb, 1, split, 1, a->slots[0]);
       else run_body(h, ar, nullptr, B, W.gfb, true, split, 1, a->slots[0]);
-      run_head(h, B, k, K, nullptr, a->temperature, u, logits, ld_b, a->draft_tokens);
+      if ((rc = run_head(h, B, k, K, nullptr, a->temperature, u, logits, ld_b, a->draft_tokens)))
+        return rc;
     }
   }
   h->t_end(tt);
@@ -1198,7 +1209,8 @@ OSPREY_API int osprey_draft_block(osprey_handle* h, const osprey_step_args* a, i
   const int rows = B * K;
   // ---- LM head over the block's rows, then one pick per (sequence, proposal) ------------
   float* logits = a->draft_logits ? a->draft_logits : W.logits;
-  const LmPlan lp = run_head_rows(h, rows, W.b_gather, W.b_temp, logits);
+  const LmPlan lp = run_head_rows(h, rows, W.b_gather, W.b_temp, logits, rc);
+  if (rc) return rc;
   SampleArgs sm{};
   sm.block = 1;
   sm.B = B;
@@ -1299,7 +1311,8 @@ OSPREY_API int osprey_draft_tree(osprey_handle* h, const osprey_step_args* a, co
     ta.cand_r = W.tree_cr;
     if (ta.cand_v) launch_tree_topk(ta, rows, h->stream);
   };
-  select(B, run_head_tree(h, B, W.last_row));
+  select(B, run_head_tree(h, B, W.last_row, rc));
+  if (rc) return rc;
   launch_tree_step(ta, h->stream);
   // every further depth: the frontier's B k rows through the body and the LM head
   const int rows = B * k;
@@ -1308,7 +1321,8 @@ OSPREY_API int osprey_draft_tree(osprey_handle* h, const osprey_step_args* a, co
     TreePass tp{W.r_node, W.r_anc, W.r_pos, W.bslot};
     run_body_mr(h, rm, W.r_cu, B, W.r_s, 1, split, k, -1, &tp);
     ta.pass = p;
-    select(rows, run_head_tree(h, rows, nullptr));
+    select(rows, run_head_tree(h, rows, nullptr, rc));
+    if (rc) return rc;
     launch_tree_step(ta, h->stream);
   }
   launch_tree_final(ta, h->stream);

@@ -466,12 +466,15 @@ static void sk_launch(int mt, dim3 grid, const GemvArgs& a, int T, int kc, hipSt
   else hipLaunchKernelGGL((k_skinny<4, SRC, EPI>), grid, dim3(kSkThreads), 0, st, a, T, kc);
 }
 
-void launch_lm_head(const GemvArgs& a, const LmPlan& p, bool norm_in, hipStream_t st) {
+bool lm_head_norm_in_supported(int rows, int Kd) { return rows == 1 && Kd <= 8 * kSkThreads; }
+
+bool launch_lm_head(const GemvArgs& a, const LmPlan& p, bool norm_in, hipStream_t st) {
   // the fp32 input is normalised in the head for one row only (batch 1), of at most
-  // 8 x kSkThreads columns
-  if (norm_in && (a.max_rows != 1 || a.Kd > 8 * kSkThreads)) std::abort();
+  // 8 x kSkThreads columns; anything else is refused (nothing launched)
+  if (norm_in && !lm_head_norm_in_supported(a.max_rows, a.Kd)) return false;
   if (norm_in) sk_launch<SK_NORM, SK_LOGITS>(1, dim3(p.grid), a, p.T, 0, st);
   else sk_launch<SK_PREP, SK_LOGITS>(p.mt, dim3(p.grid), a, p.T, 0, st);
+  return true;
 }
 
 // ---- projections --------------------------------------------------------------------------

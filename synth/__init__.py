@@ -103,6 +103,11 @@ WORKLOADS: Dict[str, Workload] = {
     "c2": Workload(name="c2", cfg_id=2, vocab_draft=151936, vocab_target=151936,
                    target_hidden=4096, batch=1, K=7, ctx_lo=2048, ctx_hi=2048, temps=(1.0,),
                    sigma=1.0, **_QWEN_DRAFTER),
+    # The same step with a greedy target (T = 0; the other temperature the configuration
+    # names): prefix match against the target's argmax, bonus = argmax.
+    "c2t0": Workload(name="c2t0", cfg_id=10, vocab_draft=151936, vocab_target=151936,
+                     target_hidden=4096, batch=1, K=7, ctx_lo=2048, ctx_hi=2048, temps=(0.0,),
+                     sigma=1.0, **_QWEN_DRAFTER),
     # Llama-3.3-70B-shaped target: partial surjective map 151936 -> 128256.
     "c3": Workload(name="c3", cfg_id=3, vocab_draft=151936, vocab_target=128256,
                    target_hidden=8192, batch=8, K=6, ctx_lo=4096, ctx_hi=4096, temps=(1.0,),

@@ -128,3 +128,33 @@ def tree_flags(res, target_logits, tokens, parents, T, u_acc, u_bonus) -> bool:
             return margin < 1e-6 * run[-1] + 1e-12
         cur = int(nxt)
     return False
+
+
+def tree_near_tie_keys(tree, tol: float) -> set:
+    """Path keys of the candidates a near tie may move, over every selection the oracle's
+    tree growth made: where two neighbouring values that decide the outcome (the cut
+    between kept and dropped, and for a node's top-k children also their rank order)
+    are closer than `tol`, every candidate whose value lies within `tol` of that pair."""
+    out = set()
+    for vals, keys, k, kind in tree.selections:
+        pairs = range(min(k, len(vals) - 1)) if kind == "topk" else [k - 1]
+        for i in pairs:
+            if i + 1 >= len(vals) or not np.isfinite(vals[i + 1]):
+                continue
+            if vals[i] - vals[i + 1] < tol:
+                lo, hi = vals[i + 1] - tol, vals[i] + tol
+                out.update(key for v, key in zip(vals, keys) if lo <= v <= hi)
+    return out
+
+
+def tree_mismatch_excused(gpu_keys, oracle_keys, near: set) -> bool:
+    """True when every node on which the two trees differ depends on a near tie: the
+    node's own path key, or the key of one of its ancestors, is in `near`.  With equal
+    node sets the differing positions are compared (a near tie in a rank order changes
+    the generation order), otherwise the nodes only one tree holds."""
+    g, o = list(gpu_keys), list(oracle_keys)
+    if set(g) == set(o):
+        diff = {a for a, b in zip(g, o) if a != b} | {b for a, b in zip(g, o) if a != b}
+    else:
+        diff = set(g) ^ set(o)
+    return all(any(key[:j] in near for j in range(1, len(key) + 1)) for key in diff)

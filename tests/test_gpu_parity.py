@@ -134,7 +134,10 @@ def _run_parity(w, n_iters, seqs, tol):
     WL.reset_sequences(s)
     out = WL.alloc_outputs(s)
     live = set(seqs)
-    stats = dict(compared=0, flagged=0, max_delta=0.0, accepted=0)
+    # exact_*: comparisons that were made and came out equal, unflagged -- draft ids,
+    # acceptance decisions (one per draft the rule tested) and the resampled / bonus token
+    stats = dict(compared=0, flagged=0, max_delta=0.0, accepted=0, exact_drafts=0,
+                 exact_accepts=0, exact_bonus=0)
     for it in range(n_iters):
         inp = WL.iter_inputs(s, it)
         WL.draft(s, it, inp, out)
@@ -162,11 +165,17 @@ def _run_parity(w, n_iters, seqs, tol):
                         (w.name, b, it, k, g_drafts[b, k], rec.drafts[k])
                     ok = False
                     break
+                stats["exact_drafts"] += 1
             if ok:
                 same = (g_a[b] == rec.result.accept_len and
                         np.array_equal(g_mask[b], rec.result.mask) and
                         np.array_equal(g_tok[b], rec.result.tokens))
-                if not same:
+                if same:
+                    # decisions tested: the a accepted drafts, plus the rejection if a < K
+                    stats["exact_accepts"] += int(rec.result.accept_len) + \
+                        int(rec.result.accept_len < w.K)
+                    stats["exact_bonus"] += 1
+                else:
                     delta = max(_delta(g_logits[b, k], rec.draft_logits[k]) for k in range(w.K))
                     assert parity.verify_flags(rec.result, rec.target_logits, rec.draft_logits,
                                                d2t, rec.drafts, T, synth.u_accept(w, it)[b],
@@ -182,6 +191,13 @@ def _run_parity(w, n_iters, seqs, tol):
     _say(f"[parity] {w.name}: {stats}")
     assert stats["flagged"] <= max(1, stats["compared"] // 5), stats
     return stats
+
+
+def _assert_exact_comparisons(stats, name):
+    """A case passes on flags alone only if nothing was compared exactly: require at
+    least one unflagged draft id, acceptance decision and resampled / bonus token."""
+    for key in ("exact_drafts", "exact_accepts", "exact_bonus"):
+        assert stats[key] >= 1, (name, key, stats)
 
 
 @pytest.mark.parametrize("name", ["p_tiny_f32", "p_qwen_small", "p_partial", "p_inject",
@@ -260,10 +276,10 @@ def test_runs_are_deterministic_and_page_order_free():
 # ----------------------------------------------------------------------------------------
 # full-size workloads, sampled sequences (the GPU runs the whole batch)
 # ----------------------------------------------------------------------------------------
-@pytest.mark.parametrize("name,seqs,iters", [("c2", [0], 2), ("c2g", [0], 2), ("c3", [7], 2),
-                                             ("c4", [31], 1), ("c5", [62, 63], 2),
-                                             ("osprey_2l", [0], 2), ("c2b", [0], 2),
-                                             ("dflash_4l", [0], 2)])
+@pytest.mark.parametrize("name,seqs,iters", [("c2", [0], 2), ("c2t0", [0], 2), ("c2g", [0], 2),
+                                             ("c3", [7], 2), ("c4", [30, 31], 2),
+                                             ("c5", [62, 63], 2), ("osprey_2l", [0], 2),
+                                             ("c2b", [0], 2), ("dflash_4l", [0], 2)])
 def test_full_size_sampled_sequences_match_oracle(name, seqs, iters):
     """Benchmark-size shapes in the launch configuration the benchmark uses; the oracle
     follows the sampled sequences one by one (sequences of a batch are independent)."""
@@ -271,6 +287,7 @@ def test_full_size_sampled_sequences_match_oracle(name, seqs, iters):
     w = synth.get(name)
     stats = _run_parity(w, iters, seqs, 2e-2)
     assert stats["compared"] >= len(seqs)
+    _assert_exact_comparisons(stats, name)
 
 
 def test_block_with_packed_rows_matches_oracle():

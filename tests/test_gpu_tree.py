@@ -198,8 +198,10 @@ def test_draft_tree_matches_oracle(wl, topk, depth, n_nodes, seqs):
             assert err <= 2e-2, (wl, step, b, err)
             max_err = max(max_err, err)
             if not (np.array_equal(tk[b], t.tokens) and np.array_equal(pr[b], t.parents)):
-                assert t.min_gap < 4.0 * err + 1e-9, (wl, step, b, tk[b], t.tokens, pr[b],
-                                                       t.parents, t.min_gap, err)
+                near = parity.tree_near_tie_keys(t, 4.0 * err + 1e-9)
+                assert parity.tree_mismatch_excused(_path_keys(tk[b], pr[b]),
+                                                    _path_keys(t.tokens, t.parents), near), \
+                    (wl, step, b, tk[b], t.tokens, pr[b], t.parents, t.min_gap, err)
                 flagged += 1
             # commit: the first child of each node for two levels, then the root's first child
             path, cur = [], -1

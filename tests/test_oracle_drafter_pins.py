@@ -201,3 +201,55 @@ def test_pruned_backbone_sizes(key, kw, vocab):
     c_cols = w.n_layers * w.qkv_rows * w.d_model
     n = body_param_count(w) - c_cols - w.d_model * w.tap_width + vocab * w.d_model + w.d_model
     assert abs(n - printed) <= rounding / 2, (key, n)
+
+
+def _hf_model_mapped(w, weights, d2t):
+    """transformers' Qwen3 over target ids: its output layer holds, for every target id,
+    the LM-head row that maps to it (zero when none does; those ids are masked below)."""
+    lm = np.zeros((w.vocab_target, w.d_model))
+    rows = np.flatnonzero(d2t >= 0)
+    lm[d2t[rows]] = np.asarray(weights["lm_head"], dtype=np.float64)[rows]
+    return _hf_model(w, dict(weights, lm_head=lm))
+
+
+@pytest.mark.parametrize("vmap,V_d", [("identity", 97), ("inject", 61)])
+def test_greedy_chain_equals_library_qwen3_greedy_continuation(vmap, V_d):
+    """Section 3.4's autoregressive loop (step k >= 1 feeds draft k-1 at position
+    committed + k - 1).  With the expansion columns zero (Eq. 3) the fed-back hidden
+    state is multiplied by zero, so the drafter is its pruned backbone and a T = 0
+    chain of K drafts must be transformers' Qwen3 greedy continuation of the committed
+    prefix: the same fed tokens at the same positions, logits within the float32-RoPE
+    tolerance, drafts emitted as target ids through the vocabulary map.  The prefix
+    arrives in two draft calls, the first one's drafts rolled back, so the committed
+    length carried between calls is pinned as well."""
+    w = _tiny(expansion="zero", vocab_draft=V_d, vocab_map=vmap, K=5)
+    weights = synth.make_weights(w)
+    d2t = synth.make_d2t(w)
+    dr = Drafter(w, weights, d2t)
+    prefix = synth.prompt_tokens(w, 2, 13)
+    taps = np.random.default_rng(12).standard_normal((13, w.tap_width))
+    seq = Sequence(w, 32)
+    _, _, _, committed = dr.draft(seq, prefix[:9], taps[:9], 2, 0.0, np.zeros(2))
+    assert committed == 9
+    dr.rollback(seq, committed)
+    drafts, logits, rows, committed = dr.draft(seq, prefix[9:], taps[9:], w.K, 0.0, np.zeros(w.K))
+    assert committed == 13
+    m = _hf_model_mapped(w, weights, d2t)
+    reach = np.zeros(w.vocab_target, dtype=bool)
+    reach[d2t[d2t >= 0]] = True
+    ids = [int(t) for t in prefix]
+    for k in range(w.K):
+        ref = _hf_logits(m, ids)[-1]
+        ref[~reach] = -np.inf
+        ours = np.full(w.vocab_target, -np.inf)
+        mapped = d2t >= 0
+        ours[d2t[mapped]] = logits[k][mapped]
+        assert np.array_equal(np.isfinite(ours), np.isfinite(ref))
+        fin = np.isfinite(ref)
+        np.testing.assert_allclose(ours[fin], ref[fin], atol=2e-6, rtol=0)
+        top2 = np.sort(ref[fin])[-2:]
+        assert top2[1] - top2[0] > 1e-4          # no near tie: the argmax is decided
+        nxt = int(np.argmax(ref))
+        assert int(drafts[k]) == nxt, (k, int(drafts[k]), nxt)
+        assert int(d2t[rows[k]]) == nxt
+        ids.append(nxt)
