@@ -12,11 +12,16 @@ region.  Because the whole path is deterministic, a first (untimed) pass
 records the trajectory and its target logits; the timed pass replays it from
 the same starting state.
 
+The timed iterations run twice: as stream launches, and each iteration as one
+HIP graph (osprey_graph_capture, captured before the timed region over that
+iteration's staged inputs); the faster mode gives the headline and both are
+reported.
+
 Prints one JSON line: whole-job draft+verify tokens/s (sum over sequences of
 accepted drafts + 1 per iteration, divided by the time of the draft_step and
-verify calls), µs per draft step, the LM-head kernel against the HBM roofline
-(timed with HIP events on the library's stream), and the CPU oracle on a
-bounded sample.
+verify calls), µs per draft step, the LM-head kernel and the attention against
+the HBM roofline (timed with HIP events on the library's stream), and the CPU
+oracle on a bounded sample (all cores and one thread).
 """
 from __future__ import annotations
 
@@ -41,6 +46,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="time stream launches only (no HIP-graph pass)")
+    ap.add_argument("--long-contexts", default="16384,32768",
+                    help="batch-1 attention is also timed at these contexts ('' = none)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="first copy a buffer of this many MiB device-to-device three times "
                          "(a reference for HBM traffic counters)")
@@ -76,6 +85,20 @@ def step_bytes(w, ctx_mean: float) -> dict:
     lm = w.vocab_draft * d * el
     kv = w.batch * ctx_mean * L * 2 * w.n_kv_heads * hd * el
     return dict(body=body, lm=lm, kv=kv, total=body + lm + kv)
+
+
+def iteration_bytes(w, sb: dict) -> int:
+    """Algorithmic bytes of one iteration (all sequences): the ingest pass (W_c, the
+    body, the LM head over each sequence's last row, the context), K - 1 autoregressive
+    steps (the same without W_c), the K drafter logit rows written, and verification
+    (the K + 1 target rows and one drafter row per sequence).  Block drafting: one pass
+    (W_c, body, context, one LM head) and the same verification."""
+    el = 2 if w.dtype == "bf16" else 4
+    wc = w.tap_width * w.d_model * el
+    verify = w.batch * ((w.K + 1) * w.vocab_target + w.vocab_draft) * 4
+    logits = w.batch * w.K * w.vocab_draft * 4
+    steps = 1 if w.drafting == "block" else w.K
+    return int(wc + steps * sb["total"] + logits + verify)
 
 
 def measured_traffic(workload: str):
@@ -155,25 +178,36 @@ def run_gpu(args):
     assert (got == rec_accept[args.warmup:]).all(), "replay diverged from the recorded trajectory"
     tokens = int((got + 1).sum())
     elapsed = max(gpu_ms / 1e3, 1e-9)
-    res = dict(tokens=tokens, seconds=elapsed, wall=wall, mean_accept=float(got.mean()))
+    res = dict(tokens=tokens, seconds=elapsed, wall=wall, mean_accept=float(got.mean()),
+               modes={"stream": dict(seconds=elapsed, tokens=tokens)})
+    if not args.no_graph and args.warmup >= 1:
+        res["modes"]["graph"] = time_graph(s, w, staged, args.warmup, n_it, rec_accept, rewind,
+                                           replay, out)
+    res["trajectory"] = rec_accept
 
     # ---- per-call and per-kernel timing: the same steps again, with HIP events on the
     #      library's stream; each event idles the stream for a few microseconds, so one
     #      replay brackets whole calls only and another the LM-head launches only -----------
     if not args.no_kernel_timing:
         kt = {}
-        for fams in ((BD.KERNEL_DRAFT_STEP, BD.KERNEL_VERIFY), (BD.KERNEL_LM_HEAD,)):
+        for fams in ((BD.KERNEL_DRAFT_STEP, BD.KERNEL_VERIFY), (BD.KERNEL_LM_HEAD,),
+                     (BD.KERNEL_ATTENTION,)):
             rewind()
             replay(0, args.warmup)
             s.drafter.kernel_timing(fams)
             replay(args.warmup, n_it)
             torch.cuda.synchronize()
             for name, fam in (("lm_head", BD.KERNEL_LM_HEAD), ("verify", BD.KERNEL_VERIFY),
-                              ("draft_step", BD.KERNEL_DRAFT_STEP)):
+                              ("draft_step", BD.KERNEL_DRAFT_STEP),
+                              ("attention", BD.KERNEL_ATTENTION)):
                 if fam in fams:
                     kt[name] = s.drafter.kernel_time(fam)
             s.drafter.kernel_timing(())
         res["kernels"] = kt
+        res["attention_bytes"] = attention_bytes(w, s.ctx, rec_accept, args.warmup, n_it)
+        lens = [int(c) for c in args.long_contexts.split(",") if c.strip()]
+        if lens and w.dtype == "bf16" and w.batch == 1 and w.drafting == "chain":
+            res["attention_long"] = [time_attention_long(w, c) for c in lens]
         res["tree_verify"] = time_tree_verify(s, w)
         if w.dtype == "bf16" and w.K >= TREE_TOPK:
             rewind()
@@ -181,6 +215,116 @@ def run_gpu(args):
     assert s.drafter.device_errors() == 0
     res["ctx_mean"] = float(np.mean(s.ctx))
     return w, res
+
+
+def time_graph(s, w, staged, warmup, n_it, rec_accept, rewind, replay, out):
+    """The timed iterations again, each launched as one HIP graph (osprey_graph_capture
+    of its pending draft call + verification over its staged inputs, captured before the
+    timed region), on a stream of its own; the trajectory must be the recorded one."""
+    import torch
+
+    import synth
+    dev, B = s.device, w.batch
+    torch.cuda.synchronize()
+    prev = s.drafter.stream
+    st = torch.cuda.Stream(device=dev)
+    s.drafter.set_stream(st)
+    rewind()
+    replay(0, warmup)
+    accs = [torch.empty(B, dtype=torch.int32, device=dev) for _ in range(warmup, n_it)]
+    mask = synth.mask_token(w) if w.drafting == "block" else None
+    graphs = []
+    for j, it in enumerate(range(warmup, n_it)):
+        inp, tl = staged[it]
+        graphs.append(s.drafter.capture_iteration(
+            list(range(B)), w.K, inp.taps, s.draft_temperature, inp.u_draft, out.drafts,
+            out.logits, tl, s.temperature, inp.u_accept, inp.u_bonus, accs[j], out.mask,
+            out.tokens, max_context=int(s.drafter.cfg.max_seq_len), taps_stride=w.K + 1,
+            mask_token=mask))
+    st.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(st)
+    for g in graphs:
+        g.launch()
+    ev1.record(st)
+    st.synchronize()
+    ms = ev0.elapsed_time(ev1)
+    got = torch.stack(accs).cpu().numpy()
+    assert (got == rec_accept[warmup:]).all(), "graph replay diverged from the recorded trajectory"
+    for g in graphs:
+        g.close()
+    s.drafter.set_stream(prev)
+    return dict(seconds=max(ms / 1e3, 1e-9), tokens=int((got + 1).sum()))
+
+
+def attention_bytes(w, ctx, traj, warmup: int, n_it: int) -> int:
+    """Algorithmic bytes of every attention pass of the timed iterations: each sequence's
+    context keys and values once per layer and pass.  Iteration `it` of sequence b
+    commits L = ctx_b + sum_{j<it} (a_j + 1) positions; its ingest pass reads L of them,
+    chain step k (1 <= k < K) reads L + k, a block pass L + K - 1."""
+    import numpy as np
+    el = 2 if w.dtype == "bf16" else 4
+    tok = w.n_layers * 2 * w.n_kv_heads * w.head_dim * el
+    total = 0
+    for b in range(w.batch):
+        L = int(ctx[b])
+        for it in range(n_it):
+            if it > 0:
+                L += int(traj[it - 1][b]) + 1
+            if it < warmup:
+                continue
+            if w.drafting == "block":
+                total += (L + w.K - 1) * tok
+            else:
+                total += (L * w.K + w.K * (w.K - 1) // 2) * tok
+    return int(total)
+
+
+def time_attention_long(w, ctx_len: int, iters: int = 3):
+    """Batch-1 attention (split pass + merge) of the drafter's AR steps at a long
+    context: the same attention shape (heads, head dim, layers) with a small vocabulary
+    (the attention does not depend on it), `iters` draft calls of K steps from the
+    same committed prefix, HIP-event time per launch against each launch's context
+    bytes."""
+    import torch
+
+    import synth
+    from paper_2609_09338_amd import binding as BD
+    from paper_2609_09338_amd import workload as WL
+    wl = w.with_(name=f"{w.name}_ctx{ctx_len}", vocab_draft=4096, vocab_target=4096,
+                 target_hidden=256, ctx_lo=ctx_len, ctx_hi=ctx_len)
+    s = WL.make_drafter(wl, 1)
+    WL.reset_sequences(s)
+    out = WL.alloc_outputs(s)
+    inp = WL.iter_inputs(s, 0)
+    # (a drafted slot is verified before it is rewound; any target logits do)
+    tl = torch.zeros((1, wl.K + 1, wl.vocab_target), dtype=torch.float32, device=s.device)
+    WL.draft(s, 0, inp, out)
+    WL.verify(s, inp, tl, out)
+    torch.cuda.synchronize()
+    el = 2 if wl.dtype == "bf16" else 4
+    tok = 2 * wl.n_kv_heads * wl.head_dim * el
+    s.drafter.kernel_timing((BD.KERNEL_ATTENTION,))
+    nbytes = 0
+    for _ in range(iters):
+        s.drafter.seq_truncate(0, ctx_len - 1)
+        WL.draft(s, 0, inp, out)
+        WL.verify(s, inp, tl, out)
+        # ingest pass: ctx positions; AR step k: ctx + k (per layer)
+        nbytes += wl.n_layers * tok * (ctx_len * wl.K + wl.K * (wl.K - 1) // 2)
+    torch.cuda.synchronize()
+    ms, n = s.drafter.kernel_time(BD.KERNEL_ATTENTION)
+    s.drafter.kernel_timing(())
+    assert s.drafter.device_errors() == 0
+    single_ms = ms / 8.0                # every timed pair ran 8 times between its events
+    launches = n // 8
+    gbs = nbytes / (single_ms * 1e-3) / 1e9
+    s.drafter.close()
+    del s
+    torch.cuda.empty_cache()
+    return dict(context=ctx_len, batch=1, us_per_launch=round(single_ms * 1e3 / max(launches, 1), 3),
+                bytes_per_launch=int(nbytes / max(launches, 1)), achieved_gbs=round(gbs, 1),
+                frac=round(gbs / HBM_PEAK_GBS, 4))
 
 
 TREE_NODES, TREE_TOPK = 15, 4
@@ -268,24 +412,36 @@ def time_tree_draft(s, w, ctx_mean: float, reps: int = 10):
 
 
 def run_cpu_baseline(w, seconds: float):
-    """The oracle, untuned, on one sequence of the same workload for ~`seconds`."""
-    import numpy as np
-    from threadpoolctl import threadpool_info
+    """The oracle, untuned, on one sequence of the same workload for ~`seconds`, twice:
+    with every core of this process's affinity mask available to numpy's BLAS, and with
+    one thread.  `cores` is the affinity mask's size; the all-core run is the headline
+    figure and the one-thread run is reported next to it."""
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     from oracle import harness as OH
+    cores = len(os.sched_getaffinity(0))
     dr = OH.build_drafter(w)
-    t0 = time.perf_counter()
-    tokens, iters = 0, 0
-    seq_iters = OH.run_sequence_timed(w, 0, 512, seconds, drafter=dr)
-    for it in seq_iters:
-        tokens += it.result.accept_len + 1
-        iters += 1
-    dt = time.perf_counter() - t0
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    return dict(value=tokens / dt, unit="tokens/s", cores=int(threads), kind="oracle",
-                sample=f"{iters} iteration(s) of sequence 0 of workload {w.name} "
+
+    def run(threads):
+        with threadpool_limits(limits=threads):
+            used = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+            t0 = time.perf_counter()
+            tokens, iters = 0, 0
+            for it in OH.run_sequence_timed(w, 0, 512, seconds, drafter=dr):
+                tokens += it.result.accept_len + 1
+                iters += 1
+            dt = time.perf_counter() - t0
+        return tokens / dt, iters, dt, used
+
+    v_all, it_all, dt_all, used_all = run(cores)
+    v_one, it_one, dt_one, _ = run(1)
+    return dict(value=v_all, unit="tokens/s", cores=cores, kind="oracle",
+                blas_threads=int(used_all),
+                single_thread={"value": v_one, "unit": "tokens/s", "cores": 1,
+                               "sample": f"{it_one} iteration(s), {dt_one:.1f} s"},
+                sample=f"{it_all} iteration(s) of sequence 0 of workload {w.name} "
                        f"(K={w.K}, {w.K} drafter forward passes + verify each), "
-                       f"{dt:.1f} s incl. setup, numpy float64")
+                       f"{dt_all:.1f} s incl. setup, numpy float64")
 
 
 def main():
@@ -298,9 +454,14 @@ def main():
         copy_calibration(args.calibrate_copy_mib)
     w, r = run_gpu(args)
     K = args.steps
-    ms_per_step = r["seconds"] * 1e3 / K
-    value = r["tokens"] / r["seconds"]
+    # the faster launch mode is the headline; both are reported
+    modes = r["modes"]
+    mode = min(modes, key=lambda m: modes[m]["seconds"])
+    seconds, tokens = modes[mode]["seconds"], modes[mode]["tokens"]
+    ms_per_step = seconds * 1e3 / K
+    value = tokens / seconds
     sb = step_bytes(w, r["ctx_mean"])
+    it_bytes = iteration_bytes(w, sb)
     line = {
         "metric": "draft+verify tokens/s per GPU; µs per draft step at batch 1; % HBM peak",
         "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1, "steps": K,
@@ -318,7 +479,13 @@ def main():
                                + (", block drafting" if w.drafting == "block" else ""),
                    "batch": w.batch, "K": w.K},
         "mean_accepted_drafts": round(r["mean_accept"], 3),
-        "tokens_timed": r["tokens"],
+        "tokens_timed": tokens,
+        "launch_mode": mode,
+        "launch_modes": {m: {"ms_per_step": round(v["seconds"] * 1e3 / K, 4),
+                             "tokens_per_s": round(v["tokens"] / v["seconds"], 2)}
+                         for m, v in modes.items()},
+        "iteration_algorithmic_bytes": int(it_bytes),
+        "iteration_hbm_frac": round(it_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
     }
     kt = r.get("kernels")
     if kt:
@@ -355,6 +522,20 @@ def main():
             line["ar_step_algorithmic_bytes"] = int(sb["total"])
             ar_us = ds_ms * 1e3 / max(ds_n, 1) / w.K
             line["draft_token_hbm_frac"] = round(sb["total"] / (ar_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+        at_ms, at_n = kt["attention"]
+        if at_n:
+            # every timed attention pass ran 8 times between its events
+            at_s = at_ms / 8.0 * 1e-3
+            at_gbs = r["attention_bytes"] / at_s / 1e9
+            line["attention_roofline"] = {
+                "bound": "hbm", "kernel": "attention (paged split pass + split merge), every pass "
+                "of the timed iterations", "achieved": round(at_gbs, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(at_gbs / HBM_PEAK_GBS, 4),
+                "us_per_launch": round(at_s * 1e6 / max(at_n // 8, 1), 3),
+                "bytes_per_launch": int(r["attention_bytes"] / max(at_n // 8, 1)),
+                "launches": at_n // 8}
+        if "attention_long" in r:
+            line["attention_long_context"] = r["attention_long"]
         line["tree_verify"] = r["tree_verify"]
         if "tree_draft" in r:
             line["tree_draft"] = r["tree_draft"]

@@ -356,6 +356,37 @@ int osprey_verify_rows(osprey_handle* h, const osprey_verify_rows_args* a);
  * osprey_verify_tree_args).  No slot state is involved. */
 int osprey_verify_tree(osprey_handle* h, const osprey_verify_tree_args* a);
 
+/* One steady-state iteration as a HIP graph.  At batch 1 an iteration is a chain of
+ * about a hundred dependent kernels, each short enough that its launch is a large
+ * part of its cost; the drafter's latency is what its shallow depth buys (Section
+ * 3.2), so the iteration can be captured once and replayed with one launch.
+ *
+ * osprey_graph_capture records, without running it, a pending-mode draft call
+ * (osprey_draft_step, or osprey_draft_block when mask_token >= 0) followed by
+ * osprey_verify with these arguments, into a graph (osprey_graph, host handle).
+ * The graph reads and writes exactly the buffers the arguments name, at these
+ * addresses: write each iteration's inputs (taps, temperatures, uniforms, target
+ * logits) there before launching it, stream-ordered.  Requirements: step->n_new ==
+ * NULL (the ingest is the tokens the last verification committed), the same batch,
+ * K and slots in both argument sets, taps_stride >= K + 1, kernel timing off, and a
+ * stream other than the null stream (osprey_set_stream).  Attention is planned for
+ * contexts up to max_context positions (<= max_seq_len): every launch must keep each
+ * slot's committed length + pending tokens + K - 1 within it.  Capturing changes no
+ * state and enqueues nothing; errors are those of the two calls.
+ *
+ * osprey_graph_launch enqueues one iteration on the handle's stream: the same
+ * checks as the two calls (every slot VERIFIED, capacity within its pages and
+ * max_context, else OSPREY_E_STATE / OSPREY_E_CAPACITY with nothing enqueued) and
+ * the same state transitions (the slots end VERIFIED).  The graph stays valid
+ * across launches; osprey_graph_destroy releases it (after the stream has finished
+ * with it). */
+typedef struct osprey_graph osprey_graph;
+int osprey_graph_capture(osprey_handle* h, const osprey_step_args* step, int32_t mask_token,
+                         const osprey_verify_args* verify, int32_t max_context,
+                         osprey_graph** out /* (host) */);
+int osprey_graph_launch(osprey_handle* h, osprey_graph* g);
+int osprey_graph_destroy(osprey_graph* g);
+
 /* Synchronise, read and clear the device error flags (host out):
  * bit 0 an ingest row count outside [1, max new rows] (pending without verify),
  * bit 1 a token id outside [0, V_T), bit 2 a sequence beyond its KV pages,
@@ -366,13 +397,13 @@ int osprey_device_errors(osprey_handle* h, uint32_t* flags);
 /* Kernel timing for roofline reports.  `families` is a bit mask: bit f enables HIP
  * event timing of family f on the handle's stream (0 disables; every call clears
  * the records).  Families: 0 = LM head (final norm + vocabulary GEMV + softmax
- * statistics), 1 = attention (split pass), 2 = verify (all four kernels), 3 = a
- * whole draft_step, 4 = expanded-QKV GEMV.  Each event adds a few microseconds of
- * idle time to the stream, so time few families at once.  A timed LM head runs
- * 8 times back to back between its events (the same outputs again), so its events'
- * overhead is shared by 8 launches.  osprey_kernel_time synchronises and returns
- * the summed duration (ms) and the number of launches since the last
- * osprey_kernel_timing call. */
+ * statistics), 1 = attention (split pass + split merge), 2 = verify (all its
+ * kernels), 3 = a whole draft_step, 4 = expanded-QKV GEMV.  Each event adds a few
+ * microseconds of idle time to the stream, so time few families at once.  A timed
+ * LM head, and a timed attention, runs 8 times back to back between its events
+ * (the same outputs again), so its events' overhead is shared by 8 launches.
+ * osprey_kernel_time synchronises and returns the summed duration (ms) and the
+ * number of launches since the last osprey_kernel_timing call. */
 int osprey_kernel_timing(osprey_handle* h, int32_t families);
 int osprey_kernel_time(osprey_handle* h, int32_t family, double* total_ms, int64_t* launches);
 

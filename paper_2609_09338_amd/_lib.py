@@ -5,7 +5,9 @@ import ctypes as C
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libosprey.so")
+# OSPREY_LIB names another build of the same library (the host-sanitized one of the CPU
+# tests); there is no fallback either way
+LIB_PATH = os.environ.get("OSPREY_LIB") or os.path.join(_HERE, "libosprey.so")
 
 OSPREY_OK, OSPREY_E_INVALID, OSPREY_E_SHAPE, OSPREY_E_CAPACITY, OSPREY_E_STATE, \
     OSPREY_E_DEVICE, OSPREY_E_UNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
@@ -95,6 +97,10 @@ SIGNATURES = {
     "osprey_kernel_time": (C.c_int, [_H, C.c_int32, C.POINTER(C.c_double),
                                      C.POINTER(C.c_int64)]),
     "osprey_set_stream": (C.c_int, [_H, _P]),
+    "osprey_graph_capture": (C.c_int, [_H, C.POINTER(osprey_step_args), C.c_int32,
+                                       C.POINTER(osprey_verify_args), C.c_int32, C.POINTER(_P)]),
+    "osprey_graph_launch": (C.c_int, [_H, _P]),
+    "osprey_graph_destroy": (C.c_int, [_P]),
     "osprey_draft_destroy": (C.c_int, [_H]),
     "osprey_last_error": (C.c_char_p, []),
 }

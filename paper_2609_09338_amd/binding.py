@@ -175,22 +175,8 @@ class Drafter:
         _need(draft_logits, B * K * c.vocab_draft, torch.float32, "draft_logits")
         if n_new is not None:
             _need(new_tokens, int(sum(n_new)), torch.int32, "new_tokens")
-        a = L.osprey_step_args()
-        a.batch = B
-        a.K = K
-        sl = _i32_array(slots)
-        a.slots = C.cast(sl, C.POINTER(C.c_int32))
-        nn = None
-        if n_new is not None:
-            nn = _i32_array(n_new)
-            a.n_new = C.cast(nn, C.POINTER(C.c_int32))
-        a.new_tokens = _ptr(new_tokens)
-        a.taps = _ptr(taps)
-        a.taps_stride = taps_stride
-        a.temperature = _ptr(temperature)
-        a.u_draft = _ptr(u_draft)
-        a.draft_tokens = _ptr(draft_tokens)
-        a.draft_logits = _ptr(draft_logits)
+        a, keep = _step_args(slots, K, taps, temperature, u_draft, n_new, new_tokens,
+                             taps_stride, draft_tokens, draft_logits)
         if mask_token is None:
             _check(_lib().osprey_draft_step(self.h, C.byref(a)))
         else:
@@ -244,20 +230,48 @@ class Drafter:
         _need(accept_mask, B * K, torch.uint8, "accept_mask")
         _need(out_tokens, B * (K + 1), torch.int32, "out_tokens")
         _need(draft_temperature, B, torch.float32, "draft_temperature")
-        a = L.osprey_verify_args()
-        a.batch = B
-        a.K = K
-        sl = _i32_array(slots)
-        a.slots = C.cast(sl, C.POINTER(C.c_int32))
-        a.target_logits = _ptr(target_logits)
-        a.temperature = _ptr(temperature)
-        a.u_accept = _ptr(u_accept)
-        a.u_bonus = _ptr(u_bonus)
-        a.accept_len = _ptr(accept_len)
-        a.accept_mask = _ptr(accept_mask)
-        a.out_tokens = _ptr(out_tokens)
-        a.draft_temperature = _ptr(draft_temperature)
+        a, keep = _verify_args(slots, K, target_logits, temperature, u_accept, u_bonus,
+                               accept_len, accept_mask, out_tokens, draft_temperature)
         _check(_lib().osprey_verify(self.h, C.byref(a)))
+
+    # -- one iteration as a HIP graph ---------------------------------------------------
+    def set_stream(self, stream) -> None:
+        """Enqueue subsequent calls on `stream` (a torch.cuda.Stream)."""
+        _check(_lib().osprey_set_stream(self.h, C.c_void_p(stream.cuda_stream)))
+        self.stream = stream
+
+    def capture_iteration(self, slots, K: int, taps, draft_temperature, u_draft, draft_tokens,
+                          draft_logits, target_logits, temperature, u_accept, u_bonus,
+                          accept_len, accept_mask, out_tokens, max_context: int,
+                          taps_stride: int, mask_token=None) -> "IterationGraph":
+        """osprey_graph_capture: a pending-mode draft call and its verification recorded
+        as one HIP graph over exactly these buffers (see IterationGraph)."""
+        torch, c = self.torch, self.cfg
+        B = len(slots)
+        _need(taps, B * taps_stride * c.n_taps * c.target_hidden, self._wdtype, "taps")
+        _need(draft_temperature, B, torch.float32, "draft_temperature")
+        _need(u_draft, B * K, torch.float32, "u_draft")
+        _need(draft_tokens, B * K, torch.int32, "draft_tokens")
+        _need(draft_logits, B * K * c.vocab_draft, torch.float32, "draft_logits")
+        _need(target_logits, B * (K + 1) * c.vocab_target, torch.float32, "target_logits")
+        _need(temperature, B, torch.float32, "temperature")
+        _need(u_accept, B * K, torch.float32, "u_accept")
+        _need(u_bonus, B, torch.float32, "u_bonus")
+        _need(accept_len, B, torch.int32, "accept_len")
+        _need(accept_mask, B * K, torch.uint8, "accept_mask")
+        _need(out_tokens, B * (K + 1), torch.int32, "out_tokens")
+        sa, k1 = _step_args(slots, K, taps, draft_temperature, u_draft, None, None, taps_stride,
+                            draft_tokens, draft_logits)
+        va, k2 = _verify_args(slots, K, target_logits, temperature, u_accept, u_bonus,
+                              accept_len, accept_mask, out_tokens, draft_temperature)
+        g = C.c_void_p()
+        _check(_lib().osprey_graph_capture(self.h, C.byref(sa),
+                                           -1 if mask_token is None else int(mask_token),
+                                           C.byref(va), int(max_context), C.byref(g)))
+        # the graph holds raw pointers: keep the tensors alive with it
+        return IterationGraph(self, g, (taps, draft_temperature, u_draft, draft_tokens,
+                                        draft_logits, target_logits, temperature, u_accept,
+                                        u_bonus, accept_len, accept_mask, out_tokens))
 
     def verify_rows(self, K: int, target_logits, draft_logits, draft_tokens, temperature,
                     u_accept, u_bonus, accept_len, accept_mask, out_tokens,
@@ -348,6 +362,67 @@ class Drafter:
             self.close()
         except Exception:
             pass
+
+
+class IterationGraph:
+    """A captured iteration (osprey_graph_*): launch() enqueues it on the drafter's
+    stream; close() releases it (after the stream has finished with it)."""
+
+    def __init__(self, drafter: Drafter, g, tensors):
+        self.drafter, self.g, self._tensors = drafter, g, tensors
+
+    def launch(self) -> None:
+        _check(_lib().osprey_graph_launch(self.drafter.h, self.g))
+
+    def close(self) -> None:
+        if getattr(self, "g", None):
+            _lib().osprey_graph_destroy(self.g)
+            self.g = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _step_args(slots, K, taps, temperature, u_draft, n_new, new_tokens, taps_stride,
+               draft_tokens, draft_logits):
+    a = L.osprey_step_args()
+    a.batch = len(slots)
+    a.K = K
+    sl = _i32_array(slots)
+    a.slots = C.cast(sl, C.POINTER(C.c_int32))
+    nn = None
+    if n_new is not None:
+        nn = _i32_array(n_new)
+        a.n_new = C.cast(nn, C.POINTER(C.c_int32))
+    a.new_tokens = _ptr(new_tokens)
+    a.taps = _ptr(taps)
+    a.taps_stride = taps_stride
+    a.temperature = _ptr(temperature)
+    a.u_draft = _ptr(u_draft)
+    a.draft_tokens = _ptr(draft_tokens)
+    a.draft_logits = _ptr(draft_logits)
+    return a, (sl, nn)
+
+
+def _verify_args(slots, K, target_logits, temperature, u_accept, u_bonus, accept_len,
+                 accept_mask, out_tokens, draft_temperature):
+    a = L.osprey_verify_args()
+    a.batch = len(slots)
+    a.K = K
+    sl = _i32_array(slots)
+    a.slots = C.cast(sl, C.POINTER(C.c_int32))
+    a.target_logits = _ptr(target_logits)
+    a.temperature = _ptr(temperature)
+    a.u_accept = _ptr(u_accept)
+    a.u_bonus = _ptr(u_bonus)
+    a.accept_len = _ptr(accept_len)
+    a.accept_mask = _ptr(accept_mask)
+    a.out_tokens = _ptr(out_tokens)
+    a.draft_temperature = _ptr(draft_temperature)
+    return a, (sl,)
 
 
 KERNEL_LM_HEAD, KERNEL_ATTENTION, KERNEL_VERIFY, KERNEL_DRAFT_STEP, KERNEL_QKV = range(5)

@@ -67,9 +67,56 @@ def build(jobs: int = 6, debug: bool = False, verbose: bool = True) -> str:
     return LIB
 
 
+# Sources whose host code holds the library's logic (validation, planning, the slot
+# state machine, the graph entry points); the other sources' host code is
+# kernel-launch stubs.
+HOST_LOGIC = ["osprey.cpp"]
+SANITIZED = os.path.join(BUILD, "sanitized", "libosprey.so")
+
+
+def build_sanitized(verbose: bool = True) -> str:
+    """A build of the library whose host code in HOST_LOGIC is instrumented with
+    AddressSanitizer and UndefinedBehaviorSanitizer (host only: no GPU code is
+    instrumented; the other objects are the regular ones).  The sanitizer runtime is
+    not linked in: load the library into a process that preloads it."""
+    if not all(os.path.exists(os.path.join(BUILD, os.path.splitext(s)[0] + ".o")) for s in SOURCES):
+        build(verbose=False)
+    out = os.path.dirname(SANITIZED)
+    os.makedirs(out, exist_ok=True)
+    objs = []
+    for src in SOURCES:
+        obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+        if src in HOST_LOGIC:
+            obj = os.path.join(out, os.path.splitext(src)[0] + ".o")
+            cmd = [hipcc()] + flags(False) + [
+                "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer",
+                "-g", "-c", os.path.join(CSRC, src), "-o", obj]
+            if src.endswith(".cpp"):
+                cmd[1:1] = ["-x", "hip"]
+            r = subprocess.run(cmd, capture_output=True, text=True)
+            if r.returncode != 0:
+                raise RuntimeError(f"compiling {src} (sanitized) failed:\n{r.stdout}\n{r.stderr}")
+        objs.append(obj)
+    tmp = SANITIZED + ".tmp"
+    r = subprocess.run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs,
+                       capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"linking the sanitized library failed:\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, SANITIZED)
+    if verbose:
+        print(f"built {SANITIZED}", file=sys.stderr)
+    return SANITIZED
+
+
 if __name__ == "__main__":
     ap = argparse.ArgumentParser()
     ap.add_argument("--jobs", type=int, default=6)
     ap.add_argument("--debug", action="store_true")
+    ap.add_argument("--sanitize", action="store_true",
+                    help="build the host-sanitized library instead (see build_sanitized)")
     args = ap.parse_args()
-    build(args.jobs, args.debug)
+    if args.sanitize:
+        build_sanitized()
+    else:
+        build(args.jobs, args.debug)

@@ -307,6 +307,10 @@ struct SetupArgs {
 };
 void launch_setup(const SetupArgs& a, hipStream_t st);
 
+// Sets the message osprey_last_error() returns on this thread ("" with OSPREY_OK) and
+// returns `code`.
+int report_error(int code, const char* msg);
+
 // Verification.
 struct VerifyArgs {
   int B;
@@ -331,9 +335,9 @@ struct VerifyArgs {
   const QStat* qstat;
   int ld_qstat;
   double* res_part;         // [B][nchunk_t][2]: residual and p sums per chunk
+  double* res_sub;          // [B][nchunk_t][kVSub][2]: the same per 64 consecutive ids
   int32_t* vstate;          // [B][4]: a, argmax of p_a, one-hot drafter row of q_a (T_d = 0)
   double* vstat;            // [B][4]: M_a, S_a (target), m_a, s_a (draft)
-  uint32_t* counters;       // [2*B] last-arriver counters
   int32_t* accept_len;
   uint8_t* accept_mask;
   int32_t* out_tokens;
@@ -353,6 +357,7 @@ struct VerifyArgs {
 };
 void launch_verify(const VerifyArgs& a, hipStream_t st);
 constexpr int kMaxTreeNodes = 64;
+constexpr int kVSub = 64;     // 64-id sub-ranges per 4096-id verification chunk
 void launch_verify_tree(const VerifyArgs& a, hipStream_t st);
 
 // Draft-tree growth (see tree.hip).

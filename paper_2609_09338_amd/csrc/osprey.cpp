@@ -83,9 +83,9 @@ struct Ws {
   float* u_zero;
   float* v_part;
   double* v_res;
+  double* v_sub;
   int32_t* vstate;
   double* vstat;
-  uint32_t* counters;
   int32_t* tree_removed;
   // draft-tree growth
   void* tree_kv;              // [B * kMaxTreeProc][n_layers][2][nkv][hd], cache dtype
@@ -219,9 +219,9 @@ size_t plan(const osprey_config& c, char* base, Ws* w) {
     W.b_temp = (float*)take(4L * rows);
   }
   W.v_res = (double*)take(16L * D.B * D.nchunk_t);
+  W.v_sub = (double*)take(16L * kVSub * D.B * D.nchunk_t);
   W.vstate = (int32_t*)take(16L * D.B);
   W.vstat = (double*)take(32L * D.B);
-  W.counters = (uint32_t*)take(8L * D.B);
   return (off + 255) & ~size_t(255);
 }
 
@@ -266,6 +266,17 @@ int validate(const osprey_config* c) {
   return ok();
 }
 
+}  // namespace
+
+namespace osp {
+int report_error(int code, const char* msg) {
+  g_err = msg ? msg : "";
+  return code;
+}
+}  // namespace osp
+
+namespace {
+
 struct TimerRec {
   int family;
   hipEvent_t a, b;
@@ -294,6 +305,9 @@ struct osprey_handle {
   std::vector<int> last_slots;
   float* last_logits = nullptr;
   long last_ld_b = 0;
+  // graph capture: attention splits are planned for contexts up to this bound (0: the
+  // call's own contexts), so that replays of a captured iteration stay covered
+  long ctx_plan = 0;
   // timing: bit f of `timing` enables event timing of family f
   int timing = 0;
   std::vector<TimerRec> timers;
@@ -345,8 +359,8 @@ int hip_last() {
 // Context splits of the attention: fixed-length pieces (a multiple of one page).
 // Every block pays a fixed start-up (query staging, page-table and first page
 // latency) and end (wavefront merge, partial write), so splits are as long as
-// possible while the grid still holds about 320 working blocks (a little over one
-// per CU), but not beyond kEvenSplitLen tokens, so that sequences of very different
+// possible while the grid still holds the target number of working blocks (below),
+// but not beyond kEvenSplitLen tokens, so that sequences of very different
 // lengths still split into blocks of about equal work; no sequence needs more than
 // kMaxSplit of them, and a split is at most kMaxSplitLen tokens (64 pages per
 // wavefront of the attention kernel).
@@ -354,7 +368,10 @@ struct SplitPlan {
   int n_split, split_len;
 };
 SplitPlan plan_splits(const osprey_handle* h, long ctx_max, long ctx_total, int max_split = kMaxSplit) {
-  const long target_blocks = 320;
+  // one sequence: as many blocks as can be resident (two per CU: the kernel's register
+  // and LDS budget), the most pages in flight for a long context; several sequences: a
+  // little over one per CU, which keeps the ragged batches' blocks of about equal work
+  const long target_blocks = ctx_total <= ctx_max ? 2L * h->n_cu : 320;
   long len = (ctx_total * h->cfg.n_kv_heads + target_blocks - 1) / target_blocks;
   len = std::min<long>(std::max<long>(len, 64), kEvenSplitLen);
   len = std::max<long>(len, (ctx_max + max_split - 1) / max_split);
@@ -364,6 +381,20 @@ SplitPlan plan_splits(const osprey_handle* h, long ctx_max, long ctx_total, int 
   p.split_len = (int)len;
   p.n_split = (int)std::max<long>(1, (ctx_max + len - 1) / len);
   return p;
+}
+
+// Attention over the cache and the merge of its context splits.  Timed (family 1),
+// the pair runs kTimedRepeats times back to back between the events: it is idempotent
+// (a new row's keys and values are written again with the same values, every output is
+// overwritten), so the events' own overhead is shared by as many launches.
+void run_attention(osprey_handle* h, const AttnArgs& a) {
+  const int t = h->t_begin(1);
+  const int reps = t >= 0 ? kTimedRepeats : 1;
+  for (int rep = 0; rep < reps; ++rep) {
+    launch_attention(h->cfg.dtype, a, h->stream);
+    launch_attn_combine(a, h->stream);
+  }
+  h->t_end(t, reps);
 }
 
 // One forward pass of the body over `rows`; `s` holds the conditioning rows.
@@ -437,10 +468,7 @@ void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, c
     a.part = W.attn_part;
     a.o = W.o;
     a.err = W.err;
-    t = h->t_begin(1);
-    launch_attention(c.dtype, a, h->stream);
-    h->t_end(t);
-    launch_attn_combine(a, h->stream);
+    run_attention(h, a);
     // O projection + residual
     GemvArgs go{};
     go.max_rows = rows.max_rows;
@@ -613,10 +641,7 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
       launch_rows_qkv(c.dtype, a, W.o, h->stream);
       a.q_prep = W.o;
     }
-    t = h->t_begin(1);
-    launch_attention(c.dtype, a, h->stream);
-    h->t_end(t);
-    launch_attn_combine(a, h->stream);
+    run_attention(h, a);
     // O projection; residual + post-attention RMSNorm
     GemvArgs go = gb;
     go.ld_xa = nq * hd;
@@ -833,9 +858,9 @@ void fill_verify_common(osprey_handle* h, VerifyArgs& v, int B, int K) {
   v.nchunk_d = h->D.nchunk_d;
   v.part = h->W.v_part;
   v.res_part = h->W.v_res;
+  v.res_sub = h->W.v_sub;
   v.vstate = h->W.vstate;
   v.vstat = h->W.vstat;
-  v.counters = h->W.counters;
   v.err = h->W.err;
 }
 
@@ -933,8 +958,7 @@ OSPREY_API int osprey_draft_init(const osprey_config* cfg, const osprey_weights*
       hipMemset(W.pend_tok, 0, 4L * B * (cfg->max_k + 1)) != hipSuccess ||
       hipMemset(W.err, 0, 16) != hipSuccess ||
       hipMemset(W.u_zero, 0, 4L * B * h->D.Km) != hipSuccess ||
-      hipMemset(W.n_cand, 0, 4L * B) != hipSuccess ||
-      hipMemset(W.counters, 0, 8 * B) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
+      hipMemset(W.n_cand, 0, 4L * B) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
     return bail(fail(OSPREY_E_DEVICE, "clearing the workspace failed"));
   *out = h;
   return ok();
@@ -1058,6 +1082,10 @@ int step_ingest(osprey_handle* h, const osprey_step_args* a, int K, int extra, S
     return fail(OSPREY_E_CAPACITY, "%ld new rows exceed max_new_rows", rows);
 
   const Ws& W = h->W;
+  if (h->ctx_plan > 0) {
+    ctx_max = std::max(ctx_max, h->ctx_plan);
+    ctx_total = std::max(ctx_total, h->ctx_plan * B);
+  }
   split = plan_splits(h, ctx_max, ctx_total, max_split);
   if (split.n_split > max_split)
     return fail(OSPREY_E_UNSUPPORTED, "a context of %ld positions needs %d splits (at most %d)", ctx_max,
@@ -1433,6 +1461,127 @@ OSPREY_API int osprey_verify_tree(osprey_handle* h, const osprey_verify_tree_arg
   launch_verify_tree(v, h->stream);
   h->t_end(t);
   return hip_last();
+}
+
+// ---- one steady-state iteration as a HIP graph -------------------------------------------
+struct osprey_graph {
+  osprey_handle* h = nullptr;
+  hipGraphExec_t exec = nullptr;
+  int B = 0, K = 0, taps_stride = 0;
+  long max_context = 0;
+  std::vector<int> slots;
+};
+
+namespace {
+
+// Positions a pending iteration of `g` may reach on `slot`: its committed length, the
+// pending ingest and the K - 1 positions past it (chain steps or block mask rows).
+long graph_need(const osprey_handle* h, const osprey_graph* g, int slot) {
+  const SlotHost& s = h->slots[slot];
+  return s.len_max + (s.drafted_k + 1) + (g->K - 1);
+}
+
+}  // namespace
+
+OSPREY_API int osprey_graph_capture(osprey_handle* h, const osprey_step_args* step, int32_t mask_token,
+                                    const osprey_verify_args* v, int32_t max_context, osprey_graph** out) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (!step || !v || !out) return fail(OSPREY_E_INVALID, "arguments are NULL");
+  if (!h->stream) return fail(OSPREY_E_INVALID, "capture needs a stream other than the null stream (osprey_set_stream)");
+  if (h->timing) return fail(OSPREY_E_STATE, "kernel timing is on: disable it (osprey_kernel_timing(h, 0)) before capturing");
+  if (step->n_new) return fail(OSPREY_E_INVALID, "a captured iteration ingests the pending tokens: n_new must be NULL");
+  const int B = step->batch, K = step->K;
+  if (B < 1 || B > h->cfg.max_batch || K < 1) return fail(OSPREY_E_INVALID, "batch %d / K %d", B, K);
+  if (v->batch != B || v->K != K || !step->slots || !v->slots)
+    return fail(OSPREY_E_INVALID, "draft and verify arguments must have the same batch, K and slots");
+  for (int b = 0; b < B; ++b)
+    if (step->slots[b] != v->slots[b]) return fail(OSPREY_E_INVALID, "draft and verify slots differ at %d", b);
+  if (max_context < 1 || max_context > h->cfg.max_seq_len)
+    return fail(OSPREY_E_INVALID, "max_context %d not in [1, %d]", max_context, h->cfg.max_seq_len);
+  if (step->taps_stride < K + 1) return fail(OSPREY_E_INVALID, "taps_stride %d < K + 1", step->taps_stride);
+  osprey_graph probe;
+  probe.K = K;
+  for (int b = 0; b < B; ++b) {
+    if ((rc = check_slot(h, step->slots[b]))) return rc;
+    if (graph_need(h, &probe, step->slots[b]) > max_context)
+      return fail(OSPREY_E_CAPACITY, "slot %d already needs more than max_context %d positions", step->slots[b], max_context);
+  }
+  // the calls below validate everything else and update the host state as if they ran:
+  // keep that state and put it back afterwards (launches advance it)
+  const std::vector<SlotHost> saved = h->slots;
+  const int sB = h->last_B, sK = h->last_K;
+  const std::vector<int> sslots = h->last_slots;
+  float* slog = h->last_logits;
+  const long sld = h->last_ld_b;
+  hipError_t e = hipStreamBeginCapture(h->stream, hipStreamCaptureModeThreadLocal);
+  if (e != hipSuccess) return fail(OSPREY_E_DEVICE, "hipStreamBeginCapture: %s", hipGetErrorString(e));
+  h->ctx_plan = max_context;
+  rc = mask_token < 0 ? osprey_draft_step(h, step) : osprey_draft_block(h, step, mask_token);
+  if (rc == OSPREY_OK) rc = osprey_verify(h, v);
+  h->ctx_plan = 0;
+  const std::string msg = g_err;
+  hipGraph_t graph = nullptr;
+  e = hipStreamEndCapture(h->stream, &graph);
+  h->slots = saved;
+  h->last_B = sB;
+  h->last_K = sK;
+  h->last_slots = sslots;
+  h->last_logits = slog;
+  h->last_ld_b = sld;
+  if (rc != OSPREY_OK) {
+    if (graph) hipGraphDestroy(graph);
+    g_err = msg;
+    return rc;
+  }
+  if (e != hipSuccess || !graph) return fail(OSPREY_E_DEVICE, "hipStreamEndCapture: %s", hipGetErrorString(e));
+  hipGraphExec_t exec = nullptr;
+  e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+  hipGraphDestroy(graph);
+  if (e != hipSuccess) return fail(OSPREY_E_DEVICE, "hipGraphInstantiate: %s", hipGetErrorString(e));
+  osprey_graph* g = new osprey_graph();
+  g->h = h;
+  g->exec = exec;
+  g->B = B;
+  g->K = K;
+  g->taps_stride = step->taps_stride;
+  g->max_context = max_context;
+  g->slots.assign(step->slots, step->slots + B);
+  *out = g;
+  return ok();
+}
+
+OSPREY_API int osprey_graph_launch(osprey_handle* h, osprey_graph* g) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (!g || g->h != h) return fail(OSPREY_E_INVALID, "graph is NULL or was captured on another handle");
+  for (int slot : g->slots) {
+    const SlotHost& s = h->slots[slot];
+    if (s.state != S_VERIFIED) return fail(OSPREY_E_STATE, "slot %d has no verified tokens pending", slot);
+    if (s.drafted_k + 1 > g->taps_stride)
+      return fail(OSPREY_E_INVALID, "slot %d: %d pending rows exceed the captured taps_stride %d", slot,
+                  s.drafted_k + 1, g->taps_stride);
+    const long need = graph_need(h, g, slot);
+    if (need > g->max_context || need > (long)s.nblocks * h->cfg.kv_block)
+      return fail(OSPREY_E_CAPACITY, "slot %d: up to %ld positions exceed the graph's max_context %ld or its pages",
+                  slot, need, g->max_context);
+  }
+  HIP_TRY(hipGraphLaunch(g->exec, h->stream));
+  for (int slot : g->slots) {
+    SlotHost& s = h->slots[slot];
+    s.len_max += s.drafted_k + 1;
+    s.drafted_k = g->K;
+    s.state = S_VERIFIED;
+  }
+  h->last_B = 0;
+  return ok();
+}
+
+OSPREY_API int osprey_graph_destroy(osprey_graph* g) {
+  if (!g) return ok();
+  if (g->exec) hipGraphExecDestroy(g->exec);
+  delete g;
+  return ok();
 }
 
 OSPREY_API int osprey_device_errors(osprey_handle* h, uint32_t* flags) {

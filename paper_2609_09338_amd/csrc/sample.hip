@@ -25,7 +25,7 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
   __shared__ int s_wi[4];
   __shared__ double s_scan[4];
   __shared__ double s_before;
-  __shared__ int s_blk, s_row;
+  __shared__ int s_blk, s_row, s_map;
 
   const int k = a.block ? (int)blockIdx.y : a.k;  // (block drafting: proposal k of sequence b)
   const int prow = a.block ? b * a.K + k : b;     // its records' and logits' row
@@ -139,10 +139,12 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
       const int r1 = min(r0 + a.blk_rows, a.V);
       const float* lg = a.logits + (long)b * a.ld_logits + (a.block ? (long)k * a.V : 0L);
       float pre[kScanPre];
+      int pmap[kScanPre];   // the range's vocabulary map, requested with its logits
 #pragma unroll
       for (int q = 0; q < kScanPre; ++q) {
         const int i = r0 + q * OSP_WAVE + lane;
         pre[q] = i < r1 ? lg[i] : -INFINITY;
+        pmap[q] = a.d2t[min(i, a.V - 1)];
       }
       double run = s_before;
       int last_pos = -1, found = -1;
@@ -161,13 +163,21 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
         if (hit) { found = c0 + __builtin_ctzll(hit); break; }
         run += (double)__shfl(inc, 63, OSP_WAVE);
       }
-      if (lane == 0) s_row = found >= 0 ? found : (last_pos >= 0 ? last_pos : am);
+      const int pick = found >= 0 ? found : (last_pos >= 0 ? last_pos : am);
+      // its target id from the prefetched map when it lies in the prefetched part
+      int dmap = -2;
+#pragma unroll
+      for (int q = 0; q < kScanPre; ++q) {
+        const int l = pick - r0 - q * OSP_WAVE;
+        if (l >= 0 && l < OSP_WAVE) dmap = __shfl(pmap[q], l, OSP_WAVE);
+      }
+      if (lane == 0) { s_row = pick; s_map = dmap; }
     }
     __syncthreads();
     row = s_row;
   }
   row = min(max(row, 0), a.V - 1);
-  const int d = a.d2t[row];
+  const int d = (T > 0.f && M > -INFINITY && s_map != -2 && s_row == row) ? s_map : a.d2t[row];
   if (tid == 0) {
     a.drafts[(long)b * a.ld_drafts + k] = d;
     if (a.drafts_out) a.drafts_out[(long)b * a.K + k] = d;

@@ -14,20 +14,26 @@
 //                          by the draft step's sampling kernel)
 //   k_vaccept (B)          merges chunks in order; accepts d_k while
 //                          u_k < min(1, p_k(d_k)/q_k(d_k)) (T = 0: d_k equals
-//                          the target argmax); writes a, the mask and d_0..d_{a-1}
-//   k_vresid  (B x chunks) per chunk of target row a: sum of the residual
-//                          max(0, p_a - q_a) (q = 0 when a = K) and of p_a
-//   k_vfinal  (B)          inverse CDF over the residual (or p_a if it is empty)
-//                          in ascending target ids -> the token at index a;
-//                          stateful verify also records the a + 1 committed
-//                          tokens as the slot's pending ingest
+//                          the target argmax); writes a, the mask and d_0..d_{a-1};
+//                          at T = 0 also the token at index a (the argmax of p_a)
+//   k_vresid  (B x chunks) per chunk of target row a (T > 0): sums of the residual
+//                          max(0, p_a - q_a) (q = 0 when a = K) and of p_a, per
+//                          64-id sub-range and per chunk
+//   k_vfinal  (B, one wavefront) inverse CDF over the residual (or p_a if it is
+//                          empty) in ascending target ids: chunk, sub-range, id
+//                          -> the token at index a
 //
-// Draft trees (deterministic top-k children, accepted in turn with the target's
-// probability renormalised over the children not yet rejected; the bonus from the
-// target without the rejected tokens): k_vstats over the K + 1 target rows, then
-//   k_tree_walk (B)        row statistics, every node's target probability in its
-//                          parent's row, the walk from the root; the last node's
-//                          row and rejected tokens go to k_vresid / k_vfinal
+// Either way the stateful verify records the a + 1 committed tokens as the slot's
+// pending ingest.  Draft trees (deterministic top-k children, accepted in turn with
+// the target's probability renormalised over the children not yet rejected; the bonus
+// from the target without the rejected tokens) replace k_vaccept by k_tree_walk (B),
+// which walks the tree from the root; the last node's row and rejected tokens go to
+// k_vresid / k_vfinal.
+//
+// (Finishing a sequence in the last block of the statistics or residual kernel to
+// arrive, instead of in the small kernels, needs an agent-scope release before the
+// arrival count -- an L2 write-back per block -- and measured slower: 48.6 against
+// 45.4 us at batch 1, 1031 against 118 us at batch 64.)
 #include "common.h"
 #include "internal.h"
 
@@ -64,13 +70,8 @@ OSP_DEV void block_stats(float& m, int& am, double& s, float* sm, int* si, doubl
 // sum, and the chunk needs no block barrier.  Four jobs per block.
 constexpr int kVWaveElems = 4096 / 64;   // elements per lane (chunk / 64)
 
-__global__ void __launch_bounds__(kVThreads) k_vstats(VerifyArgs a) {
-  const int b = blockIdx.x;
+OSP_DEV void chunk_stats(const VerifyArgs& a, int b, int j, int nt, int nj) {
   const int lane = threadIdx.x & 63;
-  const int j = blockIdx.y * (kVThreads / 64) + (threadIdx.x >> 6);
-  const int nt = (a.K + 1) * a.nchunk_t;
-  const int nj = nt + (a.qstat || a.tree_par ? 0 : a.K * a.nchunk_d);
-  if (j >= nj) return;
   const float* row;
   int V, c;
   if (j < nt) {
@@ -177,15 +178,28 @@ OSP_DEV void merge_row(const float* p, int n, float T, float& M, double& S, int&
   S = wave_sum_d(s);
 }
 
-// One block per sequence: all row statistics are merged in parallel (one
-// wavefront per row), then thread k decides draft k, and the accepted length is
-// the first rejection.
-__global__ void __launch_bounds__(kVThreads) k_vaccept(VerifyArgs a) {
+// The token at index idx of sequence b's output, and (stateful verify) the slot's
+// pending ingest: d_0 .. d_{A-1}, then `tok`.  One thread.
+OSP_DEV void finalize(const VerifyArgs& a, int b, int idx, int A, int tok) {
+  a.out_tokens[(long)b * (a.K + 1) + idx] = tok;
+  if (a.bslot) {
+    const int slot = a.bslot[b];
+    const int32_t* dr = a.drafts + (long)b * a.ld_drafts;
+    a.pend_n[slot] = A + 1;
+    for (int k = 0; k < A; ++k) a.pend_tok[(long)slot * a.pend_ld + k] = dr[k];
+    a.pend_tok[(long)slot * a.pend_ld + A] = tok;
+  }
+}
+
+// Acceptance of sequence b's chain (one block): the chunk records of every row are
+// merged in parallel (one wavefront per row), thread k decides draft k, and the
+// accepted length is the first rejection.  At T = 0 the sequence is finished here (the
+// next token is the argmax of row a).
+OSP_DEV void accept_tail(const VerifyArgs& a, int b) {
   __shared__ float s_M[2 * 64 + 1];
   __shared__ double s_S[2 * 64 + 1];
   __shared__ int s_am[2 * 64 + 1];
   __shared__ int s_ok[64];
-  const int b = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int K = a.K;
   const int nt = (K + 1) * a.nchunk_t;
@@ -259,6 +273,8 @@ __global__ void __launch_bounds__(kVThreads) k_vaccept(VerifyArgs a) {
     // greedy drafting: the drafter row q_a is one-hot at (-1: no drafter row / a = K)
     a.vstate[b * 4 + 2] = (dq && !(Td > 0.f)) ? s_am[K + 1 + A] : -1;
   }
+  __syncthreads();   // (the token at index A is written after the -1 above)
+  if (tid == 0 && !(T > 0.f)) finalize(a, b, A, A, s_am[A]);
 }
 
 // Residual weight max(0, p(v) - q(v)) and p(v) of target id v in row a.  The
@@ -287,6 +303,15 @@ struct ResidRow {
     if (!dl || s < 0) return 0.0;
     if (!(Td > 0.f)) return s == onehot ? 1.0 : 0.0;
     return l > -INFINITY ? (double)__expf((l - Md) / Td) * iSd : 0.0;
+  }
+  // Residual weight (which = 0) or target probability (which = 1) of id v (0 at or past V).
+  OSP_DEV double eval_one(int v, int V, int which) const {
+    const bool in = v < V;
+    const float t = in ? tl[v] : -INFINITY;
+    const int s = (in && dl && !which) ? t2d[v] : -1;
+    const float d = (s >= 0 && Td > 0.f) ? dl[s] : -INFINITY;
+    const double p = t > -INFINITY ? (double)__expf((t - Mt) / T) * iSt : 0.0;
+    return which ? p : resid(p, v, s, d);
   }
   // Residual weights (which = 0) or target probabilities (which = 1) of the kVPer
   // ids i0 + q*stride, q < kVPer (0 past V_T); all loads of a phase are issued together.
@@ -329,12 +354,113 @@ OSP_DEV ResidRow resid_row(const VerifyArgs& a, int b) {
   return r;
 }
 
-// Per chunk of target row a: the sums of the residual weights and of p.  Only the
-// chunk totals are kept (k_vfinal rescans the chosen chunk in id order), so thread t
-// takes ids t, t + 256, ...: every wavefront load is 256 contiguous bytes, and both
-// sums come from one pass over the row.
+// Sums of V = 2^LOGV float64 values per lane over the 64 lanes at once: on return
+// v[0] of lane l holds the total of value index l >> (6 - LOGV) (V + 6 shuffle steps
+// instead of 6 V).  Fixed order.
+template <int LOGV>
+OSP_DEV double transpose_reduce_d(double* v, int lane) {
+  constexpr int V = 1 << LOGV;
+#pragma unroll
+  for (int s = 0; s < LOGV; ++s) {
+    const int m = 32 >> s;
+    const int h = (V >> s) >> 1;
+    const bool hi = (lane & m) != 0;
+#pragma unroll
+    for (int i = 0; i < h; ++i) {
+      const double mine = hi ? v[i + h] : v[i];
+      const double other = hi ? v[i] : v[i + h];
+      v[i] = mine + __shfl_xor(other, m, OSP_WAVE);
+    }
+  }
+#pragma unroll
+  for (int m = 32 >> LOGV; m >= 1; m >>= 1) v[0] += __shfl_xor(v[0], m, OSP_WAVE);
+  return v[0];
+}
+static_assert(kVPer == 16 && kVSub == 4 * kVPer, "one sub-range per (id group q, wavefront)");
+
+// The draw of sequence b (one wavefront): the inverse CDF over the residual (or over
+// p_a if the residual is empty) in ascending target ids, in three steps -- the chunk (totals in order), the 64-id
+// sub-range within it (its kVSub sums), the id (one id per lane) -- each falling back,
+// where rounding leaves the draw point past the last positive entry, to the last
+// positive entry of that level.
+OSP_DEV void final_tail(const VerifyArgs& a, int b, const ResidRow& rr) {
+  const int lane = threadIdx.x & 63;
+  if (threadIdx.x >= 64) return;
+  const int n = a.nchunk_t;
+  const double* rp = a.res_part + (long)b * n * 2;
+  double W = 0.0;
+  for (int c0 = 0; c0 < n; c0 += 64) {
+    const int c = c0 + lane;
+    W += wave_sum_d(c < n ? rp[c * 2] : 0.0);
+  }
+  const int which = W > 0.0 ? 0 : 1;
+  double tot = W;
+  if (which) {
+    tot = 0.0;
+    for (int c0 = 0; c0 < n; c0 += 64) {
+      const int c = c0 + lane;
+      tot += wave_sum_d(c < n ? rp[c * 2 + 1] : 0.0);
+    }
+  }
+  const double target = (double)a.u_bonus[b] * tot;
+  // 1. the chunk
+  double run = 0.0, before = 0.0, before_last = 0.0;
+  int ch = -1, last = -1;
+  for (int c0 = 0; c0 < n && ch < 0; c0 += 64) {
+    const int c = c0 + lane;
+    const double v = c < n ? rp[c * 2 + which] : 0.0;
+    const double inc = wave_incl_scan<double>(v);
+    const unsigned long long pos = __ballot(c < n && v > 0.0);
+    if (pos) {
+      const int l = 63 - __builtin_clzll(pos);
+      last = c0 + l;
+      before_last = run + __shfl(inc, l, OSP_WAVE) - __shfl(v, l, OSP_WAVE);
+    }
+    const unsigned long long hit = __ballot(c < n && v > 0.0 && run + inc > target);
+    if (hit) {
+      const int l = __builtin_ctzll(hit);
+      ch = c0 + l;
+      before = run + __shfl(inc, l, OSP_WAVE) - __shfl(v, l, OSP_WAVE);
+    }
+    run += __shfl(inc, 63, OSP_WAVE);
+  }
+  int tok = -1;
+  if (ch < 0 && last >= 0) { ch = last; before = before_last; }
+  if (ch >= 0) {
+    // 2. the 64-id sub-range (j covers ids ch * chunk + (j / 4) * 256 + (j % 4) * 64 ..)
+    const double* sub = a.res_sub + ((long)b * n + ch) * kVSub * 2;
+    const double v = sub[lane * 2 + which];
+    const double inc = wave_incl_scan<double>(v);
+    const unsigned long long pos = __ballot(v > 0.0);
+    const unsigned long long hit = __ballot(v > 0.0 && before + inc > target);
+    int j = -1;
+    if (hit) j = __builtin_ctzll(hit);
+    else if (pos) j = 63 - __builtin_clzll(pos);
+    if (j >= 0) {
+      const double before2 = before + __shfl(inc, j, OSP_WAVE) - __shfl(v, j, OSP_WAVE);
+      // 3. the id
+      const int i1 = min(a.V_T, ch * a.chunk + a.chunk);
+      const int id = ch * a.chunk + (j >> 2) * kVThreads + (j & 3) * 64 + lane;
+      const double x = rr.eval_one(id, i1, which);
+      const double inc2 = wave_incl_scan<double>(x);
+      const unsigned long long pos2 = __ballot(x > 0.0);
+      const unsigned long long hit2 = __ballot(x > 0.0 && before2 + inc2 > target);
+      if (hit2) tok = __shfl(id, __builtin_ctzll(hit2), OSP_WAVE);
+      else if (pos2) tok = __shfl(id, 63 - __builtin_clzll(pos2), OSP_WAVE);
+    }
+  }
+  if (tok < 0) tok = a.vstate[b * 4 + 1];   // nothing positive at all: the argmax
+  if (lane == 0)
+    finalize(a, b, a.tree_par ? a.accept_len[b] : a.vstate[b * 4 + 0], a.vstate[b * 4 + 0], tok);
+}
+
+// Per chunk of target row a: the sums of the residual weights and of p, per 64-id
+// sub-range and per chunk (the chunk total is the ordered sum of its sub-ranges).
+// Thread t takes ids t, t + 256, ... of the chunk: every wavefront load is 256
+// contiguous bytes, and both sums come from one pass over the row.  Greedy sequences
+// (T = 0) were finished by the acceptance.
 __global__ void __launch_bounds__(kVThreads) k_vresid(VerifyArgs a) {
-  __shared__ double sw_[kVThreads / 64], sp_[kVThreads / 64];
+  __shared__ double s_sub[kVSub][2];
   const int b = blockIdx.x, c = blockIdx.y;
   if (!(a.temp[b] > 0.f)) return;
   const ResidRow rr = resid_row(a, b);
@@ -353,152 +479,54 @@ __global__ void __launch_bounds__(kVThreads) k_vresid(VerifyArgs a) {
   float dv[kVPer];
 #pragma unroll
   for (int q = 0; q < kVPer; ++q) dv[q] = (sidx[q] >= 0 && rr.Td > 0.f) ? rr.dl[sidx[q]] : -INFINITY;
-  double sw = 0.0, sp = 0.0;
+  double sw[kVPer], sp[kVPer];
 #pragma unroll
   for (int q = 0; q < kVPer; ++q) {
     const double p = tv[q] > -INFINITY ? (double)__expf((tv[q] - rr.Mt) / rr.T) * rr.iSt : 0.0;
-    sw += rr.resid(p, i0 + q * kVThreads, sidx[q], dv[q]);
-    sp += p;
+    sw[q] = rr.resid(p, i0 + q * kVThreads, sidx[q], dv[q]);
+    sp[q] = p;
   }
-  // fixed-order block sums in float64
-  sw = wave_sum_d(sw);
-  sp = wave_sum_d(sp);
-  if (lane == 0) { sw_[wave] = sw; sp_[wave] = sp; }
+  // the 64 ids of (q, this wavefront) are consecutive: one sub-range each
+  const double tw = transpose_reduce_d<4>(sw, lane);
+  const double tp = transpose_reduce_d<4>(sp, lane);
+  if ((lane & 3) == 0) {
+    s_sub[(lane >> 2) * 4 + wave][0] = tw;
+    s_sub[(lane >> 2) * 4 + wave][1] = tp;
+  }
   __syncthreads();
+  double* sub = a.res_sub + ((long)b * a.nchunk_t + c) * kVSub * 2;
+  if (tid < kVSub) {
+    sub[tid * 2 + 0] = s_sub[tid][0];
+    sub[tid * 2 + 1] = s_sub[tid][1];
+  }
   if (tid == 0) {
-    double tw = 0.0, tp = 0.0;
-    for (int w = 0; w < kVThreads / 64; ++w) { tw += sw_[w]; tp += sp_[w]; }
-    a.res_part[((long)b * a.nchunk_t + c) * 2 + 0] = tw;
-    a.res_part[((long)b * a.nchunk_t + c) * 2 + 1] = tp;
+    double w = 0.0, pp = 0.0;
+    for (int j = 0; j < kVSub; ++j) { w += s_sub[j][0]; pp += s_sub[j][1]; }
+    a.res_part[((long)b * a.nchunk_t + c) * 2 + 0] = w;
+    a.res_part[((long)b * a.nchunk_t + c) * 2 + 1] = pp;
   }
 }
 
-__global__ void __launch_bounds__(kVThreads) k_vfinal(VerifyArgs a) {
-  __shared__ double sm[4];
-  __shared__ int s_chunk, s_tok;
-  __shared__ double s_before, s_target;
-  __shared__ int s_wlast[kVThreads / 64];
-  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int A = a.vstate[b * 4 + 0];
-  const float T = a.temp[b];
-  int tok;
-  if (!(T > 0.f)) {
-    tok = a.vstate[b * 4 + 1];
-  } else {
-    const ResidRow rr = resid_row(a, b);
-    if (wave == 0) {
-      // chunk totals in order: which = 0 residual, 1 = p (when the residual is empty)
-      const double* rp = a.res_part + (long)b * a.nchunk_t * 2;
-      double W = 0.0;
-      for (int c0 = 0; c0 < a.nchunk_t; c0 += 64) {
-        const int c = c0 + lane;
-        W += wave_sum_d(c < a.nchunk_t ? rp[c * 2] : 0.0);
-      }
-      const int which = W > 0.0 ? 0 : 1;
-      double tot = W;
-      if (which) {
-        tot = 0.0;
-        for (int c0 = 0; c0 < a.nchunk_t; c0 += 64) {
-          const int c = c0 + lane;
-          tot += wave_sum_d(c < a.nchunk_t ? rp[c * 2 + 1] : 0.0);
-        }
-      }
-      const double target = (double)a.u_bonus[b] * tot;
-      double run = 0.0;
-      int ch = -1;
-      double before = 0.0;
-      for (int c0 = 0; c0 < a.nchunk_t; c0 += 64) {
-        const int c = c0 + lane;
-        const double v = c < a.nchunk_t ? rp[c * 2 + which] : 0.0;
-        const double inc = wave_incl_scan<double>(v);
-        const unsigned long long hit = __ballot(c < a.nchunk_t && v > 0.0 && run + inc > target);
-        if (hit) {
-          const int l = __builtin_ctzll(hit);
-          ch = c0 + l;
-          before = run + __shfl(inc, l, OSP_WAVE) - __shfl(v, l, OSP_WAVE);
-          break;
-        }
-        run += __shfl(inc, 63, OSP_WAVE);
-      }
-      if (ch < 0) {                      // rounding: the last chunk
-        ch = a.nchunk_t - 1;
-        before = run - rp[(long)ch * 2 + which];
-      }
-      if (lane == 0) {
-        s_chunk = ch * 2 + which;
-        s_before = before;
-        s_target = target;
-        s_tok = -1;
-      }
-    }
-    __syncthreads();
-    const int ch = s_chunk >> 1, which = s_chunk & 1;
-    const int c0 = ch * a.chunk;
-    const int i1 = min(a.V_T, c0 + a.chunk);
-    const int t0 = c0 + tid * kVPer;
-    double x[kVPer];
-    rr.eval_many(t0, 1, i1, which, x);
-    double loc = 0.0;
-#pragma unroll
-    for (int q = 0; q < kVPer; ++q) loc += x[q];
-    double incl_l, tot_l;
-    const double excl_l = block_scan<kVThreads, double>(loc, sm, incl_l, tot_l);
-    const double target = s_target;
-    const double excl = s_before + excl_l;
-    if (excl <= target && s_before + incl_l > target) {
-      double run = excl;
-      int hit = -1;
-#pragma unroll
-      for (int q = 0; q < kVPer; ++q) {
-        if (hit < 0 && t0 + q < i1 && x[q] > 0.0) {
-          if (run + x[q] > target) hit = q; else run += x[q];
-        }
-      }
-      if (hit >= 0) s_tok = t0 + hit;
-    }
-    __syncthreads();
-    if (s_tok < 0) {     // rounding: the last positive id of the chunk
-      int last = -1;
-#pragma unroll
-      for (int q = 0; q < kVPer; ++q)
-        if (t0 + q < i1 && x[q] > 0.0) last = t0 + q;
-      const int wl = wave_max_i(last);
-      if (lane == 0) s_wlast[wave] = wl;
-      __syncthreads();
-      if (tid == 0) {
-        int best = -1;
-        for (int w = 0; w < kVThreads / 64; ++w) best = max(best, s_wlast[w]);
-        s_tok = best >= 0 ? best : a.vstate[b * 4 + 1];
-      }
-    }
-    __syncthreads();
-    tok = s_tok;
-  }
-  if (tid == 0) {
-    // (draft trees: the bonus follows the accepted path)
-    a.out_tokens[(long)b * (a.K + 1) + (a.tree_par ? a.accept_len[b] : A)] = tok;
-    if (a.bslot) {
-      const int slot = a.bslot[b];
-      a.pend_n[slot] = A + 1;
-      for (int k = 0; k <= A; ++k)
-        a.pend_tok[(long)slot * a.pend_ld + k] = a.out_tokens[(long)b * (a.K + 1) + k];
-    }
-  }
+// One wavefront per sequence: the draw (final_tail) over the residual kernel's sums.
+__global__ void __launch_bounds__(64) k_vfinal(VerifyArgs a) {
+  const int b = blockIdx.x;
+  if (!(a.temp[b] > 0.f)) return;
+  final_tail(a, b, resid_row(a, b));
 }
 
-// One block per sequence.  Every node's token, parent, uniform and target logit in its
-// parent's row are read at once (thread c: node c), the K + 1 row statistics merged
-// in parallel (one wavefront per row); one thread then walks the tree from the root:
-// the children of a node follow it in index order, so the walk ends within K steps.
-__global__ void __launch_bounds__(kVThreads) k_tree_walk(VerifyArgs a) {
+// Walk of sequence b's draft tree (one block).  Every node's token, parent, uniform and target logit in its parent's row are read at
+// once (thread c: node c), the K + 1 row statistics merged in parallel (one wavefront
+// per row); one thread then walks the tree from the root: the children of a node
+// follow it in index order, so the walk ends within K steps.  At T = 0 the bonus (the
+// argmax of the last node's row) is written here.
+OSP_DEV void walk_tail(const VerifyArgs& a, int b) {
   __shared__ float s_M[kMaxTreeNodes + 1];
   __shared__ double s_S[kMaxTreeNodes + 1];
   __shared__ int s_am[kMaxTreeNodes + 1];
   __shared__ int s_tok[kMaxTreeNodes], s_par[kMaxTreeNodes], s_path[kMaxTreeNodes];
   __shared__ float s_lt[kMaxTreeNodes], s_u[kMaxTreeNodes];
   __shared__ int s_rem[kMaxTreeNodes];
-  __shared__ int s_A, s_nrem;
-  const int b = blockIdx.x;
+  __shared__ int s_A, s_nrem, s_row;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int N = a.K;
   const float T = a.temp[b];
@@ -554,6 +582,7 @@ __global__ void __launch_bounds__(kVThreads) k_tree_walk(VerifyArgs a) {
     s_A = A;
     s_nrem = T > 0.f ? nrem : 0;
     const int row = cur + 1;
+    s_row = row;
     a.accept_len[b] = A;
     a.vstate[b * 4 + 0] = row;
     a.vstate[b * 4 + 1] = s_am[row];
@@ -570,14 +599,28 @@ __global__ void __launch_bounds__(kVThreads) k_tree_walk(VerifyArgs a) {
   for (int i = tid; i < N; i += kVThreads) a.tree_path[(long)b * N + i] = i < A ? s_path[i] : -1;
   for (int i = tid; i <= N; i += kVThreads)
     if (i != A) a.out_tokens[(long)b * (N + 1) + i] = i < A ? s_tok[s_path[i]] : -1;
+  if (tid == 0 && !(T > 0.f)) finalize(a, b, A, A, s_am[s_row]);
 }
+
+// Chunk statistics of every target row (and, for verify_rows, drafter row), one
+// wavefront per 4096-id chunk.
+__global__ void __launch_bounds__(kVThreads) k_vstats(VerifyArgs a) {
+  const int b = blockIdx.x;
+  const int j = blockIdx.y * (kVThreads / 64) + (threadIdx.x >> 6);
+  const int nt = (a.K + 1) * a.nchunk_t;
+  const int nj = nt + (a.qstat || a.tree_par ? 0 : a.K * a.nchunk_d);
+  if (j < nj) chunk_stats(a, b, j, nt, nj);
+}
+
+__global__ void __launch_bounds__(kVThreads) k_vaccept(VerifyArgs a) { accept_tail(a, blockIdx.x); }
+__global__ void __launch_bounds__(kVThreads) k_tree_walk(VerifyArgs a) { walk_tail(a, blockIdx.x); }
 
 void launch_verify_tree(const VerifyArgs& a, hipStream_t st) {
   const int nj = (a.K + 1) * a.nchunk_t;
   hipLaunchKernelGGL(k_vstats, dim3(a.B, (nj + kVThreads / 64 - 1) / (kVThreads / 64)), dim3(kVThreads), 0, st, a);
   hipLaunchKernelGGL(k_tree_walk, dim3(a.B), dim3(kVThreads), 0, st, a);
   hipLaunchKernelGGL(k_vresid, dim3(a.B, a.nchunk_t), dim3(kVThreads), 0, st, a);
-  hipLaunchKernelGGL(k_vfinal, dim3(a.B), dim3(kVThreads), 0, st, a);
+  hipLaunchKernelGGL(k_vfinal, dim3(a.B), dim3(64), 0, st, a);
 }
 
 void launch_verify(const VerifyArgs& a, hipStream_t st) {
@@ -585,7 +628,7 @@ void launch_verify(const VerifyArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(k_vstats, dim3(a.B, (nj + kVThreads / 64 - 1) / (kVThreads / 64)), dim3(kVThreads), 0, st, a);
   hipLaunchKernelGGL(k_vaccept, dim3(a.B), dim3(kVThreads), 0, st, a);
   hipLaunchKernelGGL(k_vresid, dim3(a.B, a.nchunk_t), dim3(kVThreads), 0, st, a);
-  hipLaunchKernelGGL(k_vfinal, dim3(a.B), dim3(kVThreads), 0, st, a);
+  hipLaunchKernelGGL(k_vfinal, dim3(a.B), dim3(64), 0, st, a);
 }
 
 }  // namespace osp

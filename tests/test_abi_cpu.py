@@ -111,3 +111,14 @@ def test_product_path_fails_loudly_without_the_library(tmp_path):
             L.load(str(tmp_path / "missing.so"))
     finally:
         L._lib = saved
+
+
+def test_host_side_errors_of_the_newer_entry_points(lib):
+    """The graph entry points refuse bad arguments before touching the device."""
+    from paper_2609_09338_amd import _lib as L
+    g = C.c_void_p()
+    s, v = L.osprey_step_args(), L.osprey_verify_args()
+    assert lib.osprey_graph_capture(None, C.byref(s), -1, C.byref(v), 64, C.byref(g)) == L.OSPREY_E_INVALID
+    assert lib.osprey_graph_launch(None, None) == L.OSPREY_E_INVALID
+    assert lib.osprey_graph_destroy(None) == L.OSPREY_OK
+    assert lib.osprey_draft_destroy(None) == L.OSPREY_OK

@@ -1,0 +1,39 @@
+"""The host-only ABI checks (tests/test_abi_cpu.py) again, against a build of the
+library whose host code -- validation, planning, state machine, the graph and
+graph entry points -- is instrumented with AddressSanitizer and
+UndefinedBehaviorSanitizer (paper_2609_09338_amd.build.build_sanitized), in a child
+process that preloads the sanitizer runtime.  Any report fails the test."""
+import glob
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _asan_runtime():
+    hits = sorted(glob.glob("/opt/rocm/llvm/lib/clang/*/lib/linux/libclang_rt.asan-x86_64.so"))
+    return hits[-1] if hits else None
+
+
+def test_abi_checks_pass_under_address_and_ub_sanitizers():
+    rt = _asan_runtime()
+    if rt is None:
+        pytest.skip("no AddressSanitizer runtime in this toolchain")
+    from paper_2609_09338_amd import build
+    lib = build.build_sanitized(verbose=False)
+    env = dict(os.environ)
+    # the sanitizer runtime first, then whatever the environment preloads already
+    env["LD_PRELOAD"] = rt + (":" + env["LD_PRELOAD"] if env.get("LD_PRELOAD") else "")
+    env["ASAN_OPTIONS"] = "detect_leaks=0:abort_on_error=0:exitcode=97"
+    env["UBSAN_OPTIONS"] = "halt_on_error=1:print_stacktrace=1:exitcode=98"
+    env["OSPREY_LIB"] = lib
+    r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_abi_cpu.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    out = r.stdout + r.stderr
+    assert "AddressSanitizer" not in out and "runtime error" not in out, out[-4000:]
+    assert r.returncode == 0, out[-4000:]
+    assert " passed" in out
