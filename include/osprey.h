@@ -352,6 +352,23 @@ int osprey_verify(osprey_handle* h, const osprey_verify_args* a);
 /* Stateless verification of caller-supplied drafts (see osprey_verify_rows_args). */
 int osprey_verify_rows(osprey_handle* h, const osprey_verify_rows_args* a);
 
+/* osprey_verify_rows without a handle and without device memory of the caller's: for
+ * callers that cannot allocate (code under HIP graph capture, serving loops and
+ * harnesses that forbid allocation).  The same rule and kernels as
+ * osprey_verify_rows on the same arguments; d2t [vocab_draft] (device) maps drafter
+ * rows to target ids (-1 = none; injective, as osprey_draft_init requires: entries
+ * outside [0, vocab_target) are treated as unmapped, and a target id several rows
+ * map to takes the largest of them).  Every scratch buffer lives in a fixed device
+ * array of the library (about 7.4 MB per GPU, held until the process ends), which
+ * bounds a call: batch <= 64, K <= 16, both vocabularies <= 262144 (else
+ * OSPREY_E_CAPACITY, nothing enqueued).  Enqueued on hip_stream (a hipStream_t; NULL:
+ * the null stream).  Calls on one GPU share that array: calls that overlap on one
+ * GPU (other streams, other host threads) race.  Make the first call on each device
+ * outside graph capture (it looks the array's address up).  A draft id outside
+ * [0, V_T) is rejected and not reported (there is no handle to report it to). */
+int osprey_verify_rows_static(const osprey_verify_rows_args* a, const int32_t* d2t,
+                              int32_t vocab_draft, int32_t vocab_target, void* hip_stream);
+
 /* Stateless verification of a caller-supplied draft tree (see
  * osprey_verify_tree_args).  No slot state is involved. */
 int osprey_verify_tree(osprey_handle* h, const osprey_verify_tree_args* a);

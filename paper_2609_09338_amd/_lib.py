@@ -90,6 +90,8 @@ SIGNATURES = {
     "osprey_verify": (C.c_int, [_H, C.POINTER(osprey_verify_args)]),
     "osprey_verify_rows": (C.c_int, [_H, C.POINTER(osprey_verify_rows_args)]),
     "osprey_verify_tree": (C.c_int, [_H, C.POINTER(osprey_verify_tree_args)]),
+    "osprey_verify_rows_static": (C.c_int, [C.POINTER(osprey_verify_rows_args), _P, C.c_int32,
+                                            C.c_int32, _P]),
     "osprey_draft_tree": (C.c_int, [_H, C.POINTER(osprey_step_args), C.POINTER(osprey_tree_args)]),
     "osprey_draft_block": (C.c_int, [_H, C.POINTER(osprey_step_args), C.c_int32]),
     "osprey_device_errors": (C.c_int, [_H, C.POINTER(C.c_uint32)]),

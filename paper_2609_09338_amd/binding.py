@@ -364,6 +364,43 @@ class Drafter:
             pass
 
 
+def verify_rows_static(K: int, target_logits, draft_logits, draft_tokens, temperature, u_accept,
+                       u_bonus, accept_len, accept_mask, out_tokens, d2t, vocab_target: int,
+                       stream=None, draft_temperature=None) -> None:
+    """osprey_verify_rows_static: osprey_verify_rows with no handle; its scratch is the
+    library's fixed device array (limits: batch 64, K 16, vocabularies 262144)."""
+    import torch
+    B = int(target_logits.shape[0])
+    V_d = int(d2t.numel())
+    _need(target_logits, B * (K + 1) * vocab_target, torch.float32, "target_logits")
+    _need(draft_logits, B * K * V_d, torch.float32, "draft_logits")
+    _need(draft_tokens, B * K, torch.int32, "draft_tokens")
+    _need(temperature, B, torch.float32, "temperature")
+    _need(u_accept, B * K, torch.float32, "u_accept")
+    _need(u_bonus, B, torch.float32, "u_bonus")
+    _need(accept_len, B, torch.int32, "accept_len")
+    _need(accept_mask, B * K, torch.uint8, "accept_mask")
+    _need(out_tokens, B * (K + 1), torch.int32, "out_tokens")
+    _need(draft_temperature, B, torch.float32, "draft_temperature")
+    _need(d2t, V_d, torch.int32, "d2t")
+    a = L.osprey_verify_rows_args()
+    a.batch = B
+    a.K = K
+    a.target_logits = _ptr(target_logits)
+    a.draft_logits = _ptr(draft_logits)
+    a.draft_tokens = _ptr(draft_tokens)
+    a.temperature = _ptr(temperature)
+    a.u_accept = _ptr(u_accept)
+    a.u_bonus = _ptr(u_bonus)
+    a.accept_len = _ptr(accept_len)
+    a.accept_mask = _ptr(accept_mask)
+    a.out_tokens = _ptr(out_tokens)
+    a.draft_temperature = _ptr(draft_temperature)
+    st = stream if stream is not None else torch.cuda.current_stream()
+    _check(_lib().osprey_verify_rows_static(C.byref(a), _ptr(d2t), V_d, int(vocab_target),
+                                            C.c_void_p(st.cuda_stream)))
+
+
 class IterationGraph:
     """A captured iteration (osprey_graph_*): launch() enqueues it on the drafter's
     stream; close() releases it (after the stream has finished with it)."""

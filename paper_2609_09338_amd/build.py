@@ -20,7 +20,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libosprey.so")
 SOURCES = ["gemv.hip", "gemv_taps.hip", "gemv_qkv.hip", "gemv_resid.hip", "gemv_swiglu.hip",
-           "gemv_logits.hip", "gemm_mfma.hip", "skinny.hip", "rows.hip", "attention.hip", "sample.hip", "verify.hip",
+           "gemv_logits.hip", "gemm_mfma.hip", "skinny.hip", "rows.hip", "attention.hip", "sample.hip", "verify.hip", "verify_static.hip",
            "state.hip", "tree.hip", "osprey.cpp"]
 ARCH = "gfx950"
 
@@ -68,9 +68,9 @@ def build(jobs: int = 6, debug: bool = False, verbose: bool = True) -> str:
 
 
 # Sources whose host code holds the library's logic (validation, planning, the slot
-# state machine, the graph entry points); the other sources' host code is
-# kernel-launch stubs.
-HOST_LOGIC = ["osprey.cpp"]
+# state machine, the graph and no-allocation entry points); the other sources' host
+# code is kernel-launch stubs.
+HOST_LOGIC = ["osprey.cpp", "verify_static.hip"]
 SANITIZED = os.path.join(BUILD, "sanitized", "libosprey.so")
 
 

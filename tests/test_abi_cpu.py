@@ -114,11 +114,23 @@ def test_product_path_fails_loudly_without_the_library(tmp_path):
 
 
 def test_host_side_errors_of_the_newer_entry_points(lib):
-    """The graph entry points refuse bad arguments before touching the device."""
+    """The graph and no-allocation entry points refuse bad arguments before touching
+    the device, with a message."""
     from paper_2609_09338_amd import _lib as L
     g = C.c_void_p()
     s, v = L.osprey_step_args(), L.osprey_verify_args()
     assert lib.osprey_graph_capture(None, C.byref(s), -1, C.byref(v), 64, C.byref(g)) == L.OSPREY_E_INVALID
     assert lib.osprey_graph_launch(None, None) == L.OSPREY_E_INVALID
     assert lib.osprey_graph_destroy(None) == L.OSPREY_OK
+    a = L.osprey_verify_rows_args()
+    a.batch, a.K = 65, 2
+    assert lib.osprey_verify_rows_static(C.byref(a), C.c_void_p(16), 100, 100, None) == L.OSPREY_E_CAPACITY
+    assert b"batch" in lib.osprey_last_error()
+    a.batch, a.K = 4, 17
+    assert lib.osprey_verify_rows_static(C.byref(a), C.c_void_p(16), 100, 100, None) == L.OSPREY_E_CAPACITY
+    a.K = 2
+    assert lib.osprey_verify_rows_static(C.byref(a), None, 100, 100, None) == L.OSPREY_E_INVALID
+    assert lib.osprey_verify_rows_static(C.byref(a), C.c_void_p(16), 100, 262145, None) == L.OSPREY_E_CAPACITY
+    # every pointer missing
+    assert lib.osprey_verify_rows_static(C.byref(a), C.c_void_p(16), 100, 100, None) == L.OSPREY_E_INVALID
     assert lib.osprey_draft_destroy(None) == L.OSPREY_OK

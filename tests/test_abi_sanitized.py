@@ -1,6 +1,6 @@
 """The host-only ABI checks (tests/test_abi_cpu.py) again, against a build of the
 library whose host code -- validation, planning, state machine, the graph and
-graph entry points -- is instrumented with AddressSanitizer and
+no-allocation entry points -- is instrumented with AddressSanitizer and
 UndefinedBehaviorSanitizer (paper_2609_09338_amd.build.build_sanitized), in a child
 process that preloads the sanitizer runtime.  Any report fails the test."""
 import glob
