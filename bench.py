@@ -101,12 +101,15 @@ def iteration_bytes(w, sb: dict) -> int:
     return int(wc + steps * sb["total"] + logits + verify)
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per LM-head launch from the committed rocprofv3 --pmc summary, or None
-    when there is none for this workload or the kernel source changed since."""
+def measured_traffic(workload: str, kernel: str = "lm_head"):
+    """HBM bytes per launch of the LM head (or, kernel="attention", per attention pass)
+    from the committed rocprofv3 --pmc summary, or None when there is none for this
+    workload or the kernel's source changed since."""
     import hashlib
     try:
         t = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))[workload]
+        if kernel != "lm_head":
+            t = t[kernel]
         sha = hashlib.sha256(open(os.path.join(ROOT, t["source"]), "rb").read()).hexdigest()
     except (OSError, KeyError, ValueError):
         return None
@@ -184,6 +187,10 @@ def run_gpu(args):
         res["modes"]["graph"] = time_graph(s, w, staged, args.warmup, n_it, rec_accept, rewind,
                                            replay, out)
     res["trajectory"] = rec_accept
+    # every attention pass of one pass over the iterations (the record pass, the timed
+    # pass and the graph pass all run this same trajectory)
+    passes = n_it * w.n_layers * (1 if w.drafting == "block" else w.K)
+    res["attention_bytes_per_pass"] = attention_bytes(w, s.ctx, rec_accept, 0, n_it) / passes
 
     # ---- per-call and per-kernel timing: the same steps again, with HIP events on the
     #      library's stream; each event idles the stream for a few microseconds, so one
@@ -485,6 +492,7 @@ def main():
                              "tokens_per_s": round(v["tokens"] / v["seconds"], 2)}
                          for m, v in modes.items()},
         "iteration_algorithmic_bytes": int(it_bytes),
+        "attention_bytes_per_pass": int(r["attention_bytes_per_pass"]),
         "iteration_hbm_frac": round(it_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
     }
     kt = r.get("kernels")
@@ -531,6 +539,7 @@ def main():
                 "bound": "hbm", "kernel": "attention (paged split pass + split merge), every pass "
                 "of the timed iterations", "achieved": round(at_gbs, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(at_gbs / HBM_PEAK_GBS, 4),
+                "traffic": measured_traffic(args.workload, "attention"),
                 "us_per_launch": round(at_s * 1e6 / max(at_n // 8, 1), 3),
                 "bytes_per_launch": int(r["attention_bytes"] / max(at_n // 8, 1)),
                 "launches": at_n // 8}

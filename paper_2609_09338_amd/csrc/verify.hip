@@ -354,26 +354,27 @@ OSP_DEV ResidRow resid_row(const VerifyArgs& a, int b) {
   return r;
 }
 
-// Sums of V = 2^LOGV float64 values per lane over the 64 lanes at once: on return
-// v[0] of lane l holds the total of value index l >> (6 - LOGV) (V + 6 shuffle steps
-// instead of 6 V).  Fixed order.
-template <int LOGV>
-OSP_DEV double transpose_reduce_d(double* v, int lane) {
-  constexpr int V = 1 << LOGV;
+// Sums of 16 float64 values per lane over the 64 lanes at once: on return v[0] of lane l
+// holds the total of value index l >> 2 (21 shuffle steps instead of 6 x 16).  Fixed
+// order.  Every step is a template with compile-time indices, so the values stay in
+// registers (a loop whose bounds the compiler cannot resolve indexes them by runtime
+// selects).
+template <int H, int M>
+OSP_DEV void tr_step(double* v, bool hi) {
 #pragma unroll
-  for (int s = 0; s < LOGV; ++s) {
-    const int m = 32 >> s;
-    const int h = (V >> s) >> 1;
-    const bool hi = (lane & m) != 0;
-#pragma unroll
-    for (int i = 0; i < h; ++i) {
-      const double mine = hi ? v[i + h] : v[i];
-      const double other = hi ? v[i] : v[i + h];
-      v[i] = mine + __shfl_xor(other, m, OSP_WAVE);
-    }
+  for (int i = 0; i < H; ++i) {
+    const double mine = hi ? v[i + H] : v[i];
+    const double other = hi ? v[i] : v[i + H];
+    v[i] = mine + __shfl_xor(other, M, OSP_WAVE);
   }
-#pragma unroll
-  for (int m = 32 >> LOGV; m >= 1; m >>= 1) v[0] += __shfl_xor(v[0], m, OSP_WAVE);
+}
+OSP_DEV double transpose_reduce16_d(double* v, int lane) {
+  tr_step<8, 32>(v, (lane & 32) != 0);
+  tr_step<4, 16>(v, (lane & 16) != 0);
+  tr_step<2, 8>(v, (lane & 8) != 0);
+  tr_step<1, 4>(v, (lane & 4) != 0);
+  v[0] += __shfl_xor(v[0], 2, OSP_WAVE);
+  v[0] += __shfl_xor(v[0], 1, OSP_WAVE);
   return v[0];
 }
 static_assert(kVPer == 16 && kVSub == 4 * kVPer, "one sub-range per (id group q, wavefront)");
@@ -455,7 +456,7 @@ OSP_DEV void final_tail(const VerifyArgs& a, int b, const ResidRow& rr) {
 }
 
 // Per chunk of target row a: the sums of the residual weights and of p, per 64-id
-// sub-range and per chunk (the chunk total is the ordered sum of its sub-ranges).
+// sub-range and per chunk (the chunk total is the sum of its sub-ranges).
 // Thread t takes ids t, t + 256, ... of the chunk: every wavefront load is 256
 // contiguous bytes, and both sums come from one pass over the row.  Greedy sequences
 // (T = 0) were finished by the acceptance.
@@ -487,23 +488,25 @@ __global__ void __launch_bounds__(kVThreads) k_vresid(VerifyArgs a) {
     sp[q] = p;
   }
   // the 64 ids of (q, this wavefront) are consecutive: one sub-range each
-  const double tw = transpose_reduce_d<4>(sw, lane);
-  const double tp = transpose_reduce_d<4>(sp, lane);
+  const double tw = transpose_reduce16_d(sw, lane);
+  const double tp = transpose_reduce16_d(sp, lane);
   if ((lane & 3) == 0) {
     s_sub[(lane >> 2) * 4 + wave][0] = tw;
     s_sub[(lane >> 2) * 4 + wave][1] = tp;
   }
   __syncthreads();
-  double* sub = a.res_sub + ((long)b * a.nchunk_t + c) * kVSub * 2;
+  // wavefront 0: the sub-range sums out, and the chunk's totals (a fixed butterfly
+  // order over the 64 sub-ranges)
   if (tid < kVSub) {
-    sub[tid * 2 + 0] = s_sub[tid][0];
-    sub[tid * 2 + 1] = s_sub[tid][1];
-  }
-  if (tid == 0) {
-    double w = 0.0, pp = 0.0;
-    for (int j = 0; j < kVSub; ++j) { w += s_sub[j][0]; pp += s_sub[j][1]; }
-    a.res_part[((long)b * a.nchunk_t + c) * 2 + 0] = w;
-    a.res_part[((long)b * a.nchunk_t + c) * 2 + 1] = pp;
+    double* sub = a.res_sub + ((long)b * a.nchunk_t + c) * kVSub * 2;
+    const double w = s_sub[tid][0], pp = s_sub[tid][1];
+    sub[tid * 2 + 0] = w;
+    sub[tid * 2 + 1] = pp;
+    const double tw2 = wave_sum_d(w), tp2 = wave_sum_d(pp);
+    if (tid == 0) {
+      a.res_part[((long)b * a.nchunk_t + c) * 2 + 0] = tw2;
+      a.res_part[((long)b * a.nchunk_t + c) * 2 + 1] = tp2;
+    }
   }
 }
 
