@@ -46,6 +46,9 @@ constexpr int kMaxSplit = 64;
 constexpr int kMaxSplitLen = 4096;
 constexpr int kEvenSplitLen = 1024;   // longer splits save little and unbalance ragged batches
 constexpr int kVerifyChunk = 4096;
+// A single sequence's pass of at most this many rows prepares its queries in the
+// attention blocks (no separate row kernel).
+constexpr int kOwnPrepRows = 8;
 
 enum SlotState { S_EMPTY = 0, S_READY = 1, S_DRAFTED = 2, S_VERIFIED = 3 };
 
@@ -635,9 +638,11 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     a.err = W.err;
     // Several rows per sequence: one row kernel prepares q (norm, RoPE, scale) and
     // appends k / v once, instead of every split block of the sequence doing it.  One
-    // row per sequence (draft steps): the attention blocks sum the QKV partials and
-    // prepare their own queries, one launch fewer per layer.
-    if (rows_per_seq > 1 || tree) {
+    // row per sequence (draft steps), or a few rows of a single sequence (the ingest at
+    // batch 1): the attention blocks sum the QKV partials and prepare their own queries,
+    // one launch fewer per layer.
+    const bool own_prep = rows_per_seq == 1 || (B == 1 && rows_per_seq <= kOwnPrepRows);
+    if (!own_prep || tree) {
       launch_rows_qkv(c.dtype, a, W.o, h->stream);
       a.q_prep = W.o;
     }
