@@ -371,10 +371,10 @@ struct SplitPlan {
   int n_split, split_len;
 };
 SplitPlan plan_splits(const osprey_handle* h, long ctx_max, long ctx_total, int max_split = kMaxSplit) {
-  // one sequence: as many blocks as can be resident (two per CU: the kernel's register
-  // and LDS budget), the most pages in flight for a long context; several sequences: a
-  // little over one per CU, which keeps the ragged batches' blocks of about equal work
-  const long target_blocks = ctx_total <= ctx_max ? 2L * h->n_cu : 320;
+  // as many blocks as can be resident (two per CU: the kernel's register and LDS
+  // budget), the most pages in flight; splits of at most kEvenSplitLen keep the blocks
+  // of ragged batches of about equal work
+  const long target_blocks = 2L * h->n_cu;
   long len = (ctx_total * h->cfg.n_kv_heads + target_blocks - 1) / target_blocks;
   len = std::min<long>(std::max<long>(len, 64), kEvenSplitLen);
   len = std::max<long>(len, (ctx_max + max_split - 1) / max_split);
