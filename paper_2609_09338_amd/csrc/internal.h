@@ -27,7 +27,10 @@ enum SrcKind {
                   // c < seg from (xs_hi, xs_lo) row r, else (xa_hi, xa_lo) row gather[r] or r
   SRC_SWIGLU = 5, // matrix-core passes of <= 64 rows: X[r][c] = silu(g) u with g, u the sums of
                   // the gate/up K-split partials part_in[k][r][c] and part_in[k][r][Kd + c]
+  SRC_ATTN = 6,   // matrix-core passes of <= 64 rows: X[r][c] = the attention output of row r,
+                  // head c / hd, merged from its context splits (attn_part) on staging
 };
+constexpr int kAttnMergeMaxSplit = 8;   // SRC_ATTN: splits per row (bound; else a merge kernel)
 enum EpiKind {
   EPI_STORE = 0,   // y[r][n] = acc
   EPI_RESID = 1,   // y[r][n] += acc
@@ -85,6 +88,14 @@ struct GemvArgs {
   int ks_in;
   long part_in_split;
   int ld_in;
+  // SRC_ATTN inputs: attention partials [rows][Kd / attn_hd heads][attn_nsplit][attn_hd + 2]
+  // (max, sum, unnormalised output per split); splits past pos[r] / attn_split_len hold
+  // nothing for row r
+  const float* attn_part;
+  const int32_t* attn_pos;
+  int attn_nsplit;
+  int attn_split_len;
+  int attn_hd;
   uint32_t* err;
 };
 constexpr int kMaxKSplit = 16;

@@ -390,12 +390,12 @@ SplitPlan plan_splits(const osprey_handle* h, long ctx_max, long ctx_total, int 
 // the pair runs kTimedRepeats times back to back between the events: it is idempotent
 // (a new row's keys and values are written again with the same values, every output is
 // overwritten), so the events' own overhead is shared by as many launches.
-void run_attention(osprey_handle* h, const AttnArgs& a) {
+void run_attention(osprey_handle* h, const AttnArgs& a, bool merge = true) {
   const int t = h->t_begin(1);
   const int reps = t >= 0 ? kTimedRepeats : 1;
   for (int rep = 0; rep < reps; ++rep) {
     launch_attention(h->cfg.dtype, a, h->stream);
-    launch_attn_combine(a, h->stream);
+    if (merge) launch_attn_combine(a, h->stream);
   }
   h->t_end(t, reps);
 }
@@ -646,7 +646,13 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
       launch_rows_qkv(c.dtype, a, W.o, h->stream);
       a.q_prep = W.o;
     }
-    run_attention(h, a);
+    // Passes of at most 16 rows that are not tree passes merge the context splits while
+    // the O projection stages its inputs (one launch fewer per layer); otherwise the
+    // merge kernel writes o as the projection's input pairs.  (At 32-64 rows each O
+    // block would read about four times its inputs' bytes of split records, in several
+    // rounds: c4 / c5 gained nothing.)
+    const bool merge_in_o = skinny && rows.max_rows <= 16 && !tree && sp.n_split <= kAttnMergeMaxSplit;
+    run_attention(h, a, !merge_in_o);
     // O projection; residual + post-attention RMSNorm
     GemvArgs go = gb;
     go.ld_xa = nq * hd;
@@ -656,7 +662,16 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     RowArgs rn = ra;
     rn.W = d;
     rn.ldp = d;
-    rn.ks = gemm(SRC_PREP, EPI_STORE, go);
+    if (merge_in_o) {
+      go.attn_part = W.attn_part;
+      go.attn_pos = rows.pos;
+      go.attn_nsplit = sp.n_split;
+      go.attn_split_len = sp.split_len;
+      go.attn_hd = hd;
+      rn.ks = gemm(SRC_ATTN, EPI_STORE, go);
+    } else {
+      rn.ks = gemm(SRC_PREP, EPI_STORE, go);
+    }
     rn.gamma = L.post_norm;
     launch_rows_resid_norm(rn, h->stream);
     // gate/up, SwiGLU

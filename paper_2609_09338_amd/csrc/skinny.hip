@@ -45,7 +45,7 @@ constexpr int kSkDepthMax = 3;            // register ring of units (64 rows: 2)
 constexpr int kSkTmaxHead = 5;            // tiles per wavefront (bound): LM head
 constexpr int kSkTmaxProj = 1;            // projections: one tile, K split across blocks
 
-enum SkSrc { SK_PREP = 0, SK_NORM = 1, SK_TAPS = 2, SK_SWIGLU = 3 };
+enum SkSrc { SK_PREP = 0, SK_NORM = 1, SK_TAPS = 2, SK_SWIGLU = 3, SK_ATTN = 4 };
 enum SkEpi { SK_LOGITS = 0, SK_PART = 1 };
 
 // Input columns resident per block and phase: 64 rows x 512 or 32 rows x 1024
@@ -178,6 +178,41 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
     }
     __syncthreads();
   }
+  // attention output: the weights f_s / L of every (row, head of this block's K range,
+  // split) of the merge max-rescaled splits, once, into LDS (kSkAttnHeads heads of at
+  // least 64 columns cover a K range of at most 256 columns)
+  constexpr int kSkAttnHeads = 4;
+  __shared__ float s_af[SRC == SK_ATTN ? ROWS * kSkAttnHeads * kAttnMergeMaxSplit : 1];
+  if constexpr (SRC == SK_ATTN) {
+    const int hd = a.attn_hd, ns_all = a.attn_nsplit, nh = a.Kd / hd;
+    const int h0 = k_lo / hd;
+    // one lane per (row, local head): wavefront-free, at most 64 x 4 of them
+    for (int t = tid; t < R * kSkAttnHeads; t += kSkThreads) {
+      const int r = t / kSkAttnHeads, hh = t % kSkAttnHeads, h = h0 + hh;
+      if (h >= nh || h * hd >= k_hi) continue;
+      const int ns = min(ns_all, a.attn_pos[r] / a.attn_split_len + 1);
+      const float* pp = a.attn_part + ((long)r * nh + h) * ns_all * (hd + 2);
+      float m[kAttnMergeMaxSplit], l[kAttnMergeMaxSplit];
+#pragma unroll
+      for (int sp = 0; sp < kAttnMergeMaxSplit; ++sp) {
+        m[sp] = sp < ns ? pp[(long)sp * (hd + 2)] : -INFINITY;
+        l[sp] = sp < ns ? pp[(long)sp * (hd + 2) + 1] : 0.f;
+      }
+      float M = -INFINITY;
+#pragma unroll
+      for (int sp = 0; sp < kAttnMergeMaxSplit; ++sp) M = fmaxf(M, m[sp]);
+      float f[kAttnMergeMaxSplit], L = 0.f;
+#pragma unroll
+      for (int sp = 0; sp < kAttnMergeMaxSplit; ++sp) {
+        f[sp] = m[sp] > -INFINITY ? __expf(m[sp] - M) : 0.f;
+        L += l[sp] * f[sp];
+      }
+#pragma unroll
+      for (int sp = 0; sp < kAttnMergeMaxSplit; ++sp)
+        s_af[(r * kSkAttnHeads + hh) * kAttnMergeMaxSplit + sp] = L > 0.f ? f[sp] / L : 0.f;
+    }
+    __syncthreads();
+  }
   for (int ph = 0; ph < nphase; ++ph) {
     const int k0 = k_lo + ph * KC;
     if constexpr (SRC != SK_NORM) {
@@ -190,7 +225,8 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
     const int span8 = (EPI == SK_PART ? kc : KC) / 8;      // 16-byte pieces per row
     const int nitems = R * span8;
     // (the LM head holds 20 MT accumulators: smaller batches for more rows)
-    constexpr int BATCH = EPI == SK_LOGITS ? (MT == 4 ? 1 : (MT == 2 ? 2 : 4)) : 4;
+    // (attention outputs: 16 loads per piece already)
+    constexpr int BATCH = EPI == SK_LOGITS ? (MT == 4 ? 1 : (MT == 2 ? 2 : 4)) : (SRC == SK_ATTN ? 1 : 4);
 #pragma unroll 1
     for (int b0 = 0; b0 < nitems; b0 += BATCH * kSkThreads) {
       uint4 hv[BATCH], lv[BATCH];
@@ -233,6 +269,39 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
             float y[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) y[e] = g[e] / (1.0f + __expf(-g[e])) * u[e];
+            split_bf16x2(y[0], y[1], h.x, l.x);
+            split_bf16x2(y[2], y[3], h.y, l.y);
+            split_bf16x2(y[4], y[5], h.z, l.z);
+            split_bf16x2(y[6], y[7], h.w, l.w);
+          } else if constexpr (SRC == SK_ATTN) {
+            // columns c .. c + 7 of row r: one head h, dims e .. e + 7; the splits'
+            // unnormalised outputs weighted by s_af, in split order
+            const int hd = a.attn_hd, hq = c / hd, e = c - hq * hd, nh = a.Kd / hd;
+            const int ns_all = a.attn_nsplit;
+            const float* pp = a.attn_part + ((long)r * nh + hq) * ns_all * (hd + 2) + 2 + e;
+            const float* fw = s_af + (r * kSkAttnHeads + (hq - k_lo / hd)) * kAttnMergeMaxSplit;
+            // (a split's record is hd + 2 floats: its outputs are 8-byte aligned, so they
+            // are read as float2)
+            float2 v[kAttnMergeMaxSplit][4];
+#pragma unroll
+            for (int sp = 0; sp < kAttnMergeMaxSplit; ++sp) {
+              // (splits past this row's hold nothing: their weight is 0 and they are
+              // not read)
+              const bool in = sp < ns_all && fw[sp] != 0.f;
+#pragma unroll
+              for (int q = 0; q < 4; ++q)
+                v[sp][q] = in ? *reinterpret_cast<const float2*>(pp + (long)sp * (hd + 2) + 2 * q)
+                              : make_float2(0.f, 0.f);
+            }
+            float y[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) y[q] = 0.f;
+#pragma unroll
+            for (int sp = 0; sp < kAttnMergeMaxSplit; ++sp) {
+              const float w = fw[sp];
+#pragma unroll
+              for (int q = 0; q < 4; ++q) { y[2 * q] += w * v[sp][q].x; y[2 * q + 1] += w * v[sp][q].y; }
+            }
             split_bf16x2(y[0], y[1], h.x, l.x);
             split_bf16x2(y[2], y[3], h.y, l.y);
             split_bf16x2(y[4], y[5], h.z, l.z);
@@ -500,11 +569,14 @@ int skinny_splits(int rows, int Kd) {
 int launch_skinny(SrcKind src, const GemvArgs& a, hipStream_t st) {
   const int mt = sk_mt(a.max_rows);
   const int NR = a.w1 ? 2 * a.N : a.N;
-  const int kc = skinny_kc(a.max_rows, NR, a.Kd);
+  // (attention outputs: K ranges of one unit, so that a block's range holds at most 4
+  // heads)
+  const int kc = src == SRC_ATTN ? kSkUnit : skinny_kc(a.max_rows, NR, a.Kd);
   const int ks = (a.Kd + kc - 1) / kc;
   const dim3 grid((((NR + 15) / 16) + kSkWaves - 1) / kSkWaves, ks);
   if (src == SRC_TAPS) sk_launch<SK_TAPS, SK_PART>(mt, grid, a, 1, kc, st);
   else if (src == SRC_SWIGLU) sk_launch<SK_SWIGLU, SK_PART>(mt, grid, a, 1, kc, st);
+  else if (src == SRC_ATTN) sk_launch<SK_ATTN, SK_PART>(mt, grid, a, 1, kc, st);
   else sk_launch<SK_PREP, SK_PART>(mt, grid, a, 1, kc, st);
   return ks;
 }
