@@ -288,14 +288,17 @@ int osprey_config_validate(const osprey_config* cfg);
  * Returns 0 for an invalid configuration. */
 size_t osprey_kv_bytes(const osprey_config* cfg);
 
-/* Bytes of device workspace the library needs (activations, statistics, slot state).
- * Returns 0 for an invalid configuration. */
+/* Bytes of device workspace the library needs (activations, statistics, slot state,
+ * and for bf16 weights a copy of the LM head, [V_d][d] bf16 rounded up to 16 rows and
+ * 256 columns).  Returns 0 for an invalid configuration. */
 size_t osprey_workspace_bytes(const osprey_config* cfg);
 
 /* Validate, carve the caller's KV pool and workspace (256-byte aligned), copy
  * the vocabulary map and build its inverse (d2t must be injective on mapped
  * rows and map at least one row), upload the RoPE table (computed in float64)
- * and reset every slot to EMPTY.  hip_stream is a hipStream_t (NULL: the null
+ * and reset every slot to EMPTY.  bf16 weights: the LM head is copied into the
+ * workspace in the order the matrix cores take it, and later calls read that copy
+ * (a change to w->lm_head after this call is not seen).  hip_stream is a hipStream_t (NULL: the null
  * stream).  Synchronises the stream.  *out receives the handle (host). */
 int osprey_draft_init(const osprey_config* cfg, const osprey_weights* w, void* kv_pool,
                       size_t kv_bytes, void* workspace, size_t ws_bytes, void* hip_stream,

@@ -122,12 +122,21 @@ struct LmPlan {
 };
 constexpr int kLmMaxRows = 64;
 LmPlan lm_head_plan(int rows, int N, int n_cu);
+// The head's weights a.w0 are the packed copy that launch_pack_head writes, of the
+// [N][Kd] bf16 matrix with N = a.N and Kd = a.Kd.
 // norm_in: inputs are the fp32 rows xin (ldx, gathered), normalised with gamma / eps
 // in the kernel (one row of at most 4096 columns: lm_head_norm_in_supported); else
 // prepared pairs xa_hi / xa_lo.  Returns false, launching nothing, for an unsupported
 // norm_in shape.
 bool lm_head_norm_in_supported(int rows, int Kd);
 bool launch_lm_head(const GemvArgs& a, const LmPlan& p, bool norm_in, hipStream_t st);
+// Packed head: [ceil(N / 16) tiles][ceil(Kd / 256) units][8 k steps][64 lanes][8] bf16,
+// lane (r, g) of step s of unit u in tile t holding row 16 t + r, columns
+// 256 u + 8 g + 32 s .. + 8 (zero past N or Kd): the order in which the matrix cores
+// take the weights.  packed_head_bytes: its size; launch_pack_head fills it from the
+// row-major [N][Kd] matrix w (Kd a multiple of 8), on stream st.
+long packed_head_bytes(int N, int Kd);
+void launch_pack_head(const void* w, int N, int Kd, void* packed, hipStream_t st);
 
 // Projections of passes of at most kLmMaxRows rows on the same streaming kernel:
 // src SRC_PREP (pairs; [xs ; xa] when seg > 0), SRC_TAPS, or SRC_SWIGLU (the down

@@ -103,6 +103,7 @@ struct Ws {
   float* b_temp;
   float* r_s;                 // [B * kMaxTopk][d]
   float* ones;                // [B * kMaxTopk] temperature 1 for the tree's LM-head records
+  void* head_pk;              // bf16 drafters: the LM head in the matrix cores' order
 };
 
 struct Dims {
@@ -221,6 +222,7 @@ size_t plan(const osprey_config& c, char* base, Ws* w) {
     W.b_gather = (int32_t*)take(4L * rows);
     W.b_temp = (float*)take(4L * rows);
   }
+  W.head_pk = c.dtype == OSPREY_BF16 ? take(packed_head_bytes(c.vocab_draft, c.d_model)) : nullptr;
   W.v_res = (double*)take(16L * D.B * D.nchunk_t);
   W.v_sub = (double*)take(16L * kVSub * D.B * D.nchunk_t);
   W.vstate = (int32_t*)take(16L * D.B);
@@ -747,7 +749,7 @@ int run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, const
   g.eps = c.rms_eps;
   g.d_norm = c.d_model;
   g.Kd = c.d_model;
-  g.w0 = h->w.lm_head;
+  g.w0 = mr ? W.head_pk : h->w.lm_head;
   g.N = c.vocab_draft;
   g.y = logits + (long)k * c.vocab_draft;
   g.ld_logits = ld_b * c.vocab_draft;
@@ -831,7 +833,7 @@ LmPlan run_head_rows(osprey_handle* h, int rows, const int32_t* gather, const fl
   g.eps = c.rms_eps;
   g.d_norm = c.d_model;
   g.Kd = c.d_model;
-  g.w0 = h->w.lm_head;
+  g.w0 = W.head_pk;
   g.N = c.vocab_draft;
   g.ld_logits = c.vocab_draft;
   g.d2t = h->w.d2t;
@@ -972,6 +974,8 @@ OSPREY_API int osprey_draft_init(const osprey_config* cfg, const osprey_weights*
   const long B = h->D.B;
   // temperature 1 for the LM-head records of draft-tree passes
   launch_fill_i32(reinterpret_cast<int32_t*>(W.ones), 0x3f800000, B * kMaxTopk, h->stream);
+  // bf16 heads are read from a packed copy (the matrix cores' order)
+  if (W.head_pk) launch_pack_head(w->lm_head, Vd, cfg->d_model, W.head_pk, h->stream);
   if (hipMemset(W.slot_len, 0, 4 * B) != hipSuccess || hipMemset(W.pend_n, 0, 4 * B) != hipSuccess ||
       hipMemset(W.slot_nblocks, 0, 4 * B) != hipSuccess ||
       hipMemset(W.block_table, 0, 4L * B * h->D.max_blocks) != hipSuccess ||

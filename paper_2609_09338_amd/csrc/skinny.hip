@@ -37,6 +37,7 @@ namespace osp {
 
 typedef __bf16 sk_bf16x8 __attribute__((ext_vector_type(8)));
 typedef float sk_f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned sk_u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kSkWaves = 8;
 constexpr int kSkThreads = kSkWaves * 64;
@@ -103,6 +104,26 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
     for (int ks = 0; ks < 8; ++ks)
       w[ks] = *reinterpret_cast<const uint4*>(wr + min(kb + 32 * ks, a.Kd - 8));
   };
+  // LM head: the packed copy (pack_head_index), one contiguous kilobyte per load of the
+  // wavefront.  The head is read once per pass and outsizes the last-level cache, so
+  // its loads are non-temporal: they leave the drafter body's weights and the KV cache,
+  // which every draft step reads again, in that cache.  Tiles past the head and units
+  // past Kd are clamped into the copy (their products are dropped, or meet zero inputs).
+  auto load_unit_packed = [&](uint4* w, int k0, int u) {
+    const int nu_row = (a.Kd + kSkUnit - 1) / kSkUnit;
+    const int t = min(t0 + u / nch, nt16 - 1);
+    const int uu = min(k0 / kSkUnit + u % nch, nu_row - 1);
+    const sk_u32x4* p = reinterpret_cast<const sk_u32x4*>(a.w0) + (long)(t * nu_row + uu) * 8 * 64 + lane;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+      const sk_u32x4 v = __builtin_nontemporal_load(p + 64 * ks);
+      w[ks] = make_uint4(v[0], v[1], v[2], v[3]);
+    }
+  };
+  auto load = [&](uint4* w, int k0, int u) {
+    if constexpr (EPI == SK_LOGITS) load_unit_packed(w, k0, u);
+    else load_unit(w, k0, u);
+  };
   const int nphase = (k_hi - k_lo + KC - 1) / KC;
   const int nu = ntiles * nch;                          // units per phase
   // single normalised row: thread t stages columns [8t, 8t + 8) (Kd <= 8 x 512), read
@@ -129,7 +150,7 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
   auto prefetch_phase = [&](int k0) {
 #pragma unroll
     for (int u = 0; u + 1 < kSkDepth; ++u)
-      if (SRC == SK_NORM || real(k0, u)) load_unit(ring[u], k0, u);
+      if (SRC == SK_NORM || real(k0, u)) load(ring[u], k0, u);
   };
   prefetch_phase(k_lo);
   // LM head: the map entries of this lane's columns (one per tile), read from a clamped
@@ -337,7 +358,7 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
     for (int u = 0; u < NU; ++u) {
       // (a unit that is not real still requests the one kSkDepth - 1 places ahead, which
       // may be)
-      if (real(k0, u + kSkDepth - 1)) load_unit(ring[(u + kSkDepth - 1) % kSkDepth], k0, u + kSkDepth - 1);
+      if (real(k0, u + kSkDepth - 1)) load(ring[(u + kSkDepth - 1) % kSkDepth], k0, u + kSkDepth - 1);
       if (real(k0, u)) {
         // keep each unit's work in place: hoisting later units' LDS reads or loads
         // above this point only raises register pressure
@@ -559,6 +580,30 @@ static int skinny_kc(int rows, int N2, int Kd) {
   while (kc > kSkUnit && (long)nb * ((Kd + kc - 1) / kc) < 256 && (Kd + kc / 2 - 1) / (kc / 2) <= kMaxKSplit)
     kc /= 2;
   return kc;
+}
+
+long packed_head_bytes(int N, int Kd) {
+  return 2L * ((N + 15) / 16) * 16 * ((Kd + kSkUnit - 1) / kSkUnit) * kSkUnit;
+}
+
+// One thread per 16-byte piece of the packed copy.
+__global__ void k_pack_head(const bf16_t* __restrict__ w, int N, int Kd, long pieces, uint4* __restrict__ out) {
+  const long i = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (i >= pieces) return;
+  const int nu_row = (Kd + kSkUnit - 1) / kSkUnit;
+  const int lane = (int)(i & 63), s = (int)((i >> 6) & 7);
+  const long tu = i >> 9;                       // tile * nu_row + unit
+  const int u = (int)(tu % nu_row), t = (int)(tu / nu_row);
+  const int row = 16 * t + (lane & 15);
+  const int col = kSkUnit * u + 8 * (lane >> 4) + 32 * s;
+  out[i] = (row < N && col < Kd) ? *reinterpret_cast<const uint4*>(w + (long)row * Kd + col)
+                                 : make_uint4(0u, 0u, 0u, 0u);
+}
+
+void launch_pack_head(const void* w, int N, int Kd, void* packed, hipStream_t st) {
+  const long pieces = packed_head_bytes(N, Kd) / 16;
+  hipLaunchKernelGGL(k_pack_head, dim3((unsigned)((pieces + 255) / 256)), dim3(256), 0, st,
+                     reinterpret_cast<const bf16_t*>(w), N, Kd, pieces, reinterpret_cast<uint4*>(packed));
 }
 
 int skinny_splits(int rows, int Kd) {
