@@ -18,6 +18,8 @@
 //              from its two segments with no concatenated copy; in layer 0 x is
 //              the embedding row of the token (one wavefront materialises it)
 //   SRC_TAPS   target hidden-state taps (Eq. 1)
+//   SRC_ATTN   one row's attention output, merged from its context splits by the
+//              block into LDS before the products (single rows, Kd <= 2048)
 // and the epilogue writes, accumulates into the residual, applies SwiGLU, or
 // writes masked logits plus, per wavefront range, the (max, sum exp((l-max)/T),
 // lowest argmax) statistics that sampling merges.
@@ -141,9 +143,13 @@ template <int RB, int NW, int XV, bool NORMED> struct GemvOcc {
   static constexpr int value = (RB * NW * XV <= 8 && RB * XV <= 4) ? (NORMED ? 2 : 4) : 1;
 };
 
+// SRC_ATTN: every thread holds its segment of every split's output (one block per CU).
+constexpr int kGemvAttnMaxSplit = 20;   // splits merged in the input stage (bound)
+constexpr int kGemvAttnMaxHeads = 16;   // heads of the merged row (bound)
+
 template <typename TW, int SRC, int EPI, int RB, int NW, int XV, bool CACHED>
 __global__ void __launch_bounds__(kGemvThreads,
-                                  (GemvOcc<RB, NW, XV, (SRC == SRC_NORM || SRC == SRC_QKV)>::value))
+                                  (SRC == SRC_ATTN ? 1 : GemvOcc<RB, NW, XV, (SRC == SRC_NORM || SRC == SRC_QKV)>::value))
 k_gemv(GemvArgs a, int rows_per_wave) {
   constexpr int VEC = Vec<TW>::N;
   constexpr int NWV = (EPI == EPI_SWIGLU) ? 2 * NW : NW;
@@ -156,7 +162,8 @@ k_gemv(GemvArgs a, int rows_per_wave) {
   const int lane = threadIdx.x & (OSP_WAVE - 1);
   const int gw = blockIdx.x * kGemvWavesPerBlock + (threadIdx.x >> 6);
   const int n_lo = gw * rows_per_wave;
-  if (n_lo >= a.N) return;
+  // (the split merge of SRC_ATTN needs every wavefront of the block at its barriers)
+  if (SRC != SRC_ATTN && n_lo >= a.N) return;
   const int n_hi = min(a.N, n_lo + rows_per_wave);
   const int rows = a.count ? min(*a.count, a.max_rows) : a.max_rows;
   const TW* __restrict__ w0 = reinterpret_cast<const TW*>(a.w0);
@@ -185,6 +192,73 @@ k_gemv(GemvArgs a, int rows_per_wave) {
   load_w(wr, n_lo, 0);
   bool have_w = true;
 
+  // SRC_ATTN (one row, Kd <= 8 kGemvThreads): thread t merges columns [8t, 8t + 8) of
+  // head h = 8t / hd.  Split s of head h holds (max m, sum l, unnormalised output o) at
+  // attn_part + (h n_split + s)(hd + 2); splits past pos / split_len hold nothing for the
+  // row and are dropped by selection (their words are stale).  x = sum_s f_s o_s with
+  // f_s = exp(m_s - M) / sum_s' exp(m_s' - M) l_s', M the head's largest m_s.
+  __shared__ float s_x[SRC == SRC_ATTN ? 8 * kGemvThreads : 1];
+  if constexpr (SRC == SRC_ATTN) {
+    __shared__ float s_f[kGemvAttnMaxHeads * 2 * 16];
+    const int tid = threadIdx.x;
+    const int hd = a.attn_hd, nsp = a.attn_nsplit, rec = a.attn_hd + 2;
+    const int c0 = 8 * tid;
+    const bool seg = c0 < a.Kd;
+    const int h = seg ? c0 / hd : 0;
+    // every split's segment requested at once, before the row position is known
+    const float* po = a.attn_part + (long)h * nsp * rec + 2 + (seg ? c0 - h * hd : 0);
+    float2 ov[kGemvAttnMaxSplit][4];
+#pragma unroll
+    for (int sp = 0; sp < kGemvAttnMaxSplit; ++sp)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        ov[sp][q] = (seg && sp < nsp) ? *reinterpret_cast<const float2*>(po + (long)sp * rec + 2 * q)
+                                      : make_float2(0.f, 0.f);
+    // merge weights: 16 threads per head, splits i and i + 16
+    const int hh = tid >> 4, i = tid & 15;
+    const int nh = a.Kd / hd;
+    const float* pm = a.attn_part + (long)hh * nsp * rec;
+    float m0 = -INFINITY, l0 = 0.f, m1 = -INFINITY, l1 = 0.f;
+    if (hh < nh && i < nsp) { m0 = pm[(long)i * rec]; l0 = pm[(long)i * rec + 1]; }
+    if (hh < nh && i + 16 < nsp) { m1 = pm[(long)(i + 16) * rec]; l1 = pm[(long)(i + 16) * rec + 1]; }
+    const int ns = min(nsp, a.attn_pos[0] / a.attn_split_len + 1);
+    if (i >= ns) { m0 = -INFINITY; l0 = 0.f; }
+    if (i + 16 >= ns) { m1 = -INFINITY; l1 = 0.f; }
+    float M = fmaxf(m0, m1);
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) M = fmaxf(M, __shfl_xor(M, o, OSP_WAVE));
+    const float f0 = m0 > -INFINITY ? __expf(m0 - M) : 0.f;
+    const float f1 = m1 > -INFINITY ? __expf(m1 - M) : 0.f;
+    float L = l0 * f0 + l1 * f1;
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) L += __shfl_xor(L, o, OSP_WAVE);
+    if (hh < kGemvAttnMaxHeads) {
+      s_f[hh * 32 + i] = L > 0.f ? f0 / L : 0.f;
+      s_f[hh * 32 + i + 16] = L > 0.f ? f1 / L : 0.f;
+    }
+    __syncthreads();
+    float x[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = 0.f;
+#pragma unroll
+    for (int sp = 0; sp < kGemvAttnMaxSplit; ++sp) {
+      if (sp < ns) {
+        const float f = s_f[h * 32 + sp];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          x[2 * q] = fmaf(f, ov[sp][q].x, x[2 * q]);
+          x[2 * q + 1] = fmaf(f, ov[sp][q].y, x[2 * q + 1]);
+        }
+      }
+    }
+    if (seg) {
+      *reinterpret_cast<float4*>(s_x + c0) = make_float4(x[0], x[1], x[2], x[3]);
+      *reinterpret_cast<float4*>(s_x + c0 + 4) = make_float4(x[4], x[5], x[6], x[7]);
+    }
+    __syncthreads();
+    if (n_lo >= a.N) return;
+  }
+
   for (int r0 = 0; r0 < rows; r0 += RB) {
     float xc[RB][XV][VEC];                     // this lane's input values (cached mode)
     float inv_rms[RB];
@@ -210,7 +284,13 @@ k_gemv(GemvArgs a, int rows_per_wave) {
           const int j = lane + OSP_WAVE * u;
           isn[u] = false;
           if (r0 + r < rows && j < nvec) {
-            isn[u] = load_x_raw<TW, SRC, VEC>(a, r0 + r, j * VEC, xc[r][u]);
+            if constexpr (SRC == SRC_ATTN) {
+#pragma unroll
+              for (int e = 0; e < VEC; ++e) xc[r][u][e] = s_x[j * VEC + e];
+              isn[u] = false;
+            } else {
+              isn[u] = load_x_raw<TW, SRC, VEC>(a, r0 + r, j * VEC, xc[r][u]);
+            }
             if (isn[u]) {
 #pragma unroll
               for (int e = 0; e < VEC; ++e) ss += xc[r][u][e] * xc[r][u][e];
@@ -408,12 +488,17 @@ void launch_gemv_t(const GemvArgs& a, int rpw, hipStream_t st) {
   const int waves = (a.N + rpw - 1) / rpw;
   const int grid = (waves + kGemvWavesPerBlock - 1) / kGemvWavesPerBlock;
   const bool cached = a.Kd / Vec<TW>::N <= OSP_WAVE * XV;
-  if (cached)
-    hipLaunchKernelGGL((k_gemv<TW, SRC, EPI, RB, NW, XV, true>), dim3(grid), dim3(kGemvThreads), 0,
-                       st, a, rpw);
-  else
-    hipLaunchKernelGGL((k_gemv<TW, SRC, EPI, RB, NW, XV, false>), dim3(grid), dim3(kGemvThreads), 0,
-                       st, a, rpw);
+  if constexpr (SRC == SRC_ATTN) {
+    // (only the cached form exists: gemv_attn_supported bounds Kd)
+    hipLaunchKernelGGL((k_gemv<TW, SRC, EPI, RB, NW, XV, true>), dim3(grid), dim3(kGemvThreads), 0, st, a, rpw);
+  } else {
+    if (cached)
+      hipLaunchKernelGGL((k_gemv<TW, SRC, EPI, RB, NW, XV, true>), dim3(grid), dim3(kGemvThreads), 0,
+                         st, a, rpw);
+    else
+      hipLaunchKernelGGL((k_gemv<TW, SRC, EPI, RB, NW, XV, false>), dim3(grid), dim3(kGemvThreads), 0,
+                         st, a, rpw);
+  }
 }
 
 template <typename TW, int SRC, int EPI, int RB, int XV>

@@ -27,8 +27,9 @@ enum SrcKind {
                   // c < seg from (xs_hi, xs_lo) row r, else (xa_hi, xa_lo) row gather[r] or r
   SRC_SWIGLU = 5, // matrix-core passes of <= 64 rows: X[r][c] = silu(g) u with g, u the sums of
                   // the gate/up K-split partials part_in[k][r][c] and part_in[k][r][Kd + c]
-  SRC_ATTN = 6,   // matrix-core passes of <= 64 rows: X[r][c] = the attention output of row r,
-                  // head c / hd, merged from its context splits (attn_part) on staging
+  SRC_ATTN = 6,   // X[r][c] = the attention output of row r, head c / hd, merged from its
+                  // context splits (attn_part) on staging: matrix-core passes of <= 64 rows,
+                  // and the single-row vector O projection
 };
 constexpr int kAttnMergeMaxSplit = 8;   // SRC_ATTN: splits per row (bound; else a merge kernel)
 enum EpiKind {
@@ -101,6 +102,11 @@ struct GemvArgs {
 constexpr int kMaxKSplit = 16;
 
 void launch_gemv(int wdtype, SrcKind src, EpiKind epi, const GemvArgs& a, hipStream_t st);
+// Single-row O projection + residual whose input row is the attention output merged from
+// its context splits while the kernel stages it (attn_* fields; bf16 weights, one row,
+// Kd = heads x hd <= 2048, at most 16 heads and 20 splits: gemv_attn_supported).
+bool gemv_attn_supported(int wdtype, int rows, int Kd, int hd, int n_split);
+void launch_gemv_attn_resid(const GemvArgs& a, hipStream_t st);
 
 // Matrix-core GEMM for passes of several rows of bf16 weights: src SRC_TAPS or
 // SRC_PREP; epi EPI_STORE or EPI_SWIGLU (K-split partial sums into split_buf, summed

@@ -372,13 +372,14 @@ int hip_last() {
 struct SplitPlan {
   int n_split, split_len;
 };
-SplitPlan plan_splits(const osprey_handle* h, long ctx_max, long ctx_total, int max_split = kMaxSplit) {
+SplitPlan plan_splits(const osprey_handle* h, long ctx_max, long ctx_total, int max_split = kMaxSplit,
+                      int min_len = 64) {
   // as many blocks as can be resident (two per CU: the kernel's register and LDS
   // budget), the most pages in flight; splits of at most kEvenSplitLen keep the blocks
   // of ragged batches of about equal work
   const long target_blocks = 2L * h->n_cu;
   long len = (ctx_total * h->cfg.n_kv_heads + target_blocks - 1) / target_blocks;
-  len = std::min<long>(std::max<long>(len, 64), kEvenSplitLen);
+  len = std::min<long>(std::max<long>(len, min_len), kEvenSplitLen);
   len = std::max<long>(len, (ctx_max + max_split - 1) / max_split);
   len = std::min<long>(len, kMaxSplitLen);
   len = (len + 15) / 16 * 16;
@@ -473,7 +474,10 @@ void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, c
     a.part = W.attn_part;
     a.o = W.o;
     a.err = W.err;
-    run_attention(h, a);
+    // A single row's O projection merges the context splits while it stages its input
+    // (one launch fewer per layer); otherwise the merge kernel writes o.
+    const bool merge_in_o = gemv_attn_supported(c.dtype, rows.max_rows, nq * hd, hd, sp.n_split);
+    run_attention(h, a, !merge_in_o);
     // O projection + residual
     GemvArgs go{};
     go.max_rows = rows.max_rows;
@@ -486,7 +490,16 @@ void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, c
     go.y = W.x;
     go.ldy = d;
     go.split_buf = W.split;
-    launch_gemv(c.dtype, SRC_PLAIN, EPI_RESID, go, h->stream);
+    if (merge_in_o) {
+      go.attn_part = W.attn_part;
+      go.attn_pos = rows.pos;
+      go.attn_nsplit = sp.n_split;
+      go.attn_split_len = sp.split_len;
+      go.attn_hd = hd;
+      launch_gemv_attn_resid(go, h->stream);
+    } else {
+      launch_gemv(c.dtype, SRC_PLAIN, EPI_RESID, go, h->stream);
+    }
     // post-attention RMSNorm + gate/up + SwiGLU
     GemvArgs gu{};
     gu.max_rows = rows.max_rows;
@@ -1110,7 +1123,12 @@ int step_ingest(osprey_handle* h, const osprey_step_args* a, int K, int extra, S
     ctx_max = std::max(ctx_max, h->ctx_plan);
     ctx_total = std::max(ctx_total, h->ctx_plan * B);
   }
-  split = plan_splits(h, ctx_max, ctx_total, max_split);
+  // A single sequence's bf16 chain takes splits of at least 128 positions: its draft
+  // steps attend faster over a 2K context in 17 splits than in 33, and their O
+  // projection merges that few splits itself.  (Block passes and fp32 caches, whose
+  // attention only loses by it, and trees keep 64.)
+  const bool chain1 = B == 1 && c.dtype == OSPREY_BF16 && block_mask < 0 && K >= 2;
+  split = plan_splits(h, ctx_max, ctx_total, max_split, chain1 ? 128 : 64);
   if (split.n_split > max_split)
     return fail(OSPREY_E_UNSUPPORTED, "a context of %ld positions needs %d splits (at most %d)", ctx_max,
                 split.n_split, max_split);
