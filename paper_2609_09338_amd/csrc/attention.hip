@@ -384,6 +384,7 @@ typedef float att_f32x4 __attribute__((ext_vector_type(4)));
 template <int HD> struct MPage {
   uint4 k[HD / 32];
   uint2 v[HD / 16];
+  bool ok;   // a page of the sequence (else its words come from page 0 and are dropped)
   OSP_DEV void load(const bf16_t* kb, const bf16_t* vb, int lane) {
     const int row = lane & 15, grp = lane >> 4;
 #pragma unroll
@@ -455,14 +456,15 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
   const int n_pg = p_hi > p_lo ? (p_hi - p_lo + PG - 1) / PG : 0;
   const int n_mine = min(64, n_pg > wave ? (n_pg - wave + 3) / 4 : 0);
   const int bt_reg = (lane < n_mine && pid < nblocks) ? bt_any : -1;
+  // Every page is requested with no condition on its index or its table entry: with a
+  // load under a condition the compiler cannot count the loads in flight, and it then
+  // waits for all of them -- the pages requested ahead included -- before using one.
+  // A missing table entry reads page 0 (always in the pool) and drops it in page_step.
   auto load_page = [&](MPage<HD>& pg, int i) {
     const int phys = __shfl(bt_reg, i, OSP_WAVE);
-    if (phys >= 0) {
-      const long base = (long)phys * blk_elems;
-      pg.load(kvb + base + k_off, kvb + base + v_off, lane);
-    } else {
-      pg.zero();
-    }
+    pg.ok = phys >= 0;
+    const long base = (long)max(phys, 0) * blk_elems;
+    pg.load(kvb + base + k_off, kvb + base + v_off, lane);
   };
 
   // ---- 0. the first page early when it holds only older positions ---------------------
@@ -527,9 +529,10 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int p = t0 + 4 * grp + e;
-        s4[e] = (p < p_hi && p <= qpos) ? sc[e] : -INFINITY;
+        const bool in = pg.ok && p < p_hi;
+        s4[e] = (in && p <= qpos) ? sc[e] : -INFINITY;
         bm = fmaxf(bm, s4[e]);
-        if (p < p_hi) keep[e >> 1] |= (e & 1) ? 0xffff0000u : 0x0000ffffu;
+        if (in) keep[e >> 1] |= (e & 1) ? 0xffff0000u : 0x0000ffffu;
       }
 #pragma unroll
       for (int n = 0; n < NT; ++n) { pg.v[n].x &= keep[0]; pg.v[n].y &= keep[1]; }
@@ -556,16 +559,19 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
         acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pl, acc[n], 0, 0, 0);
       }
     };
-    if (n_mine > 0 && !(early && j0 == 0)) load_page(ring[0], 0);
+    // (pages past the wavefront's last are requested as that last page again: an L2 hit,
+    // never used)
+    if (n_mine > 0) {
+      if (!(early && j0 == 0)) load_page(ring[0], 0);
 #pragma unroll
-    for (int u = 1; u + 1 < DEPTH; ++u)
-      if (u < n_mine) load_page(ring[u], u);
+      for (int u = 1; u + 1 < DEPTH; ++u) load_page(ring[u], min(u, n_mine - 1));
+    }
     for (int i0 = 0; i0 < n_mine; i0 += DEPTH) {
 #pragma unroll
       for (int u = 0; u < DEPTH; ++u) {
         const int i = i0 + u;
         if (i < n_mine) {
-          if (i + DEPTH - 1 < n_mine) load_page(ring[(u + DEPTH - 1) % DEPTH], i + DEPTH - 1);
+          load_page(ring[(u + DEPTH - 1) % DEPTH], min(i + DEPTH - 1, n_mine - 1));
           page_step(ring[u], i);
         }
       }
