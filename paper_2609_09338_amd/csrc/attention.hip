@@ -381,18 +381,37 @@ typedef float att_f32x4 __attribute__((ext_vector_type(4)));
 // One 16-token page as matrix-core operands: lane l holds
 //   k[c] = K[token l%16][32 c + 8 (l/16) .. +8]          (A of S^T = K Q^T)
 //   v[n] = V^T[16 n + l%16][tokens 4 (l/16) .. +4]       (A of O^T = V^T P^T)
+typedef unsigned att_u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned att_u32x2 __attribute__((ext_vector_type(2)));
+// STREAM: non-temporal loads, for passes whose context outsizes the last-level cache
+// (they read faster and leave the drafter's weights in that cache).
 template <int HD> struct MPage {
   uint4 k[HD / 32];
   uint2 v[HD / 16];
   bool ok;   // a page of the sequence (else its words come from page 0 and are dropped)
+  template <bool STREAM>
   OSP_DEV void load(const bf16_t* kb, const bf16_t* vb, int lane) {
     const int row = lane & 15, grp = lane >> 4;
 #pragma unroll
-    for (int c = 0; c < HD / 32; ++c)
-      k[c] = *reinterpret_cast<const uint4*>(kb + kv_k_at(row, 32 * c + 8 * grp, HD));
+    for (int c = 0; c < HD / 32; ++c) {
+      const bf16_t* p = kb + kv_k_at(row, 32 * c + 8 * grp, HD);
+      if constexpr (STREAM) {
+        const att_u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const att_u32x4*>(p));
+        k[c] = make_uint4(x[0], x[1], x[2], x[3]);
+      } else {
+        k[c] = *reinterpret_cast<const uint4*>(p);
+      }
+    }
 #pragma unroll
-    for (int n = 0; n < HD / 16; ++n)
-      v[n] = *reinterpret_cast<const uint2*>(vb + kv_v_at(4 * grp, 16 * n + row, 16));
+    for (int n = 0; n < HD / 16; ++n) {
+      const bf16_t* p = vb + kv_v_at(4 * grp, 16 * n + row, 16);
+      if constexpr (STREAM) {
+        const att_u32x2 x = __builtin_nontemporal_load(reinterpret_cast<const att_u32x2*>(p));
+        v[n] = make_uint2(x[0], x[1]);
+      } else {
+        v[n] = *reinterpret_cast<const uint2*>(p);
+      }
+    }
   }
   OSP_DEV void zero() {
 #pragma unroll
@@ -402,7 +421,7 @@ template <int HD> struct MPage {
   }
 };
 
-template <int HD, int DEPTH>
+template <int HD, int DEPTH, bool STREAM>
 __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
   constexpr int PG = 16;               // tokens per KV page
   constexpr int NV = 16;               // query vectors per pass
@@ -464,7 +483,7 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
     const int phys = __shfl(bt_reg, i, OSP_WAVE);
     pg.ok = phys >= 0;
     const long base = (long)max(phys, 0) * blk_elems;
-    pg.load(kvb + base + k_off, kvb + base + v_off, lane);
+    pg.template load<STREAM>(kvb + base + k_off, kvb + base + v_off, lane);
   };
 
   // ---- 0. the first page early when it holds only older positions ---------------------
@@ -818,8 +837,13 @@ static void launch_hd(const AttnArgs& a, hipStream_t st) {
 void launch_attention(int kvdtype, const AttnArgs& a, hipStream_t st) {
   if (kvdtype == 1) {
     dim3 grid(a.nkv, a.B * a.n_split);
-    if (a.hd == 128) hipLaunchKernelGGL((k_attn_mfma<128, kAttnDepth>), grid, dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((k_attn_mfma<64, kAttnDepth>), grid, dim3(256), 0, st, a);
+    if (a.kv_stream) {
+      if (a.hd == 128) hipLaunchKernelGGL((k_attn_mfma<128, kAttnDepth, true>), grid, dim3(256), 0, st, a);
+      else hipLaunchKernelGGL((k_attn_mfma<64, kAttnDepth, true>), grid, dim3(256), 0, st, a);
+    } else {
+      if (a.hd == 128) hipLaunchKernelGGL((k_attn_mfma<128, kAttnDepth, false>), grid, dim3(256), 0, st, a);
+      else hipLaunchKernelGGL((k_attn_mfma<64, kAttnDepth, false>), grid, dim3(256), 0, st, a);
+    }
   } else {
     if (a.hd == 128) launch_hd<float, 128>(a, st); else launch_hd<float, 64>(a, st);
   }

@@ -218,6 +218,8 @@ struct AttnArgs {
   float scale;
   int n_split;              // grid splits; split sp covers positions [sp * split_len, + split_len)
   int split_len;            // tokens per split (multiple of 64; 0: ceil(n_ctx / n_split) per sequence)
+  int kv_stream;            // bf16 pages read with non-temporal loads (a context larger than
+                            // the last-level cache, streamed once per pass)
   const int32_t* items;     // work list from k_setup (b | split << 16), *n_items entries;
   const int32_t* n_items;   // nullable: block y = split * B + b
   const float* q_prep;      // [rows][nq][hd] queries already normalised, rotated and scaled, with

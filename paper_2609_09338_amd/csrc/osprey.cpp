@@ -369,8 +369,10 @@ int hip_last() {
 // lengths still split into blocks of about equal work; no sequence needs more than
 // kMaxSplit of them, and a split is at most kMaxSplitLen tokens (64 pages per
 // wavefront of the attention kernel).
+constexpr long kKvStreamBytes = 160L << 20;   // pages of a pass over every layer
 struct SplitPlan {
   int n_split, split_len;
+  bool kv_stream;   // the context's pages over every layer outsize the last-level cache
 };
 SplitPlan plan_splits(const osprey_handle* h, long ctx_max, long ctx_total, int max_split = kMaxSplit,
                       int min_len = 64) {
@@ -386,6 +388,11 @@ SplitPlan plan_splits(const osprey_handle* h, long ctx_max, long ctx_total, int 
   SplitPlan p;
   p.split_len = (int)len;
   p.n_split = (int)std::max<long>(1, (ctx_max + len - 1) / len);
+  // Pages that cannot stay in the 256 MB last-level cache from one pass to the next are
+  // read non-temporally (faster, and the weights stay cached); a smaller context is
+  // read again by every draft step and keeps plain loads.
+  const long el = h->cfg.dtype == OSPREY_BF16 ? 2 : 4;
+  p.kv_stream = ctx_total * h->cfg.n_layers * h->cfg.n_kv_heads * h->cfg.head_dim * 2 * el > kKvStreamBytes;
   return p;
 }
 
@@ -468,6 +475,7 @@ void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, c
     a.scale = 1.0f / std::sqrt((float)hd);
     a.n_split = sp.n_split;
     a.split_len = sp.split_len;
+    a.kv_stream = sp.kv_stream;
     // the longest-first work list only matters for several sequences
     a.items = B == 1 ? nullptr : W.attn_items;
     a.n_items = B == 1 ? nullptr : W.attn_n_items;
@@ -635,6 +643,7 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     a.scale = 1.0f / std::sqrt((float)hd);
     a.n_split = sp.n_split;
     a.split_len = sp.split_len;
+    a.kv_stream = sp.kv_stream;
     // the longest-first work list only matters for several sequences (it lists the
     // step's sequences, not a tree pass's branches)
     a.items = (B == 1 || tree) ? nullptr : W.attn_items;
