@@ -434,7 +434,13 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
           for (int e = 0; e < 4; ++e) {
             const float lv = (n < a.N && dmap[j] >= 0) ? acc[j][mt][e] : -INFINITY;
             acc[j][mt][e] = lv;
-            if (mt * 16 + 4 * grp + e < R && n < a.N) yc[(long)(mt * 16 + e) * a.ld_logits] = lv;
+            // (64-row passes write 39 MB of logits per launch, read back only at a few
+            // entries: non-temporal stores keep them out of the last-level cache)
+            if (mt * 16 + 4 * grp + e < R && n < a.N) {
+              float* dst = yc + (long)(mt * 16 + e) * a.ld_logits;
+              if constexpr (MT == 4) __builtin_nontemporal_store(lv, dst);
+              else *dst = lv;
+            }
           }
       }
     }
