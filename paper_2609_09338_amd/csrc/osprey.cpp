@@ -44,7 +44,7 @@ int ok() {
 
 constexpr int kMaxSplit = 64;
 constexpr int kMaxSplitLen = 4096;
-constexpr int kEvenSplitLen = 1024;   // longer splits save little and unbalance ragged batches
+constexpr int kEvenSplitLen = 2048;   // longer splits unbalance ragged batches
 constexpr int kVerifyChunk = 4096;
 // A single sequence's pass of at most this many rows prepares its queries in the
 // attention blocks (no separate row kernel).
