@@ -536,8 +536,9 @@ def main():
             at_s = at_ms / 8.0 * 1e-3
             at_gbs = r["attention_bytes"] / at_s / 1e9
             line["attention_roofline"] = {
-                "bound": "hbm", "kernel": "attention (paged split pass + split merge), every pass "
-                "of the timed iterations", "achieved": round(at_gbs, 1), "peak": HBM_PEAK_GBS,
+                "bound": "hbm", "kernel": "attention (paged split pass, and the split merge kernel "
+                "where one runs: passes whose O projection merges the splits launch none), every "
+                "pass of the timed iterations", "achieved": round(at_gbs, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(at_gbs / HBM_PEAK_GBS, 4),
                 "traffic": measured_traffic(args.workload, "attention"),
                 "us_per_launch": round(at_s * 1e6 / max(at_n // 8, 1), 3),
