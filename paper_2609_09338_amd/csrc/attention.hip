@@ -478,9 +478,12 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
   // Every page is requested with no condition on its index or its table entry: with a
   // load under a condition the compiler cannot count the loads in flight, and it then
   // waits for all of them -- the pages requested ahead included -- before using one.
-  // A missing table entry reads page 0 (always in the pool) and drops it in page_step.
+  // A missing table entry, or an index past the wavefront's pages (i >= n_mine: a
+  // request the ring makes at its end), reads page 0 (always in the pool, and cached
+  // after the first such read) and is dropped in page_step or never used.
   auto load_page = [&](MPage<HD>& pg, int i) {
-    const int phys = __shfl(bt_reg, i, OSP_WAVE);
+    const int e = __shfl(bt_reg, min(i, OSP_WAVE - 1), OSP_WAVE);
+    const int phys = i < n_mine ? e : -1;
     pg.ok = phys >= 0;
     const long base = (long)max(phys, 0) * blk_elems;
     pg.template load<STREAM>(kvb + base + k_off, kvb + base + v_off, lane);
@@ -578,19 +581,17 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
         acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pl, acc[n], 0, 0, 0);
       }
     };
-    // (pages past the wavefront's last are requested as that last page again: an L2 hit,
-    // never used)
     if (n_mine > 0) {
       if (!(early && j0 == 0)) load_page(ring[0], 0);
 #pragma unroll
-      for (int u = 1; u + 1 < DEPTH; ++u) load_page(ring[u], min(u, n_mine - 1));
+      for (int u = 1; u + 1 < DEPTH; ++u) load_page(ring[u], u);
     }
     for (int i0 = 0; i0 < n_mine; i0 += DEPTH) {
 #pragma unroll
       for (int u = 0; u < DEPTH; ++u) {
         const int i = i0 + u;
         if (i < n_mine) {
-          load_page(ring[(u + DEPTH - 1) % DEPTH], min(i + DEPTH - 1, n_mine - 1));
+          load_page(ring[(u + DEPTH - 1) % DEPTH], i + DEPTH - 1);
           page_step(ring[u], i);
         }
       }
