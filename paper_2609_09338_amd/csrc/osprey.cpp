@@ -670,12 +670,12 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
       launch_rows_qkv(c.dtype, a, W.o, h->stream);
       a.q_prep = W.o;
     }
-    // Passes of at most 16 rows that are not tree passes merge the context splits while
-    // the O projection stages its inputs (one launch fewer per layer); otherwise the
-    // merge kernel writes o as the projection's input pairs.  (At 32-64 rows each O
-    // block would read about four times its inputs' bytes of split records, in several
-    // rounds: c4 / c5 gained nothing.)
-    const bool merge_in_o = skinny && rows.max_rows <= 16 && !tree && sp.n_split <= kAttnMergeMaxSplit;
+    // Passes that are not tree passes and have at most kAttnMergeMaxSplit splits merge
+    // the context splits while the O projection stages its inputs (one launch fewer per
+    // layer); otherwise the merge kernel writes o as the projection's input pairs.  (At
+    // 32-64 rows each O block reads its inputs' bytes once per split: with 1024-position
+    // splits c4 / c5 gained nothing, with 2048 (at most 3-5 splits) c5 3.168 -> 3.151 ms.)
+    const bool merge_in_o = skinny && !tree && sp.n_split <= kAttnMergeMaxSplit;
     run_attention(h, a, !merge_in_o);
     // O projection; residual + post-attention RMSNorm
     GemvArgs go = gb;
