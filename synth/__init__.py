@@ -181,6 +181,13 @@ PARITY: Dict[str, Workload] = {
                             vocab_target=4513, target_hidden=192, batch=1, K=5, ctx_lo=47,
                             ctx_hi=47, temps=(0.0,), sigma=0.05, vocab_map="inject",
                             shuffle_blocks=True),
+    # One sequence over a 1100-position context: its draft steps merge 9 context splits
+    # in the single-row O projection, its ingest passes through the split merge kernel.
+    "p_single_splits": Workload(name="p_single_splits", cfg_id=20, dtype="bf16", n_layers=2,
+                                d_model=256, n_q_heads=4, n_kv_heads=2, head_dim=128, d_ffn=512,
+                                vocab_draft=3001, vocab_target=4513, target_hidden=192, batch=1,
+                                K=5, ctx_lo=1100, ctx_hi=1100, temps=(1.0,), sigma=0.5,
+                                vocab_map="inject"),
     "p_inject": Workload(name="p_inject", cfg_id=14, dtype="bf16", n_layers=1, d_model=256,
                          n_q_heads=4, n_kv_heads=1, head_dim=128, d_ffn=512, vocab_draft=3001,
                          vocab_target=4513, target_hidden=192, batch=2, K=3, ctx_lo=1, ctx_hi=16,
