@@ -69,7 +69,12 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
   __shared__ __attribute__((aligned(16))) bf16_t xh[ROWS * PITCH];
   __shared__ __attribute__((aligned(16))) bf16_t xl[EXACT ? 8 : ROWS * PITCH];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // (the LM head takes the wavefront index through readfirstlane: the compiler then
+  // knows that its tile range and every condition on it are uniform, and tests them
+  // with scalar branches instead of masking each unit and store; the projections,
+  // one tile per wavefront, measured slower that way)
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = EPI == SK_LOGITS ? __builtin_amdgcn_readfirstlane(tid >> 6) : tid >> 6;
   const int wrow = lane & 15, grp = lane >> 4;
   // rows of this pass: the device-side count when there is one (the host bound may
   // exceed it, and index rows past it, such as tap_row entries, are stale)
@@ -422,26 +427,44 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
     constexpr int V = 4 * MT;
     constexpr int NH = V == 16 ? 4 : (V == 8 ? 3 : 2);    // halving steps (then plain)
     // masked logits (written here, after the stream: stores issued between the ring's
-    // loads would lengthen every wait on them)
+    // loads would lengthen every wait on them).  Conditions that hold for the whole
+    // wavefront (every row of the pass present, a tile inside the vocabulary) are taken
+    // once per tile, and per-element ones are selects: tested per element, the compiler
+    // gave every store and update a branch of its own (about 500 at 64 rows).
+    const bool all_rows = R == ROWS;
 #pragma unroll
     for (int j = 0; j < TMAX; ++j) {
       if (j < ntiles) {
         const int n = (t0 + j) * 16 + wrow;
-        float* yc = a.y + (long)(4 * grp) * a.ld_logits + n;
+        const bool keep = n < a.N && dmap[j] >= 0;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float lv = (n < a.N && dmap[j] >= 0) ? acc[j][mt][e] : -INFINITY;
-            acc[j][mt][e] = lv;
-            // (64-row passes write 39 MB of logits per launch, read back only at a few
-            // entries: non-temporal stores keep them out of the last-level cache)
-            if (mt * 16 + 4 * grp + e < R && n < a.N) {
+          for (int e = 0; e < 4; ++e) acc[j][mt][e] = keep ? acc[j][mt][e] : -INFINITY;
+        float* yc = a.y + (long)(4 * grp) * a.ld_logits + n;
+        // (64-row passes write 39 MB of logits per launch, read back only at a few
+        // entries: non-temporal stores keep them out of the last-level cache)
+        if (all_rows && (t0 + j + 1) * 16 <= a.N) {
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
               float* dst = yc + (long)(mt * 16 + e) * a.ld_logits;
-              if constexpr (MT == 4) __builtin_nontemporal_store(lv, dst);
-              else *dst = lv;
+              if constexpr (MT == 4) __builtin_nontemporal_store(acc[j][mt][e], dst);
+              else *dst = acc[j][mt][e];
             }
-          }
+        } else {
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              float* dst = yc + (long)(mt * 16 + e) * a.ld_logits;
+              if (mt * 16 + 4 * grp + e < R && n < a.N) {
+                if constexpr (MT == 4) __builtin_nontemporal_store(acc[j][mt][e], dst);
+                else *dst = acc[j][mt][e];
+              }
+            }
+        }
       }
     }
     float rv[V];
@@ -451,8 +474,12 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
       rv[k] = -INFINITY;
       ri[k] = 0x7fffffff;
 #pragma unroll
-      for (int j = 0; j < TMAX; ++j)
-        if (j < ntiles && acc[j][k / 4][k % 4] > rv[k]) { rv[k] = acc[j][k / 4][k % 4]; ri[k] = (t0 + j) * 16 + wrow; }
+      for (int j = 0; j < TMAX; ++j) {
+        const float v = acc[j][k / 4][k % 4];
+        const bool up = j < ntiles && v > rv[k];
+        rv[k] = up ? v : rv[k];
+        ri[k] = up ? (t0 + j) * 16 + wrow : ri[k];
+      }
     }
     // (1) max and lowest argmax
 #pragma unroll
@@ -497,14 +524,17 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
       const float Mk = __shfl(rv[0], (lane & ~15) | lane_of_row(k), OSP_WAVE);
       const int m = (k / 4) * 16 + 4 * grp + (k % 4);
       const float Tk = m < R ? tk[k] : 0.f;
+      // (masked entries add exp(-inf) = 0; a row with no sum -- T = 0, or every entry
+      // masked, where the terms are NaN -- is selected to 0 after the loop)
+      const bool live = Tk > 0.f && Mk > -INFINITY;
+      const float iT = 1.0f / (live ? Tk : 1.0f);
       float sum = 0.f;
-      if (Tk > 0.f && Mk > -INFINITY) {
-        const float iT = 1.0f / Tk;
 #pragma unroll
-        for (int j = 0; j < TMAX; ++j)
-          if (j < ntiles && acc[j][k / 4][k % 4] > -INFINITY) sum += __expf((acc[j][k / 4][k % 4] - Mk) * iT);
+      for (int j = 0; j < TMAX; ++j) {
+        const float t = __expf((acc[j][k / 4][k % 4] - Mk) * iT);
+        sum += j < ntiles ? t : 0.f;
       }
-      sv[k] = sum;
+      sv[k] = live ? sum : 0.f;
     }
     // (3) sums, reduced like the maxima
 #pragma unroll
