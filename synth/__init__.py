@@ -188,6 +188,12 @@ PARITY: Dict[str, Workload] = {
                                 vocab_draft=3001, vocab_target=4513, target_hidden=192, batch=1,
                                 K=5, ctx_lo=1100, ctx_hi=1100, temps=(1.0,), sigma=0.5,
                                 vocab_map="inject"),
+    # The same with 64-wide heads (8 of them in the merged row).
+    "p_single_splits64": Workload(name="p_single_splits64", cfg_id=21, dtype="bf16", n_layers=2,
+                                  d_model=256, n_q_heads=8, n_kv_heads=2, head_dim=64, d_ffn=512,
+                                  vocab_draft=4001, vocab_target=4001, target_hidden=128, batch=1,
+                                  K=6, ctx_lo=1100, ctx_hi=1100, temps=(0.7,), sigma=1.0,
+                                  vocab_map="identity"),
     "p_inject": Workload(name="p_inject", cfg_id=14, dtype="bf16", n_layers=1, d_model=256,
                          n_q_heads=4, n_kv_heads=1, head_dim=128, d_ffn=512, vocab_draft=3001,
                          vocab_target=4513, target_hidden=192, batch=2, K=3, ctx_lo=1, ctx_hi=16,
