@@ -15,15 +15,18 @@
 
 namespace osp {
 
-constexpr int kSampleThreads = 256;
+// (threads per sequence: 64 / 128 / 256 / 512 / 1024 measured 1009 / 939 / 913 / 904 / 909 us
+// per c2 draft call: the records' per-thread serial work outweighs the barriers)
+constexpr int kSampleThreads = 512;
+constexpr int kSampleWaves = kSampleThreads / OSP_WAVE;
 constexpr int kPer = (kGemvMaxWaves + kSampleThreads - 1) / kSampleThreads;  // records per thread
 
 __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
   const int b = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  __shared__ float s_wm[4];
-  __shared__ int s_wi[4];
-  __shared__ double s_scan[4];
+  __shared__ float s_wm[kSampleWaves];
+  __shared__ int s_wi[kSampleWaves];
+  __shared__ double s_scan[kSampleWaves];
   __shared__ double s_before;
   __shared__ int s_blk, s_row, s_map;
 
@@ -34,7 +37,7 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
   const float u = a.u[(long)b * a.K + k];
   // the hidden state fed back to the next step does not depend on the pick: read it
   // now, with the records, so its load is not one more round trip at the end
-  constexpr int kFbPer = 4;            // d <= kSampleThreads * 4 * kFbPer
+  constexpr int kFbPer = 4096 / (kSampleThreads * 4);   // d <= 4096 = kSampleThreads * 4 * kFbPer
   const int xr = a.gather ? a.gather[b] : b;
   float4 fb[kFbPer];
 #pragma unroll
@@ -73,7 +76,7 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
     __syncthreads();
     float gm = -INFINITY;
     int gi = 0x7fffffff;
-    for (int w = 0; w < 4; ++w) {
+    for (int w = 0; w < kSampleWaves; ++w) {
       if (s_wm[w] > gm) { gm = s_wm[w]; gi = s_wi[w]; }
       else if (s_wm[w] == gm && s_wi[w] < gi) gi = s_wi[w];
     }
