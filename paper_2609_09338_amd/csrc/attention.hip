@@ -121,8 +121,34 @@ struct Page {
 
 constexpr int kMaxSplitAttn = 64;   // context splits per row (bound; the host keeps to it)
 
-// Element `off` of the projections: the sum of the K-split partials (in split
-// order) on the matrix-core path, else the plain row.
+// Elements off[j] (j < N) of the projections: the sums of the K-split partials
+// (in split order) on the matrix-core path, else the plain row.  Every split's load of
+// every element is requested at once, from a clamped address (loads past the last
+// split re-read it and add zero), so no load waits on a condition.
+template <int N>
+OSP_DEV void qkv_get(const AttnArgs& a, const long (&off)[N], float (&out)[N]) {
+  if (a.qkv_ks <= 1) {
+#pragma unroll
+    for (int j = 0; j < N; ++j) out[j] = a.qkv[off[j]];
+    return;
+  }
+  float v[N][kMaxKSplit];
+#pragma unroll
+  for (int k = 0; k < kMaxKSplit; ++k)
+#pragma unroll
+    for (int j = 0; j < N; ++j) v[j][k] = a.qkv[min(k, a.qkv_ks - 1) * a.qkv_split + off[j]];
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < kMaxKSplit; ++k) s += k < a.qkv_ks ? v[j][k] : 0.f;
+    out[j] = s;
+  }
+}
+
+// Element `off` of the projections, as qkv_get does, one element per request: the
+// loads of its splits are issued back to back under uniform branches (no wait between
+// them), with fewer registers held than a batched request needs.
 OSP_DEV float qkv_at(const AttnArgs& a, long off) {
   if (a.qkv_ks <= 1) return a.qkv[off];
   float v[kMaxKSplit];
@@ -132,6 +158,30 @@ OSP_DEV float qkv_at(const AttnArgs& a, long off) {
 #pragma unroll
   for (int k = 0; k < kMaxKSplit; ++k) s += v[k];
   return s;
+}
+
+// The projection elements a wavefront's lanes < hd / 2 need: columns base + lane and
+// base + lane + hd / 2 of each base in `base`.  The matrix-core attention with bf16
+// pages requests all of them at once (its register count allows it: two waves per SIMD
+// either way); the other attention kernels request one element at a time.
+template <typename TKV, int HD>
+constexpr bool kBatchQkv = HD == 128 && sizeof(TKV) == 2;
+
+template <int HD, bool BATCH, int N>
+OSP_DEV void qkv_lanes(const AttnArgs& a, const long (&base)[N], int lane, float (&out)[2 * N]) {
+  constexpr int HALF = HD / 2;
+#pragma unroll
+  for (int j = 0; j < 2 * N; ++j) out[j] = 0.f;
+  if (lane >= HALF) return;
+  if constexpr (BATCH) {
+    long off[2 * N];
+#pragma unroll
+    for (int j = 0; j < N; ++j) { off[2 * j] = base[j] + lane; off[2 * j + 1] = base[j] + lane + HALF; }
+    qkv_get<2 * N>(a, off, out);
+  } else {
+#pragma unroll
+    for (int j = 0; j < N; ++j) { out[2 * j] = qkv_at(a, base[j] + lane); out[2 * j + 1] = qkv_at(a, base[j] + lane + HALF); }
+  }
 }
 
 // Block (kv head blockIdx.x, work item blockIdx.y) -> (sequence, split): from the
@@ -166,9 +216,10 @@ OSP_DEV void append_new_kv(const AttnArgs& a, int r_beg, int r_end, int p_lo, in
     if (blk >= nblocks) { if (lane == 0) atomicOr(a.err, 1u << 3); continue; }
     const long ko = (long)r * a.qkv_w + (a.nq + g) * HD;
     const long vo = (long)r * a.qkv_w + (a.nq + a.nkv + g) * HD;
-    float k1 = lane < HALF ? qkv_at(a, ko + lane) : 0.f, k2 = lane < HALF ? qkv_at(a, ko + lane + HALF) : 0.f;
-    const float v1 = lane < HALF ? qkv_at(a, vo + lane) : 0.f;
-    const float v2 = lane < HALF ? qkv_at(a, vo + lane + HALF) : 0.f;
+    float kv[4];
+    qkv_lanes<HD, kBatchQkv<TKV, HD>>(a, {ko, vo}, lane, kv);
+    float k1 = kv[0], k2 = kv[1];
+    const float v1 = kv[2], v2 = kv[3];
     norm_rope<TKV, HD>(a, a.k_norm, pos, lane, k1, k2);
     const long base = (long)bt[blk] * blk_elems;
     const int w = pos - blk * a.kv_block;
@@ -199,7 +250,9 @@ OSP_DEV void stage_queries(const AttnArgs& a, float (*sm_q)[HD], int j0, int nve
     } else if (jj < nvec) {
       const int r = r_beg + jj / G, h = g * G + jj % G;
       const long qo = (long)r * a.qkv_w + h * HD;
-      float q1 = lane < HALF ? qkv_at(a, qo + lane) : 0.f, q2 = lane < HALF ? qkv_at(a, qo + lane + HALF) : 0.f;
+      float qv[2];
+      qkv_lanes<HD, kBatchQkv<TKV, HD>>(a, {qo}, lane, qv);
+      float q1 = qv[0], q2 = qv[1];
       norm_rope<TKV, HD>(a, a.q_norm, a.rows.pos[r], lane, q1, q2);
       if (lane < HALF) { sm_q[j][lane] = q1 * a.scale; sm_q[j][lane + HALF] = q2 * a.scale; }
     } else if (lane < HALF) {
@@ -648,7 +701,9 @@ __global__ void __launch_bounds__(256) k_rows_qkv(AttnArgs a, float* q_out) {
   const int pos = a.tree_pos ? a.tree_pos[r] : a.rows.pos[r];
   if (hh < a.nq) {
     const long qo = (long)r * a.qkv_w + (long)hh * HD;
-    float q1 = lane < HALF ? qkv_at(a, qo + lane) : 0.f, q2 = lane < HALF ? qkv_at(a, qo + lane + HALF) : 0.f;
+    float qv[2];
+    qkv_lanes<HD, true>(a, {qo}, lane, qv);
+    float q1 = qv[0], q2 = qv[1];
     norm_rope<TKV, HD>(a, a.q_norm, pos, lane, q1, q2);
     if (lane < HALF) {
       float* qp = q_out + ((long)r * a.nq + hh) * HD;
@@ -660,9 +715,10 @@ __global__ void __launch_bounds__(256) k_rows_qkv(AttnArgs a, float* q_out) {
   const int g = hh - a.nq;
   const long ko = (long)r * a.qkv_w + (long)(a.nq + g) * HD;
   const long vo = (long)r * a.qkv_w + (long)(a.nq + a.nkv + g) * HD;
-  float k1 = lane < HALF ? qkv_at(a, ko + lane) : 0.f, k2 = lane < HALF ? qkv_at(a, ko + lane + HALF) : 0.f;
-  const float v1 = lane < HALF ? qkv_at(a, vo + lane) : 0.f;
-  const float v2 = lane < HALF ? qkv_at(a, vo + lane + HALF) : 0.f;
+  float kv[4];
+  qkv_lanes<HD, true>(a, {ko, vo}, lane, kv);
+  float k1 = kv[0], k2 = kv[1];
+  const float v1 = kv[2], v2 = kv[3];
   norm_rope<TKV, HD>(a, a.k_norm, pos, lane, k1, k2);
   if (a.tree_node) {
     // draft tree: into the tree cache at the node's slot, [layer][k | v][kv head][dim]

@@ -23,21 +23,48 @@ OSP_DEV void store_pair4(uint16_t* hi, uint16_t* lo, long o, float4 v) {
   *reinterpret_cast<uint2*>(lo + o) = make_uint2(l[0], l[1]);
 }
 
-// Sum over the K splits of columns [col, col + 4) of row r, in split order; the loads
-// of four splits are requested together.
-OSP_DEV float4 sum_parts4(const RowArgs& a, int r, int col) {
-  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-  const float* p = a.part + (long)r * a.ldp + col;
-  const long stride = (long)a.max_rows * a.ldp;
-  for (int k0 = 0; k0 < a.ks; k0 += 4) {
-    float4 v[4];
+// Sum over the K splits of columns [col, col + 4) of row r, in split order.  The loads
+// of a round of kMaxKSplit splits are requested at once, from clamped addresses: a
+// round's loads past the last split read that split again (a cache hit) and add zero,
+// so no load waits on a condition.  One round covers the projections (at most
+// kMaxKSplit splits); the tap projection over n_taps x target_hidden columns can take
+// more (24 at 3 x 8192), hence the further rounds.
+template <int N>
+OSP_DEV void add_round4(const float* const (&p)[N], long stride, int k0, int ks, float4 (&s)[N]) {
+  float4 v[N][kMaxKSplit];
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      v[q] = k0 + q < a.ks ? *reinterpret_cast<const float4*>(p + (k0 + q) * stride) : make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int q = 0; q < kMaxKSplit; ++q)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) { s.x += v[q].x; s.y += v[q].y; s.z += v[q].z; s.w += v[q].w; }
+    for (int j = 0; j < N; ++j) v[j][q] = *reinterpret_cast<const float4*>(p[j] + min(k0 + q, ks - 1) * stride);
+#pragma unroll
+  for (int j = 0; j < N; ++j)
+#pragma unroll
+    for (int q = 0; q < kMaxKSplit; ++q) {
+      const bool in = k0 + q < ks;
+      s[j].x += in ? v[j][q].x : 0.f; s[j].y += in ? v[j][q].y : 0.f;
+      s[j].z += in ? v[j][q].z : 0.f; s[j].w += in ? v[j][q].w : 0.f;
+    }
+}
+
+// Columns [col[j], col[j] + 4) of row r for each j < N (all requested together).
+template <int N>
+OSP_DEV void sum_parts(const RowArgs& a, int r, const int (&col)[N], float4 (&s)[N]) {
+  const float* p[N];
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    p[j] = a.part + (long)r * a.ldp + col[j];
+    s[j] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  return s;
+  const long stride = (long)a.max_rows * a.ldp;
+  __builtin_assume(a.ks >= 1);   // (every producer writes at least one split)
+  add_round4<N>(p, stride, 0, a.ks, s);
+  for (int k0 = kMaxKSplit; k0 < a.ks; k0 += kMaxKSplit) add_round4<N>(p, stride, k0, a.ks, s);
+}
+
+OSP_DEV float4 sum_parts4(const RowArgs& a, int r, int col) {
+  float4 s[1];
+  sum_parts<1>(a, r, {col}, s);
+  return s[0];
 }
 
 OSP_DEV float block_sum(float v, float* sm) {
@@ -51,16 +78,33 @@ OSP_DEV float block_sum(float v, float* sm) {
   return t;
 }
 
-// x[r] is final: out = rmsnorm(x[r]) * gamma as hi / lo.
-OSP_DEV void norm_out(const RowArgs& a, int r, float ss, float* sm) {
+// Column groups of a row per thread: W <= 4 kRowThreads kRowGroups (= 4096, the largest
+// d_model the library accepts).
+constexpr int kRowGroups = 4;
+
+// Row r's final values are v (column group i at (threadIdx.x + i kRowThreads) 4) and its
+// gain gr: out = rmsnorm(x[r]) * gamma as hi / lo, from registers.
+OSP_DEV void norm_out(const RowArgs& a, int r, const float4 (&v)[kRowGroups], const uint2 (&gr)[kRowGroups],
+                      float ss, float* sm) {
   const float inv = 1.0f / sqrtf(block_sum(ss, sm) / (float)a.W + a.eps);
+#pragma unroll
+  for (int i = 0; i < kRowGroups; ++i) {
+    const int c = (threadIdx.x + i * kRowThreads) * 4;
+    if (c < a.W) {
+      const float4 y = make_float4(v[i].x * inv * bf16_lo(gr[i].x), v[i].y * inv * bf16_hi(gr[i].x),
+                                   v[i].z * inv * bf16_lo(gr[i].y), v[i].w * inv * bf16_hi(gr[i].y));
+      store_pair4(a.out_hi, a.out_lo, (long)r * a.W + c, y);
+    }
+  }
+}
+
+// The gain of this thread's column groups (requested early, used by norm_out).
+OSP_DEV void load_gain(const RowArgs& a, uint2 (&gr)[kRowGroups]) {
   const bf16_t* g = reinterpret_cast<const bf16_t*>(a.gamma);
-  for (int c = threadIdx.x * 4; c < a.W; c += kRowThreads * 4) {
-    const float4 v = *reinterpret_cast<const float4*>(a.x + (long)r * a.W + c);
-    const uint2 gr = *reinterpret_cast<const uint2*>(g + c);
-    const float4 y = make_float4(v.x * inv * bf16_lo(gr.x), v.y * inv * bf16_hi(gr.x),
-                                 v.z * inv * bf16_lo(gr.y), v.w * inv * bf16_hi(gr.y));
-    store_pair4(a.out_hi, a.out_lo, (long)r * a.W + c, y);
+#pragma unroll
+  for (int i = 0; i < kRowGroups; ++i) {
+    const int c = (threadIdx.x + i * kRowThreads) * 4;
+    gr[i] = *reinterpret_cast<const uint2*>(g + min(c, a.W - 4));
   }
 }
 
@@ -69,24 +113,38 @@ __global__ void __launch_bounds__(kRowThreads) k_rows_prep(RowArgs a) {
   const int r = blockIdx.x;
   const int rows = a.count ? min(*a.count, a.max_rows) : a.max_rows;
   if (r >= rows) return;
-  // conditioning segment: tap projection (sum of its splits) or the fed-back state
-  for (int c = threadIdx.x * 4; c < a.W; c += kRowThreads * 4) {
-    const float4 v = a.s_src ? *reinterpret_cast<const float4*>(a.s_src + (long)r * a.W + c)
-                             : sum_parts4(a, r, c);
-    store_pair4(a.s_hi, a.s_lo, (long)r * a.W + c, v);
-  }
-  // token segment: x = embed[tok], then its normalised copy
+  // the token row and the gain are requested first, ahead of the conditioning segment
   int t = a.tok[r];
   t = min(max(t, 0), a.vocab_embed - 1);
   const bf16_t* e = reinterpret_cast<const bf16_t*>(a.embed) + (long)t * a.W;
-  float ss = 0.f;
-  for (int c = threadIdx.x * 4; c < a.W; c += kRowThreads * 4) {
-    const uint2 er = *reinterpret_cast<const uint2*>(e + c);
-    const float4 v = make_float4(bf16_lo(er.x), bf16_hi(er.x), bf16_lo(er.y), bf16_hi(er.y));
-    *reinterpret_cast<float4*>(a.x + (long)r * a.W + c) = v;
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  uint2 gr[kRowGroups], er[kRowGroups];
+  load_gain(a, gr);
+#pragma unroll
+  for (int i = 0; i < kRowGroups; ++i)
+    er[i] = *reinterpret_cast<const uint2*>(e + min(((int)threadIdx.x + i * kRowThreads) * 4, a.W - 4));
+  // conditioning segment: tap projection (sum of its splits) or the fed-back state
+#pragma unroll
+  for (int i = 0; i < kRowGroups; ++i) {
+    const int c = (threadIdx.x + i * kRowThreads) * 4;
+    if (c < a.W) {
+      const float4 v = a.s_src ? *reinterpret_cast<const float4*>(a.s_src + (long)r * a.W + c)
+                               : sum_parts4(a, r, c);
+      store_pair4(a.s_hi, a.s_lo, (long)r * a.W + c, v);
+    }
   }
-  norm_out(a, r, ss, sm);
+  // token segment: x = embed[tok], then its normalised copy
+  float4 v[kRowGroups];
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < kRowGroups; ++i) {
+    const int c = (threadIdx.x + i * kRowThreads) * 4;
+    v[i] = make_float4(bf16_lo(er[i].x), bf16_hi(er[i].x), bf16_lo(er[i].y), bf16_hi(er[i].y));
+    if (c < a.W) {
+      *reinterpret_cast<float4*>(a.x + (long)r * a.W + c) = v[i];
+      ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
+    }
+  }
+  norm_out(a, r, v, gr, ss, sm);
 }
 
 __global__ void __launch_bounds__(kRowThreads) k_rows_resid_norm(RowArgs a) {
@@ -94,16 +152,27 @@ __global__ void __launch_bounds__(kRowThreads) k_rows_resid_norm(RowArgs a) {
   const int r = blockIdx.x;
   const int rows = a.count ? min(*a.count, a.max_rows) : a.max_rows;
   if (r >= rows) return;
-  float ss = 0.f;
-  for (int c = threadIdx.x * 4; c < a.W; c += kRowThreads * 4) {
-    float4* xp = reinterpret_cast<float4*>(a.x + (long)r * a.W + c);
-    const float4 p = sum_parts4(a, r, c);
-    float4 v = *xp;
-    v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
-    *xp = v;
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  // the residual and the gain are requested before the partials, in the same round trip
+  uint2 gr[kRowGroups];
+  load_gain(a, gr);
+  float4 v[kRowGroups];
+#pragma unroll
+  for (int i = 0; i < kRowGroups; ++i) {
+    const int c = (threadIdx.x + i * kRowThreads) * 4;
+    v[i] = *reinterpret_cast<const float4*>(a.x + (long)r * a.W + min(c, a.W - 4));
   }
-  norm_out(a, r, ss, sm);
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < kRowGroups; ++i) {
+    const int c = (threadIdx.x + i * kRowThreads) * 4;
+    if (c < a.W) {
+      const float4 p = sum_parts4(a, r, c);
+      v[i].x += p.x; v[i].y += p.y; v[i].z += p.z; v[i].w += p.w;
+      *reinterpret_cast<float4*>(a.x + (long)r * a.W + c) = v[i];
+      ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
+    }
+  }
+  norm_out(a, r, v, gr, ss, sm);
 }
 
 // Elementwise: the columns of a row are spread over gridDim.y blocks.
@@ -112,8 +181,9 @@ __global__ void __launch_bounds__(kRowThreads) k_rows_swiglu(RowArgs a) {
   const int rows = a.count ? min(*a.count, a.max_rows) : a.max_rows;
   if (r >= rows) return;
   for (int c = (blockIdx.y * kRowThreads + threadIdx.x) * 4; c < a.W; c += gridDim.y * kRowThreads * 4) {
-    const float4 g = sum_parts4(a, r, c);
-    const float4 u = sum_parts4(a, r, a.W + c);
+    float4 gu[2];
+    sum_parts<2>(a, r, {c, a.W + c}, gu);
+    const float4 g = gu[0], u = gu[1];
     const float4 h = make_float4(g.x / (1.0f + __expf(-g.x)) * u.x, g.y / (1.0f + __expf(-g.y)) * u.y,
                                  g.z / (1.0f + __expf(-g.z)) * u.z, g.w / (1.0f + __expf(-g.w)) * u.w);
     store_pair4(a.out_hi, a.out_lo, (long)r * a.W + c, h);
