@@ -184,19 +184,21 @@ OSP_DEV void qkv_lanes(const AttnArgs& a, const long (&base)[N], int lane, float
   }
 }
 
-// Block (kv head blockIdx.x, work item blockIdx.y) -> (sequence, split): from the
-// setup kernel's longest-first list, or split-major when there is none.  False for
-// grid slots past the list.
-OSP_DEV bool attn_block(const AttnArgs& a, int& b, int& sp) {
+// Block (kv head blockIdx.x, work item blockIdx.y) -> (sequence, split, cache slot):
+// from the setup kernel's longest-first list (which carries the slot), or split-major
+// when there is none.  False for grid slots past the list.
+OSP_DEV bool attn_block(const AttnArgs& a, int& b, int& sp, int& slot) {
   const int it = blockIdx.y;
   if (a.items) {
     if (it >= *a.n_items) return false;
     const int v = a.items[it];
-    b = v & 0xffff;
+    b = v & 0xff;
+    slot = (v >> 8) & 0xff;
     sp = v >> 16;
   } else {
     b = it % a.B;
     sp = it / a.B;
+    slot = a.slot0 >= 0 ? a.slot0 : a.bslot[b];
   }
   return true;
 }
@@ -272,8 +274,8 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   __shared__ float sm_l[4][QV];
   __shared__ float sm_o[4][QV][HD];
 
-  int b, sp;
-  if (!attn_block(a, b, sp)) return;
+  int b, sp, slot;
+  if (!attn_block(a, b, sp, slot)) return;
   const int g = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int dseg = (lane & 15) * DPL;  // this lane's head dims
@@ -290,7 +292,6 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   const int p_lo = sp * a.split_len;
   if (p_lo >= n_ctx) return;           // beyond this sequence: the combine reads no partial here
   const int p_hi = min(n_ctx, p_lo + a.split_len);
-  const int slot = a.slot0 >= 0 ? a.slot0 : a.bslot[b];
   const int nblocks = a.slot_nblocks[slot];
   const int32_t* bt = a.block_table + (long)slot * a.max_blocks;
   TKV* kvb = reinterpret_cast<TKV*>(a.kv);
@@ -489,15 +490,14 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
   // being held in registers, which leaves room for a deeper page ring
   __shared__ __attribute__((aligned(16))) uint4 sm_qf[KC][2][64];
 
-  int b, sp;
-  if (!attn_block(a, b, sp)) return;
+  int b, sp, slot;
+  if (!attn_block(a, b, sp, slot)) return;
   const int g = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int row = lane & 15, grp = lane >> 4;
-  // The slot first (an argument for a batch of one), so that the page-table entries of
-  // a whole split, the slot's page count and the row positions are requested together
-  // and the first page follows after one round trip.
-  const int slot = a.slot0 >= 0 ? a.slot0 : a.bslot[b];
+  // The slot comes with the work item (an argument for a batch of one), so that the
+  // page-table entries of a whole split, the slot's page count and the row positions
+  // are requested together and the first page follows after one round trip.
   const int32_t* bt = a.block_table + (long)slot * a.max_blocks;
   const int pg_lo = sp * a.split_len / PG;   // split_len is a multiple of a page
   // this wavefront's pages: split pages wave, wave + 4, ... (at most 64: the host keeps

@@ -220,7 +220,7 @@ struct AttnArgs {
   int split_len;            // tokens per split (multiple of 64; 0: ceil(n_ctx / n_split) per sequence)
   int kv_stream;            // bf16 pages read with non-temporal loads (a context larger than
                             // the last-level cache, streamed once per pass)
-  const int32_t* items;     // work list from k_setup (b | split << 16), *n_items entries;
+  const int32_t* items;     // work list from k_setup (b | slot << 8 | split << 16), *n_items entries;
   const int32_t* n_items;   // nullable: block y = split * B + b
   const float* q_prep;      // [rows][nq][hd] queries already normalised, rotated and scaled, with
                             // the new keys/values already in the cache (nullable: done here)
@@ -321,7 +321,7 @@ struct SetupArgs {
   // attention work list (longest first) for splits of split_len positions, sized
   // for the longest context of the step (ingest + K - 1 draft positions)
   int split_len;
-  int32_t* attn_items;      // [B * n_split]: b | split << 16
+  int32_t* attn_items;      // [B * n_split]: b | slot << 8 | split << 16 (b, slot < kMaxBatch = 256)
   int32_t* attn_n_items;
   uint32_t* err;
   // block drafting (extra > 0): every sequence's rows are its new tokens, then `extra`

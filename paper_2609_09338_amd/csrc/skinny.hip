@@ -252,7 +252,10 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
     const int nitems = R * span8;
     // (the LM head holds 20 MT accumulators: smaller batches for more rows)
     // (attention outputs: 16 loads per piece already)
-    constexpr int BATCH = EPI == SK_LOGITS ? (MT == 4 ? 1 : (MT == 2 ? 2 : 4)) : (SRC == SK_ATTN ? 1 : 4);
+    // (SwiGLU inputs, at most 16 rows: one piece per thread at the usual K range, each
+    // piece kSwRound splits' loads)
+    constexpr int BATCH = EPI == SK_LOGITS ? (MT == 4 ? 1 : (MT == 2 ? 2 : 4)) : ((SRC == SK_ATTN || SRC == SK_SWIGLU) ? 1 : 4);
+    constexpr int kSwRound = 4;
 #pragma unroll 1
     for (int b0 = 0; b0 < nitems; b0 += BATCH * kSkThreads) {
       uint4 hv[BATCH], lv[BATCH];
@@ -267,31 +270,39 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
             h = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16_t*>(a.taps) +
                                                 (long)a.tap_row[r] * a.ldt + c);
           } else if constexpr (SRC == SK_SWIGLU) {
-            // SwiGLU of the gate/up products: their K-split partials added in split order
+            // SwiGLU of the gate/up products: their K-split partials added in split order.
+            // The loads of kSwRound splits are requested at once, from clamped addresses
+            // (a round's loads past the last split re-read it and add zero), so that none
+            // waits on a condition: one round trip for the usual 4 splits.
             const float* pr = a.part_in + (long)r * a.ld_in + c;
             float g[8], u[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) { g[e] = 0.f; u[e] = 0.f; }
-            for (int k0 = 0; k0 < a.ks_in; k0 += 2) {      // two splits' loads at a time
-              float4 gv[2][2], uv[2][2];
+            auto sw_round = [&](int k0) {
+              float4 gv[kSwRound][2], uv[kSwRound][2];
 #pragma unroll
-              for (int q = 0; q < 2; ++q) {
+              for (int q = 0; q < kSwRound; ++q) {
+                const float* pk = pr + (long)min(k0 + q, a.ks_in - 1) * a.part_in_split;
+                gv[q][0] = *reinterpret_cast<const float4*>(pk);
+                gv[q][1] = *reinterpret_cast<const float4*>(pk + 4);
+                uv[q][0] = *reinterpret_cast<const float4*>(pk + a.Kd);
+                uv[q][1] = *reinterpret_cast<const float4*>(pk + a.Kd + 4);
+              }
+#pragma unroll
+              for (int q = 0; q < kSwRound; ++q) {
                 const bool in = k0 + q < a.ks_in;
-                const float* pk = pr + (long)(k0 + q) * a.part_in_split;
                 const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
-                gv[q][0] = in ? *reinterpret_cast<const float4*>(pk) : z;
-                gv[q][1] = in ? *reinterpret_cast<const float4*>(pk + 4) : z;
-                uv[q][0] = in ? *reinterpret_cast<const float4*>(pk + a.Kd) : z;
-                uv[q][1] = in ? *reinterpret_cast<const float4*>(pk + a.Kd + 4) : z;
+                const float4 g0 = in ? gv[q][0] : z, g1 = in ? gv[q][1] : z;
+                const float4 u0 = in ? uv[q][0] : z, u1 = in ? uv[q][1] : z;
+                g[0] += g0.x; g[1] += g0.y; g[2] += g0.z; g[3] += g0.w;
+                g[4] += g1.x; g[5] += g1.y; g[6] += g1.z; g[7] += g1.w;
+                u[0] += u0.x; u[1] += u0.y; u[2] += u0.z; u[3] += u0.w;
+                u[4] += u1.x; u[5] += u1.y; u[6] += u1.z; u[7] += u1.w;
               }
-#pragma unroll
-              for (int q = 0; q < 2; ++q) {
-                g[0] += gv[q][0].x; g[1] += gv[q][0].y; g[2] += gv[q][0].z; g[3] += gv[q][0].w;
-                g[4] += gv[q][1].x; g[5] += gv[q][1].y; g[6] += gv[q][1].z; g[7] += gv[q][1].w;
-                u[0] += uv[q][0].x; u[1] += uv[q][0].y; u[2] += uv[q][0].z; u[3] += uv[q][0].w;
-                u[4] += uv[q][1].x; u[5] += uv[q][1].y; u[6] += uv[q][1].z; u[7] += uv[q][1].w;
-              }
-            }
+            };
+            __builtin_assume(a.ks_in >= 1);   // (the gate/up product wrote at least one split)
+            sw_round(0);
+            for (int k0 = kSwRound; k0 < a.ks_in; k0 += kSwRound) sw_round(k0);
             float y[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) y[e] = g[e] / (1.0f + __expf(-g[e])) * u[e];

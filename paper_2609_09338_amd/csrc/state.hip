@@ -93,7 +93,9 @@ __global__ void __launch_bounds__(kSetupThreads) k_setup(SetupArgs a) {
   }
   // ---- attention work list: every split but the last of each sequence covers
   //      split_len positions; those come first (sequence-major), then the last
-  //      splits by decreasing length, so the longest blocks start first --------------
+  //      splits by decreasing length, so the longest blocks start first.  An item
+  //      carries the sequence's slot, so that a block finds its page table without
+  //      one more dependent load ---------------------------------------------------------
   if (a.attn_items) {
     __shared__ int s_last[kSetupThreads];
     const int nmax = act ? len + n + (a.K > 0 ? a.K - 1 : 0) : 0;
@@ -117,10 +119,10 @@ __global__ void __launch_bounds__(kSetupThreads) k_setup(SetupArgs a) {
     }
     if (act) {
       const int f0 = fbefore + finc - nfull;
-      for (int sp = 0; sp < nfull; ++sp) a.attn_items[f0 + sp] = b | (sp << 16);
+      for (int sp = 0; sp < nfull; ++sp) a.attn_items[f0 + sp] = b | (slot << 8) | (sp << 16);
       int rank = 0;
       for (int o = 0; o < a.B; ++o) rank += (s_last[o] > last || (s_last[o] == last && o < b)) ? 1 : 0;
-      a.attn_items[ftotal + rank] = b | (nfull << 16);
+      a.attn_items[ftotal + rank] = b | (slot << 8) | (nfull << 16);
     }
     if (b == 0) a.attn_n_items[0] = ftotal + a.B;
   }
