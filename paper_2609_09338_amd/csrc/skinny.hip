@@ -83,10 +83,12 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
   const int NR = (EPI == SK_PART && a.w1) ? 2 * a.N : a.N;   // weight rows
   const int nt16 = (NR + 15) >> 4;
   const int t0 = wg * T;
-  const int ntiles = max(0, min(T, nt16 - t0));
+  const int ntiles = max(0, min(min(T, TMAX), nt16 - t0));
   const int k_lo = EPI == SK_PART ? blockIdx.y * kc : 0;
   const int k_hi = EPI == SK_PART ? min(a.Kd, k_lo + kc) : a.Kd;
-  const int nch = EPI == SK_PART ? kc / kSkUnit : NCH;  // units per tile and phase
+  // units per tile and phase (attention outputs: one 256-column unit, a constant, so that
+  // the prefetch below is known to be a single unit)
+  const int nch = EPI == SK_PART ? (SRC == SK_ATTN ? 1 : kc / kSkUnit) : NCH;
   // LM head blocks with no tile at all leave at once (block-uniform, before any barrier)
   if (EPI == SK_LOGITS && blockIdx.x * kSkWaves * T >= nt16) return;
 
@@ -129,7 +131,9 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
     if constexpr (EPI == SK_LOGITS) load_unit_packed(w, k0, u);
     else load_unit(w, k0, u);
   };
-  const int nphase = (k_hi - k_lo + KC - 1) / KC;
+  // (attention outputs: one 256-column unit, one phase; a constant, so that nothing of
+  // the merge is hoisted out of a phase loop ahead of the loads it should follow)
+  const int nphase = SRC == SK_ATTN ? 1 : (k_hi - k_lo + KC - 1) / KC;
   const int nu = ntiles * nch;                          // units per phase
   // single normalised row: thread t stages columns [8t, 8t + 8) (Kd <= 8 x 512), read
   // before the weights are requested (addresses clamped into the row; pieces past Kd
@@ -148,15 +152,31 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
   // multiple of KC) are neither loaded nor multiplied
   auto real = [&](int k0, int u) { return u < nu && k0 + (u % nch) * kSkUnit < k_hi; };
   // the first units of a phase are requested before its inputs are staged.  The
-  // single normalised row requests them with no condition (the addresses are clamped;
-  // a unit that is not real is never used), so that the waits on its input loads need
-  // not assume an unknown number of loads in between; elsewhere a unit past the block's
-  // range could be a whole unit of another block's weights
+  // single normalised row, and the attention outputs' one unit, request them with no
+  // condition (the addresses are clamped; a unit that is not real is never used), so
+  // that the waits on the input loads need not assume an unknown number of loads in
+  // between; elsewhere a unit past the block's range could be a whole unit of another
+  // block's weights
   auto prefetch_phase = [&](int k0) {
 #pragma unroll
     for (int u = 0; u + 1 < kSkDepth; ++u)
-      if (SRC == SK_NORM || real(k0, u)) load(ring[u], k0, u);
+      if (SRC == SK_NORM || (SRC == SK_ATTN && u == 0) || real(k0, u)) load(ring[u], k0, u);
   };
+  // attention outputs: the merge records of item t = (row, head of the K range) and the
+  // item's row position, requested first (the merge weights wait for these alone)
+  constexpr int kSkAttnHeads = 4;   // heads of at least 64 columns in a 256-column K range
+  const int t_r = tid / kSkAttnHeads, t_hh = tid % kSkAttnHeads;
+  float2 ml[SRC == SK_ATTN ? kAttnMergeMaxSplit : 1];
+  int t_pos = 0;
+  if constexpr (SRC == SK_ATTN) {
+    const int hd = a.attn_hd, nh = a.Kd / hd, ns_all = a.attn_nsplit;
+    const int t_h = min(k_lo / hd + t_hh, nh - 1), t_rc = min(t_r, min(a.max_rows, ROWS) - 1);
+    const float* pm = a.attn_part + ((long)t_rc * nh + t_h) * ns_all * (hd + 2);
+#pragma unroll
+    for (int sp = 0; sp < kAttnMergeMaxSplit; ++sp)
+      ml[sp] = *reinterpret_cast<const float2*>(pm + (long)min(sp, ns_all - 1) * (hd + 2));
+    t_pos = a.attn_pos[t_rc];
+  }
   prefetch_phase(k_lo);
   // LM head: the map entries of this lane's columns (one per tile), read from a clamped
   // address with no condition: a value tested where it is loaded would make the
@@ -204,41 +224,7 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
     }
     __syncthreads();
   }
-  // attention output: the weights f_s / L of every (row, head of this block's K range,
-  // split) of the merge max-rescaled splits, once, into LDS (kSkAttnHeads heads of at
-  // least 64 columns cover a K range of at most 256 columns)
-  constexpr int kSkAttnHeads = 4;
   __shared__ float s_af[SRC == SK_ATTN ? ROWS * kSkAttnHeads * kAttnMergeMaxSplit : 1];
-  if constexpr (SRC == SK_ATTN) {
-    const int hd = a.attn_hd, ns_all = a.attn_nsplit, nh = a.Kd / hd;
-    const int h0 = k_lo / hd;
-    // one lane per (row, local head): wavefront-free, at most 64 x 4 of them
-    for (int t = tid; t < R * kSkAttnHeads; t += kSkThreads) {
-      const int r = t / kSkAttnHeads, hh = t % kSkAttnHeads, h = h0 + hh;
-      if (h >= nh || h * hd >= k_hi) continue;
-      const int ns = min(ns_all, a.attn_pos[r] / a.attn_split_len + 1);
-      const float* pp = a.attn_part + ((long)r * nh + h) * ns_all * (hd + 2);
-      float m[kAttnMergeMaxSplit], l[kAttnMergeMaxSplit];
-#pragma unroll
-      for (int sp = 0; sp < kAttnMergeMaxSplit; ++sp) {
-        m[sp] = sp < ns ? pp[(long)sp * (hd + 2)] : -INFINITY;
-        l[sp] = sp < ns ? pp[(long)sp * (hd + 2) + 1] : 0.f;
-      }
-      float M = -INFINITY;
-#pragma unroll
-      for (int sp = 0; sp < kAttnMergeMaxSplit; ++sp) M = fmaxf(M, m[sp]);
-      float f[kAttnMergeMaxSplit], L = 0.f;
-#pragma unroll
-      for (int sp = 0; sp < kAttnMergeMaxSplit; ++sp) {
-        f[sp] = m[sp] > -INFINITY ? __expf(m[sp] - M) : 0.f;
-        L += l[sp] * f[sp];
-      }
-#pragma unroll
-      for (int sp = 0; sp < kAttnMergeMaxSplit; ++sp)
-        s_af[(r * kSkAttnHeads + hh) * kAttnMergeMaxSplit + sp] = L > 0.f ? f[sp] / L : 0.f;
-    }
-    __syncthreads();
-  }
   for (int ph = 0; ph < nphase; ++ph) {
     const int k0 = k_lo + ph * KC;
     if constexpr (SRC != SK_NORM) {
@@ -251,11 +237,111 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
     const int span8 = (EPI == SK_PART ? kc : KC) / 8;      // 16-byte pieces per row
     const int nitems = R * span8;
     // (the LM head holds 20 MT accumulators: smaller batches for more rows)
-    // (attention outputs: 16 loads per piece already)
     // (SwiGLU inputs, at most 16 rows: one piece per thread at the usual K range, each
     // piece kSwRound splits' loads)
-    constexpr int BATCH = EPI == SK_LOGITS ? (MT == 4 ? 1 : (MT == 2 ? 2 : 4)) : ((SRC == SK_ATTN || SRC == SK_SWIGLU) ? 1 : 4);
+    constexpr int BATCH = EPI == SK_LOGITS ? (MT == 4 ? 1 : (MT == 2 ? 2 : 4)) : (SRC == SK_SWIGLU ? 1 : 4);
     constexpr int kSwRound = 4;
+    if constexpr (SRC == SK_ATTN) {
+      // Attention outputs (K range of one 256-column unit: 32 pieces per row, MT pieces
+      // per thread).  Piece (row r, columns c .. c + 7 = dims e .. e + 7 of head hq) is
+      // the splits' unnormalised outputs weighted by f_s / L (the merge of max-rescaled
+      // splits, M the largest max of the row's splits), added in split order.  Thread t
+      // also computes the weights of item t = (row, head of the range).  Everything is
+      // requested at once with the unit of weights: the items' positions and split
+      // records, then the first AS splits' outputs of the pieces (32 float2 per thread:
+      // 1 x 8 at 16 rows, 2 x 4 at 32, 4 x 2 at 64), from clamped addresses below the
+      // host's row bound, so that no load waits on the device row count or a position.
+      // A split past the row's own count (weight 0) is dropped by selection, never
+      // multiplied (its record may be stale); rows past the count are not stored.  (The
+      // items' records were requested before the weights, above.)
+      constexpr int AB = MT, AS = kAttnMergeMaxSplit / MT;
+      const int hd = a.attn_hd, nh = a.Kd / hd, ns_all = a.attn_nsplit, rec = hd + 2;
+      const int rb = min(a.max_rows, ROWS);
+      const int h0 = k_lo / hd;
+      // the pieces' outputs, first round
+      const float* pp[AB];
+      int pr[AB], pc[AB];
+#pragma unroll
+      for (int q = 0; q < AB; ++q) {
+        const int i = tid + q * kSkThreads;
+        pr[q] = i / span8;
+        pc[q] = (i - pr[q] * span8) * 8;
+        const int c = min(k0 + pc[q], k_hi - 8), hq = c / hd;
+        pp[q] = a.attn_part + ((long)min(pr[q], rb - 1) * nh + hq) * ns_all * rec + 2 + (c - hq * hd);
+      }
+      float2 v[AB][AS][4];
+      auto load_round = [&](int s0) {
+#pragma unroll
+        for (int q = 0; q < AB; ++q)
+#pragma unroll
+          for (int sp = 0; sp < AS; ++sp)
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+              v[q][sp][t] = *reinterpret_cast<const float2*>(pp[q] + (long)min(s0 + sp, ns_all - 1) * rec + 2 * t);
+      };
+      load_round(0);
+      // (the first round is consumed here, ahead of the barrier below: left to itself the
+      // compiler requests it after the barrier, one round trip later)
+#pragma unroll
+      for (int q = 0; q < AB; ++q)
+#pragma unroll
+        for (int sp = 0; sp < AS; ++sp)
+#pragma unroll
+          for (int t = 0; t < 4; ++t) asm volatile("" ::"v"(v[q][sp][t].x), "v"(v[q][sp][t].y));
+      // weights of item t into LDS (rows past the bound and heads past the range get 0)
+      if (tid < ROWS * kSkAttnHeads) {
+        const bool t_ok = t_r < rb && h0 + t_hh < nh && (h0 + t_hh) * hd < k_hi;
+        const int ns = min(ns_all, t_pos / a.attn_split_len + 1);
+        float M = -INFINITY;
+#pragma unroll
+        for (int sp = 0; sp < kAttnMergeMaxSplit; ++sp) M = sp < ns ? fmaxf(M, ml[sp].x) : M;
+        float f[kAttnMergeMaxSplit], L = 0.f;
+#pragma unroll
+        for (int sp = 0; sp < kAttnMergeMaxSplit; ++sp) {
+          f[sp] = (sp < ns && ml[sp].x > -INFINITY) ? __expf(ml[sp].x - M) : 0.f;
+          L = f[sp] > 0.f ? L + ml[sp].y * f[sp] : L;
+        }
+#pragma unroll
+        for (int sp = 0; sp < kAttnMergeMaxSplit; ++sp)
+          s_af[(t_r * kSkAttnHeads + t_hh) * kAttnMergeMaxSplit + sp] = (t_ok && L > 0.f) ? f[sp] / L : 0.f;
+      }
+      __syncthreads();
+      float y[AB][8];
+#pragma unroll
+      for (int q = 0; q < AB; ++q)
+#pragma unroll
+        for (int t = 0; t < 8; ++t) y[q][t] = 0.f;
+      for (int s0 = 0; s0 < ns_all; s0 += AS) {
+        if (s0 > 0) load_round(s0);
+#pragma unroll
+        for (int q = 0; q < AB; ++q) {
+          const int c = min(k0 + pc[q], k_hi - 8), hq = c / hd;
+          const float* fw = s_af + (min(pr[q], ROWS - 1) * kSkAttnHeads + (hq - h0)) * kAttnMergeMaxSplit;
+#pragma unroll
+          for (int sp = 0; sp < AS; ++sp) {
+            const float w = s0 + sp < ns_all ? fw[min(s0 + sp, kAttnMergeMaxSplit - 1)] : 0.f;
+            const bool in = w != 0.f;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              y[q][2 * t] = in ? y[q][2 * t] + w * v[q][sp][t].x : y[q][2 * t];
+              y[q][2 * t + 1] = in ? y[q][2 * t + 1] + w * v[q][sp][t].y : y[q][2 * t + 1];
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < AB; ++q) {
+        if (pr[q] < R && k0 + pc[q] < k_hi) {
+          uint4 h, l;
+          split_bf16x2(y[q][0], y[q][1], h.x, l.x);
+          split_bf16x2(y[q][2], y[q][3], h.y, l.y);
+          split_bf16x2(y[q][4], y[q][5], h.z, l.z);
+          split_bf16x2(y[q][6], y[q][7], h.w, l.w);
+          *reinterpret_cast<uint4*>(xh + pr[q] * PITCH + pc[q]) = h;
+          *reinterpret_cast<uint4*>(xl + pr[q] * PITCH + pc[q]) = l;
+        }
+      }
+    } else {
 #pragma unroll 1
     for (int b0 = 0; b0 < nitems; b0 += BATCH * kSkThreads) {
       uint4 hv[BATCH], lv[BATCH];
@@ -310,39 +396,6 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
             split_bf16x2(y[2], y[3], h.y, l.y);
             split_bf16x2(y[4], y[5], h.z, l.z);
             split_bf16x2(y[6], y[7], h.w, l.w);
-          } else if constexpr (SRC == SK_ATTN) {
-            // columns c .. c + 7 of row r: one head h, dims e .. e + 7; the splits'
-            // unnormalised outputs weighted by s_af, in split order
-            const int hd = a.attn_hd, hq = c / hd, e = c - hq * hd, nh = a.Kd / hd;
-            const int ns_all = a.attn_nsplit;
-            const float* pp = a.attn_part + ((long)r * nh + hq) * ns_all * (hd + 2) + 2 + e;
-            const float* fw = s_af + (r * kSkAttnHeads + (hq - k_lo / hd)) * kAttnMergeMaxSplit;
-            // (a split's record is hd + 2 floats: its outputs are 8-byte aligned, so they
-            // are read as float2)
-            float2 v[kAttnMergeMaxSplit][4];
-#pragma unroll
-            for (int sp = 0; sp < kAttnMergeMaxSplit; ++sp) {
-              // (splits past this row's hold nothing: their weight is 0 and they are
-              // not read)
-              const bool in = sp < ns_all && fw[sp] != 0.f;
-#pragma unroll
-              for (int q = 0; q < 4; ++q)
-                v[sp][q] = in ? *reinterpret_cast<const float2*>(pp + (long)sp * (hd + 2) + 2 * q)
-                              : make_float2(0.f, 0.f);
-            }
-            float y[8];
-#pragma unroll
-            for (int q = 0; q < 8; ++q) y[q] = 0.f;
-#pragma unroll
-            for (int sp = 0; sp < kAttnMergeMaxSplit; ++sp) {
-              const float w = fw[sp];
-#pragma unroll
-              for (int q = 0; q < 4; ++q) { y[2 * q] += w * v[sp][q].x; y[2 * q + 1] += w * v[sp][q].y; }
-            }
-            split_bf16x2(y[0], y[1], h.x, l.x);
-            split_bf16x2(y[2], y[3], h.y, l.y);
-            split_bf16x2(y[4], y[5], h.z, l.z);
-            split_bf16x2(y[6], y[7], h.w, l.w);
           } else if (c < a.seg) {
             const long o = (long)r * a.ld_xs + c;
             h = *reinterpret_cast<const uint4*>(a.xs_hi + o);
@@ -365,6 +418,7 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
           if constexpr (!EXACT) *reinterpret_cast<uint4*>(xl + r * PITCH + col) = lv[q];
         }
       }
+    }
     }
     __syncthreads();
     }
