@@ -194,6 +194,12 @@ PARITY: Dict[str, Workload] = {
                                   vocab_draft=4001, vocab_target=4001, target_hidden=128, batch=1,
                                   K=6, ctx_lo=1100, ctx_hi=1100, temps=(0.7,), sigma=1.0,
                                   vocab_map="identity"),
+    # Taps of 3 x 8192 columns: the pending ingest's tap projection (18 rows) has 24 K
+    # splits, more than one round of the row kernel's split sum.
+    "p_wide_taps": Workload(name="p_wide_taps", cfg_id=22, dtype="bf16", n_layers=2, d_model=256,
+                            n_q_heads=4, n_kv_heads=2, head_dim=64, d_ffn=512, vocab_draft=3001,
+                            vocab_target=3001, target_hidden=8192, batch=3, K=5, ctx_lo=20,
+                            ctx_hi=44, temps=(1.0, 0.0, 0.7), sigma=0.5, shuffle_blocks=True),
     "p_inject": Workload(name="p_inject", cfg_id=14, dtype="bf16", n_layers=1, d_model=256,
                          n_q_heads=4, n_kv_heads=1, head_dim=128, d_ffn=512, vocab_draft=3001,
                          vocab_target=4513, target_hidden=192, batch=2, K=3, ctx_lo=1, ctx_hi=16,

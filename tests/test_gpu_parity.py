@@ -202,7 +202,7 @@ def _assert_exact_comparisons(stats, name):
 
 @pytest.mark.parametrize("name", ["p_tiny_f32", "p_qwen_small", "p_partial", "p_inject",
                                   "p_greedy_draft", "p_single64", "p_single128", "p_single_splits",
-                                  "p_single_splits64", "p_block", "p_block_single"])
+                                  "p_single_splits64", "p_block", "p_block_single", "p_wide_taps"])
 def test_iterations_match_oracle(name):
     _require_gpu()
     w = synth.get(name)
