@@ -40,7 +40,7 @@ typedef float mfma_f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kMmRows = 64;          // input rows per pass (4 M tiles)
 constexpr int kMmKc = 256;           // K columns per chunk
-constexpr int kMmPitch = kMmKc + 8;  // LDS row pitch in bf16 (pads banks)
+constexpr int kMmPitch = kMmKc + 16;  // LDS row pitch in bf16: a 32-byte skew per row (16 bytes left bank conflicts)
 
 // Block shape: 8 wavefronts, two weight tiles each.
 template <int EPI> struct MmShape {

@@ -59,7 +59,10 @@ template <int MT, int SRC, int EPI>
 __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc) {
   constexpr int KC = SkCfg<MT>::KC;
   constexpr int ROWS = 16 * MT;
-  constexpr int PITCH = KC + 8;           // bf16 per LDS row (16-byte skew per row)
+  // bf16 per LDS row: a 32-byte skew per row.  (A 16-byte skew -- or 48, 80 -- left the
+  // A-fragment reads about 3.7 bank-conflict cycles per instruction; 32 bytes leaves
+  // none, rocprofv3 SQ_LDS_BANK_CONFLICT.)
+  constexpr int PITCH = KC + 16;
   constexpr int NCH = KC / kSkUnit;       // units per tile and phase
   constexpr int TMAX = EPI == SK_LOGITS ? kSkTmaxHead : kSkTmaxProj;
   constexpr int NU = TMAX * NCH;          // units per phase (bound)
