@@ -349,17 +349,17 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
           float s = 0.f;
 #pragma unroll
           for (int e = 0; e < DPL; ++e) s = fmaf(q[j][e], pg.k[u].get(e), s);
-          s += __shfl_xor(s, 1, OSP_WAVE);
-          s += __shfl_xor(s, 2, OSP_WAVE);
-          s += __shfl_xor(s, 4, OSP_WAVE);
-          s += __shfl_xor(s, 8, OSP_WAVE);
+          s += xor_lane_c(s, 1);
+          s += xor_lane_c(s, 2);
+          s += xor_lane_c(s, 4);
+          s += xor_lane_c(s, 8);
           const int p = t0 + 4 * u + tsub;
           if (p >= p_hi || p > qpos[j] || blk >= nblocks) s = -INFINITY;
           sc[u] = s;
           bm = fmaxf(bm, s);
         }
-        bm = fmaxf(bm, __shfl_xor(bm, 16, OSP_WAVE));
-        bm = fmaxf(bm, __shfl_xor(bm, 32, OSP_WAVE));
+        bm = fmaxf(bm, xor_lane_c(bm, 16));
+        bm = fmaxf(bm, xor_lane_c(bm, 32));
         const float mn = fmaxf(m[j], bm);
         if (mn == -INFINITY) continue;
         const float so = __expf(m[j] - mn);
@@ -385,9 +385,9 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
     for (int j = 0; j < QV; ++j) {
 #pragma unroll
       for (int sft = 16; sft < 64; sft <<= 1) {
-        l[j] += __shfl_xor(l[j], sft, OSP_WAVE);
+        l[j] += xor_lane_c(l[j], sft);
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) o[j][e] += __shfl_xor(o[j][e], sft, OSP_WAVE);
+        for (int e = 0; e < DPL; ++e) o[j][e] += xor_lane_c(o[j][e], sft);
       }
       if (lane < 16) {
 #pragma unroll
@@ -535,7 +535,7 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
   // request the ring makes at its end), reads page 0 (always in the pool, and cached
   // after the first such read) and is dropped in page_step or never used.
   auto load_page = [&](MPage<HD>& pg, int i) {
-    const int e = __shfl(bt_reg, min(i, OSP_WAVE - 1), OSP_WAVE);
+    const int e = lane_i(bt_reg, min(i, OSP_WAVE - 1));
     const int phys = i < n_mine ? e : -1;
     pg.ok = phys >= 0;
     const long base = (long)max(phys, 0) * blk_elems;
@@ -611,8 +611,8 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
       }
 #pragma unroll
       for (int n = 0; n < NT; ++n) { pg.v[n].x &= keep[0]; pg.v[n].y &= keep[1]; }
-      bm = fmaxf(bm, __shfl_xor(bm, 16, OSP_WAVE));
-      bm = fmaxf(bm, __shfl_xor(bm, 32, OSP_WAVE));
+      bm = fmaxf(bm, xor_lane_c(bm, 16));
+      bm = fmaxf(bm, xor_lane_c(bm, 32));
       const float mn = fmaxf(m, bm);
       const float f = (mn == -INFINITY) ? 1.f : __expf(m - mn);
       float pe[4];
@@ -650,8 +650,8 @@ __global__ void __launch_bounds__(256) k_attn_mfma(AttnArgs a) {
       }
     }
     // ---- merge the wavefronts: lane holds O^T[16 n + 4 grp + e][row] ------------------
-    lsum += __shfl_xor(lsum, 16, OSP_WAVE);
-    lsum += __shfl_xor(lsum, 32, OSP_WAVE);
+    lsum += xor_lane_c(lsum, 16);
+    lsum += xor_lane_c(lsum, 32);
     if (grp == 0) { sm_m[wave][row] = m; sm_l[wave][row] = lsum; }
 #pragma unroll
     for (int n = 0; n < NT; ++n)
@@ -775,7 +775,7 @@ OSP_DEV void tree_partial(const AttnArgs& a, int r, int h, int lane, float& m, f
   bool run = true;                                // leading valid slots only
 #pragma unroll
   for (int i = 0; i < kMaxTreeDepth; ++i) {
-    const int slot = __shfl(my, i, OSP_WAVE);
+    const int slot = lane_i(my, i);
     run = run && slot >= 0 && slot < a.tree_slots;
     ok[i] = run;
     const long kb = ((((long)(run ? slot : 0) * a.n_layers + a.layer) * 2 + 0) * a.nkv + g) * HD + lane * DPL;

@@ -85,6 +85,50 @@ OSP_DEV double lane_d(double v, int l) {
   return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
 }
 
+// The value of lane l ^ M, for every lane l (all 64 lanes active), by VALU operations:
+// DPP within 16-lane rows (quad permutations for 1 and 2; the half-row mirror, lane ^ 7,
+// then the quad reversal, lane ^ 3, for 4; the row rotation by 8 for 8) and the gfx950
+// swaps across rows (v_permlane16_swap / v_permlane32_swap of a register with itself
+// yield rows {0, 0, 2, 2} and {1, 1, 3, 3}, or halves {lo, lo} and {hi, hi}; the lane's
+// row or half bit picks the partner's).  Same partners as a shuffle by xor, so results
+// are the same bit for bit.
+template <int M> OSP_DEV int xor_lane_i(int v, int lane) {
+  if constexpr (M == 1) return dpp_i<kDppXor1>(v);
+  else if constexpr (M == 2) return dpp_i<kDppXor2>(v);
+  else if constexpr (M == 4) return dpp_i<0x1B>(dpp_i<kDppHalfMirror>(v));   // quad_perm [3, 2, 1, 0]
+  else if constexpr (M == 8) return dpp_i<0x128>(v);                          // row_ror:8
+  else if constexpr (M == 16) {
+    const auto p = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v, false, false);
+    return (int)((lane & 16) ? p[0] : p[1]);
+  } else {
+    static_assert(M == 32, "xor mask");
+    const auto p = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+    return (int)((lane & 32) ? p[0] : p[1]);
+  }
+}
+template <int M> OSP_DEV float xor_lane(float v, int lane) { return __int_as_float(xor_lane_i<M>(__float_as_int(v), lane)); }
+template <int M> OSP_DEV double xor_lane_d(double v, int lane) {
+  const long long b = __double_as_longlong(v);
+  const int lo = xor_lane_i<M>((int)(b & 0xffffffffll), lane), hi = xor_lane_i<M>((int)(b >> 32), lane);
+  return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+}
+
+// The same for a mask that is a constant once loops are unrolled.
+OSP_DEV int xor_lane_ci(int v, int m) {
+  const int lane = __lane_id();
+  switch (m) {
+    case 1: return xor_lane_i<1>(v, lane);
+    case 2: return xor_lane_i<2>(v, lane);
+    case 4: return xor_lane_i<4>(v, lane);
+    case 8: return xor_lane_i<8>(v, lane);
+    case 16: return xor_lane_i<16>(v, lane);
+    default: return xor_lane_i<32>(v, lane);
+  }
+}
+OSP_DEV float xor_lane_c(float v, int m) { return __int_as_float(xor_lane_ci(__float_as_int(v), m)); }
+// The value of lane l (the same l on every lane) on every lane.
+OSP_DEV int lane_i(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+
 OSP_DEV float wave_sum(float v) {
   v += dpp_f<kDppXor1>(v);
   v += dpp_f<kDppXor2>(v);
@@ -111,24 +155,31 @@ OSP_DEV float wave_max(float v) {
 // v[0] of lane l holds the full sum of value index (l >> (6 - LOGV)); every
 // lane of that group holds the same total.  Costs about V + 6 shuffles
 // instead of 6 V.
-template <int LOGV>
-OSP_DEV float transpose_reduce(float* v, int lane) {
-  constexpr int V = 1 << LOGV;
-#pragma unroll
-  for (int s = 0; s < LOGV; ++s) {
-    const int m = 32 >> s;
-    const int c = V >> s;
-    const int h = c >> 1;
+template <int S, int LOGV>
+OSP_DEV void tr_half(float* v, int lane) {
+  if constexpr (S < LOGV) {
+    constexpr int m = 32 >> S, h = (1 << LOGV) >> (S + 1);
     const bool hi = (lane & m) != 0;
 #pragma unroll
     for (int i = 0; i < h; ++i) {
-      float mine = hi ? v[i + h] : v[i];
-      float other = hi ? v[i] : v[i + h];
-      v[i] = mine + __shfl_xor(other, m, OSP_WAVE);
+      const float mine = hi ? v[i + h] : v[i];
+      const float other = hi ? v[i] : v[i + h];
+      v[i] = mine + xor_lane<m>(other, lane);
     }
+    tr_half<S + 1, LOGV>(v, lane);
   }
-#pragma unroll
-  for (int m = 32 >> LOGV; m >= 1; m >>= 1) v[0] += __shfl_xor(v[0], m, OSP_WAVE);
+}
+template <int M>
+OSP_DEV void tr_plain(float* v, int lane) {
+  if constexpr (M >= 1) {
+    v[0] += xor_lane<M>(v[0], lane);
+    tr_plain<M / 2>(v, lane);
+  }
+}
+template <int LOGV>
+OSP_DEV float transpose_reduce(float* v, int lane) {
+  tr_half<0, LOGV>(v, lane);
+  tr_plain<(32 >> LOGV)>(v, lane);
   return v[0];
 }
 

@@ -190,8 +190,8 @@ __global__ void __launch_bounds__(MmShape<EPI>::THREADS) k_gemm_mfma(GemvArgs a,
           // reduce over the 16 lanes holding row m (xor 1, 2, 4, 8)
 #pragma unroll
           for (int sft = 1; sft < 16; sft <<= 1) {
-            const float om = __shfl_xor(mx, sft, OSP_WAVE);
-            const int oa = __shfl_xor(am, sft, OSP_WAVE);
+            const float om = xor_lane_c(mx, sft);
+            const int oa = xor_lane_ci(am, sft);
             if (om > mx || (om == mx && oa < am)) { mx = om; am = oa; }
           }
           float se = 0.f;
@@ -200,7 +200,7 @@ __global__ void __launch_bounds__(MmShape<EPI>::THREADS) k_gemm_mfma(GemvArgs a,
             for (int wt = 0; wt < kMmWT; ++wt)
               if (lv[wt] > -INFINITY) se += __expf((lv[wt] - mx) / T[mt][e]);
 #pragma unroll
-          for (int sft = 1; sft < 16; sft <<= 1) se += __shfl_xor(se, sft, OSP_WAVE);
+          for (int sft = 1; sft < 16; sft <<= 1) se += xor_lane_c(se, sft);
           if (ncol == 0 && m < rcount) { s_m[wave][m] = mx; s_s[wave][m] = se; s_a[wave][m] = am; }
         }
       }

@@ -226,12 +226,12 @@ k_gemv(GemvArgs a, int rows_per_wave) {
     if (i + 16 >= ns) { m1 = -INFINITY; l1 = 0.f; }
     float M = fmaxf(m0, m1);
 #pragma unroll
-    for (int o = 1; o < 16; o <<= 1) M = fmaxf(M, __shfl_xor(M, o, OSP_WAVE));
+    for (int o = 1; o < 16; o <<= 1) M = fmaxf(M, xor_lane_c(M, o));
     const float f0 = m0 > -INFINITY ? __expf(m0 - M) : 0.f;
     const float f1 = m1 > -INFINITY ? __expf(m1 - M) : 0.f;
     float L = l0 * f0 + l1 * f1;
 #pragma unroll
-    for (int o = 1; o < 16; o <<= 1) L += __shfl_xor(L, o, OSP_WAVE);
+    for (int o = 1; o < 16; o <<= 1) L += xor_lane_c(L, o);
     if (hh < kGemvAttnMaxHeads) {
       s_f[hh * 32 + i] = L > 0.f ? f0 / L : 0.f;
       s_f[hh * 32 + i + 16] = L > 0.f ? f1 / L : 0.f;

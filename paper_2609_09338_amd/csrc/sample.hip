@@ -164,7 +164,7 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
         const unsigned long long pos = __ballot(w > 0.f);
         if (pos) last_pos = c0 + 63 - __builtin_clzll(pos);
         if (hit) { found = c0 + __builtin_ctzll(hit); break; }
-        run += (double)__shfl(inc, 63, OSP_WAVE);
+        run += (double)lane_f(inc, 63);
       }
       const int pick = found >= 0 ? found : (last_pos >= 0 ? last_pos : am);
       // its target id from the prefetched map when it lies in the prefetched part
@@ -172,7 +172,7 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
 #pragma unroll
       for (int q = 0; q < kScanPre; ++q) {
         const int l = pick - r0 - q * OSP_WAVE;
-        if (l >= 0 && l < OSP_WAVE) dmap = __shfl(pmap[q], l, OSP_WAVE);
+        if (l >= 0 && l < OSP_WAVE) dmap = lane_i(pmap[q], l);
       }
       if (lane == 0) { s_row = pick; s_map = dmap; }
     }

@@ -560,15 +560,15 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
         for (int i = 0; i < half; ++i) {
           const float mv = up ? rv[i + half] : rv[i], ov = up ? rv[i] : rv[i + half];
           const int mi = up ? ri[i + half] : ri[i], oi = up ? ri[i] : ri[i + half];
-          const float pv = __shfl_xor(ov, mask, OSP_WAVE);
-          const int pi = __shfl_xor(oi, mask, OSP_WAVE);
+          const float pv = xor_lane_c(ov, mask);
+          const int pi = xor_lane_ci(oi, mask);
           const bool take = pv > mv || (pv == mv && pi < mi);
           rv[i] = take ? pv : mv;
           ri[i] = take ? pi : mi;
         }
       } else {
-        const float pv = __shfl_xor(rv[0], mask, OSP_WAVE);
-        const int pi = __shfl_xor(ri[0], mask, OSP_WAVE);
+        const float pv = xor_lane_c(rv[0], mask);
+        const int pi = xor_lane_ci(ri[0], mask);
         if (pv > rv[0] || (pv == rv[0] && pi < ri[0])) { rv[0] = pv; ri[0] = pi; }
       }
     }
@@ -614,10 +614,10 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
 #pragma unroll
         for (int i = 0; i < half; ++i) {
           const float mv = up ? sv[i + half] : sv[i], ov = up ? sv[i] : sv[i + half];
-          sv[i] = mv + __shfl_xor(ov, mask, OSP_WAVE);
+          sv[i] = mv + xor_lane_c(ov, mask);
         }
       } else {
-        sv[0] += __shfl_xor(sv[0], mask, OSP_WAVE);
+        sv[0] += xor_lane_c(sv[0], mask);
       }
     }
     if ((lane & ((16 >> NH) - 1)) == 0) {

@@ -30,8 +30,8 @@ OSP_DEV bool tk_better(float v1, int r1, float v2, int r2) { return v1 > v2 || (
 OSP_DEV void wave_best(float& v, int& r) {
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) {
-    const float ov = __shfl_xor(v, m, OSP_WAVE);
-    const int orow = __shfl_xor(r, m, OSP_WAVE);
+    const float ov = xor_lane_c(v, m);
+    const int orow = xor_lane_ci(r, m);
     if (tk_better(ov, orow, v, r)) { v = ov; r = orow; }
   }
 }

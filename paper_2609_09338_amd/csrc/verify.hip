@@ -363,21 +363,22 @@ OSP_DEV ResidRow resid_row(const VerifyArgs& a, int b) {
 // registers (a loop whose bounds the compiler cannot resolve indexes them by runtime
 // selects).
 template <int H, int M>
-OSP_DEV void tr_step(double* v, bool hi) {
+OSP_DEV void tr_step(double* v, int lane) {
+  const bool hi = (lane & M) != 0;
 #pragma unroll
   for (int i = 0; i < H; ++i) {
     const double mine = hi ? v[i + H] : v[i];
     const double other = hi ? v[i] : v[i + H];
-    v[i] = mine + __shfl_xor(other, M, OSP_WAVE);
+    v[i] = mine + xor_lane_d<M>(other, lane);
   }
 }
 OSP_DEV double transpose_reduce16_d(double* v, int lane) {
-  tr_step<8, 32>(v, (lane & 32) != 0);
-  tr_step<4, 16>(v, (lane & 16) != 0);
-  tr_step<2, 8>(v, (lane & 8) != 0);
-  tr_step<1, 4>(v, (lane & 4) != 0);
-  v[0] += __shfl_xor(v[0], 2, OSP_WAVE);
-  v[0] += __shfl_xor(v[0], 1, OSP_WAVE);
+  tr_step<8, 32>(v, lane);
+  tr_step<4, 16>(v, lane);
+  tr_step<2, 8>(v, lane);
+  tr_step<1, 4>(v, lane);
+  v[0] += xor_lane_d<2>(v[0], lane);
+  v[0] += xor_lane_d<1>(v[0], lane);
   return v[0];
 }
 static_assert(kVPer == 16 && kVSub == 4 * kVPer, "one sub-range per (id group q, wavefront)");
@@ -418,15 +419,15 @@ OSP_DEV void final_tail(const VerifyArgs& a, int b, const ResidRow& rr) {
     if (pos) {
       const int l = 63 - __builtin_clzll(pos);
       last = c0 + l;
-      before_last = run + __shfl(inc, l, OSP_WAVE) - __shfl(v, l, OSP_WAVE);
+      before_last = run + lane_d(inc, l) - lane_d(v, l);
     }
     const unsigned long long hit = __ballot(c < n && v > 0.0 && run + inc > target);
     if (hit) {
       const int l = __builtin_ctzll(hit);
       ch = c0 + l;
-      before = run + __shfl(inc, l, OSP_WAVE) - __shfl(v, l, OSP_WAVE);
+      before = run + lane_d(inc, l) - lane_d(v, l);
     }
-    run += __shfl(inc, 63, OSP_WAVE);
+    run += lane_d(inc, 63);
   }
   int tok = -1;
   if (ch < 0 && last >= 0) { ch = last; before = before_last; }
@@ -441,7 +442,7 @@ OSP_DEV void final_tail(const VerifyArgs& a, int b, const ResidRow& rr) {
     if (hit) j = __builtin_ctzll(hit);
     else if (pos) j = 63 - __builtin_clzll(pos);
     if (j >= 0) {
-      const double before2 = before + __shfl(inc, j, OSP_WAVE) - __shfl(v, j, OSP_WAVE);
+      const double before2 = before + lane_d(inc, j) - lane_d(v, j);
       // 3. the id
       const int i1 = min(a.V_T, ch * a.chunk + a.chunk);
       const int id = ch * a.chunk + (j >> 2) * kVThreads + (j & 3) * 64 + lane;
@@ -449,8 +450,8 @@ OSP_DEV void final_tail(const VerifyArgs& a, int b, const ResidRow& rr) {
       const double inc2 = wave_incl_scan<double>(x);
       const unsigned long long pos2 = __ballot(x > 0.0);
       const unsigned long long hit2 = __ballot(x > 0.0 && before2 + inc2 > target);
-      if (hit2) tok = __shfl(id, __builtin_ctzll(hit2), OSP_WAVE);
-      else if (pos2) tok = __shfl(id, 63 - __builtin_clzll(pos2), OSP_WAVE);
+      if (hit2) tok = lane_i(id, __builtin_ctzll(hit2));
+      else if (pos2) tok = lane_i(id, 63 - __builtin_clzll(pos2));
     }
   }
   if (tok < 0) tok = a.vstate[b * 4 + 1];   // nothing positive at all: the argmax
