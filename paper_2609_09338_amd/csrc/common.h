@@ -193,15 +193,36 @@ OSP_DEV uint32_t float_key(float f) {
 
 namespace osp {
 
-// Inclusive prefix sum across the 64 lanes of a wavefront (fixed order).
+// DPP moves that shift data between lanes (lanes with no source read `zero`): within
+// each 16-lane row by n, across the whole wavefront by one, and the broadcast of lane 15
+// (31) of a row to the next row (rows 2 and 3) -- the row mask leaves the others at 0.
+template <int CTRL, int ROWS> OSP_DEV int dpp_shift_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xF, true);
+}
+template <int CTRL, int ROWS> OSP_DEV float dpp_shift(float v) {
+  return __int_as_float(dpp_shift_i<CTRL, ROWS>(__float_as_int(v)));
+}
+template <int CTRL, int ROWS> OSP_DEV double dpp_shift(double v) {
+  const long long b = __double_as_longlong(v);
+  const int lo = dpp_shift_i<CTRL, ROWS>((int)(b & 0xffffffffll)), hi = dpp_shift_i<CTRL, ROWS>((int)(b >> 32));
+  return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+}
+constexpr int kDppRowShr = 0x110;   // + n: row_shr:n
+constexpr int kDppWaveShr1 = 0x138; // wave_shr:1
+constexpr int kDppBcast15 = 0x142;  // row_bcast:15
+constexpr int kDppBcast31 = 0x143;  // row_bcast:31
+
+// Inclusive prefix sum across the 64 lanes of a wavefront (fixed order): a Kogge-Stone
+// scan within each row by DPP row shifts 1, 2, 4, 8, then each row adds the totals of the
+// rows before it (lane 15 broadcast to rows 1 and 3, lane 31 to rows 2 and 3).
 template <typename T>
 OSP_DEV T wave_incl_scan(T v) {
-  const int lane = threadIdx.x & (OSP_WAVE - 1);
-#pragma unroll
-  for (int s = 1; s < OSP_WAVE; s <<= 1) {
-    const T o = __shfl_up(v, s, OSP_WAVE);
-    if (lane >= s) v += o;
-  }
+  v += dpp_shift<kDppRowShr + 1, 0xF>(v);
+  v += dpp_shift<kDppRowShr + 2, 0xF>(v);
+  v += dpp_shift<kDppRowShr + 4, 0xF>(v);
+  v += dpp_shift<kDppRowShr + 8, 0xF>(v);
+  v += dpp_shift<kDppBcast15, 0xA>(v);
+  v += dpp_shift<kDppBcast31, 0xC>(v);
   return v;
 }
 
@@ -214,7 +235,8 @@ OSP_DEV T block_scan(T v, T* sm, T& incl, T& tot) {
   constexpr int NW = NT / OSP_WAVE;
   const int lane = threadIdx.x & (OSP_WAVE - 1), wave = threadIdx.x >> 6;
   const T inc = wave_incl_scan<T>(v);
-  T prev = __shfl_up(inc, 1, OSP_WAVE);
+  // (the inclusive prefix of lane - 1, moved as data: [excl, incl) of neighbours meet)
+  T prev = dpp_shift<kDppWaveShr1, 0xF>(inc);
   if (lane == 0) prev = T(0);
   if (lane == OSP_WAVE - 1) sm[wave] = inc;
   __syncthreads();
