@@ -126,6 +126,24 @@ OSP_DEV int xor_lane_ci(int v, int m) {
   }
 }
 OSP_DEV float xor_lane_c(float v, int m) { return __int_as_float(xor_lane_ci(__float_as_int(v), m)); }
+// The value of lane c of each lane's 16-lane row (DPP row_newbcast), for c a constant
+// once loops are unrolled.
+template <int C> OSP_DEV int row_lane_i(int v) { return __builtin_amdgcn_update_dpp(0, v, 0x150 + C, 0xF, 0xF, false); }
+OSP_DEV float row_lane_c(float v, int c) {
+  const int x = __float_as_int(v);
+  int r;
+  switch (c) {
+    case 0: r = row_lane_i<0>(x); break;    case 1: r = row_lane_i<1>(x); break;
+    case 2: r = row_lane_i<2>(x); break;    case 3: r = row_lane_i<3>(x); break;
+    case 4: r = row_lane_i<4>(x); break;    case 5: r = row_lane_i<5>(x); break;
+    case 6: r = row_lane_i<6>(x); break;    case 7: r = row_lane_i<7>(x); break;
+    case 8: r = row_lane_i<8>(x); break;    case 9: r = row_lane_i<9>(x); break;
+    case 10: r = row_lane_i<10>(x); break;  case 11: r = row_lane_i<11>(x); break;
+    case 12: r = row_lane_i<12>(x); break;  case 13: r = row_lane_i<13>(x); break;
+    case 14: r = row_lane_i<14>(x); break;  default: r = row_lane_i<15>(x); break;
+  }
+  return __int_as_float(r);
+}
 // The value of lane l (the same l on every lane) on every lane.
 OSP_DEV int lane_i(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
 
@@ -199,6 +217,7 @@ namespace osp {
 template <int CTRL, int ROWS> OSP_DEV int dpp_shift_i(int v) {
   return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xF, true);
 }
+template <int CTRL, int ROWS> OSP_DEV int dpp_shift(int v) { return dpp_shift_i<CTRL, ROWS>(v); }
 template <int CTRL, int ROWS> OSP_DEV float dpp_shift(float v) {
   return __int_as_float(dpp_shift_i<CTRL, ROWS>(__float_as_int(v)));
 }

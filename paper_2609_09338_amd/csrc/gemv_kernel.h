@@ -404,8 +404,8 @@ k_gemv(GemvArgs a, int rows_per_wave) {
       const float tot = transpose_reduce<LOGV>(acc, lane);
       if constexpr (EPI == EPI_SWIGLU) {
         // gate rows are values [0, NW), up rows [NW, 2 NW)
-        const int up_lane = ((vi + NW) * RB + rsel) << SH;
-        const float up = __shfl(tot, up_lane < OSP_WAVE ? up_lane : 0, OSP_WAVE);
+        // (the up value of a gate lane sits 32 lanes on: V << SH = 64, up = gate index + V / 2)
+        const float up = xor_lane_c(tot, 32);
         if (owner && vi < NW && rr < rows && n < n_hi)
           a.y[(long)rr * a.ldy + n] = tot / (1.0f + __expf(-tot)) * up;
       } else if constexpr (EPI == EPI_LOGITS) {

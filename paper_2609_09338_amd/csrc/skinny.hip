@@ -589,7 +589,7 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
     float sv[V];
 #pragma unroll
     for (int k = 0; k < V; ++k) {
-      const float Mk = __shfl(rv[0], (lane & ~15) | lane_of_row(k), OSP_WAVE);
+      const float Mk = row_lane_c(rv[0], lane_of_row(k));
       const int m = (k / 4) * 16 + 4 * grp + (k % 4);
       const float Tk = m < R ? tk[k] : 0.f;
       // (masked entries add exp(-inf) = 0; a row with no sum -- T = 0, or every entry

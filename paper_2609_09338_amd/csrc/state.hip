@@ -32,13 +32,7 @@ __global__ void __launch_bounds__(kSetupThreads) k_setup(SetupArgs a) {
   const int m = act ? a.extra : 0;
   // exclusive prefixes over the batch (integer scans: wave scan + wave totals) of the
   // rows (n + m) and of the new rows alone (packed tap rows)
-  int inc = n + m, incn = n;
-#pragma unroll
-  for (int s = 1; s < 64; s <<= 1) {
-    const int o = __shfl_up(inc, s, OSP_WAVE);
-    const int on = __shfl_up(incn, s, OSP_WAVE);
-    if (lane >= s) { inc += o; incn += on; }
-  }
+  const int inc = wave_incl_scan<int>(n + m), incn = wave_incl_scan<int>(n);
   __shared__ int s_totn[4];
   if (lane == 63) { s_tot[wave] = inc; s_totn[wave] = incn; }
   __syncthreads();
@@ -103,12 +97,7 @@ __global__ void __launch_bounds__(kSetupThreads) k_setup(SetupArgs a) {
     const int nfull = ns > 0 ? ns - 1 : 0;
     const int last = act ? nmax - nfull * a.split_len : -1;
     s_last[b] = last;
-    int finc = nfull;
-#pragma unroll
-    for (int s = 1; s < 64; s <<= 1) {
-      const int o = __shfl_up(finc, s, OSP_WAVE);
-      if (lane >= s) finc += o;
-    }
+    const int finc = wave_incl_scan<int>(nfull);
     __syncthreads();
     if (lane == 63) s_tot[wave] = finc;
     __syncthreads();
