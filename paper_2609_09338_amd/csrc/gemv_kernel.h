@@ -20,6 +20,9 @@
 //   SRC_TAPS   target hidden-state taps (Eq. 1)
 //   SRC_ATTN   one row's attention output, merged from its context splits by the
 //              block into LDS before the products (single rows, Kd <= 2048)
+//   SRC_QKV_PICK  SRC_QKV of layer 0 for one sequence: every block draws the step's
+//              token itself from the LM head's records (pick.h) while its first
+//              weights are in flight, so that no sampling kernel runs in between
 // and the epilogue writes, accumulates into the residual, applies SwiGLU, or
 // writes masked logits plus, per wavefront range, the (max, sum exp((l-max)/T),
 // lowest argmax) statistics that sampling merges.
@@ -27,11 +30,15 @@
 
 #include "common.h"
 #include "internal.h"
+#include "pick.h"
 
 namespace osp {
 
 constexpr int kGemvThreads = 256;
 constexpr int kGemvWavesPerBlock = kGemvThreads / OSP_WAVE;
+
+// Expanded-QKV input kinds (the token's own draw aside, the same input).
+constexpr bool src_qkv(int src) { return src == SRC_QKV || src == SRC_QKV_PICK; }
 
 template <int N> struct Log2 { static constexpr int v = 1 + Log2<N / 2>::v; };
 template <> struct Log2<1> { static constexpr int v = 0; };
@@ -74,8 +81,9 @@ OSP_DEV void load_f4s(const float* p, float* out, int n) {
 
 // Raw input values X[rr][col .. col+VEC) before normalisation, and whether they
 // belong to the normalised segment (norm factor still to be applied).
+// (SRC_QKV_PICK: `tok` is the token the block drew; the other kinds ignore it.)
 template <typename TW, int SRC, int VEC>
-OSP_DEV bool load_x_raw(const GemvArgs& a, int rr, int col, float* out) {
+OSP_DEV bool load_x_raw(const GemvArgs& a, int rr, int col, float* out, int tok = 0) {
   if constexpr (SRC == SRC_PLAIN) {
     load_f4s(a.xin + (long)rr * a.ldx + col, out, VEC);
     return false;
@@ -84,7 +92,7 @@ OSP_DEV bool load_x_raw(const GemvArgs& a, int rr, int col, float* out) {
     return false;
   } else {
     int c = col;
-    if constexpr (SRC == SRC_QKV) {
+    if constexpr (src_qkv(SRC)) {
       if (col < a.d_norm) {   // conditioning segment, used as is
         const int sr = a.s_gather ? a.s_gather[rr] : rr;
         load_f4s(a.s + (long)sr * a.lds + col, out, VEC);
@@ -92,7 +100,7 @@ OSP_DEV bool load_x_raw(const GemvArgs& a, int rr, int col, float* out) {
       }
       c = col - a.d_norm;
       if (a.embed) {
-        int t = a.tok[rr];
+        int t = SRC == SRC_QKV_PICK ? tok : a.tok[rr];
         t = min(max(t, 0), a.vocab_embed - 1);
         load_vec<TW>(reinterpret_cast<const TW*>(a.embed) + (long)t * a.d_norm + c, out);
         return true;
@@ -107,7 +115,7 @@ OSP_DEV bool load_x_raw(const GemvArgs& a, int rr, int col, float* out) {
 // Apply RMSNorm factor and gain to a normalised-segment vector.
 template <typename TW, int SRC, int VEC>
 OSP_DEV void norm_x(const GemvArgs& a, int col, float inv_rms, float* v) {
-  const int c = (SRC == SRC_QKV) ? col - a.d_norm : col;
+  const int c = src_qkv(SRC) ? col - a.d_norm : col;
   float g[VEC];
   load_vec<TW>(reinterpret_cast<const TW*>(a.gamma) + c, g);
 #pragma unroll
@@ -116,18 +124,18 @@ OSP_DEV void norm_x(const GemvArgs& a, int col, float inv_rms, float* v) {
 
 // Column of the gain vector that input column `col` uses (negative: not normalised).
 template <int SRC>
-OSP_DEV int gain_col(const GemvArgs& a, int col) { return SRC == SRC_QKV ? col - a.d_norm : col; }
+OSP_DEV int gain_col(const GemvArgs& a, int col) { return src_qkv(SRC) ? col - a.d_norm : col; }
 
 // 1 / sqrt(mean(x^2) + eps) of the normalised segment of row rr, by one wavefront.
 template <typename TW, int SRC>
-OSP_DEV float row_inv_rms(const GemvArgs& a, int rr, int lane) {
+OSP_DEV float row_inv_rms(const GemvArgs& a, int rr, int lane, int tok) {
   constexpr int VEC = Vec<TW>::N;
   const int d = a.d_norm;
-  const int base = (SRC == SRC_QKV) ? d : 0;
+  const int base = src_qkv(SRC) ? d : 0;
   float ss = 0.f;
   for (int c = lane * VEC; c < d; c += OSP_WAVE * VEC) {
     float v[VEC];
-    load_x_raw<TW, SRC, VEC>(a, rr, base + c, v);
+    load_x_raw<TW, SRC, VEC>(a, rr, base + c, v, tok);
 #pragma unroll
     for (int e = 0; e < VEC; ++e) ss += v[e] * v[e];
   }
@@ -149,21 +157,22 @@ constexpr int kGemvAttnMaxHeads = 16;   // heads of the merged row (bound)
 
 template <typename TW, int SRC, int EPI, int RB, int NW, int XV, bool CACHED>
 __global__ void __launch_bounds__(kGemvThreads,
-                                  (SRC == SRC_ATTN ? 1 : GemvOcc<RB, NW, XV, (SRC == SRC_NORM || SRC == SRC_QKV)>::value))
+                                  (SRC == SRC_ATTN ? 1 : GemvOcc<RB, NW, XV, (SRC == SRC_NORM || src_qkv(SRC))>::value))
 k_gemv(GemvArgs a, int rows_per_wave) {
   constexpr int VEC = Vec<TW>::N;
   constexpr int NWV = (EPI == EPI_SWIGLU) ? 2 * NW : NW;
   constexpr int V = NWV * RB;
   constexpr int LOGV = Log2<V>::v;
   constexpr int SH = 6 - LOGV;
-  constexpr bool NORMED = (SRC == SRC_NORM || SRC == SRC_QKV);
+  constexpr bool NORMED = (SRC == SRC_NORM || src_qkv(SRC));
   static_assert((1 << LOGV) == V && V <= 64, "values per lane must be a power of two <= 64");
 
   const int lane = threadIdx.x & (OSP_WAVE - 1);
   const int gw = blockIdx.x * kGemvWavesPerBlock + (threadIdx.x >> 6);
   const int n_lo = gw * rows_per_wave;
-  // (the split merge of SRC_ATTN needs every wavefront of the block at its barriers)
-  if (SRC != SRC_ATTN && n_lo >= a.N) return;
+  // (the split merge of SRC_ATTN and the pick of SRC_QKV_PICK need every wavefront of
+  // the block at their barriers)
+  if (SRC != SRC_ATTN && SRC != SRC_QKV_PICK && n_lo >= a.N) return;
   const int n_hi = min(a.N, n_lo + rows_per_wave);
   const int rows = a.count ? min(*a.count, a.max_rows) : a.max_rows;
   const TW* __restrict__ w0 = reinterpret_cast<const TW*>(a.w0);
@@ -179,18 +188,70 @@ k_gemv(GemvArgs a, int rows_per_wave) {
 #pragma unroll
       for (int u = 0; u < XV; ++u) {
         const int j = jb + lane + OSP_WAVE * u;
-        if (n < n_hi && j < nvec)
+        if constexpr (SRC == SRC_QKV_PICK) {
+          // clamped addresses, no condition: the compiler must count these loads exactly
+          // for the pick's waits not to cover them (rows past n_hi are never stored;
+          // columns past Kd meet zero inputs, and the clamped weights are finite)
+          wr[i][u].load(w0 + (long)min(n, a.N - 1) * a.Kd + min(j, nvec - 1) * VEC);
+        } else if (n < n_hi && j < nvec) {
           wr[i][u].load(((EPI == EPI_SWIGLU && i >= NW) ? w1 : w0) + (long)n * a.Kd + j * VEC);
-        else
+        } else {
           wr[i][u].zero();
+        }
       }
     }
   };
+  // SRC_QKV_PICK: the LM head's records are requested first.  The wavefront's memory
+  // counter is in order, so whatever is requested after the weights arrives no earlier
+  // than they do; the pick's chain (records, then the chosen range's logits, then the
+  // token's embedding row) would otherwise start only once the weights are in.
+  constexpr int kPickPer = kPickMaxRecords / kGemvThreads;
+  PickRecs<SRC == SRC_QKV_PICK ? kPickPer : 1> rec;
+  int pk_pos = 0;   // the step's position (block 0, thread 0 writes it out at the end)
+  if constexpr (SRC == SRC_QKV_PICK) {
+    pick_request<kGemvThreads, kPickPer>(rec, a.pick.part, a.pick.nblk);
+    pk_pos = a.pick.committed[0] + a.pick.k;
+  }
+
   // The first step's weights do not depend on the input rows: they are requested
   // before the rows, their norm and the gains, so that those latencies overlap.
   WRaw<TW> wr[NWV][XV];
   load_w(wr, n_lo, 0);
   bool have_w = true;
+
+  // SRC_QKV_PICK (one row, held in registers): this lane's conditioning values (row 0
+  // of s) and gains do not depend on the token, so they are requested with the
+  // weights, like the embedding values after the pick from clamped addresses with no
+  // condition (the row's loads then wait on one another only once)
+  static_assert(SRC != SRC_QKV_PICK || RB == 1, "the drawing projection takes one row");
+  constexpr bool PK = SRC == SRC_QKV_PICK && CACHED;
+  float xs_pk[PK ? XV : 1][VEC];
+  WRaw<TW> g_pk[PK ? XV : 1];
+  if constexpr (PK) {
+#pragma unroll
+    for (int u = 0; u < XV; ++u) {
+      const int col = (lane + OSP_WAVE * u) * VEC;
+      load_f4s(a.s + min(col, a.d_norm - VEC), xs_pk[u], VEC);
+      g_pk[u].load(reinterpret_cast<const TW*>(a.gamma) + min(max(col - a.d_norm, 0), a.d_norm - VEC));
+    }
+  }
+
+  // (nothing that reads the records may be scheduled above this point: every request
+  // above is issued before the first wait)
+  if constexpr (SRC == SRC_QKV_PICK) __builtin_amdgcn_sched_barrier(0);
+
+  // SRC_QKV_PICK: the step's token, drawn by the whole block (every block draws the same
+  // one); block 0 writes the draft, the next position and the row statistics out when
+  // it is done (their stores would hold up its next loads: the counter is in order)
+  int tok = 0;
+  Pick pk_res{};
+  if constexpr (SRC == SRC_QKV_PICK) {
+    const PickArgs& pk = a.pick;
+    pk_res = pick_draft<kGemvThreads, kPickPer>(rec, pk.part, pk.nblk, pk.blk_rows, pk.logits, pk.V,
+                                                pk.d2t, pk.temp[0], pk.u[0]);
+    tok = pk_res.tok;
+    if (n_lo >= a.N) return;
+  }
 
   // SRC_ATTN (one row, Kd <= 8 kGemvThreads): thread t merges columns [8t, 8t + 8) of
   // head h = 8t / hd.  Split s of head h holds (max m, sum l, unnormalised output o) at
@@ -264,7 +325,45 @@ k_gemv(GemvArgs a, int rows_per_wave) {
     float inv_rms[RB];
 #pragma unroll
     for (int r = 0; r < RB; ++r) inv_rms[r] = 1.f;
-    if constexpr (cached) {
+    if constexpr (PK) {
+      // the embedding row of the drawn token, then the RMS of that segment
+      const int t = min(max(tok, 0), a.vocab_embed - 1);
+      const TW* er = reinterpret_cast<const TW*>(a.embed) + (long)t * a.d_norm;
+      float ev[XV][VEC];
+#pragma unroll
+      for (int u = 0; u < XV; ++u)   // every vector requested before any is used
+        load_vec<TW>(er + min(max((lane + OSP_WAVE * u) * VEC - a.d_norm, 0), a.d_norm - VEC), ev[u]);
+      bool isn[XV];
+      float ss = 0.f;
+#pragma unroll
+      for (int u = 0; u < XV; ++u) {
+        const int j = lane + OSP_WAVE * u;
+        const bool live = j < nvec;
+        isn[u] = live && j * VEC >= a.d_norm;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          xc[0][u][e] = !live ? 0.f : isn[u] ? ev[u][e] : xs_pk[u][e];
+          ss += isn[u] ? ev[u][e] * ev[u][e] : 0.f;
+        }
+      }
+      ss = wave_sum(ss);
+      inv_rms[0] = 1.0f / sqrtf(ss / (float)a.d_norm + a.eps);
+#pragma unroll
+      for (int u = 0; u < XV; ++u) {
+        if (isn[u]) {
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) xc[0][u][e] = xc[0][u][e] * inv_rms[0] * g_pk[u].get(e);
+        }
+        // x = embed[token] for the residual, each vector written by one wavefront
+        const int jn = lane + OSP_WAVE * u - a.d_norm / VEC;
+        if (a.x_out && isn[u] && jn % ((a.N + rows_per_wave - 1) / rows_per_wave) == gw) {
+          float* xo = a.x_out + jn * VEC;
+#pragma unroll
+          for (int e = 0; e < VEC; e += 4)
+            *reinterpret_cast<float4*>(xo + e) = make_float4(ev[u][e], ev[u][e + 1], ev[u][e + 2], ev[u][e + 3]);
+        }
+      }
+    } else if constexpr (cached) {
       // gains of this lane's columns, requested with the rows
       WRaw<TW> gr[XV];
       if constexpr (NORMED) {
@@ -289,13 +388,13 @@ k_gemv(GemvArgs a, int rows_per_wave) {
               for (int e = 0; e < VEC; ++e) xc[r][u][e] = s_x[j * VEC + e];
               isn[u] = false;
             } else {
-              isn[u] = load_x_raw<TW, SRC, VEC>(a, r0 + r, j * VEC, xc[r][u]);
+              isn[u] = load_x_raw<TW, SRC, VEC>(a, r0 + r, j * VEC, xc[r][u], tok);
             }
             if (isn[u]) {
 #pragma unroll
               for (int e = 0; e < VEC; ++e) ss += xc[r][u][e] * xc[r][u][e];
             }
-            if constexpr (SRC == SRC_QKV) {
+            if constexpr (src_qkv(SRC)) {
               // layer 0: x = embed[token] for the residual, each vector written by one
               // wavefront (the one whose index matches it modulo the working wavefronts)
               if (a.embed && a.x_out && isn[u]) {
@@ -328,14 +427,14 @@ k_gemv(GemvArgs a, int rows_per_wave) {
     } else if constexpr (NORMED) {
 #pragma unroll
       for (int r = 0; r < RB; ++r)
-        if (r0 + r < rows) inv_rms[r] = row_inv_rms<TW, SRC>(a, r0 + r, lane);
+        if (r0 + r < rows) inv_rms[r] = row_inv_rms<TW, SRC>(a, r0 + r, lane, tok);
     }
     // layer 0 of the expanded QKV (rows not held in registers): one wavefront writes
     // x = embed[token] for the residual
-    if constexpr (SRC == SRC_QKV && !cached) {
+    if constexpr (src_qkv(SRC) && !cached) {
       if (a.embed && a.x_out && gw == 0) {
         for (int r = 0; r < RB && r0 + r < rows; ++r) {
-          int t = a.tok[r0 + r];
+          int t = SRC == SRC_QKV_PICK ? tok : a.tok[r0 + r];
           t = min(max(t, 0), a.vocab_embed - 1);
           const TW* e = reinterpret_cast<const TW*>(a.embed) + (long)t * a.d_norm;
           for (int c = lane; c < a.d_norm; c += OSP_WAVE)
@@ -381,7 +480,7 @@ k_gemv(GemvArgs a, int rows_per_wave) {
             for (int u = 0; u < XV; ++u) {
               const int j = jb + lane + OSP_WAVE * u;
               if (r0 + r < rows && j < nvec) {
-                const bool isn = load_x_raw<TW, SRC, VEC>(a, r0 + r, j * VEC, xc[r][u]);
+                const bool isn = load_x_raw<TW, SRC, VEC>(a, r0 + r, j * VEC, xc[r][u], tok);
                 if constexpr (NORMED)
                   if (isn) norm_x<TW, SRC, VEC>(a, j * VEC, inv_rms[r], xc[r][u]);
               } else {
@@ -448,6 +547,16 @@ k_gemv(GemvArgs a, int rows_per_wave) {
           p[3] = 0.f;
         }
       }
+    }
+  }
+  if constexpr (SRC == SRC_QKV_PICK) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      const PickArgs& pk = a.pick;
+      pk.draft[0] = pk_res.tok;
+      if (pk.draft_out) pk.draft_out[0] = pk_res.tok;
+      pk.ar_tok[0] = pk_res.tok;
+      pk.ar_pos[0] = pk_pos;
+      if (pk.qstat) pk.qstat[0] = QStat{pk_res.S, pk_res.M, pk_res.am};
     }
   }
 }

@@ -30,6 +30,8 @@ enum SrcKind {
   SRC_ATTN = 6,   // X[r][c] = the attention output of row r, head c / hd, merged from its
                   // context splits (attn_part) on staging: matrix-core passes of <= 64 rows,
                   // and the single-row vector O projection
+  SRC_QKV_PICK = 7, // SRC_QKV of layer 0 for one sequence whose token the kernel draws itself
+                    // from the previous LM head's records and logits (GemvArgs::pick)
 };
 constexpr int kAttnMergeMaxSplit = 8;   // SRC_ATTN: splits per row (bound; else a merge kernel)
 enum EpiKind {
@@ -38,6 +40,37 @@ enum EpiKind {
   EPI_SWIGLU = 2,  // y[r][n] = silu(acc_gate) * acc_up (two weight matrices)
   EPI_LOGITS = 3,  // logits with -inf for unmapped rows + per-block softmax statistics
 };
+
+// Statistics of one drafter logit row at the temperature its draft was drawn at:
+// S = sum exp((l - M) / T_d) over mapped rows (T_d = 0: unused), M the max and am the
+// lowest argmax row (-1: every row masked).
+struct QStat {
+  double S;
+  float M;
+  int am;
+};
+
+// SRC_QKV_PICK: the draft of step k of a single sequence (sequence 0), drawn in every
+// block of the layer-0 projection that consumes it (pick.h); block 0 writes it out as
+// the sampling kernel would.
+struct PickArgs {
+  const float* part;        // the LM head's records of the row (nblk <= kPickMaxRecords)
+  int nblk;
+  int blk_rows;             // logits per record
+  const float* logits;      // the row's logits [V]
+  int V;
+  const int32_t* d2t;
+  const float* temp;        // the sequence's temperature
+  const float* u;           // the step's uniform
+  int k;
+  int32_t* draft;           // the step's draft slot (workspace)
+  int32_t* draft_out;       // the caller's copy of it (nullable)
+  int32_t* ar_tok;          // next AR token / position (position = committed + k)
+  int32_t* ar_pos;
+  const int32_t* committed;
+  QStat* qstat;             // the step's row statistics (nullable)
+};
+constexpr int kPickMaxRecords = 2048;   // 256 threads x 8 records
 
 struct GemvArgs {
   int max_rows;
@@ -97,6 +130,10 @@ struct GemvArgs {
   int attn_nsplit;
   int attn_split_len;
   int attn_hd;
+  // SRC_QKV_PICK: the draft pick of the step; SK_NORM LM head: where block 0 also copies
+  // its fp32 input row (the fed-back hidden state, so that no sampling kernel need copy it)
+  PickArgs pick;
+  float* fb_out;
   uint32_t* err;
 };
 constexpr int kMaxKSplit = 16;
@@ -107,6 +144,10 @@ void launch_gemv(int wdtype, SrcKind src, EpiKind epi, const GemvArgs& a, hipStr
 // Kd = heads x hd <= 2048, at most 16 heads and 20 splits: gemv_attn_supported).
 bool gemv_attn_supported(int wdtype, int rows, int Kd, int hd, int n_split);
 void launch_gemv_attn_resid(const GemvArgs& a, hipStream_t st);
+// Layer-0 expanded QKV of a single sequence that draws its own token (SRC_QKV_PICK; bf16
+// weights, one row, a.pick.nblk <= kPickMaxRecords: gemv_pick_supported).
+bool gemv_pick_supported(int wdtype, int rows, int nblk);
+void launch_gemv_qkv_pick(const GemvArgs& a, hipStream_t st);
 
 // Matrix-core GEMM for passes of several rows of bf16 weights: src SRC_TAPS or
 // SRC_PREP; epi EPI_STORE or EPI_SWIGLU (K-split partial sums into split_buf, summed
@@ -248,15 +289,6 @@ void launch_rows_qkv(int kvdtype, const AttnArgs& a, float* q_out, hipStream_t s
 void launch_attn_combine(const AttnArgs& a, hipStream_t st);
 
 // Sampling from the LM-head block statistics.
-// Statistics of one drafter logit row at the temperature its draft was drawn at:
-// S = sum exp((l - M) / T_d) over mapped rows (T_d = 0: unused), M the max and am the
-// lowest argmax row (-1: every row masked).
-struct QStat {
-  double S;
-  float M;
-  int am;
-};
-
 struct SampleArgs {
   int B;
   int k;                    // draft step index

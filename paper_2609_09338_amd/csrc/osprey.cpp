@@ -410,9 +410,11 @@ void run_attention(osprey_handle* h, const AttnArgs& a, bool merge = true) {
   h->t_end(t, reps);
 }
 
-// One forward pass of the body over `rows`; `s` holds the conditioning rows.
+// One forward pass of the body over `rows`; `s` holds the conditioning rows.  `pick`
+// (a single sequence's draft step): layer 0 draws the step's token itself.
 void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, const float* s,
-              bool from_embed, const SplitPlan& sp, int rows_per_seq, int slot0) {
+              bool from_embed, const SplitPlan& sp, int rows_per_seq, int slot0,
+              const PickArgs* pick = nullptr) {
   const osprey_config& c = h->cfg;
   const Ws& W = h->W;
   const int d = c.d_model, hd = c.head_dim, nq = c.n_q_heads, nkv = c.n_kv_heads;
@@ -443,7 +445,12 @@ void run_body(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, c
     g.ldy = qkv_w;
     g.split_buf = W.split;
     int t = h->t_begin(4);
-    launch_gemv(c.dtype, SRC_QKV, EPI_STORE, g, h->stream);
+    if (l == 0 && pick) {
+      g.pick = *pick;
+      launch_gemv_qkv_pick(g, h->stream);
+    } else {
+      launch_gemv(c.dtype, SRC_QKV, EPI_STORE, g, h->stream);
+    }
     h->t_end(t);
     // QK-norm + RoPE + KV append, attention, split combine
     AttnArgs a{};
@@ -739,9 +746,11 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
   }
 }
 
-// Final norm + LM head + block statistics, then the draft pick of step k.
+// Final norm + LM head + block statistics, then the draft pick of step k.  `defer`
+// (a single sequence whose next step's projection draws the token, gemv_pick_supported):
+// no sampling kernel; the head copies the fed-back row and *defer receives the pick.
 int run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, const float* temp,
-             const float* u, float* logits, long ld_b, int32_t* drafts_out) {
+             const float* u, float* logits, long ld_b, int32_t* drafts_out, PickArgs* defer = nullptr) {
   const osprey_config& c = h->cfg;
   const Ws& W = h->W;
   // bf16 heads run on the matrix cores at every batch size; the rows come prepared
@@ -779,6 +788,7 @@ int run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, const
   g.temp = temp;
   g.part = W.lm_part;
   g.nblk = nblk;
+  if (defer) g.fb_out = W.gfb;
   int t = h->t_begin(0);
   const int reps = t >= 0 ? kTimedRepeats : 1;
   for (int rep = 0; rep < reps; ++rep) {
@@ -806,6 +816,25 @@ int run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, const
   }
   }
   h->t_end(t, reps);
+  if (defer) {
+    PickArgs& p = *defer;
+    p.part = W.lm_part;
+    p.nblk = nblk;
+    p.blk_rows = tn;
+    p.logits = logits + (long)k * c.vocab_draft;
+    p.V = c.vocab_draft;
+    p.d2t = h->w.d2t;
+    p.temp = temp;
+    p.u = u + k;
+    p.k = k;
+    p.draft = W.drafts + k;
+    p.draft_out = drafts_out ? drafts_out + k : nullptr;
+    p.ar_tok = W.ar_tok;
+    p.ar_pos = W.ar_pos;
+    p.committed = W.committed;
+    p.qstat = W.qstat + k;
+    return OSPREY_OK;
+  }
   SampleArgs s{};
   s.B = B;
   s.k = k;
@@ -1246,14 +1275,21 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
   const long ld_b = a->draft_logits ? K : h->D.Km;
   const float* u = a->u_draft ? a->u_draft : W.u_zero;
   if (K >= 1) {
-    if ((rc = run_head(h, B, 0, K, W.last_row, a->temperature, u, logits, ld_b, a->draft_tokens)))
-      return rc;
     RowMeta ar{nullptr, W.ar_pos, W.ar_tok, nullptr, B};
     const bool ar_mr = gemm_use_mfma(c.dtype, B);
+    // A single sequence on the vector body draws each draft (but the last) in the next
+    // step's layer-0 projection instead of a sampling kernel (one launch fewer per step).
+    const bool fuse = !ar_mr && c.dtype == OSPREY_BF16 && lm_head_norm_in_supported(B, c.d_model) &&
+                      gemv_pick_supported(c.dtype, B, lm_head_plan(B, c.vocab_draft, h->n_cu).nblk);
+    PickArgs pick{};
+    if ((rc = run_head(h, B, 0, K, W.last_row, a->temperature, u, logits, ld_b, a->draft_tokens,
+                       fuse && K > 1 ? &pick : nullptr)))
+      return rc;
     for (int k = 1; k < K; ++k) {
       if (ar_mr) run_body_mr(h, ar, nullptr, B, W.gfb, 1, split, 1, a->slots[0]);
-      else run_body(h, ar, nullptr, B, W.gfb, true, split, 1, a->slots[0]);
-      if ((rc = run_head(h, B, k, K, nullptr, a->temperature, u, logits, ld_b, a->draft_tokens)))
+      else run_body(h, ar, nullptr, B, W.gfb, true, split, 1, a->slots[0], fuse ? &pick : nullptr);
+      if ((rc = run_head(h, B, k, K, nullptr, a->temperature, u, logits, ld_b, a->draft_tokens,
+                         fuse && k + 1 < K ? &pick : nullptr)))
         return rc;
     }
   }

@@ -224,6 +224,11 @@ __global__ void __launch_bounds__(kSkThreads) k_skinny(GemvArgs a, int T, int kc
       split_bf16x2(nx1.z * inv * bf16_lo(ng.w), nx1.w * inv * bf16_hi(ng.w), h.w, l.w);
       *reinterpret_cast<uint4*>(xh + c) = h;
       *reinterpret_cast<uint4*>(xl + c) = l;
+      // the fp32 row is also the next draft step's conditioning input: block 0 copies it
+      if (a.fb_out && blockIdx.x == 0) {
+        *reinterpret_cast<float4*>(a.fb_out + c) = nx0;
+        *reinterpret_cast<float4*>(a.fb_out + c + 4) = nx1;
+      }
     }
     __syncthreads();
   }

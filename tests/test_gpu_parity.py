@@ -330,3 +330,44 @@ def test_block_with_packed_rows_matches_oracle():
                 assert parity.draw_flag(logits[k], Td, float(u[b, k]), delta), (b, k)
                 flagged += 1
     assert flagged <= 1
+
+
+@pytest.mark.parametrize("name", ["p_single64", "p_partial"])
+def test_draft_pick_extreme_uniforms(name):
+    """Draws at u = 0, just below 1 and in between -- the inverse CDF's first entry, its
+    rounding fallbacks at the end of the row, ordinary points -- pick what the oracle's
+    inverse CDF picks on the same drafter logit rows (single sequences draw inside the
+    next step's layer-0 projection, batches in the sampling kernel; p_partial leaves
+    drafter rows unmapped)."""
+    _require_gpu()
+    from paper_2609_09338_amd import workload as WL
+    w = synth.get(name)
+    _say(f"[parity] {w.name}: draft picks at extreme uniforms")
+    s = WL.make_drafter(w, 1)
+    WL.reset_sequences(s)
+    inp = WL.iter_inputs(s, 0)
+    pattern = [0.0, 1.0 - 2.0 ** -24, 0.5, 2.0 ** -30, 0.999, 1.0 - 2.0 ** -20, 0.25]
+    u = np.array([[pattern[(b + k) % len(pattern)] for k in range(w.K)] for b in range(w.batch)],
+                 dtype=np.float32)
+    inp.u_draft = torch.from_numpy(u).to(s.device)
+    out = WL.alloc_outputs(s)
+    WL.draft(s, 0, inp, out)
+    torch.cuda.synchronize()
+    assert s.drafter.device_errors() == 0
+    g_logits, g_drafts = out.logits.cpu().numpy(), out.drafts.cpu().numpy()
+    d2t = synth.make_d2t(w)
+    exact = 0
+    for b in range(w.batch):
+        Td = w.draft_temperature(b)
+        for k in range(w.K):
+            row = g_logits[b, k].astype(np.float64)
+            assert np.isfinite(row).any()
+            mapped = set(int(t) for t in d2t[np.isfinite(row)])
+            assert int(g_drafts[b, k]) in mapped, (b, k, g_drafts[b, k])
+            want = int(d2t[OS.pick(row, Td, float(u[b, k]))])
+            if int(g_drafts[b, k]) == want:
+                exact += 1
+            else:
+                # the GPU's exponentials are fp32: allow a boundary within their error
+                assert parity.draw_flag(row, Td, float(u[b, k]), 1e-5), (b, k, g_drafts[b, k], want)
+    assert exact >= (w.batch * w.K) // 2, exact
