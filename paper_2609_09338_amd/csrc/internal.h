@@ -50,25 +50,33 @@ struct QStat {
   int am;
 };
 
-// SRC_QKV_PICK: the draft of step k of a single sequence (sequence 0), drawn in every
-// block of the layer-0 projection that consumes it (pick.h); block 0 writes it out as
-// the sampling kernel would.
+// The draft of step k of sequence r, drawn where the next step consumes it instead of
+// by the sampling kernel (pick.h): in every block of the single sequence's layer-0 QKV
+// GEMV (SRC_QKV_PICK, r = 0), or in row r's block of the matrix-core body's row
+// preparation (RowArgs::pick).  Pointers are those of sequence 0 at step k; sequence
+// r's are r strides on.  One block writes each draft out as the sampling kernel would.
 struct PickArgs {
-  const float* part;        // the LM head's records of the row (nblk <= kPickMaxRecords)
+  const float* part;        // the LM head's records (nblk <= kPickMaxRecords per row)
+  long ld_part;
   int nblk;
   int blk_rows;             // logits per record
-  const float* logits;      // the row's logits [V]
+  const float* logits;      // the rows' logits [V]
+  long ld_logits;
   int V;
   const int32_t* d2t;
-  const float* temp;        // the sequence's temperature
+  const float* temp;        // [r] the sequence's temperature
   const float* u;           // the step's uniform
+  int ld_u;
   int k;
   int32_t* draft;           // the step's draft slot (workspace)
+  int ld_draft;
   int32_t* draft_out;       // the caller's copy of it (nullable)
-  int32_t* ar_tok;          // next AR token / position (position = committed + k)
+  int ld_draft_out;
+  int32_t* ar_tok;          // [r] next AR token / position (position = committed + k)
   int32_t* ar_pos;
   const int32_t* committed;
   QStat* qstat;             // the step's row statistics (nullable)
+  int ld_qstat;
 };
 constexpr int kPickMaxRecords = 2048;   // 256 threads x 8 records
 
@@ -213,6 +221,9 @@ struct RowArgs {
   const void* embed;
   const int32_t* tok;
   int vocab_embed;
+  // (prep) pick.part non-null: row r's token is drawn here (PickArgs), not read from tok;
+  // the conditioning rows s_src may then be the rows x that this kernel overwrites
+  PickArgs pick;
 };
 // s = sum of partials or s_src -> (s_hi, s_lo); x = embed[tok]; out = rmsnorm(x) * gamma.
 void launch_rows_prep(const RowArgs& a, hipStream_t st);

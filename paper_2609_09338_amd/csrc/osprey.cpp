@@ -563,7 +563,7 @@ struct TreePass {
 
 void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B, const float* s_src,
                  int ks_taps, const SplitPlan& sp, int rows_per_seq, int slot0,
-                 const TreePass* tree = nullptr) {
+                 const TreePass* tree = nullptr, const PickArgs* pick = nullptr) {
   const osprey_config& c = h->cfg;
   const Ws& W = h->W;
   // passes of at most kLmMaxRows rows stream the weights once with the inputs
@@ -596,6 +596,7 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
     p.embed = h->w.embed;
     p.tok = rows.tok;
     p.vocab_embed = c.vocab_target;
+    if (pick) p.pick = *pick;   // each row draws its own token (autoregressive rows only)
     launch_rows_prep(p, h->stream);
   }
   GemvArgs gb{};
@@ -746,9 +747,11 @@ void run_body_mr(osprey_handle* h, const RowMeta& rows, const int32_t* cu, int B
   }
 }
 
-// Final norm + LM head + block statistics, then the draft pick of step k.  `defer`
-// (a single sequence whose next step's projection draws the token, gemv_pick_supported):
-// no sampling kernel; the head copies the fed-back row and *defer receives the pick.
+// Final norm + LM head + block statistics, then the draft pick of step k.  `defer` (the
+// next step draws the tokens where it consumes them: a single sequence's layer-0 QKV
+// GEMV, gemv_pick_supported, or the matrix-core body's row preparation): no sampling
+// kernel; *defer receives the pick, and a single normalised row is copied to the
+// fed-back buffer by the head.
 int run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, const float* temp,
              const float* u, float* logits, long ld_b, int32_t* drafts_out, PickArgs* defer = nullptr) {
   const osprey_config& c = h->cfg;
@@ -788,7 +791,7 @@ int run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, const
   g.temp = temp;
   g.part = W.lm_part;
   g.nblk = nblk;
-  if (defer) g.fb_out = W.gfb;
+  if (defer && !prepared) g.fb_out = W.gfb;
   int t = h->t_begin(0);
   const int reps = t >= 0 ? kTimedRepeats : 1;
   for (int rep = 0; rep < reps; ++rep) {
@@ -819,20 +822,26 @@ int run_head(osprey_handle* h, int B, int k, int K, const int32_t* gather, const
   if (defer) {
     PickArgs& p = *defer;
     p.part = W.lm_part;
+    p.ld_part = (long)nblk * 4;
     p.nblk = nblk;
     p.blk_rows = tn;
     p.logits = logits + (long)k * c.vocab_draft;
+    p.ld_logits = ld_b * c.vocab_draft;
     p.V = c.vocab_draft;
     p.d2t = h->w.d2t;
     p.temp = temp;
     p.u = u + k;
+    p.ld_u = K;
     p.k = k;
     p.draft = W.drafts + k;
+    p.ld_draft = h->D.Km;
     p.draft_out = drafts_out ? drafts_out + k : nullptr;
+    p.ld_draft_out = K;
     p.ar_tok = W.ar_tok;
     p.ar_pos = W.ar_pos;
     p.committed = W.committed;
     p.qstat = W.qstat + k;
+    p.ld_qstat = h->D.Km;
     return OSPREY_OK;
   }
   SampleArgs s{};
@@ -1277,19 +1286,28 @@ OSPREY_API int osprey_draft_step(osprey_handle* h, const osprey_step_args* a) {
   if (K >= 1) {
     RowMeta ar{nullptr, W.ar_pos, W.ar_tok, nullptr, B};
     const bool ar_mr = gemm_use_mfma(c.dtype, B);
-    // A single sequence on the vector body draws each draft (but the last) in the next
-    // step's layer-0 projection instead of a sampling kernel (one launch fewer per step).
-    const bool fuse = !ar_mr && c.dtype == OSPREY_BF16 && lm_head_norm_in_supported(B, c.d_model) &&
-                      gemv_pick_supported(c.dtype, B, lm_head_plan(B, c.vocab_draft, h->n_cu).nblk);
+    // Each draft but the last is drawn where the next step consumes it instead of by a
+    // sampling kernel (one launch fewer per step): a single sequence on the vector body
+    // draws in its layer-0 QKV GEMV (the head copies its gathered input row to the
+    // fed-back buffer), the rows of the matrix-core body in their row preparation, whose
+    // conditioning input is then the rows x themselves.  The latter needs row b of x to
+    // be sequence b's, so the first draft, whose head reads the ingest's gathered last
+    // rows (packed, several per sequence), keeps its sampling kernel there.
+    const int lm_nblk = lm_head_plan(std::min(B, kLmMaxRows), c.vocab_draft, h->n_cu).nblk;
+    const bool fuse = c.dtype == OSPREY_BF16 &&
+                      (ar_mr ? lm_nblk <= kPickMaxRecords
+                             : lm_head_norm_in_supported(B, c.d_model) && gemv_pick_supported(c.dtype, B, lm_nblk));
+    auto deferred = [&](int k) { return fuse && k + 1 < K && (k >= 1 || !ar_mr); };
     PickArgs pick{};
     if ((rc = run_head(h, B, 0, K, W.last_row, a->temperature, u, logits, ld_b, a->draft_tokens,
-                       fuse && K > 1 ? &pick : nullptr)))
+                       deferred(0) ? &pick : nullptr)))
       return rc;
     for (int k = 1; k < K; ++k) {
-      if (ar_mr) run_body_mr(h, ar, nullptr, B, W.gfb, 1, split, 1, a->slots[0]);
-      else run_body(h, ar, nullptr, B, W.gfb, true, split, 1, a->slots[0], fuse ? &pick : nullptr);
+      const bool drawn = deferred(k - 1);
+      if (ar_mr) run_body_mr(h, ar, nullptr, B, drawn ? W.x : W.gfb, 1, split, 1, a->slots[0], nullptr, drawn ? &pick : nullptr);
+      else run_body(h, ar, nullptr, B, W.gfb, true, split, 1, a->slots[0], drawn ? &pick : nullptr);
       if ((rc = run_head(h, B, k, K, nullptr, a->temperature, u, logits, ld_b, a->draft_tokens,
-                         fuse && k + 1 < K ? &pick : nullptr)))
+                         deferred(k) ? &pick : nullptr)))
         return rc;
     }
   }

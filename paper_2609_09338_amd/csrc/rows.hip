@@ -10,6 +10,7 @@
 // consecutive columns per step.
 #include "common.h"
 #include "internal.h"
+#include "pick.h"
 
 namespace osp {
 
@@ -108,17 +109,47 @@ OSP_DEV void load_gain(const RowArgs& a, uint2 (&gr)[kRowGroups]) {
   }
 }
 
+// DRAW: row r's token is drawn here from the LM head's records and logits (a.pick), and
+// the conditioning rows s_src may be the rows x that this block overwrites (each thread
+// reads its columns of row r before it writes them).
+template <bool DRAW>
 __global__ void __launch_bounds__(kRowThreads) k_rows_prep(RowArgs a) {
   __shared__ float sm[kRowThreads / 64];
   const int r = blockIdx.x;
   const int rows = a.count ? min(*a.count, a.max_rows) : a.max_rows;
   if (r >= rows) return;
-  // the token row and the gain are requested first, ahead of the conditioning segment
-  int t = a.tok[r];
+  uint2 gr[kRowGroups], er[kRowGroups];
+  int t;
+  float4 sv[DRAW ? kRowGroups : 1];
+  Pick pk_res{};
+  int pk_pos = 0;
+  if constexpr (DRAW) {
+    // the records first (the memory counter is in order: whatever is requested after
+    // them arrives no earlier), then the conditioning row and the gain, whose loads do
+    // not depend on the token
+    constexpr int PER = kPickMaxRecords / kRowThreads;
+    const PickArgs& pk = a.pick;
+    const float* part = pk.part + r * pk.ld_part;
+    PickRecs<PER> rec;
+    pick_request<kRowThreads, PER>(rec, part, pk.nblk);
+#pragma unroll
+    for (int i = 0; i < kRowGroups; ++i)
+      sv[i] = *reinterpret_cast<const float4*>(a.s_src + (long)r * a.W +
+                                               min(((int)threadIdx.x + i * kRowThreads) * 4, a.W - 4));
+    load_gain(a, gr);
+    pk_pos = pk.committed[r] + pk.k;
+    // (nothing that reads the records may be scheduled above this point)
+    __builtin_amdgcn_sched_barrier(0);
+    pk_res = pick_draft<kRowThreads, PER>(rec, part, pk.nblk, pk.blk_rows, pk.logits + r * pk.ld_logits, pk.V,
+                                          pk.d2t, pk.temp[r], pk.u[(long)r * pk.ld_u]);
+    t = pk_res.tok;
+  } else {
+    // the token row and the gain are requested first, ahead of the conditioning segment
+    t = a.tok[r];
+  }
   t = min(max(t, 0), a.vocab_embed - 1);
   const bf16_t* e = reinterpret_cast<const bf16_t*>(a.embed) + (long)t * a.W;
-  uint2 gr[kRowGroups], er[kRowGroups];
-  load_gain(a, gr);
+  if constexpr (!DRAW) load_gain(a, gr);
 #pragma unroll
   for (int i = 0; i < kRowGroups; ++i)
     er[i] = *reinterpret_cast<const uint2*>(e + min(((int)threadIdx.x + i * kRowThreads) * 4, a.W - 4));
@@ -127,8 +158,9 @@ __global__ void __launch_bounds__(kRowThreads) k_rows_prep(RowArgs a) {
   for (int i = 0; i < kRowGroups; ++i) {
     const int c = (threadIdx.x + i * kRowThreads) * 4;
     if (c < a.W) {
-      const float4 v = a.s_src ? *reinterpret_cast<const float4*>(a.s_src + (long)r * a.W + c)
-                               : sum_parts4(a, r, c);
+      float4 v;
+      if constexpr (DRAW) v = sv[i];
+      else v = a.s_src ? *reinterpret_cast<const float4*>(a.s_src + (long)r * a.W + c) : sum_parts4(a, r, c);
       store_pair4(a.s_hi, a.s_lo, (long)r * a.W + c, v);
     }
   }
@@ -145,6 +177,18 @@ __global__ void __launch_bounds__(kRowThreads) k_rows_prep(RowArgs a) {
     }
   }
   norm_out(a, r, v, gr, ss, sm);
+  // the draft, its position and the row statistics, written once the row is done (their
+  // stores would otherwise hold up this wavefront's next loads)
+  if constexpr (DRAW) {
+    if (threadIdx.x == 0) {
+      const PickArgs& pk = a.pick;
+      pk.draft[(long)r * pk.ld_draft] = pk_res.tok;
+      if (pk.draft_out) pk.draft_out[(long)r * pk.ld_draft_out] = pk_res.tok;
+      pk.ar_tok[r] = pk_res.tok;
+      pk.ar_pos[r] = pk_pos;
+      if (pk.qstat) pk.qstat[(long)r * pk.ld_qstat] = QStat{pk_res.S, pk_res.M, pk_res.am};
+    }
+  }
 }
 
 __global__ void __launch_bounds__(kRowThreads) k_rows_resid_norm(RowArgs a) {
@@ -191,7 +235,8 @@ __global__ void __launch_bounds__(kRowThreads) k_rows_swiglu(RowArgs a) {
 }
 
 void launch_rows_prep(const RowArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(k_rows_prep, dim3(a.max_rows), dim3(kRowThreads), 0, st, a);
+  if (a.pick.part) hipLaunchKernelGGL(k_rows_prep<true>, dim3(a.max_rows), dim3(kRowThreads), 0, st, a);
+  else hipLaunchKernelGGL(k_rows_prep<false>, dim3(a.max_rows), dim3(kRowThreads), 0, st, a);
 }
 void launch_rows_resid_norm(const RowArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(k_rows_resid_norm, dim3(a.max_rows), dim3(kRowThreads), 0, st, a);
