@@ -207,7 +207,7 @@ k_gemv(GemvArgs a, int rows_per_wave) {
   // token's embedding row) would otherwise start only once the weights are in.
   constexpr int kPickPer = kPickMaxRecords / kGemvThreads;
   PickRecs<SRC == SRC_QKV_PICK ? kPickPer : 1> rec;
-  int pk_pos = 0;   // the step's position (block 0, thread 0 writes it out at the end)
+  int pk_pos = 0;   // the step's position (block 0, thread 0 writes it out at its end)
   if constexpr (SRC == SRC_QKV_PICK) {
     pick_request<kGemvThreads, kPickPer>(rec, a.pick.part, a.pick.nblk);
     pk_pos = a.pick.committed[0] + a.pick.k;
@@ -241,8 +241,8 @@ k_gemv(GemvArgs a, int rows_per_wave) {
   if constexpr (SRC == SRC_QKV_PICK) __builtin_amdgcn_sched_barrier(0);
 
   // SRC_QKV_PICK: the step's token, drawn by the whole block (every block draws the same
-  // one); block 0 writes the draft, the next position and the row statistics out when
-  // it is done (their stores would hold up its next loads: the counter is in order)
+  // one); block 0 writes the draft, the next position and the row statistics out at its
+  // end, after its own products
   int tok = 0;
   Pick pk_res{};
   if constexpr (SRC == SRC_QKV_PICK) {

@@ -177,8 +177,7 @@ __global__ void __launch_bounds__(kRowThreads) k_rows_prep(RowArgs a) {
     }
   }
   norm_out(a, r, v, gr, ss, sm);
-  // the draft, its position and the row statistics, written once the row is done (their
-  // stores would otherwise hold up this wavefront's next loads)
+  // the draft, its position and the row statistics, written once the row is done
   if constexpr (DRAW) {
     if (threadIdx.x == 0) {
       const PickArgs& pk = a.pick;
