@@ -210,6 +210,18 @@ def test_iterations_match_oracle(name):
     _run_parity(w, 4, list(range(w.batch)), tol)
 
 
+@pytest.mark.parametrize("name,K", [("p_single64", 2), ("p_single64", 3), ("p_partial", 2),
+                                    ("p_partial", 3), ("p_qwen_small", 3)])
+def test_short_chains_match_oracle(name, K):
+    """Chains of two and three drafts: where each draft is drawn (a single sequence: the
+    next step's QKV GEMV but for the last; batches: the sampling kernel for the first and
+    last, the next step's row preparation between) at the shortest chains."""
+    _require_gpu()
+    w = synth.get(name).with_(name=f"{name}_K{K}", K=K)
+    tol = 1e-4 if w.dtype == "f32" else 2e-2
+    _run_parity(w, 3, list(range(w.batch)), tol)
+
+
 def test_tiny_fp32_variants_match_oracle():
     """The small fp32 chain draft: zero and N(0, 0.02) expansion, greedy and T = 1,
     noise sigma 0.5 and 2 (8 runs)."""
