@@ -247,8 +247,8 @@ k_gemv(GemvArgs a, int rows_per_wave) {
   Pick pk_res{};
   if constexpr (SRC == SRC_QKV_PICK) {
     const PickArgs& pk = a.pick;
-    pk_res = pick_draft<kGemvThreads, kPickPer>(rec, pk.part, pk.nblk, pk.blk_rows, pk.logits, pk.V,
-                                                pk.d2t, pk.temp[0], pk.u[0]);
+    pk_res = pick_draft<kGemvThreads, kPickPer>(rec, pk.nblk, pk.blk_rows, pk.logits, pk.V, pk.d2t,
+                                                pk.temp[0], pk.u[0]);
     tok = pk_res.tok;
     if (n_lo >= a.N) return;
   }

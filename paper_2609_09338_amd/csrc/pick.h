@@ -44,11 +44,11 @@ OSP_DEV void pick_request(PickRecs<PER>& rec, const float* part, int nblk) {
 }
 
 // Every thread of the NT-thread block calls this (it holds block barriers) and gets
-// the same result.  rec: what pick_request loaded from part, the row's nblk records;
-// lg: the row's logits.  T and u are the row's temperature and uniform.
+// the same result.  rec: what pick_request loaded, the row's nblk records; lg: the
+// row's logits.  T and u are the row's temperature and uniform.
 template <int NT, int PER>
-OSP_DEV Pick pick_draft(const PickRecs<PER>& rec, const float* part, int nblk, int blk_rows,
-                        const float* lg, int V, const int32_t* d2t, float T, float u) {
+OSP_DEV Pick pick_draft(const PickRecs<PER>& rec, int nblk, int blk_rows, const float* lg, int V,
+                        const int32_t* d2t, float T, float u) {
   constexpr int NW = NT / OSP_WAVE;
   __shared__ float s_wm[NW];
   __shared__ int s_wi[NW];
@@ -131,18 +131,24 @@ OSP_DEV Pick pick_draft(const PickRecs<PER>& rec, const float* part, int nblk, i
       if (hit >= 0) { s_blk = i0 + hit; s_before = run; }
     }
     __syncthreads();
-    if (tid == 0 && s_blk < 0) {        // rounding pushed the target past the last record
-      int last = nblk - 1;
-      while (last > 0 && !(part[last * 4 + 0] > -INFINITY)) --last;
-      s_blk = last;
-      double run = 0.0;
-      for (int i = 0; i < last; ++i) {
-        const float mm = part[i * 4 + 0];
-        if (mm > -INFINITY) run += (double)part[i * 4 + 1] * (double)__expf((mm - M) / T);
+    if (s_blk < 0) {   // (uniform) rounding pushed the target past the last record with weight
+      int li = -1;
+      double lb = 0.0, run = excl;
+#pragma unroll
+      for (int q = 0; q < PER; ++q) {
+        if (i0 + q < nblk && bsum[q] > 0.0) { li = i0 + q; lb = run; }
+        run += bsum[q];
       }
-      s_before = run;
+      const int wl = wave_max_i(li);
+      if (lane == 0) s_wi[wave] = wl;
+      __syncthreads();
+      int last = -1;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) last = max(last, s_wi[w]);
+      if (li >= 0 && li == last) { s_blk = li; s_before = lb; }
+      if (last < 0 && tid == 0) { s_blk = 0; s_before = 0.0; }   // (no weight at all: not reached)
+      __syncthreads();
     }
-    __syncthreads();
     // ---- every wavefront scans the chosen range's logits (no barrier after); the
     //      first kScanPre x 64 are requested at once (a head range holds 16 T <= 80) ----
     constexpr int kScanPre = 2;

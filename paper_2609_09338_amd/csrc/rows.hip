@@ -140,7 +140,7 @@ __global__ void __launch_bounds__(kRowThreads) k_rows_prep(RowArgs a) {
     pk_pos = pk.committed[r] + pk.k;
     // (nothing that reads the records may be scheduled above this point)
     __builtin_amdgcn_sched_barrier(0);
-    pk_res = pick_draft<kRowThreads, PER>(rec, part, pk.nblk, pk.blk_rows, pk.logits + r * pk.ld_logits, pk.V,
+    pk_res = pick_draft<kRowThreads, PER>(rec, pk.nblk, pk.blk_rows, pk.logits + r * pk.ld_logits, pk.V,
                                           pk.d2t, pk.temp[r], pk.u[(long)r * pk.ld_u]);
     t = pk_res.tok;
   } else {

@@ -34,7 +34,7 @@ __global__ void __launch_bounds__(kSampleThreads) k_sample(SampleArgs a) {
     fb[q] = c < a.d ? *reinterpret_cast<const float4*>(a.x + (long)xr * a.d + c) : make_float4(0.f, 0.f, 0.f, 0.f);
   }
   const float* lg = a.logits + (long)b * a.ld_logits + (a.block ? (long)k * a.V : 0L);
-  const Pick p = pick_draft<kSampleThreads, kPer>(rec, part, a.nblk, a.blk_rows, lg, a.V, a.d2t, a.temp[b],
+  const Pick p = pick_draft<kSampleThreads, kPer>(rec, a.nblk, a.blk_rows, lg, a.V, a.d2t, a.temp[b],
                                                   a.u[(long)b * a.K + k]);
   if (tid == 0) {
     a.drafts[(long)b * a.ld_drafts + k] = p.tok;

@@ -346,8 +346,8 @@ def test_block_with_packed_rows_matches_oracle():
 
 @pytest.mark.parametrize("name", ["p_single64", "p_partial"])
 def test_draft_pick_extreme_uniforms(name):
-    """Draws at u = 0, just below 1 and in between -- the inverse CDF's first entry, its
-    rounding fallbacks at the end of the row, ordinary points -- pick what the oracle's
+    """Draws at u = 0, at and just below 1 and in between -- the inverse CDF's first
+    entry, its rounding fallbacks at the end of the row, ordinary points -- pick what the oracle's
     inverse CDF picks on the same drafter logit rows (single sequences draw inside the
     next step's layer-0 projection, batches in the sampling kernel; p_partial leaves
     drafter rows unmapped)."""
@@ -358,7 +358,9 @@ def test_draft_pick_extreme_uniforms(name):
     s = WL.make_drafter(w, 1)
     WL.reset_sequences(s)
     inp = WL.iter_inputs(s, 0)
-    pattern = [0.0, 1.0 - 2.0 ** -24, 0.5, 2.0 ** -30, 0.999, 1.0 - 2.0 ** -20, 0.25]
+    # (u = 1 lies outside the callers' [0, 1): it stands in for rounding that carries
+    # u S past the total, where the pick takes the last entry with weight)
+    pattern = [0.0, 1.0, 1.0 - 2.0 ** -24, 0.5, 2.0 ** -30, 0.999, 1.0 - 2.0 ** -20, 0.25]
     u = np.array([[pattern[(b + k) % len(pattern)] for k in range(w.K)] for b in range(w.batch)],
                  dtype=np.float32)
     inp.u_draft = torch.from_numpy(u).to(s.device)
