@@ -8,8 +8,9 @@
 // u * S -- the range holding that point is found from the range sums (float64 prefix),
 // then that range's logits are scanned.  The row is mapped to a target id through d2t.
 //
-// Used by the sampling kernel and, for a single sequence, by the next draft step's
-// layer-0 projection (which then needs no sampling launch before it).
+// Used by the sampling kernel and, where the next draft step consumes the draft, by that
+// step's first kernel (a single sequence's layer-0 QKV GEMV, a batch's row preparation),
+// which then needs no sampling launch before it.
 #pragma once
 
 #include "common.h"
